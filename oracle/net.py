@@ -1,0 +1,137 @@
+"""Oracle network driver: BPTrainOneBatch (Sec. 4.1.3, Alg. 1) over the fp64 oracle.
+
+TEST INFRASTRUCTURE ONLY (see ``oracle/__init__.py``).
+
+The forward loop visits the layers in order and calls each layer's
+ComputeFeature; the backward loop visits them in reverse and calls
+ComputeGradient, which yields the parameter gradients and the source layer's
+gradient (Sec. 4.1.2); the Updater (Sec. 4.1.4) then applies SGD with
+momentum to every parameter.  All arithmetic is the oracle's (fp64).
+
+Layer records are duck-typed by class name ("Conv", "Pool", "Relu", "FC",
+"SoftmaxCE") and read only through their attributes, so this module needs
+no import from outside the oracle.
+"""
+from __future__ import annotations
+
+from typing import Dict, List, Optional
+
+import numpy as np
+
+from . import (AVG, MAX, conv_bwd_data, conv_bwd_filter, conv_fwd, fc_bwd, fc_fwd,
+               pool_bwd, pool_fwd, relu_bwd, relu_fwd, sgd_momentum, softmax_ce)
+
+
+def _kind(layer) -> str:
+    return type(layer).__name__
+
+
+def forward(layers, x, params: List, labels=None) -> Dict:
+    """Forward pass.  ``params`` is a list of (w, b) in forward order of the
+    parametrised layers (conv KCRS, FC (J, I) with I flattened as (c, h, w)).
+    Returns a dict with per-layer outputs ``out[name]``, pooling argmax
+    ``argmax[name]``, and, for a stack ending in a softmax loss, ``loss`` and
+    ``dlogits``."""
+    acts = {"out": {}, "argmax": {}, "in": {}}
+    h = np.asarray(x, dtype=np.float64)
+    pi = 0
+    for l in layers:
+        k = _kind(l)
+        acts["in"][l.name] = h
+        if k == "Conv":
+            w, b = params[pi]
+            pi += 1
+            h = conv_fwd(h, w, b, pad=l.pad, stride=l.stride)
+        elif k == "Pool":
+            mode = MAX if l.mode == "max" else AVG
+            h, am = pool_fwd(h, mode, k=l.kernel, stride=l.stride, pad=l.pad, ceil_mode=l.ceil_mode)
+            acts["argmax"][l.name] = am
+        elif k == "Relu":
+            h = relu_fwd(h)
+        elif k == "FC":
+            w, b = params[pi]
+            pi += 1
+            B = h.shape[0]
+            h = fc_fwd(h.reshape(B, -1), w, b).reshape(B, -1, 1, 1)
+        elif k == "SoftmaxCE":
+            B = h.shape[0]
+            loss, dz = softmax_ce(h.reshape(B, -1), labels)
+            acts["loss"] = loss
+            acts["dlogits"] = dz.reshape(h.shape)
+        else:
+            raise ValueError("unknown layer kind %s" % k)
+        acts["out"][l.name] = h
+    return acts
+
+
+def backward(layers, params: List, acts: Dict, dy_top=None, need_input_grad: bool = False) -> Dict:
+    """Backward pass in reverse layer order.  Returns ``grad_in[name]`` (the
+    gradient w.r.t. each layer's input), and ``dw[name]``/``db[name]`` for
+    parametrised layers.  The first layer's input gradient is only computed
+    when ``need_input_grad`` is set (training never needs it)."""
+    res = {"grad_in": {}, "dw": {}, "db": {}}
+    pidx = {}
+    pi = 0
+    for l in layers:
+        if _kind(l) in ("Conv", "FC"):
+            pidx[l.name] = pi
+            pi += 1
+    g = None if dy_top is None else np.asarray(dy_top, dtype=np.float64)
+    for li in range(len(layers) - 1, -1, -1):
+        l = layers[li]
+        k = _kind(l)
+        xin = acts["in"][l.name]
+        first = li == 0
+        if k == "SoftmaxCE":
+            g = acts["dlogits"]
+        elif k == "Relu":
+            g = relu_bwd(acts["out"][l.name], g)
+        elif k == "Pool":
+            mode = MAX if l.mode == "max" else AVG
+            g = pool_bwd(g, acts["argmax"].get(l.name), xin.shape, mode, k=l.kernel,
+                         stride=l.stride, pad=l.pad, ceil_mode=l.ceil_mode)
+        elif k == "Conv":
+            w, b = params[pidx[l.name]]
+            if b is not None:
+                dw, db = conv_bwd_filter(xin, g, w.shape, pad=l.pad, stride=l.stride, with_bias=True)
+            else:
+                dw, db = conv_bwd_filter(xin, g, w.shape, pad=l.pad, stride=l.stride, with_bias=False), None
+            res["dw"][l.name], res["db"][l.name] = dw, db
+            g = conv_bwd_data(g, w, xin.shape, pad=l.pad, stride=l.stride) if (not first or need_input_grad) else None
+        elif k == "FC":
+            w, b = params[pidx[l.name]]
+            B = xin.shape[0]
+            dx, dw, db = fc_bwd(xin.reshape(B, -1), w, g.reshape(B, -1), with_bias=b is not None)
+            res["dw"][l.name], res["db"][l.name] = dw, db
+            g = dx.reshape(xin.shape)
+        else:
+            raise ValueError("unknown layer kind %s" % k)
+        res["grad_in"][l.name] = g
+    return res
+
+
+def train_one_batch(layers, x, params: List, master: Optional[List] = None, labels=None, dy_top=None,
+                    lr: float = 0.0, momentum: float = 0.0, wd: float = 0.0, velocity: Optional[List] = None,
+                    need_input_grad: bool = False) -> Dict:
+    """Alg. 1 followed by the Updater.  ``params`` are the values the layers
+    compute with; ``master`` (default: ``params``) are the values the Updater
+    steps (for bf16 compute these are the fp32 master weights).  Returns the
+    forward dict, the backward dict and the updated (w, b) and momentum."""
+    acts = forward(layers, x, params, labels=labels)
+    grads = backward(layers, params, acts, dy_top=dy_top, need_input_grad=need_input_grad)
+    master = params if master is None else master
+    names = [l.name for l in layers if _kind(l) in ("Conv", "FC")]
+    new_params, new_vel = [], []
+    for i, name in enumerate(names):
+        w, b = master[i]
+        vw, vb = (None, None) if velocity is None else velocity[i]
+        vw = np.zeros(np.shape(w)) if vw is None else vw
+        w2, vw2 = sgd_momentum(w, grads["dw"][name], vw, lr, momentum, wd)
+        if b is not None:
+            vb = np.zeros(np.shape(b)) if vb is None else vb
+            b2, vb2 = sgd_momentum(b, grads["db"][name], vb, lr, momentum, wd)
+        else:
+            b2 = vb2 = None
+        new_params.append((w2, b2))
+        new_vel.append((vw2, vb2))
+    return {"acts": acts, "grads": grads, "params": new_params, "velocity": new_vel}

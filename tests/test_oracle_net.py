@@ -1,0 +1,139 @@
+"""Pins for the oracle's network driver (BPTrainOneBatch, Sec. 4.1.3, Alg. 1).
+
+* whole-network finite differences (fp64) on a shrunken CIFAR-shaped net
+  with every layer type of the workloads (conv, max/avg pooling in ceil mode,
+  ReLU, FC, softmax-CE);
+* the same net through torch CPU float64 autograd (a library routine);
+* the listed per-layer shapes of all five workloads against the oracle's own
+  shape arithmetic.
+"""
+import numpy as np
+import pytest
+import torch
+import torch.nn.functional as F
+
+import oracle
+from oracle import net as onet
+from paper_1603_07846_amd import workloads as wl
+
+
+def _tiny_net():
+    return (
+        wl.Conv("c1", 4, 5, 1, 2, out_shape=(4, 8, 8)),
+        wl.Pool("p1", "max", 3, 2, 0, True, (4, 4, 4)),
+        wl.Relu("r1"),
+        wl.Conv("c2", 4, 5, 1, 2, out_shape=(4, 4, 4)),
+        wl.Relu("r2"),
+        wl.Pool("p2", "avg", 3, 2, 0, True, (4, 2, 2)),
+        wl.Conv("c3", 6, 3, 1, 1, out_shape=(6, 2, 2)),
+        wl.Relu("r3"),
+        wl.FC("fc", 5, out_shape=(5, 1, 1)),
+        wl.SoftmaxCE(),
+    )
+
+
+def _tiny_inputs(seed=3):
+    rng = np.random.default_rng(seed)
+    x = rng.uniform(0, 1, (2, 3, 8, 8))
+    params = [
+        (rng.standard_normal((4, 3, 5, 5)) * 0.3, rng.standard_normal(4) * 0.1),
+        (rng.standard_normal((4, 4, 5, 5)) * 0.3, rng.standard_normal(4) * 0.1),
+        (rng.standard_normal((6, 4, 3, 3)) * 0.3, rng.standard_normal(6) * 0.1),
+        (rng.standard_normal((5, 24)) * 0.3, rng.standard_normal(5) * 0.1),
+    ]
+    labels = np.array([1, 4], np.int32)
+    return x, params, labels
+
+
+def _loss(layers, x, params, labels):
+    return onet.forward(layers, x, params, labels=labels)["loss"]
+
+
+def test_net_gradients_finite_differences():
+    layers = _tiny_net()
+    x, params, labels = _tiny_inputs()
+    acts = onet.forward(layers, x, params, labels=labels)
+    grads = onet.backward(layers, params, acts, need_input_grad=True)
+    eps = 1e-6
+    rng = np.random.default_rng(0)
+    names = ["c1", "c2", "c3", "fc"]
+    for li, name in enumerate(names):
+        w, b = params[li]
+        for _ in range(4):
+            idx = tuple(rng.integers(0, d) for d in w.shape)
+            wp = [(pw.copy(), pb.copy()) for pw, pb in params]
+            wm = [(pw.copy(), pb.copy()) for pw, pb in params]
+            wp[li][0][idx] += eps
+            wm[li][0][idx] -= eps
+            fd = (_loss(layers, x, wp, labels) - _loss(layers, x, wm, labels)) / (2 * eps)
+            assert abs(fd - grads["dw"][name][idx]) < 1e-6 * max(1.0, abs(fd)), (name, idx)
+        k = int(rng.integers(0, b.shape[0]))
+        bp = [(pw.copy(), pb.copy()) for pw, pb in params]
+        bm = [(pw.copy(), pb.copy()) for pw, pb in params]
+        bp[li][1][k] += eps
+        bm[li][1][k] -= eps
+        fd = (_loss(layers, x, bp, labels) - _loss(layers, x, bm, labels)) / (2 * eps)
+        assert abs(fd - grads["db"][name][k]) < 1e-6 * max(1.0, abs(fd))
+    for _ in range(4):
+        idx = tuple(rng.integers(0, d) for d in x.shape)
+        e = np.zeros_like(x)
+        e[idx] = eps
+        fd = (_loss(layers, x + e, params, labels) - _loss(layers, x - e, params, labels)) / (2 * eps)
+        assert abs(fd - grads["grad_in"]["c1"][idx]) < 1e-6 * max(1.0, abs(fd))
+
+
+def test_net_against_torch_autograd():
+    layers = _tiny_net()
+    x, params, labels = _tiny_inputs(seed=9)
+    res = onet.train_one_batch(layers, x, params, labels=labels, lr=0.01, momentum=0.9, wd=5e-4,
+                               need_input_grad=True)
+    tp = [(torch.tensor(w, requires_grad=True), torch.tensor(b, requires_grad=True)) for w, b in params]
+    tx = torch.tensor(x, requires_grad=True)
+    h = F.conv2d(tx, tp[0][0], tp[0][1], padding=2)
+    h = F.relu(F.max_pool2d(h, 3, 2, ceil_mode=True))
+    h = F.relu(F.conv2d(h, tp[1][0], tp[1][1], padding=2))
+    h = F.avg_pool2d(h, 3, 2, ceil_mode=True, count_include_pad=True)
+    h = F.relu(F.conv2d(h, tp[2][0], tp[2][1], padding=1))
+    z = F.linear(h.reshape(2, -1), tp[3][0], tp[3][1])
+    loss = F.cross_entropy(z, torch.tensor(labels, dtype=torch.long))
+    loss.backward()
+    assert abs(res["acts"]["loss"] - loss.item()) < 1e-12
+    for li, name in enumerate(["c1", "c2", "c3", "fc"]):
+        np.testing.assert_allclose(res["grads"]["dw"][name], tp[li][0].grad.numpy(), rtol=1e-10, atol=1e-13)
+        np.testing.assert_allclose(res["grads"]["db"][name], tp[li][1].grad.numpy(), rtol=1e-10, atol=1e-13)
+    np.testing.assert_allclose(res["grads"]["grad_in"]["c1"], tx.grad.numpy(), rtol=1e-10, atol=1e-13)
+    # the update: one SGD-momentum step from zero velocity
+    opt = torch.optim.SGD([p for pair in tp for p in pair], lr=0.01, momentum=0.9, weight_decay=5e-4)
+    opt.step()
+    for li in range(4):
+        np.testing.assert_allclose(res["params"][li][0], tp[li][0].detach().numpy(), rtol=1e-13, atol=1e-15)
+        np.testing.assert_allclose(res["params"][li][1], tp[li][1].detach().numpy(), rtol=1e-13, atol=1e-15)
+
+
+@pytest.mark.parametrize("index", [1, 2, 3, 4, 5])
+def test_workload_listed_shapes_match_oracle_arithmetic(index):
+    w = wl.WORKLOADS[index]
+    c, h, ww = w.in_shape
+    for l in w.layers:
+        if isinstance(l, wl.Conv):
+            shape = (l.out_channels, oracle.conv_out(h, l.kernel, l.pad, l.stride),
+                     oracle.conv_out(ww, l.kernel, l.pad, l.stride))
+        elif isinstance(l, wl.Pool):
+            shape = (c, oracle.pool_out(h, l.kernel, l.pad, l.stride, l.ceil_mode),
+                     oracle.pool_out(ww, l.kernel, l.pad, l.stride, l.ceil_mode))
+        elif isinstance(l, wl.FC):
+            shape = (l.out_features, 1, 1)
+        else:
+            continue
+        assert shape == tuple(l.out_shape), l.name
+        c, h, ww = shape
+
+
+def test_parameter_counts():
+    # CIFAR-shaped net: 89,578 parameters; AlexNet-shaped step: 62,378,344
+    def count(w):
+        inp = wl.make_inputs(w, batch=1)
+        return sum(p.w.size + (0 if p.b is None else p.b.size) for p in inp.params)
+    assert count(wl.CFG2) == 89578
+    assert count(wl.CFG5) == 62378344
+    assert count(wl.CFG1) == 2400
