@@ -1,0 +1,202 @@
+/*
+ * singa_mi.h -- C ABI of the MI355X (gfx950) library for the data-parallel hot
+ * path of SINGA's training loop (Wang et al., "Deep Learning At Scale and At
+ * Ease", arXiv 1603.07846).
+ *
+ * The calls follow the paper's layer abstraction (Sec. 4.1.2, Fig. "Layer
+ * abstraction"): every layer has a ComputeFeature function, which maps the
+ * source layer's feature blob to this layer's blob, and a ComputeGradient
+ * function, which computes both the gradients of the layer's Param objects
+ * and the gradient of the source layer's blob.  Here
+ *     ComputeFeature   -> singa_*_fwd
+ *     ComputeGradient  -> singa_conv_bwd_data (source gradient)
+ *                       + singa_conv_bwd_filter (Param gradients)
+ * and the server-side Updater (Sec. 4.1.4) -> singa_sgd_momentum_update.
+ * BPTrainOneBatch (Sec. 4.1.3, Alg. 1) calls them forward over the layers,
+ * then backward in reverse order, then updates.
+ *
+ * General contract (applies to every call below)
+ *   - All tensor pointers are DEVICE pointers unless stated otherwise, owned
+ *     by the caller.  The library never allocates or frees device memory:
+ *     scratch space is passed in as a caller-owned workspace whose size
+ *     singa_conv_workspace_bytes() reports.
+ *   - Tensors are dense and contiguous in the declared layout.  Activations
+ *     are NHWC (SINGA_NHWC, filters KRSC) or NCHW (SINGA_NCHW, filters KCRS).
+ *     NHWC is the native layout of the kernels; NCHW calls are carried out by
+ *     permuting into the workspace around the same kernels.
+ *   - Element types: SINGA_F32 (IEEE binary32) or SINGA_BF16 (bfloat16 bit
+ *     patterns, uint16).  bf16 arithmetic accumulates in fp32 and rounds to
+ *     nearest even when it stores bf16.  Parameter gradients, biases, master
+ *     weights and momentum are always fp32.
+ *   - Every device pointer must be 16-byte aligned (SINGA_ERR_ALIGN).
+ *   - Calls are asynchronous on `stream` (a hipStream_t; NULL is the legacy
+ *     null stream).  The library never synchronizes.  A kernel fault shows
+ *     up at the caller's next synchronization.
+ *   - Validation happens before anything is enqueued: a non-zero return means
+ *     no work was launched and no output was touched.
+ *   - Functions are stateless and reentrant.  Concurrent calls on different
+ *     streams must not share output or workspace buffers.
+ */
+#ifndef SINGA_MI_H
+#define SINGA_MI_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ------------------------------------------------------------- status codes */
+#define SINGA_OK 0
+#define SINGA_ERR_NULL (-1)        /* a required pointer argument is NULL */
+#define SINGA_ERR_SHAPE (-2)       /* non-positive or inconsistent sizes, empty output */
+#define SINGA_ERR_UNSUPPORTED (-3) /* dtype/layout/parameter combination not provided */
+#define SINGA_ERR_WORKSPACE (-4)   /* workspace smaller than singa_conv_workspace_bytes() */
+#define SINGA_ERR_ALIGN (-5)       /* a device pointer is not 16-byte aligned */
+#define SINGA_ERR_HIP (-6)         /* the HIP runtime rejected a launch */
+
+typedef enum { SINGA_F32 = 0, SINGA_BF16 = 1 } singa_dtype;
+typedef enum { SINGA_NCHW = 0, SINGA_NHWC = 1 } singa_layout;
+typedef enum { SINGA_POOL_MAX = 0, SINGA_POOL_AVG = 1 } singa_pool_mode;
+typedef enum { SINGA_OP_FWD = 0, SINGA_OP_BWD_DATA = 1, SINGA_OP_BWD_FILTER = 2 } singa_conv_op;
+
+/* Activation extents (batch, channels, height, width), whatever the layout. */
+typedef struct { int n, c, h, w; } singa_shape4;
+/* Filter extents (filters, channels, rows, cols), whatever the layout. */
+typedef struct { int k, c, r, s; } singa_filter4;
+/* Zero padding and stride (dilation 1, one group). */
+typedef struct { int pad_h, pad_w, stride_h, stride_w; } singa_conv_desc;
+/* Pooling window; ceil_mode != 0 rounds the output extent up (Caffe's rule). */
+typedef struct { int mode, kh, kw, stride_h, stride_w, pad_h, pad_w, ceil_mode; } singa_pool_desc;
+
+typedef void* singa_stream; /* a hipStream_t */
+
+/* Message for a status code (static string). */
+const char* singa_strerror(int status);
+
+/* ------------------------------------------------------------ shape helpers */
+
+/* Convolution output extents: P = floor((H + 2*pad_h - R)/stride_h) + 1 and
+ * likewise Q; y->c = w->k.  Host-only; no GPU is touched.
+ * Errors: NULL, SHAPE (non-positive sizes, channel mismatch, P or Q < 1). */
+int singa_conv_out_shape(const singa_shape4* x, const singa_filter4* w,
+                         const singa_conv_desc* d, singa_shape4* y);
+
+/* Pooling output extents (Caffe's rule in ceil mode: a last window that would
+ * start inside the right padding is dropped).  Host-only.
+ * Errors: NULL, SHAPE, UNSUPPORTED (window larger than 255 cells, pad >= window). */
+int singa_pool_out_shape(const singa_shape4* x, const singa_pool_desc* d, singa_shape4* y);
+
+/* Workspace bytes that `op` needs for this problem (0 when none).  Host-only.
+ * Errors: NULL, SHAPE, UNSUPPORTED. */
+int singa_conv_workspace_bytes(int op, singa_dtype dtype, singa_layout layout,
+                               const singa_shape4* x, const singa_filter4* w,
+                               const singa_conv_desc* d, size_t* bytes);
+
+/* -------------------------------------------------------------- convolution */
+
+/* Convolution ComputeFeature (Sec. 4.1.2; the neuron layer of Table 2),
+ * cross-correlation as in Caffe's im2col that SINGA adopts (Sec. 6.2.1):
+ *   y[n,k,p,q] = bias[k] + sum_{c,r,s} W[k,c,r,s] * x[n,c,p*sh-ph+r, q*sw-pw+s]
+ * with zero padding, then y = max(y, 0) if fuse_relu.
+ *   x_ptr : dtype, shape *x in `layout`            (read)
+ *   w_ptr : dtype, shape *w (KRSC for NHWC, KCRS for NCHW)   (read)
+ *   bias  : fp32[w->k] or NULL                      (read)
+ *   y_ptr : dtype, shape singa_conv_out_shape()     (written)
+ *   ws    : workspace of singa_conv_workspace_bytes(SINGA_OP_FWD, ...) bytes
+ * Implicit GEMM on MFMA (M = N*P*Q output pixels, N = K filters,
+ * K = R*S*C taps). */
+int singa_conv_fwd(singa_dtype dtype, singa_layout layout,
+                   const singa_shape4* x, const void* x_ptr,
+                   const singa_filter4* w, const void* w_ptr, const float* bias,
+                   const singa_conv_desc* d, void* y_ptr, int fuse_relu,
+                   void* ws, size_t ws_bytes, singa_stream stream);
+
+/* Convolution ComputeGradient, gradient of the source layer (Sec. 4.1.2):
+ *   dx[n,c,h,w] = sum over (k,r,s,p,q) with p*sh-ph+r = h, q*sw-pw+s = w
+ *                 of W[k,c,r,s] * dy[n,k,p,q]
+ *   x      : shape of the layer's input (the shape of dx)
+ *   dy_ptr : dtype, shape singa_conv_out_shape()    (read)
+ *   dx_ptr : dtype, shape *x                        (overwritten)
+ * Stride 1 (and dense "fully connected" geometry) runs as an implicit GEMM on
+ * MFMA over a flipped, transposed copy of W in the workspace; other strides
+ * run a gather kernel. */
+int singa_conv_bwd_data(singa_dtype dtype, singa_layout layout,
+                        const singa_shape4* x, const singa_filter4* w, const void* w_ptr,
+                        const singa_conv_desc* d, const void* dy_ptr, void* dx_ptr,
+                        void* ws, size_t ws_bytes, singa_stream stream);
+
+/* Convolution ComputeGradient, Param gradients (Sec. 4.1.2):
+ *   dW[k,c,r,s] = sum_{n,p,q} dy[n,k,p,q] * x[n,c,p*sh-ph+r, q*sw-pw+s]
+ *   db[k]       = sum_{n,p,q} dy[n,k,p,q]
+ *   x_ptr  : dtype, shape *x                        (read)
+ *   dy_ptr : dtype, shape singa_conv_out_shape()    (read)
+ *   dw     : fp32, shape *w in the filter layout    (written, or added to)
+ *   db     : fp32[w->k] or NULL                     (written, or added to)
+ *   accumulate != 0 adds into dw/db instead of overwriting them, so a batch
+ *   can be processed in shards (dim-0 partitioning, Sec. 5.3).
+ * Split-K implicit GEMM on MFMA with a fixed-order reduction of the partial
+ * sums (bitwise deterministic; no floating-point atomics). */
+int singa_conv_bwd_filter(singa_dtype dtype, singa_layout layout,
+                          const singa_shape4* x, const void* x_ptr,
+                          const singa_filter4* w, const singa_conv_desc* d,
+                          const void* dy_ptr, float* dw, float* db, int accumulate,
+                          void* ws, size_t ws_bytes, singa_stream stream);
+
+/* ------------------------------------------------------------------ pooling */
+
+/* Pooling ComputeFeature (Caffe's pooling, adopted in Sec. 6.2.1).
+ * MAX: y = largest in-bounds value of the window, scanned row-major with the
+ *      first maximum winning; argmax[o] = r*kw + s of that cell (uint8).
+ * AVG: y = sum of in-bounds values / (window size after clipping it to
+ *      [-pad, H+pad) x [-pad, W+pad)); argmax is ignored and may be NULL.
+ *   x_ptr : dtype, shape *x (read);  y_ptr : dtype, singa_pool_out_shape() (written)
+ *   argmax: uint8, one per output element (written; required for MAX) */
+int singa_pool_fwd(singa_dtype dtype, singa_layout layout,
+                   const singa_shape4* x, const void* x_ptr, const singa_pool_desc* d,
+                   void* y_ptr, uint8_t* argmax, singa_stream stream);
+
+/* Pooling ComputeGradient: every input cell gathers, from each window that
+ * covers it, dy[o] if it is that window's argmax (MAX) or dy[o]/divisor(o)
+ * (AVG).  dx_ptr (shape *x) is overwritten; no atomics. */
+int singa_pool_bwd(singa_dtype dtype, singa_layout layout,
+                   const singa_shape4* x, const singa_pool_desc* d,
+                   const void* dy_ptr, const uint8_t* argmax, void* dx_ptr,
+                   singa_stream stream);
+
+/* --------------------------------------------------------------------- ReLU */
+
+/* y = x > 0 ? x : 0 over n elements (in place allowed: y == x). */
+int singa_relu_fwd(singa_dtype dtype, size_t n, const void* x, void* y, singa_stream stream);
+
+/* dx = y > 0 ? dy : 0 over n elements (in place allowed: dx == dy). */
+int singa_relu_bwd(singa_dtype dtype, size_t n, const void* y, const void* dy, void* dx,
+                   singa_stream stream);
+
+/* ------------------------------------------------------------ softmax loss */
+
+/* Softmax cross-entropy loss layer (Sec. 2.1 and Table 2 name the
+ * cross-entropy loss; Sec. 4.2.3 the softmax loss layer), mean over the batch:
+ *   loss    = (1/B) sum_n ( logsumexp(z[n,:]) - z[n, label[n]] )
+ *   dlogits = ( softmax(z[n,:]) - onehot(label[n]) ) / B
+ *   logits : dtype [batch][classes] (read);  labels : int32[batch] (read)
+ *   loss   : fp32 device scalar (written);   dlogits: dtype [batch][classes] (written)
+ * A label outside [0, classes) contributes nothing and its row of dlogits is
+ * the plain softmax / B. */
+int singa_softmax_ce(singa_dtype dtype, int batch, int classes, const void* logits,
+                     const int32_t* labels, float* loss, void* dlogits, singa_stream stream);
+
+/* ------------------------------------------------------------------ updater */
+
+/* Updater (Sec. 4.1.4): one fused SGD-with-momentum step over n fp32 values,
+ *   g' = g + weight_decay * w;  v = momentum * v + lr * g';  w = w - v
+ * and, if w_bf16 != NULL, w_bf16 = bf16(w) (round to nearest even), the
+ * compute copy for bf16 layers.  w, v updated in place; g read. */
+int singa_sgd_momentum_update(size_t n, float* w, const float* g, float* v, uint16_t* w_bf16,
+                              float lr, float momentum, float weight_decay, singa_stream stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* SINGA_MI_H */

@@ -1,0 +1,372 @@
+// abi.cpp -- the C entry points declared in include/singa_mi.h: argument
+// validation, workspace carving, NCHW <-> NHWC staging and kernel dispatch.
+// Nothing is enqueued unless every check passes.
+#include "singa_mi.h"
+
+#include <hip/hip_runtime.h>
+
+#include <climits>
+#include <cstdint>
+
+#include "internal.h"
+
+using namespace singa;
+
+namespace {
+
+constexpr size_t kAlign = 256;
+inline size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
+
+inline bool aligned_to(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+inline int hip_status(hipError_t e) { return e == hipSuccess ? SINGA_OK : SINGA_ERR_HIP; }
+
+bool dtype_ok(int dt) { return dt == SINGA_F32 || dt == SINGA_BF16; }
+bool layout_ok(int l) { return l == SINGA_NCHW || l == SINGA_NHWC; }
+
+bool fits_i32(long long v) { return v > 0 && v < (long long)INT_MAX; }
+
+// Shape checks shared by the convolution calls; fills s on success.
+int conv_geometry(const singa_shape4* x, const singa_filter4* w, const singa_conv_desc* d, ConvShape* s) {
+  if (!x || !w || !d) return SINGA_ERR_NULL;
+  if (x->n <= 0 || x->c <= 0 || x->h <= 0 || x->w <= 0) return SINGA_ERR_SHAPE;
+  if (w->k <= 0 || w->c <= 0 || w->r <= 0 || w->s <= 0) return SINGA_ERR_SHAPE;
+  if (w->c != x->c) return SINGA_ERR_SHAPE;
+  if (d->pad_h < 0 || d->pad_w < 0 || d->stride_h < 1 || d->stride_w < 1) return SINGA_ERR_SHAPE;
+  const long long hs = (long long)x->h + 2LL * d->pad_h - w->r;
+  const long long ws = (long long)x->w + 2LL * d->pad_w - w->s;
+  if (hs < 0 || ws < 0) return SINGA_ERR_SHAPE;
+  const long long P = hs / d->stride_h + 1, Q = ws / d->stride_w + 1;
+  // every index the kernels form must fit a signed 32-bit integer
+  if (!fits_i32((long long)x->n * x->h * x->w * x->c) || !fits_i32((long long)x->n * P * Q * w->k) ||
+      !fits_i32((long long)w->k * w->r * w->s * w->c) || !fits_i32((long long)x->n * P * Q) ||
+      !fits_i32((long long)x->h * x->w * x->c * 2))
+    return SINGA_ERR_UNSUPPORTED;
+  s->N = x->n; s->H = x->h; s->W = x->w; s->C = x->c;
+  s->K = w->k; s->R = w->r; s->S = w->s;
+  s->P = (int)P; s->Q = (int)Q;
+  s->ph = d->pad_h; s->pw = d->pad_w; s->sh = d->stride_h; s->sw = d->stride_w;
+  return SINGA_OK;
+}
+
+inline size_t act_bytes(const ConvShape& s, int dt) { return (size_t)s.N * s.H * s.W * s.C * dt_size(dt); }
+inline size_t out_bytes(const ConvShape& s, int dt) { return (size_t)s.N * s.P * s.Q * s.K * dt_size(dt); }
+inline size_t filt_bytes(const ConvShape& s, int dt) { return (size_t)s.K * s.R * s.S * s.C * dt_size(dt); }
+
+// Backward-data through the forward GEMM needs a transposed filter copy:
+// dense "fully connected" geometry, or unit stride (flipped filter).
+bool bwd_data_fc(const ConvShape& s) {
+  return s.P == 1 && s.Q == 1 && s.ph == 0 && s.pw == 0 && s.R == s.H && s.S == s.W;
+}
+bool bwd_data_gemm(const ConvShape& s) { return bwd_data_fc(s) || (s.sh == 1 && s.sw == 1); }
+
+// Workspace carving: a list of sub-buffers, each 256-byte aligned.
+struct Carve {
+  char* base;
+  size_t used = 0;
+  explicit Carve(void* b) : base((char*)b) {}
+  void* take(size_t bytes) {
+    void* p = base ? base + used : nullptr;
+    used += align_up(bytes);
+    return p;
+  }
+};
+
+// One function computes both the size and the layout of every workspace, so
+// the two can never disagree.
+struct FwdWs { void *x, *w, *y; };
+struct BwdDataWs { void *dy, *w, *wt, *dx; };
+struct BwdFilterWs { void *x, *dy; float *dw, *partial, *colsum; };
+
+size_t carve_fwd(const ConvShape& s, int dt, int layout, void* ws, FwdWs* o) {
+  Carve c(ws);
+  o->x = o->w = o->y = nullptr;
+  if (layout == SINGA_NCHW) {
+    o->x = c.take(act_bytes(s, dt));
+    o->w = c.take(filt_bytes(s, dt));
+    o->y = c.take(out_bytes(s, dt));
+  }
+  return c.used;
+}
+
+size_t carve_bwd_data(const ConvShape& s, int dt, int layout, void* ws, BwdDataWs* o) {
+  Carve c(ws);
+  o->dy = o->w = o->wt = o->dx = nullptr;
+  if (layout == SINGA_NCHW) {
+    o->dy = c.take(out_bytes(s, dt));
+    o->w = c.take(filt_bytes(s, dt));
+    o->dx = c.take(act_bytes(s, dt));
+  }
+  if (bwd_data_gemm(s)) o->wt = c.take(filt_bytes(s, dt));
+  return c.used;
+}
+
+size_t carve_bwd_filter(const ConvShape& s, int dt, int layout, void* ws, BwdFilterWs* o) {
+  Carve c(ws);
+  o->x = o->dy = nullptr;
+  o->dw = nullptr;
+  if (layout == SINGA_NCHW) {
+    o->x = c.take(act_bytes(s, dt));
+    o->dy = c.take(out_bytes(s, dt));
+    o->dw = (float*)c.take((size_t)s.K * s.R * s.S * s.C * sizeof(float));
+  }
+  o->partial = (float*)c.take(wgrad_partial_bytes(s));
+  o->colsum = (float*)c.take(colsum_partial_bytes(s.N * s.P * s.Q, s.K));
+  return c.used;
+}
+
+// Filter KCRS (NCHW callers) -> KRSC.
+hipError_t kcrs_to_krsc(int dt, const ConvShape& s, const void* in, void* out, hipStream_t st) {
+  const int RS = s.R * s.S;
+  return launch_transpose(dt, in, out, s.K, s.C, RS, (long)s.C * RS, RS, (long)RS * s.C, s.C, 0, st);
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* singa_strerror(int status) {
+  switch (status) {
+    case SINGA_OK: return "ok";
+    case SINGA_ERR_NULL: return "a required pointer argument is NULL";
+    case SINGA_ERR_SHAPE: return "non-positive or inconsistent sizes";
+    case SINGA_ERR_UNSUPPORTED: return "unsupported dtype, layout or parameter combination";
+    case SINGA_ERR_WORKSPACE: return "workspace too small";
+    case SINGA_ERR_ALIGN: return "device pointer not aligned";
+    case SINGA_ERR_HIP: return "HIP runtime error at launch";
+    default: return "unknown status";
+  }
+}
+
+int singa_conv_out_shape(const singa_shape4* x, const singa_filter4* w, const singa_conv_desc* d, singa_shape4* y) {
+  if (!y) return SINGA_ERR_NULL;
+  ConvShape s;
+  int rc = conv_geometry(x, w, d, &s);
+  if (rc != SINGA_OK) return rc;
+  y->n = s.N; y->c = s.K; y->h = s.P; y->w = s.Q;
+  return SINGA_OK;
+}
+
+int singa_pool_out_shape(const singa_shape4* x, const singa_pool_desc* d, singa_shape4* y) {
+  if (!x || !d || !y) return SINGA_ERR_NULL;
+  if (x->n <= 0 || x->c <= 0 || x->h <= 0 || x->w <= 0) return SINGA_ERR_SHAPE;
+  if (d->mode != SINGA_POOL_MAX && d->mode != SINGA_POOL_AVG) return SINGA_ERR_UNSUPPORTED;
+  if (d->kh <= 0 || d->kw <= 0 || d->stride_h < 1 || d->stride_w < 1 || d->pad_h < 0 || d->pad_w < 0)
+    return SINGA_ERR_SHAPE;
+  if (d->kh * d->kw > 256 || d->pad_h >= d->kh || d->pad_w >= d->kw) return SINGA_ERR_UNSUPPORTED;
+  long long out[2];
+  const long long in[2] = {x->h, x->w}, k[2] = {d->kh, d->kw}, p[2] = {d->pad_h, d->pad_w},
+                  st[2] = {d->stride_h, d->stride_w};
+  for (int a = 0; a < 2; ++a) {
+    const long long span = in[a] + 2 * p[a] - k[a];
+    if (span < 0) return SINGA_ERR_SHAPE;
+    if (d->ceil_mode) {
+      out[a] = (span + st[a] - 1) / st[a] + 1;
+      if (p[a] > 0 && (out[a] - 1) * st[a] >= in[a] + p[a]) out[a] -= 1;
+    } else {
+      out[a] = span / st[a] + 1;
+    }
+  }
+  if (!fits_i32((long long)x->n * x->c * x->h * x->w) || !fits_i32((long long)x->n * x->c * out[0] * out[1]))
+    return SINGA_ERR_UNSUPPORTED;
+  y->n = x->n; y->c = x->c; y->h = (int)out[0]; y->w = (int)out[1];
+  return SINGA_OK;
+}
+
+int singa_conv_workspace_bytes(int op, singa_dtype dtype, singa_layout layout, const singa_shape4* x,
+                               const singa_filter4* w, const singa_conv_desc* d, size_t* bytes) {
+  if (!bytes) return SINGA_ERR_NULL;
+  if (!dtype_ok(dtype) || !layout_ok(layout)) return SINGA_ERR_UNSUPPORTED;
+  ConvShape s;
+  int rc = conv_geometry(x, w, d, &s);
+  if (rc != SINGA_OK) return rc;
+  switch (op) {
+    case SINGA_OP_FWD: { FwdWs o; *bytes = carve_fwd(s, dtype, layout, nullptr, &o); break; }
+    case SINGA_OP_BWD_DATA: { BwdDataWs o; *bytes = carve_bwd_data(s, dtype, layout, nullptr, &o); break; }
+    case SINGA_OP_BWD_FILTER: { BwdFilterWs o; *bytes = carve_bwd_filter(s, dtype, layout, nullptr, &o); break; }
+    default: return SINGA_ERR_UNSUPPORTED;
+  }
+  return SINGA_OK;
+}
+
+int singa_conv_fwd(singa_dtype dtype, singa_layout layout, const singa_shape4* x, const void* x_ptr,
+                   const singa_filter4* w, const void* w_ptr, const float* bias, const singa_conv_desc* d,
+                   void* y_ptr, int fuse_relu, void* ws, size_t ws_bytes, singa_stream stream) {
+  if (!dtype_ok(dtype) || !layout_ok(layout)) return SINGA_ERR_UNSUPPORTED;
+  ConvShape s;
+  int rc = conv_geometry(x, w, d, &s);
+  if (rc != SINGA_OK) return rc;
+  if (!x_ptr || !w_ptr || !y_ptr) return SINGA_ERR_NULL;
+  const size_t es = dt_size(dtype);
+  if (!aligned_to(x_ptr, es) || !aligned_to(w_ptr, es) || !aligned_to(y_ptr, es) || !aligned_to(bias, 4) ||
+      !aligned_to(ws, 16))
+    return SINGA_ERR_ALIGN;
+  FwdWs o;
+  const size_t need = carve_fwd(s, dtype, layout, nullptr, &o);
+  if (need > 0 && (!ws || ws_bytes < need)) return SINGA_ERR_WORKSPACE;
+  carve_fwd(s, dtype, layout, ws, &o);
+  hipStream_t st = (hipStream_t)stream;
+  if (layout == SINGA_NHWC) return hip_status(launch_conv_fwd(dtype, s, x_ptr, w_ptr, bias, y_ptr, fuse_relu, st));
+  hipError_t e = launch_nchw_to_nhwc(dtype, x_ptr, o.x, s.N, s.C, s.H, s.W, st);
+  if (e == hipSuccess) e = kcrs_to_krsc(dtype, s, w_ptr, o.w, st);
+  if (e == hipSuccess) e = launch_conv_fwd(dtype, s, o.x, o.w, bias, o.y, fuse_relu, st);
+  if (e == hipSuccess) e = launch_nhwc_to_nchw(dtype, o.y, y_ptr, s.N, s.K, s.P, s.Q, st);
+  return hip_status(e);
+}
+
+int singa_conv_bwd_data(singa_dtype dtype, singa_layout layout, const singa_shape4* x, const singa_filter4* w,
+                        const void* w_ptr, const singa_conv_desc* d, const void* dy_ptr, void* dx_ptr, void* ws,
+                        size_t ws_bytes, singa_stream stream) {
+  if (!dtype_ok(dtype) || !layout_ok(layout)) return SINGA_ERR_UNSUPPORTED;
+  ConvShape s;
+  int rc = conv_geometry(x, w, d, &s);
+  if (rc != SINGA_OK) return rc;
+  if (!w_ptr || !dy_ptr || !dx_ptr) return SINGA_ERR_NULL;
+  const size_t es = dt_size(dtype);
+  if (!aligned_to(w_ptr, es) || !aligned_to(dy_ptr, es) || !aligned_to(dx_ptr, es) || !aligned_to(ws, 16))
+    return SINGA_ERR_ALIGN;
+  BwdDataWs o;
+  const size_t need = carve_bwd_data(s, dtype, layout, nullptr, &o);
+  if (need > 0 && (!ws || ws_bytes < need)) return SINGA_ERR_WORKSPACE;
+  carve_bwd_data(s, dtype, layout, ws, &o);
+  hipStream_t st = (hipStream_t)stream;
+  hipError_t e = hipSuccess;
+  const void* dy = dy_ptr;
+  const void* wk = w_ptr;  // KRSC filter
+  void* dx = dx_ptr;
+  if (layout == SINGA_NCHW) {
+    e = launch_nchw_to_nhwc(dtype, dy_ptr, o.dy, s.N, s.K, s.P, s.Q, st);
+    if (e == hipSuccess) e = kcrs_to_krsc(dtype, s, w_ptr, o.w, st);
+    dy = o.dy;
+    wk = o.w;
+    dx = o.dx;
+  }
+  const int RS = s.R * s.S;
+  if (e == hipSuccess) {
+    if (bwd_data_fc(s)) {
+      // dx[n][(r,s,c)] = sum_k dy[n][k] w[k][(r,s,c)]: a 1x1 "convolution" of dy
+      // with the transposed filter wt[(r,s,c)][k].
+      const int J = RS * s.C;
+      e = launch_transpose(dtype, wk, o.wt, 1, s.K, J, 0, J, 0, s.K, 0, st);
+      ConvShape g{s.N, 1, 1, s.K, J, 1, 1, 1, 1, 0, 0, 1, 1};
+      if (e == hipSuccess) e = launch_conv_fwd(dtype, g, dy, o.wt, nullptr, dx, 0, st);
+    } else if (s.sh == 1 && s.sw == 1) {
+      // unit stride: dx = conv(dy, flip(w)^T) with padding R-1-ph, S-1-pw, where
+      // wt[c][r'][s'][k] = w[k][R-1-r'][S-1-s'][c]
+      e = launch_transpose(dtype, wk, o.wt, RS, s.K, s.C, s.C, (long)RS * s.C, s.K, (long)RS * s.K, 1, st);
+      ConvShape g{s.N, s.P, s.Q, s.K, s.C, s.R, s.S, s.H, s.W, s.R - 1 - s.ph, s.S - 1 - s.pw, 1, 1};
+      if (e == hipSuccess) e = launch_conv_fwd(dtype, g, dy, o.wt, nullptr, dx, 0, st);
+    } else {
+      e = launch_conv_bwd_data_direct(dtype, s, dy, wk, dx, st);
+    }
+  }
+  if (e == hipSuccess && layout == SINGA_NCHW) e = launch_nhwc_to_nchw(dtype, dx, dx_ptr, s.N, s.C, s.H, s.W, st);
+  return hip_status(e);
+}
+
+int singa_conv_bwd_filter(singa_dtype dtype, singa_layout layout, const singa_shape4* x, const void* x_ptr,
+                          const singa_filter4* w, const singa_conv_desc* d, const void* dy_ptr, float* dw,
+                          float* db, int accumulate, void* ws, size_t ws_bytes, singa_stream stream) {
+  if (!dtype_ok(dtype) || !layout_ok(layout)) return SINGA_ERR_UNSUPPORTED;
+  ConvShape s;
+  int rc = conv_geometry(x, w, d, &s);
+  if (rc != SINGA_OK) return rc;
+  if (!x_ptr || !dy_ptr || !dw) return SINGA_ERR_NULL;
+  const size_t es = dt_size(dtype);
+  if (!aligned_to(x_ptr, es) || !aligned_to(dy_ptr, es) || !aligned_to(dw, 4) || !aligned_to(db, 4) ||
+      !aligned_to(ws, 16))
+    return SINGA_ERR_ALIGN;
+  BwdFilterWs o;
+  const size_t need = carve_bwd_filter(s, dtype, layout, nullptr, &o);
+  if (!ws || ws_bytes < need) return SINGA_ERR_WORKSPACE;
+  carve_bwd_filter(s, dtype, layout, ws, &o);
+  hipStream_t st = (hipStream_t)stream;
+  hipError_t e = hipSuccess;
+  const void* xx = x_ptr;
+  const void* dy = dy_ptr;
+  if (layout == SINGA_NCHW) {
+    e = launch_nchw_to_nhwc(dtype, x_ptr, o.x, s.N, s.C, s.H, s.W, st);
+    if (e == hipSuccess) e = launch_nchw_to_nhwc(dtype, dy_ptr, o.dy, s.N, s.K, s.P, s.Q, st);
+    xx = o.x;
+    dy = o.dy;
+  }
+  const size_t nw = (size_t)s.K * s.R * s.S * s.C;
+  if (e == hipSuccess) e = launch_conv_wgrad(dtype, s, xx, dy, o.partial, st);
+  if (e == hipSuccess) {
+    if (layout == SINGA_NHWC) {
+      e = launch_splitk_reduce(o.partial, wgrad_splits(s), nw, dw, accumulate, st);
+    } else {
+      e = launch_splitk_reduce(o.partial, wgrad_splits(s), nw, o.dw, 0, st);
+      if (e == hipSuccess) e = launch_krsc_to_kcrs_f32(o.dw, dw, s.K, s.C, s.R, s.S, accumulate, st);
+    }
+  }
+  if (e == hipSuccess && db) e = launch_colsum(dtype, dy, s.N * s.P * s.Q, s.K, o.colsum, db, accumulate, st);
+  return hip_status(e);
+}
+
+int singa_pool_fwd(singa_dtype dtype, singa_layout layout, const singa_shape4* x, const void* x_ptr,
+                   const singa_pool_desc* d, void* y_ptr, uint8_t* argmax, singa_stream stream) {
+  if (!dtype_ok(dtype) || !layout_ok(layout)) return SINGA_ERR_UNSUPPORTED;
+  singa_shape4 y;
+  int rc = singa_pool_out_shape(x, d, &y);
+  if (rc != SINGA_OK) return rc;
+  if (!x_ptr || !y_ptr || (d->mode == SINGA_POOL_MAX && !argmax)) return SINGA_ERR_NULL;
+  const size_t es = dt_size(dtype);
+  if (!aligned_to(x_ptr, es) || !aligned_to(y_ptr, es)) return SINGA_ERR_ALIGN;
+  uint8_t* am = d->mode == SINGA_POOL_MAX ? argmax : nullptr;
+  return hip_status(launch_pool_fwd(dtype, d->mode, x->n, x->c, x->h, x->w, y.h, y.w, d->kh, d->kw, d->stride_h,
+                                    d->stride_w, d->pad_h, d->pad_w, x_ptr, y_ptr, am, layout == SINGA_NCHW,
+                                    (hipStream_t)stream));
+}
+
+int singa_pool_bwd(singa_dtype dtype, singa_layout layout, const singa_shape4* x, const singa_pool_desc* d,
+                   const void* dy_ptr, const uint8_t* argmax, void* dx_ptr, singa_stream stream) {
+  if (!dtype_ok(dtype) || !layout_ok(layout)) return SINGA_ERR_UNSUPPORTED;
+  singa_shape4 y;
+  int rc = singa_pool_out_shape(x, d, &y);
+  if (rc != SINGA_OK) return rc;
+  if (!dy_ptr || !dx_ptr || (d->mode == SINGA_POOL_MAX && !argmax)) return SINGA_ERR_NULL;
+  const size_t es = dt_size(dtype);
+  if (!aligned_to(dy_ptr, es) || !aligned_to(dx_ptr, es)) return SINGA_ERR_ALIGN;
+  return hip_status(launch_pool_bwd(dtype, d->mode, x->n, x->c, x->h, x->w, y.h, y.w, d->kh, d->kw, d->stride_h,
+                                    d->stride_w, d->pad_h, d->pad_w, dy_ptr, argmax, dx_ptr, layout == SINGA_NCHW,
+                                    (hipStream_t)stream));
+}
+
+int singa_relu_fwd(singa_dtype dtype, size_t n, const void* x, void* y, singa_stream stream) {
+  if (!dtype_ok(dtype)) return SINGA_ERR_UNSUPPORTED;
+  if (n == 0) return SINGA_OK;
+  if (!x || !y) return SINGA_ERR_NULL;
+  if (!aligned_to(x, 16) || !aligned_to(y, 16)) return SINGA_ERR_ALIGN;
+  return hip_status(launch_relu_fwd(dtype, n, x, y, (hipStream_t)stream));
+}
+
+int singa_relu_bwd(singa_dtype dtype, size_t n, const void* y, const void* dy, void* dx, singa_stream stream) {
+  if (!dtype_ok(dtype)) return SINGA_ERR_UNSUPPORTED;
+  if (n == 0) return SINGA_OK;
+  if (!y || !dy || !dx) return SINGA_ERR_NULL;
+  if (!aligned_to(y, 16) || !aligned_to(dy, 16) || !aligned_to(dx, 16)) return SINGA_ERR_ALIGN;
+  return hip_status(launch_relu_bwd(dtype, n, y, dy, dx, (hipStream_t)stream));
+}
+
+int singa_softmax_ce(singa_dtype dtype, int batch, int classes, const void* logits, const int32_t* labels,
+                     float* loss, void* dlogits, singa_stream stream) {
+  if (!dtype_ok(dtype)) return SINGA_ERR_UNSUPPORTED;
+  if (batch <= 0 || classes <= 0 || !fits_i32((long long)batch * classes)) return SINGA_ERR_SHAPE;
+  if (!logits || !labels || !loss || !dlogits) return SINGA_ERR_NULL;
+  const size_t es = dt_size(dtype);
+  if (!aligned_to(logits, es) || !aligned_to(dlogits, es) || !aligned_to(labels, 4) || !aligned_to(loss, 4))
+    return SINGA_ERR_ALIGN;
+  return hip_status(launch_softmax_ce(dtype, batch, classes, logits, labels, loss, dlogits, (hipStream_t)stream));
+}
+
+int singa_sgd_momentum_update(size_t n, float* w, const float* g, float* v, uint16_t* w_bf16, float lr,
+                              float momentum, float weight_decay, singa_stream stream) {
+  if (n == 0) return SINGA_OK;
+  if (!w || !g || !v) return SINGA_ERR_NULL;
+  if (!aligned_to(w, 16) || !aligned_to(g, 16) || !aligned_to(v, 16) || !aligned_to(w_bf16, 16))
+    return SINGA_ERR_ALIGN;
+  return hip_status(launch_sgd(n, w, g, v, w_bf16, lr, momentum, weight_decay, (hipStream_t)stream));
+}
+
+}  // extern "C"

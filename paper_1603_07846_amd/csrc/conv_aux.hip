@@ -1,0 +1,242 @@
+// conv_aux.hip -- the bandwidth-bound helpers around the convolution GEMMs:
+//   * batched tiled transpose (flipped filter copies for backward-data, and the
+//     filter transpose of a dense "fully connected" layer),
+//   * direct gather backward-data for strides above one,
+//   * bias-gradient column sums in a fixed order,
+//   * NCHW <-> NHWC permutations for the NCHW entry points.
+#include "common.h"
+#include "internal.h"
+
+namespace singa {
+
+namespace {
+
+template <typename T> __device__ __forceinline__ float ld_f(const T* p);
+template <> __device__ __forceinline__ float ld_f<float>(const float* p) { return *p; }
+template <> __device__ __forceinline__ float ld_f<bf16_t>(const bf16_t* p) { return bf16_to_f32(*p); }
+
+template <typename T> __device__ __forceinline__ void st_f(T* p, float v);
+template <> __device__ __forceinline__ void st_f<float>(float* p, float v) { *p = v; }
+template <> __device__ __forceinline__ void st_f<bf16_t>(bf16_t* p, float v) { *p = f32_to_bf16(v); }
+
+// 32 x 32 tile through LDS: reads are coalesced along cols, writes along rows.
+template <typename T>
+__global__ __launch_bounds__(256) void transpose_kernel(const T* __restrict__ in, T* __restrict__ out, int batch,
+                                                        int rows, int cols, long in_bstride, long in_rstride,
+                                                        long out_bstride, long out_rstride, int flip) {
+  __shared__ T tile[32][33];
+  const int b = blockIdx.z;
+  const int r0 = blockIdx.y * 32, c0 = blockIdx.x * 32;
+  const T* src = in + (long)b * in_bstride;
+  T* dst = out + (long)(flip ? batch - 1 - b : b) * out_bstride;
+  const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;  // 32 x 8
+#pragma unroll
+  for (int k = 0; k < 32; k += 8) {
+    int r = r0 + ty + k, c = c0 + tx;
+    if (r < rows && c < cols) tile[ty + k][tx] = src[(long)r * in_rstride + c];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < 32; k += 8) {
+    int c = c0 + ty + k, r = r0 + tx;
+    if (r < rows && c < cols) dst[(long)c * out_rstride + r] = tile[tx][ty + k];
+  }
+}
+
+// dx[n,h,w,c] = sum over taps (r,s) whose output pixel (p,q) lands on a whole
+// multiple of the stride, and over k, of w[k,r,s,c] * dy[n,p,q,k].
+template <typename T>
+__global__ __launch_bounds__(256) void bwd_data_direct_kernel(ConvShape s, const T* __restrict__ dy,
+                                                              const T* __restrict__ w, T* __restrict__ dx,
+                                                              long total) {
+  for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += (long)gridDim.x * blockDim.x) {
+    const int c = (int)(i % s.C);
+    long t = i / s.C;
+    const int x = (int)(t % s.W);
+    t /= s.W;
+    const int h = (int)(t % s.H);
+    const int n = (int)(t / s.H);
+    float acc = 0.f;
+    for (int r = 0; r < s.R; ++r) {
+      const int pn = h + s.ph - r;
+      if (pn < 0 || pn % s.sh) continue;
+      const int p = pn / s.sh;
+      if (p >= s.P) continue;
+      for (int q_s = 0; q_s < s.S; ++q_s) {
+        const int qn = x + s.pw - q_s;
+        if (qn < 0 || qn % s.sw) continue;
+        const int q = qn / s.sw;
+        if (q >= s.Q) continue;
+        const T* dyr = dy + (((long)n * s.P + p) * s.Q + q) * s.K;
+        const T* wr = w + ((long)r * s.S + q_s) * s.C + c;
+        const long wk = (long)s.R * s.S * s.C;
+        for (int k = 0; k < s.K; ++k) acc += ld_f<T>(wr + k * wk) * ld_f<T>(dyr + k);
+      }
+    }
+    st_f<T>(dx + i, acc);
+  }
+}
+
+// Pass 1: partial[chunk][col] = sum of rows [chunk*RC, (chunk+1)*RC) in row order.
+constexpr int COLSUM_RC = 256;
+template <typename T>
+__global__ __launch_bounds__(256) void colsum_partial_kernel(const T* __restrict__ a, int rows, int cols,
+                                                             float* __restrict__ partial) {
+  const int chunk = blockIdx.x;
+  const int r0 = chunk * COLSUM_RC, r1 = min(rows, r0 + COLSUM_RC);
+  for (int c = threadIdx.x; c < cols; c += blockDim.x) {
+    float s = 0.f;
+    for (int r = r0; r < r1; ++r) s += ld_f<T>(a + (long)r * cols + c);
+    partial[(long)chunk * cols + c] = s;
+  }
+}
+
+// Pass 2: out[col] = (accumulate ? out : 0) + sum of the chunks in chunk order.
+__global__ __launch_bounds__(256) void colsum_final_kernel(const float* __restrict__ partial, int chunks, int cols,
+                                                           float* __restrict__ out, int accumulate) {
+  const int c = blockIdx.x * blockDim.x + threadIdx.x;
+  if (c >= cols) return;
+  float s = 0.f;
+  for (int k = 0; k < chunks; ++k) s += partial[(long)k * cols + c];
+  out[c] = (accumulate ? out[c] : 0.f) + s;
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void nchw_to_nhwc_kernel(const T* __restrict__ in, T* __restrict__ out, int C,
+                                                           int HW) {
+  // one (n) image per blockIdx.z; transpose [C][HW] -> [HW][C] with 32x32 tiles
+  __shared__ T tile[32][33];
+  const long base = (long)blockIdx.z * C * HW;
+  const int c0 = blockIdx.y * 32, s0 = blockIdx.x * 32;
+  const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
+#pragma unroll
+  for (int k = 0; k < 32; k += 8) {
+    int c = c0 + ty + k, sp = s0 + tx;
+    if (c < C && sp < HW) tile[ty + k][tx] = in[base + (long)c * HW + sp];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < 32; k += 8) {
+    int sp = s0 + ty + k, c = c0 + tx;
+    if (c < C && sp < HW) out[base + (long)sp * C + c] = tile[tx][ty + k];
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void nhwc_to_nchw_kernel(const T* __restrict__ in, T* __restrict__ out, int C,
+                                                           int HW) {
+  __shared__ T tile[32][33];
+  const long base = (long)blockIdx.z * C * HW;
+  const int s0 = blockIdx.y * 32, c0 = blockIdx.x * 32;
+  const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
+#pragma unroll
+  for (int k = 0; k < 32; k += 8) {
+    int sp = s0 + ty + k, c = c0 + tx;
+    if (c < C && sp < HW) tile[ty + k][tx] = in[base + (long)sp * C + c];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < 32; k += 8) {
+    int c = c0 + ty + k, sp = s0 + tx;
+    if (c < C && sp < HW) out[base + (long)c * HW + sp] = tile[tx][ty + k];
+  }
+}
+
+__global__ __launch_bounds__(256) void krsc_to_kcrs_kernel(const float* __restrict__ in, float* __restrict__ out,
+                                                           int K, int C, int RS, int accumulate) {
+  const long total = (long)K * C * RS;
+  for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += (long)gridDim.x * blockDim.x) {
+    // i indexes the KCRS output
+    const int rs = (int)(i % RS);
+    const long kc = i / RS;
+    const int c = (int)(kc % C);
+    const int k = (int)(kc / C);
+    const float v = in[((long)k * RS + rs) * C + c];
+    out[i] = accumulate ? out[i] + v : v;
+  }
+}
+
+unsigned grid_for(long total, int block = 256, long cap = 65536) {
+  long g = (total + block - 1) / block;
+  if (g < 1) g = 1;
+  if (g > cap) g = cap;
+  return (unsigned)g;
+}
+
+}  // namespace
+
+hipError_t launch_transpose(int dt, const void* in, void* out, int batch, int rows, int cols, long in_bstride,
+                            long in_rstride, long out_bstride, long out_rstride, int flip, hipStream_t st) {
+  dim3 grid((cols + 31) / 32, (rows + 31) / 32, batch), block(256);
+  if (dt == BF16)
+    hipLaunchKernelGGL(transpose_kernel<bf16_t>, grid, block, 0, st, (const bf16_t*)in, (bf16_t*)out, batch, rows,
+                       cols, in_bstride, in_rstride, out_bstride, out_rstride, flip);
+  else
+    hipLaunchKernelGGL(transpose_kernel<float>, grid, block, 0, st, (const float*)in, (float*)out, batch, rows,
+                       cols, in_bstride, in_rstride, out_bstride, out_rstride, flip);
+  return hipGetLastError();
+}
+
+hipError_t launch_conv_bwd_data_direct(int dt, const ConvShape& s, const void* dy, const void* w, void* dx,
+                                       hipStream_t st) {
+  const long total = (long)s.N * s.H * s.W * s.C;
+  const unsigned g = grid_for(total);
+  if (dt == BF16)
+    hipLaunchKernelGGL(bwd_data_direct_kernel<bf16_t>, dim3(g), dim3(256), 0, st, s, (const bf16_t*)dy,
+                       (const bf16_t*)w, (bf16_t*)dx, total);
+  else
+    hipLaunchKernelGGL(bwd_data_direct_kernel<float>, dim3(g), dim3(256), 0, st, s, (const float*)dy,
+                       (const float*)w, (float*)dx, total);
+  return hipGetLastError();
+}
+
+size_t colsum_partial_bytes(int rows, int cols) {
+  const size_t chunks = ((size_t)rows + COLSUM_RC - 1) / COLSUM_RC;
+  return chunks * (size_t)cols * sizeof(float);
+}
+
+hipError_t launch_colsum(int dt, const void* a, int rows, int cols, float* partial, float* out, int accumulate,
+                         hipStream_t st) {
+  const int chunks = (rows + COLSUM_RC - 1) / COLSUM_RC;
+  if (dt == BF16)
+    hipLaunchKernelGGL(colsum_partial_kernel<bf16_t>, dim3(chunks), dim3(256), 0, st, (const bf16_t*)a, rows, cols,
+                       partial);
+  else
+    hipLaunchKernelGGL(colsum_partial_kernel<float>, dim3(chunks), dim3(256), 0, st, (const float*)a, rows, cols,
+                       partial);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(colsum_final_kernel, dim3((cols + 255) / 256), dim3(256), 0, st, partial, chunks, cols, out,
+                     accumulate);
+  return hipGetLastError();
+}
+
+hipError_t launch_nchw_to_nhwc(int dt, const void* in, void* out, int N, int C, int H, int W, hipStream_t st) {
+  const int HW = H * W;
+  dim3 grid((HW + 31) / 32, (C + 31) / 32, N), block(256);
+  if (dt == BF16)
+    hipLaunchKernelGGL(nchw_to_nhwc_kernel<bf16_t>, grid, block, 0, st, (const bf16_t*)in, (bf16_t*)out, C, HW);
+  else
+    hipLaunchKernelGGL(nchw_to_nhwc_kernel<float>, grid, block, 0, st, (const float*)in, (float*)out, C, HW);
+  return hipGetLastError();
+}
+
+hipError_t launch_nhwc_to_nchw(int dt, const void* in, void* out, int N, int C, int H, int W, hipStream_t st) {
+  const int HW = H * W;
+  dim3 grid((C + 31) / 32, (HW + 31) / 32, N), block(256);
+  if (dt == BF16)
+    hipLaunchKernelGGL(nhwc_to_nchw_kernel<bf16_t>, grid, block, 0, st, (const bf16_t*)in, (bf16_t*)out, C, HW);
+  else
+    hipLaunchKernelGGL(nhwc_to_nchw_kernel<float>, grid, block, 0, st, (const float*)in, (float*)out, C, HW);
+  return hipGetLastError();
+}
+
+hipError_t launch_krsc_to_kcrs_f32(const float* in, float* out, int K, int C, int R, int S, int accumulate,
+                                   hipStream_t st) {
+  const long total = (long)K * C * R * S;
+  hipLaunchKernelGGL(krsc_to_kcrs_kernel, dim3(grid_for(total)), dim3(256), 0, st, in, out, K, C, R * S,
+                     accumulate);
+  return hipGetLastError();
+}
+
+}  // namespace singa

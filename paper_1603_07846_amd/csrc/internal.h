@@ -1,0 +1,76 @@
+// internal.h -- launchers shared between the ABI layer and the kernel files.
+// Everything here works on NHWC activations and KRSC filters; the ABI layer
+// validates arguments before calling in, so launchers assume consistent
+// shapes, 16-byte aligned pointers and 32-bit-indexable tensors.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace singa {
+
+enum Dt { F32 = 0, BF16 = 1 };
+
+inline size_t dt_size(int dt) { return dt == BF16 ? 2 : 4; }
+
+// Geometry of one convolution: input N x H x W x C, K filters R x S x C,
+// output N x P x Q x K.
+struct ConvShape {
+  int N, H, W, C, K, R, S, P, Q, ph, pw, sh, sw;
+};
+
+// Implicit-GEMM forward convolution (also used for stride-1 backward-data over
+// a flipped filter copy): y = act(conv(x, w) + bias).
+hipError_t launch_conv_fwd(int dt, const ConvShape& s, const void* x, const void* w, const float* bias,
+                           void* y, int relu, hipStream_t st);
+
+// Split-K implicit-GEMM filter gradient.  Number of K-splits used for a shape
+// and the fp32 partial-sum buffer it needs.
+int wgrad_splits(const ConvShape& s);
+size_t wgrad_partial_bytes(const ConvShape& s);
+hipError_t launch_conv_wgrad(int dt, const ConvShape& s, const void* x, const void* dy, float* partial,
+                             hipStream_t st);
+// dw = (accumulate ? dw : 0) + sum over splits of partial, in split order.
+hipError_t launch_splitk_reduce(const float* partial, int splits, size_t n, float* dw, int accumulate,
+                                hipStream_t st);
+
+// Column sums of a [rows][cols] matrix (bias gradient): two passes through a
+// fixed-order partial buffer of colsum_partial_bytes().
+size_t colsum_partial_bytes(int rows, int cols);
+hipError_t launch_colsum(int dt, const void* a, int rows, int cols, float* partial, float* out,
+                         int accumulate, hipStream_t st);
+
+// Batched 2-D transpose: for b in [0, batch): out(b)[c][r] = in(b)[r][c] with
+// in(b) = in + in_base(b), out(b) = out + out_base(b), where
+// in_base(b) = b * in_bstride and out_base(b) = (flip ? batch-1-b : b) * out_bstride.
+hipError_t launch_transpose(int dt, const void* in, void* out, int batch, int rows, int cols,
+                            long in_bstride, long in_rstride, long out_bstride, long out_rstride,
+                            int flip, hipStream_t st);
+
+// Direct (gather) backward-data for any stride: dx = conv^T(dy, w).
+hipError_t launch_conv_bwd_data_direct(int dt, const ConvShape& s, const void* dy, const void* w, void* dx,
+                                       hipStream_t st);
+
+// NCHW <-> NHWC permutations for the NCHW entry points.
+hipError_t launch_nchw_to_nhwc(int dt, const void* in, void* out, int N, int C, int H, int W, hipStream_t st);
+hipError_t launch_nhwc_to_nchw(int dt, const void* in, void* out, int N, int C, int H, int W, hipStream_t st);
+// fp32 filter gradient KRSC -> KCRS, with optional accumulation into out.
+hipError_t launch_krsc_to_kcrs_f32(const float* in, float* out, int K, int C, int R, int S, int accumulate,
+                                   hipStream_t st);
+
+// Pooling, ReLU, softmax-CE, SGD.
+hipError_t launch_pool_fwd(int dt, int mode, int N, int C, int H, int W, int P, int Q, int kh, int kw, int sh,
+                           int sw, int ph, int pw, const void* x, void* y, uint8_t* argmax, int nchw,
+                           hipStream_t st);
+hipError_t launch_pool_bwd(int dt, int mode, int N, int C, int H, int W, int P, int Q, int kh, int kw, int sh,
+                           int sw, int ph, int pw, const void* dy, const uint8_t* argmax, void* dx, int nchw,
+                           hipStream_t st);
+hipError_t launch_relu_fwd(int dt, size_t n, const void* x, void* y, hipStream_t st);
+hipError_t launch_relu_bwd(int dt, size_t n, const void* y, const void* dy, void* dx, hipStream_t st);
+hipError_t launch_softmax_ce(int dt, int B, int classes, const void* z, const int32_t* labels, float* loss,
+                             void* dz, hipStream_t st);
+hipError_t launch_sgd(size_t n, float* w, const float* g, float* v, uint16_t* wb, float lr, float mom, float wd,
+                      hipStream_t st);
+
+}  // namespace singa

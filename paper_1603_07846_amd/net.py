@@ -1,0 +1,279 @@
+"""BPTrainOneBatch (Sec. 4.1.3, Alg. 1) over the C-ABI library, one GPU.
+
+Layers mirror the paper's Layer abstraction (Sec. 4.1.2): ``compute_feature``
+maps the source layer's blob to this layer's blob, ``compute_gradient``
+produces the Param gradients and the source layer's gradient.  The whole
+step runs in the library's HIP kernels on torch's current stream; this module
+only wires buffers together.
+
+Data layout in HBM (chosen for the gfx950 kernels, not the paper's CPUs):
+  * activations and their gradients are NHWC, in the workload's dtype
+    (fp32, or bf16 with fp32 accumulation inside the kernels);
+  * filters are KRSC; a fully connected layer is a convolution whose filter
+    covers the whole input (R = H, S = W, no padding), so its weight matrix
+    is KRSC too, i.e. its input is flattened in (h, w, c) order;
+  * all parameters live in one flat fp32 master buffer (weights then bias per
+    layer, each padded to 64 elements), with a flat fp32 gradient buffer, a
+    flat fp32 momentum buffer and, for bf16 workloads, a flat bf16 shadow
+    that the fused Updater writes; per-layer tensors are views into these.
+Every buffer is allocated once, when the net is built; a step allocates
+nothing.
+
+Alg. 1 calls Update(layer.params()) inside the backward loop.  The fresh
+values only reach the layers at the next iteration's Collect, so on one GPU a
+single fused update over the flat buffer after the backward loop is the same
+computation.
+"""
+from __future__ import annotations
+
+from typing import Dict, List, Optional
+
+import numpy as np
+import torch
+
+from . import singa
+from . import workloads as wl
+
+PAD = 64  # elements; keeps every parameter view 256-byte aligned
+
+
+def _pad(n: int) -> int:
+    return (n + PAD - 1) // PAD * PAD
+
+
+class Layer:
+    name = ""
+    params: List = []
+
+    def compute_feature(self, x):
+        raise NotImplementedError
+
+    def compute_gradient(self, dy, need_dx=True):
+        raise NotImplementedError
+
+
+class ConvLayer(Layer):
+    """Convolution (or fully connected, as a whole-input convolution)."""
+
+    def __init__(self, net, spec, in_shape, fc=False):
+        self.name = spec.name
+        self.net = net
+        N, H, W, C = in_shape
+        if fc:
+            self.K, self.R, self.S, self.pad, self.stride = spec.out_features, H, W, 0, 1
+        else:
+            self.K, self.R, self.S, self.pad, self.stride = (spec.out_channels, spec.kernel, spec.kernel, spec.pad,
+                                                             spec.stride)
+        self.fc = fc
+        self.has_bias = spec.bias
+        self.in_shape = (N, H, W, C)
+        self.w_shape = (self.K, self.R, self.S, C)
+        self.out_shape = singa.conv_out_shape(self.in_shape, self.w_shape, self.pad, self.stride)
+        self.relu = False  # set when a ReLU layer directly follows and is fused
+        dev, dt = net.device, net.dtype
+        self.y = torch.empty(self.out_shape, dtype=dt, device=dev)
+        self.dx = torch.empty(self.in_shape, dtype=dt, device=dev)
+        self.x = None
+        for op in (singa.OP_FWD, singa.OP_BWD_DATA, singa.OP_BWD_FILTER):
+            net.need_workspace(singa.conv_workspace_bytes(op, dt, self.in_shape, self.w_shape, self.pad,
+                                                          self.stride))
+
+    def bind(self, w, b, w_compute, dw, db):
+        self.w, self.b, self.w_compute, self.dw, self.db = w, b, w_compute, dw, db
+
+    def compute_feature(self, x):
+        self.x = x
+        singa.conv_fwd(x, self.w_compute, self.b, self.pad, self.stride, relu=self.relu, out=self.y,
+                       workspace=self.net.workspace)
+        return self.y
+
+    def compute_gradient(self, dy, need_dx=True):
+        singa.conv_bwd_filter(self.x, dy, self.w_shape, self.pad, self.stride, with_bias=self.has_bias, dw=self.dw,
+                              db=self.db, workspace=self.net.workspace)
+        if not need_dx:
+            return None
+        singa.conv_bwd_data(dy, self.w_compute, self.in_shape, self.pad, self.stride, out=self.dx,
+                            workspace=self.net.workspace)
+        return self.dx
+
+
+class PoolLayer(Layer):
+    def __init__(self, net, spec, in_shape):
+        self.name = spec.name
+        self.mode = spec.mode
+        self.k, self.stride, self.pad, self.ceil = spec.kernel, spec.stride, spec.pad, spec.ceil_mode
+        self.in_shape = tuple(in_shape)
+        self.out_shape = singa.pool_out_shape(self.in_shape, self.mode, self.k, self.stride, self.pad, self.ceil)
+        dev, dt = net.device, net.dtype
+        self.y = torch.empty(self.out_shape, dtype=dt, device=dev)
+        self.argmax = torch.empty(self.out_shape, dtype=torch.uint8, device=dev) if self.mode == "max" else None
+        self.dx = torch.empty(self.in_shape, dtype=dt, device=dev)
+
+    def compute_feature(self, x):
+        singa.pool_fwd(x, self.mode, self.k, self.stride, self.pad, self.ceil, out=self.y, argmax=self.argmax)
+        return self.y
+
+    def compute_gradient(self, dy, need_dx=True):
+        singa.pool_bwd(dy, self.argmax, self.in_shape, self.mode, self.k, self.stride, self.pad, self.ceil,
+                       out=self.dx)
+        return self.dx
+
+
+class ReluLayer(Layer):
+    def __init__(self, net, spec, in_shape, fused_into: Optional[ConvLayer]):
+        self.name = spec.name
+        self.fused = fused_into
+        self.out_shape = tuple(in_shape)
+        self.y = None
+        if fused_into is None:
+            self.y = torch.empty(self.out_shape, dtype=net.dtype, device=net.device)
+
+    def compute_feature(self, x):
+        if self.fused is not None:
+            self.y = x  # the producing convolution already applied max(., 0)
+            return x
+        singa.relu_fwd(x, out=self.y)
+        return self.y
+
+    def compute_gradient(self, dy, need_dx=True):
+        # in place on the incoming gradient buffer
+        return singa.relu_bwd(self.y, dy, out=dy)
+
+
+class SoftmaxCELayer(Layer):
+    def __init__(self, net, spec, in_shape):
+        self.name = spec.name
+        self.in_shape = tuple(in_shape)
+        self.loss = torch.empty((1,), dtype=torch.float32, device=net.device)
+        self.dz = torch.empty(self.in_shape, dtype=net.dtype, device=net.device)
+        self.labels = None
+        self.out_shape = (1,)
+
+    def compute_feature(self, z):
+        B = z.shape[0]
+        singa.softmax_ce(z.reshape(B, -1), self.labels, loss=self.loss, dz=self.dz.reshape(B, -1))
+        return self.loss
+
+    def compute_gradient(self, dy=None, need_dx=True):
+        return self.dz
+
+
+class Net:
+    """A workload's layer stack on one GPU, with flat parameter buffers."""
+
+    def __init__(self, workload: wl.Workload, batch: Optional[int] = None, device="cuda"):
+        self.wl = workload
+        self.batch = workload.batch if batch is None else batch
+        self.device = torch.device(device)
+        self.dtype = torch.bfloat16 if workload.dtype == "bf16" else torch.float32
+        self.ws_bytes = 0
+        self.layers: List[Layer] = []
+        C, H, W = workload.in_shape
+        shape = (self.batch, H, W, C)
+        prev = None
+        for spec in workload.layers:
+            if isinstance(spec, wl.Conv):
+                layer = ConvLayer(self, spec, shape)
+            elif isinstance(spec, wl.FC):
+                layer = ConvLayer(self, spec, shape, fc=True)
+            elif isinstance(spec, wl.Pool):
+                layer = PoolLayer(self, spec, shape)
+            elif isinstance(spec, wl.Relu):
+                fuse = prev if isinstance(prev, ConvLayer) else None
+                if fuse is not None:
+                    fuse.relu = True
+                layer = ReluLayer(self, spec, shape, fuse)
+            elif isinstance(spec, wl.SoftmaxCE):
+                layer = SoftmaxCELayer(self, spec, shape)
+            else:
+                raise TypeError(spec)
+            self.layers.append(layer)
+            shape = layer.out_shape
+            prev = layer
+        self.out_shape = shape
+        self.workspace = torch.empty(max(self.ws_bytes, 256), dtype=torch.uint8, device=self.device)
+        self._build_params()
+
+    def need_workspace(self, nbytes: int):
+        self.ws_bytes = max(self.ws_bytes, int(nbytes))
+
+    def param_layers(self) -> List[ConvLayer]:
+        return [l for l in self.layers if isinstance(l, ConvLayer)]
+
+    def _build_params(self):
+        offs = []
+        total = 0
+        for l in self.param_layers():
+            nw = int(np.prod(l.w_shape))
+            nb = l.K if l.has_bias else 0
+            offs.append((total, nw, total + _pad(nw), nb))
+            total += _pad(nw) + _pad(nb)
+        self.n_params_padded = total
+        self.n_params = sum(o[1] + o[3] for o in offs)
+        dev = self.device
+        self.w_flat = torch.zeros(total, dtype=torch.float32, device=dev)
+        self.g_flat = torch.zeros(total, dtype=torch.float32, device=dev)
+        self.v_flat = torch.zeros(total, dtype=torch.float32, device=dev)
+        self.wb_flat = torch.zeros(total, dtype=torch.bfloat16, device=dev) if self.dtype == torch.bfloat16 else None
+        self.offsets = offs
+        for l, (ow, nw, ob, nb) in zip(self.param_layers(), offs):
+            w = self.w_flat[ow:ow + nw].view(l.w_shape)
+            dw = self.g_flat[ow:ow + nw].view(l.w_shape)
+            b = self.w_flat[ob:ob + nb] if nb else None
+            db = self.g_flat[ob:ob + nb] if nb else None
+            wc = self.wb_flat[ow:ow + nw].view(l.w_shape) if self.wb_flat is not None else w
+            l.bind(w, b, wc, dw, db)
+
+    # ------------------------------------------------------------ marshalling
+    def load_params(self, params: List[wl.LayerParams]):
+        """Copy fp32 master parameters (KCRS / (J, I) with I in (c, h, w) order)
+        into the flat buffers, permuted to KRSC; fill the bf16 shadow with the
+        round-to-nearest-even bf16 copy."""
+        flat = np.zeros(self.n_params_padded, np.float32)
+        for l, p, (ow, nw, ob, nb) in zip(self.param_layers(), params, self.offsets):
+            K, R, S, C = l.w_shape
+            w = np.asarray(p.w, np.float32).reshape(K, C, R, S).transpose(0, 2, 3, 1)
+            flat[ow:ow + nw] = w.ravel()
+            if nb:
+                flat[ob:ob + nb] = np.asarray(p.b, np.float32)
+        self.w_flat.copy_(torch.from_numpy(flat))
+        self.v_flat.zero_()
+        if self.wb_flat is not None:
+            bits = wl.bf16_bits(flat).view(np.int16)
+            self.wb_flat.view(torch.int16).copy_(torch.from_numpy(bits))
+
+    def to_device_input(self, x_nchw: np.ndarray) -> torch.Tensor:
+        t = torch.from_numpy(np.ascontiguousarray(np.asarray(x_nchw, np.float32).transpose(0, 2, 3, 1)))
+        return t.to(self.device).to(self.dtype)
+
+    # --------------------------------------------------------------- Alg. 1
+    def forward(self, x, labels=None):
+        h = x
+        for l in self.layers:
+            if isinstance(l, SoftmaxCELayer):
+                l.labels = labels
+            h = l.compute_feature(h)
+        return h
+
+    def backward(self, dy_top=None, need_input_grad=False):
+        g = dy_top
+        for i in range(len(self.layers) - 1, -1, -1):
+            g = self.layers[i].compute_gradient(g, need_dx=(i > 0 or need_input_grad))
+        return g
+
+    def update(self):
+        singa.sgd_momentum_update(self.w_flat, self.g_flat, self.v_flat, self.wb_flat, self.wl.lr, self.wl.momentum,
+                                  self.wl.weight_decay)
+
+    def train_one_batch(self, x, labels=None, dy_top=None, need_input_grad=False):
+        self.forward(x, labels)
+        gx = self.backward(dy_top, need_input_grad)
+        if self.wl.update:
+            self.update()
+        return gx
+
+    def layer(self, name: str) -> Layer:
+        for l in self.layers:
+            if l.name == name:
+                return l
+        raise KeyError(name)

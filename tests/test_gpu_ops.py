@@ -1,0 +1,236 @@
+"""GPU parity of every C-ABI operation against the CPU oracle.
+
+Each case draws seeded inputs (representable in the tested dtype), runs the
+HIP library through the Python binding and the fp64 oracle on the same values,
+and compares element by element: rel-L2 <= 1e-4 (fp32) or 2e-2 (bf16, fp32
+accumulation); integer outputs (max-pool argmax) must match exactly.
+Shapes are chosen to span several 128 x 128 tiles and ragged tails in M, N
+and K, channel counts that do and do not allow vector loads, strides 1/2/4 and
+the dense fully connected geometry.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from _helpers import TOL, dev_to_nchw, filt_to_kcrs, kcrs_to_dev, nchw_to_dev, phys, fphys, rel_l2
+from paper_1603_07846_amd import workloads as wl
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _singa():
+    global singa
+    from paper_1603_07846_amd import singa as s
+    singa = s
+    assert torch.cuda.is_available()
+    yield
+
+
+# N, C, H, W, K, R, S, pad, stride
+CONV_CASES = [
+    (2, 3, 13, 13, 5, 3, 3, 1, 1),       # C=3: element-wise tap loads, K tail
+    (2, 8, 9, 9, 16, 5, 5, 2, 1),        # vector loads in both dtypes
+    (3, 32, 17, 17, 40, 3, 3, 1, 2),     # stride 2, M and N tails
+    (2, 3, 35, 35, 8, 11, 11, 0, 4),     # AlexNet conv1 geometry, shrunk
+    (4, 64, 7, 7, 130, 3, 3, 1, 1),      # two N tiles
+    (2, 96, 27, 27, 256, 5, 5, 2, 1),    # AlexNet conv2 shape at batch 2
+    (3, 24, 3, 3, 10, 3, 3, 0, 1),       # fully connected as whole-input conv
+    (7, 40, 1, 1, 20, 1, 1, 0, 1),       # 1x1 on 1x1 (FC)
+    (1, 16, 6, 5, 12, 1, 1, 0, 1),       # 1x1, non-square
+    (2, 12, 8, 8, 9, 3, 3, 2, 1),        # pad 2 with a 3x3 kernel
+]
+
+
+def _ids(cases):
+    return ["x".join(str(v) for v in c) for c in cases]
+
+
+def _conv_inputs(case, dt, seed):
+    N, C, H, W, K, R, S, pad, stride = case
+    x = wl.random_array((N, C, H, W), seed, "normal", 1.0, dt)
+    w = wl.random_array((K, C, R, S), seed + 1, "normal", 0.1, dt)
+    b = wl.random_array((K,), seed + 2, "normal", 0.5, "f32")
+    P = oracle.conv_out(H, R, pad, stride)
+    Q = oracle.conv_out(W, S, pad, stride)
+    dy = wl.random_array((N, K, P, Q), seed + 3, "normal", 1.0, dt)
+    return x, w, b, dy
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("layout", ["NHWC", "NCHW"])
+@pytest.mark.parametrize("case", CONV_CASES, ids=_ids(CONV_CASES))
+def test_conv_fwd(case, layout, dt):
+    N, C, H, W, K, R, S, pad, stride = case
+    x, w, b, _ = _conv_inputs(case, dt, 10)
+    for relu in (False, True):
+        ref = oracle.conv_fwd(x, w, b, pad=pad, stride=stride)
+        if relu:
+            ref = oracle.relu_fwd(ref)
+        y = singa.conv_fwd(nchw_to_dev(x, dt, layout), kcrs_to_dev(w, dt, layout),
+                           torch.from_numpy(b).cuda(), pad, stride, relu=relu, layout=layout)
+        torch.cuda.synchronize()
+        got = dev_to_nchw(y, layout)
+        assert got.shape == ref.shape
+        err = rel_l2(got, ref)
+        assert err <= TOL[dt], (case, relu, err)
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("layout", ["NHWC", "NCHW"])
+@pytest.mark.parametrize("case", CONV_CASES, ids=_ids(CONV_CASES))
+def test_conv_bwd_data(case, layout, dt):
+    N, C, H, W, K, R, S, pad, stride = case
+    x, w, b, dy = _conv_inputs(case, dt, 20)
+    ref = oracle.conv_bwd_data(dy, w, x.shape, pad=pad, stride=stride)
+    dx = singa.conv_bwd_data(nchw_to_dev(dy, dt, layout), kcrs_to_dev(w, dt, layout), phys(x.shape, layout),
+                             pad, stride, layout=layout)
+    torch.cuda.synchronize()
+    err = rel_l2(dev_to_nchw(dx, layout), ref)
+    assert err <= TOL[dt], (case, err)
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("layout", ["NHWC", "NCHW"])
+@pytest.mark.parametrize("case", CONV_CASES, ids=_ids(CONV_CASES))
+def test_conv_bwd_filter(case, layout, dt):
+    N, C, H, W, K, R, S, pad, stride = case
+    x, w, b, dy = _conv_inputs(case, dt, 30)
+    ref_dw, ref_db = oracle.conv_bwd_filter(x, dy, w.shape, pad=pad, stride=stride)
+    dw, db = singa.conv_bwd_filter(nchw_to_dev(x, dt, layout), nchw_to_dev(dy, dt, layout), fphys(w.shape, layout),
+                                   pad, stride, layout=layout)
+    torch.cuda.synchronize()
+    # inputs are exact in dt and dw/db accumulate in fp32: fp32 tolerance applies to both dtypes
+    assert rel_l2(filt_to_kcrs(dw, layout), ref_dw) <= TOL["f32"]
+    assert rel_l2(db.cpu().numpy(), ref_db) <= TOL["f32"]
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+def test_conv_bwd_filter_accumulate_shards(dt):
+    # dim-0 partitioning: the gradient of the batch is the sum of the shards'
+    case = (6, 16, 12, 12, 24, 3, 3, 1, 1)
+    N, C, H, W, K, R, S, pad, stride = case
+    x, w, b, dy = _conv_inputs(case, dt, 40)
+    ref_dw, ref_db = oracle.conv_bwd_filter(x, dy, w.shape, pad=pad, stride=stride)
+    xd, dyd = nchw_to_dev(x, dt), nchw_to_dev(dy, dt)
+    dw, db = singa.conv_bwd_filter(xd[:2], dyd[:2], fphys(w.shape), pad, stride)
+    singa.conv_bwd_filter(xd[2:], dyd[2:], fphys(w.shape), pad, stride, dw=dw, db=db, accumulate=True)
+    full_dw, full_db = singa.conv_bwd_filter(xd, dyd, fphys(w.shape), pad, stride)
+    torch.cuda.synchronize()
+    assert rel_l2(filt_to_kcrs(dw), ref_dw) <= TOL["f32"]
+    assert rel_l2(db.cpu().numpy(), ref_db) <= TOL["f32"]
+    assert rel_l2(dw.cpu().numpy(), full_dw.cpu().numpy()) <= 1e-6
+
+
+def test_conv_bwd_filter_deterministic():
+    case = (4, 32, 15, 15, 48, 3, 3, 1, 1)
+    x, w, b, dy = _conv_inputs(case, "f32", 50)
+    xd, dyd = nchw_to_dev(x), nchw_to_dev(dy)
+    a = singa.conv_bwd_filter(xd, dyd, fphys(w.shape), 1, 1)
+    c = singa.conv_bwd_filter(xd, dyd, fphys(w.shape), 1, 1)
+    torch.cuda.synchronize()
+    assert torch.equal(a[0], c[0]) and torch.equal(a[1], c[1])
+
+
+# N, C, H, W, mode, k, stride, pad
+POOL_CASES = [
+    (2, 32, 32, 32, "max", 3, 2, 0),   # CIFAR pool1 (ceil-mode edge windows)
+    (2, 32, 16, 16, "avg", 3, 2, 0),
+    (2, 64, 8, 8, "avg", 3, 2, 0),
+    (2, 96, 55, 55, "max", 3, 2, 0),   # AlexNet pool1
+    (3, 5, 13, 13, "max", 3, 2, 0),
+    (2, 7, 9, 10, "max", 3, 2, 1),     # padded ceil mode
+    (2, 7, 9, 10, "avg", 3, 2, 1),
+    (1, 3, 7, 7, "avg", 2, 2, 0),
+]
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("layout", ["NHWC", "NCHW"])
+@pytest.mark.parametrize("case", POOL_CASES, ids=_ids(POOL_CASES))
+def test_pool(case, layout, dt):
+    N, C, H, W, mode, k, s, p = case
+    x = wl.random_array((N, C, H, W), 60, "normal", 1.0, dt)
+    m = oracle.MAX if mode == "max" else oracle.AVG
+    ref_y, ref_am = oracle.pool_fwd(x, m, k, s, p, True)
+    y, am = singa.pool_fwd(nchw_to_dev(x, dt, layout), mode, k, s, p, True, layout=layout)
+    dy = wl.random_array(ref_y.shape, 61, "normal", 1.0, dt)
+    dx = singa.pool_bwd(nchw_to_dev(dy, dt, layout), am, phys(x.shape, layout), mode, k, s, p, True, layout=layout)
+    torch.cuda.synchronize()
+    assert rel_l2(dev_to_nchw(y, layout), ref_y) <= (TOL[dt] if mode == "avg" else 0.0)
+    if mode == "max":
+        got_am = am.cpu().numpy()
+        if layout == "NHWC":
+            got_am = got_am.transpose(0, 3, 1, 2)
+        # same values compared in the same order: the argmax is exact
+        np.testing.assert_array_equal(got_am, ref_am)
+    ref_dx = oracle.pool_bwd(dy, ref_am, x.shape, m, k, s, p, True)
+    assert rel_l2(dev_to_nchw(dx, layout), ref_dx) <= TOL[dt]
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("n", [1, 7, 8, 1000, 4099, 1 << 20])
+def test_relu(n, dt):
+    x = wl.random_array((n,), 70, "normal", 1.0, dt)
+    x[: min(n, 3)] = 0.0
+    dy = wl.random_array((n,), 71, "normal", 1.0, dt)
+    xd = torch.from_numpy(x).cuda().to(torch.bfloat16 if dt == "bf16" else torch.float32)
+    y = singa.relu_fwd(xd)
+    dx = singa.relu_bwd(y, torch.from_numpy(dy).cuda().to(xd.dtype))
+    inplace = xd.clone()
+    singa.relu_fwd(inplace, out=inplace)
+    torch.cuda.synchronize()
+    ref_y = oracle.relu_fwd(x)
+    np.testing.assert_array_equal(y.float().cpu().numpy(), ref_y)
+    np.testing.assert_array_equal(inplace.float().cpu().numpy(), ref_y)
+    np.testing.assert_array_equal(dx.float().cpu().numpy(), oracle.relu_bwd(ref_y, dy))
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("shape", [(100, 10), (256, 1000), (3, 7), (1, 1)])
+def test_softmax_ce(shape, dt):
+    B, classes = shape
+    z = wl.random_array(shape, 80, "normal", 2.0, dt)
+    lab = np.random.default_rng(81).integers(0, classes, B).astype(np.int32)
+    ref_loss, ref_dz = oracle.softmax_ce(z, lab)
+    zd = torch.from_numpy(z).cuda().to(torch.bfloat16 if dt == "bf16" else torch.float32)
+    loss, dz = singa.softmax_ce(zd, torch.from_numpy(lab).cuda())
+    torch.cuda.synchronize()
+    assert abs(loss.item() - ref_loss) <= 1e-5 * max(1.0, abs(ref_loss))
+    assert rel_l2(dz.float().cpu().numpy(), ref_dz) <= TOL[dt]
+
+
+@pytest.mark.parametrize("n", [1, 5, 2400, 89578, 1 << 20])
+@pytest.mark.parametrize("shadow", [False, True])
+def test_sgd_momentum(n, shadow):
+    w = wl.random_array((n,), 90, "normal", 0.01)
+    g = wl.random_array((n,), 91, "normal", 1.0)
+    v = wl.random_array((n,), 92, "normal", 0.01)
+    wd, vd, gd = torch.from_numpy(w).cuda(), torch.from_numpy(v).cuda(), torch.from_numpy(g).cuda()
+    wb = torch.empty(n, dtype=torch.bfloat16, device="cuda") if shadow else None
+    for step in range(3):
+        singa.sgd_momentum_update(wd, gd, vd, wb, lr=0.01, momentum=0.9, weight_decay=5e-4)
+        w, v = oracle.sgd_momentum(w, g, v, 0.01, 0.9, 5e-4)
+    torch.cuda.synchronize()
+    assert rel_l2(wd.cpu().numpy(), w) <= TOL["f32"]
+    assert rel_l2(vd.cpu().numpy(), v) <= TOL["f32"]
+    if shadow:
+        # the shadow is exactly the rounded master
+        np.testing.assert_array_equal(wb.cpu().view(torch.int16).numpy().view(np.uint16),
+                                      wl.bf16_bits(wd.cpu().numpy()))
+
+
+def test_abi_errors_launch_nothing():
+    x = torch.zeros((2, 8, 8, 4), device="cuda")
+    w = torch.zeros((4, 3, 3, 4), device="cuda")
+    with pytest.raises(singa.SingaError) as e:
+        singa.conv_fwd(x, torch.zeros((4, 3, 3, 5), device="cuda"))
+    assert e.value.status == -2
+    ws = torch.zeros(16, dtype=torch.uint8, device="cuda")
+    with pytest.raises(singa.SingaError) as e:
+        singa.conv_bwd_filter(x, torch.zeros((2, 8, 8, 4), device="cuda"), (4, 3, 3, 4), 1, 1, workspace=ws)
+    assert e.value.status == -4
+    with pytest.raises(singa.SingaError) as e:
+        singa.relu_fwd(x.view(-1)[1:])
+    assert e.value.status == -5
