@@ -1,0 +1,192 @@
+#!/usr/bin/env python3
+"""Benchmark of the SINGA hot path on one MI355X.
+
+One step = BPTrainOneBatch (Alg. 1) plus the Updater on the AlexNet-shaped
+training workload: batch 256 of 3x227x227 images, bf16 compute with fp32
+accumulation and fp32 master weights, conv 96x11x11/4 - maxpool - conv
+256x5x5 - maxpool - conv 384x3x3 - conv 384x3x3 - conv 256x3x3 - maxpool -
+FC 9216-4096-4096-1000 (ReLU after every conv and the first two FC),
+softmax cross-entropy over random labels, and one fused SGD-momentum update
+(lr 0.01, momentum 0.9, weight decay 5e-4) of all 62,378,344 parameters.
+Inputs are seeded synthetic tensors resident in HBM before timing starts.
+
+Timing follows the paper's protocol by default (Sec. 6.2.2: run 100
+iterations, average iterations 30-80): 30 warm-up steps, then 50 timed steps
+between two device synchronizations.  During the timed steps the library's
+kernel trace brackets every launch with HIP events on its own stream; the
+per-kernel figures (and the roofline of the dominant kernel) come from those.
+
+Prints one JSON line.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK = {"bf16_tflops": 2516.6, "f32_tflops": 157.3, "hbm_gbs": 8000.0}
+METRIC = "conv fwd+bwd TFLOP/s (% MFMA peak) and training images/sec, 1×MI355X"
+CONV_KERNELS = ("conv_fwd_kernel", "conv_wgrad_kernel", "bwd_data_direct_kernel")
+CONV_HELPERS = ("transpose_kernel", "splitk_reduce_kernel", "colsum_partial_kernel", "colsum_final_kernel")
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=30)
+    ap.add_argument("--workload", type=int, default=5, help="workload index (5 = AlexNet-shaped training step)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-images", type=int, default=8, help="images in the oracle's timed sample")
+    return ap.parse_args()
+
+
+def cpu_baseline(w, n_images):
+    """The oracle (fp64 C, OpenMP) on a bounded sample of the same step: the
+    full forward/backward of `n_images` images of the workload plus the
+    update of all parameters."""
+    import numpy as np
+    import oracle
+    from oracle import net as onet
+    from paper_1603_07846_amd import workloads as wl
+
+    inp = wl.make_inputs(w, batch=n_images)
+    params = [(wl.round_bf16(p.w) if w.dtype == "bf16" else p.w, p.b) for p in inp.params]
+    master = [(p.w, p.b) for p in inp.params]
+    oracle.conv_out(1, 1, 0, 1)  # load the library outside the timed region
+    t0 = time.perf_counter()
+    onet.train_one_batch(w.layers, inp.x, params, master=master, labels=inp.labels, dy_top=inp.dy, lr=w.lr,
+                         momentum=w.momentum, wd=w.weight_decay,
+                         store=oracle.round_bf16 if w.dtype == "bf16" else None)
+    dt = time.perf_counter() - t0
+    threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    return {"value": n_images / dt, "unit": "images/s", "cores": threads, "kind": "oracle",
+            "sample": "%d of %d images through the full step (forward, backward, update of all %d parameters), "
+                      "fp64, %.1f s" % (n_images, w.batch, sum(p.w.size + (0 if p.b is None else p.b.size)
+                                                            for p in inp.params), dt),
+            "seconds": dt, "host_cpus": os.cpu_count()}
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py runs on exactly one GPU: this build has no multi-GPU path "
+              "(--gpus %d, WORLD_SIZE %d requested)" % (args.gpus, world), file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    from paper_1603_07846_amd import net as gnet
+    from paper_1603_07846_amd import singa
+    from paper_1603_07846_amd import workloads as wl
+
+    w = wl.WORKLOADS[args.workload]
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    inp = wl.make_inputs(w)
+    net = gnet.Net(w, device=dev)
+    net.load_params(inp.params)
+    x = net.to_device_input(inp.x)
+    labels = torch.from_numpy(inp.labels).to(dev) if inp.labels is not None else None
+    dy = net.to_device_input(inp.dy) if inp.dy is not None else None
+    torch.cuda.synchronize()
+
+    for _ in range(args.warmup):
+        net.train_one_batch(x, labels=labels, dy_top=dy)
+    torch.cuda.synchronize()
+
+    singa.trace_enable(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        net.train_one_batch(x, labels=labels, dy_top=dy)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    singa.trace_enable(False)
+    recs = singa.trace_records()
+    loss = float(net.layers[-1].loss[0].item()) if w.classes else None
+
+    ms_per_step = (t1 - t0) * 1e3 / args.steps
+    images_per_s = net.batch / (ms_per_step / 1e3)
+
+    # per-kernel aggregates over the timed steps
+    agg = {}
+    for name, ms, work, unit in recs:
+        a = agg.setdefault(name, {"launches": 0, "ms": 0.0, "work": 0.0, "unit": unit})
+        a["launches"] += 1
+        a["ms"] += ms
+        a["work"] += work
+    conv_flops = sum(a["work"] for n, a in agg.items() if n.startswith(CONV_KERNELS))
+    conv_ms = sum(a["ms"] for n, a in agg.items() if n.startswith(CONV_KERNELS + CONV_HELPERS))
+    is_bf16 = w.dtype == "bf16"
+    mfma_peak = PEAK["bf16_tflops"] if is_bf16 else PEAK["f32_tflops"]
+    conv_tflops = conv_flops / (conv_ms / 1e3) / 1e12 if conv_ms > 0 else 0.0
+    kernel_ms = sum(a["ms"] for a in agg.values())
+
+    dom_name, dom = max(agg.items(), key=lambda kv: kv[1]["ms"])
+    avg_ms = dom["ms"] / dom["launches"]
+    per_launch = dom["work"] / dom["launches"]
+    if dom["unit"] == "flop":
+        achieved = per_launch / (avg_ms / 1e3) / 1e12
+        peak = PEAK["bf16_tflops"] if "bf16" in dom_name else PEAK["f32_tflops"]
+        roof = {"bound": "mfma", "unit": "TFLOP/s"}
+    else:
+        achieved = per_launch / (avg_ms / 1e3) / 1e9
+        peak = PEAK["hbm_gbs"]
+        roof = {"bound": "hbm", "unit": "GB/s"}
+    roof.update({"kernel": dom_name, "achieved": round(achieved, 2), "peak": peak,
+                 "frac": round(achieved / peak, 4), "traffic": None,
+                 "avg_launch_ms": round(avg_ms, 4), "work_per_launch": per_launch,
+                 "launches_per_step": dom["launches"] / args.steps})
+
+    upd = agg.get("sgd_kernel")
+    update = None
+    if upd:
+        gbs = upd["work"] / (upd["ms"] / 1e3) / 1e9
+        update = {"ms_per_step": round(upd["ms"] / args.steps, 4), "GB_per_s": round(gbs, 1),
+                  "frac_hbm_peak": round(gbs / PEAK["hbm_gbs"], 4), "bytes_per_param": 22 if is_bf16 else 20}
+
+    kernels = sorted(({"kernel": n, "launches_per_step": a["launches"] / args.steps,
+                       "ms_per_step": round(a["ms"] / args.steps, 4),
+                       ("TFLOP/s" if a["unit"] == "flop" else "GB/s"):
+                           round(a["work"] / (a["ms"] / 1e3) / (1e12 if a["unit"] == "flop" else 1e9), 2)}
+                      for n, a in agg.items()), key=lambda d: -d["ms_per_step"])
+
+    out = {
+        "metric": METRIC,
+        "value": round(images_per_s, 2),
+        "unit": "images/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if is_bf16 else "f32",
+        "data": "synthetic",
+        "config": {"workload": "alexnet_shaped_train_step" if args.workload == 5 else "workload%d" % args.workload,
+                   "description": w.name, "global_batch": net.batch, "image": list(w.in_shape),
+                   "classes": w.classes, "params": net.n_params, "layout": "NHWC",
+                   "parallelism": "none (1 GPU)"},
+        "conv_fwd_bwd_tflops": round(conv_tflops, 2),
+        "conv_frac_mfma_peak": round(conv_tflops / mfma_peak, 4),
+        "conv_gflop_per_step": round(conv_flops / args.steps / 1e9, 2),
+        "conv_ms_per_step": round(conv_ms / args.steps, 4),
+        "kernel_ms_per_step": round(kernel_ms / args.steps, 4),
+        "loss": loss,
+        "roofline": roof,
+        "update": update,
+        "kernels": kernels[:16],
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(w, args.cpu_images)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -181,9 +181,11 @@ int singa_relu_bwd(singa_dtype dtype, size_t n, const void* y, const void* dy, v
  *   loss    = (1/B) sum_n ( logsumexp(z[n,:]) - z[n, label[n]] )
  *   dlogits = ( softmax(z[n,:]) - onehot(label[n]) ) / B
  *   logits : dtype [batch][classes] (read);  labels : int32[batch] (read)
- *   loss   : fp32 device scalar (written);   dlogits: dtype [batch][classes] (written)
- * A label outside [0, classes) contributes nothing and its row of dlogits is
- * the plain softmax / B. */
+ *   loss   : fp32 device array of batch + 1 values (written): loss[0] is the
+ *            mean, loss[1 + n] row n's loss
+ *   dlogits: dtype [batch][classes] (written)
+ * A label outside [0, classes) contributes a zero row loss and its row of
+ * dlogits is the plain softmax / B.  The mean is summed in a fixed order. */
 int singa_softmax_ce(singa_dtype dtype, int batch, int classes, const void* logits,
                      const int32_t* labels, float* loss, void* dlogits, singa_stream stream);
 
@@ -195,6 +197,26 @@ int singa_softmax_ce(singa_dtype dtype, int batch, int classes, const void* logi
  * compute copy for bf16 layers.  w, v updated in place; g read. */
 int singa_sgd_momentum_update(size_t n, float* w, const float* g, float* v, uint16_t* w_bf16,
                               float lr, float momentum, float weight_decay, singa_stream stream);
+
+/* ------------------------------------------------------ per-kernel timing */
+
+/* Kernel timing trace, a profiling aid for the per-iteration timing protocol
+ * of Sec. 6.2.2 (time each step, average over a window of iterations).
+ * While enabled, every kernel the library launches is bracketed by two
+ * timing events recorded on its own stream and tagged with the kernel's name
+ * and algorithmic work (flops for the matrix kernels, bytes moved for the
+ * bandwidth-bound ones).  Host-side bookkeeping only; off by default.
+ *   singa_trace_enable(on): on != 0 clears the trace and starts recording,
+ *                           0 stops recording (the trace is kept).  Returns 0.
+ *   singa_trace_count():    number of recorded launches (at most 65536).
+ *   singa_trace_get(i, ...): launch i's kernel name (static string), elapsed
+ *                           milliseconds, work and unit (0 = flop, 1 = byte).
+ *                           The launch's stream must have been synchronized.
+ *                           Returns 0, -1 (NULL argument), -2 (i out of
+ *                           range) or -6 (the events are not complete). */
+int singa_trace_enable(int on);
+int singa_trace_count(void);
+int singa_trace_get(int i, const char** kernel, double* ms, double* work, int* unit);
 
 #ifdef __cplusplus
 }

@@ -70,6 +70,7 @@ def _load():
         lib.oracle_relu_bwd.argtypes = [_i64, _dp, _dp, _dp]
         lib.oracle_softmax_ce.argtypes = [_i64, _i64, _dp, _i32p, _dp]
         lib.oracle_softmax_ce.restype = ctypes.c_double
+        lib.oracle_round_bf16.argtypes = [_i64, _dp]
         lib.oracle_sgd_momentum.argtypes = [_i64, _dp, _dp, _dp,
                                             ctypes.c_double, ctypes.c_double, ctypes.c_double]
         _lib = lib
@@ -243,6 +244,13 @@ def softmax_ce(z, labels):
     dz = np.empty_like(z)
     loss = _load().oracle_softmax_ce(B, classes, _ptr(z), _ptr(lab, _i32p), _ptr(dz))
     return float(loss), dz
+
+
+def round_bf16(x) -> np.ndarray:
+    """Values a bf16 tensor holds after an fp32 computation produced x (returns a copy)."""
+    y = _f64(x).copy()
+    _load().oracle_round_bf16(y.size, _ptr(y))
+    return y
 
 
 def sgd_momentum(w, g, v, lr, momentum, wd=0.0):

@@ -26,12 +26,14 @@ def _kind(layer) -> str:
     return type(layer).__name__
 
 
-def forward(layers, x, params: List, labels=None) -> Dict:
+def forward(layers, x, params: List, labels=None, store=None) -> Dict:
     """Forward pass.  ``params`` is a list of (w, b) in forward order of the
     parametrised layers (conv KCRS, FC (J, I) with I flattened as (c, h, w)).
     Returns a dict with per-layer outputs ``out[name]``, pooling argmax
     ``argmax[name]``, and, for a stack ending in a softmax loss, ``loss`` and
-    ``dlogits``."""
+    ``dlogits``.  ``store`` (optional) is applied to every layer output, as
+    the storage rounding of a reduced-precision pipeline."""
+    keep = (lambda a: a) if store is None else store
     acts = {"out": {}, "argmax": {}, "in": {}}
     h = np.asarray(x, dtype=np.float64)
     pi = 0
@@ -57,18 +59,22 @@ def forward(layers, x, params: List, labels=None) -> Dict:
             B = h.shape[0]
             loss, dz = softmax_ce(h.reshape(B, -1), labels)
             acts["loss"] = loss
-            acts["dlogits"] = dz.reshape(h.shape)
+            acts["dlogits"] = keep(dz.reshape(h.shape))
         else:
             raise ValueError("unknown layer kind %s" % k)
+        if k != "SoftmaxCE":
+            h = keep(h)
         acts["out"][l.name] = h
     return acts
 
 
-def backward(layers, params: List, acts: Dict, dy_top=None, need_input_grad: bool = False) -> Dict:
+def backward(layers, params: List, acts: Dict, dy_top=None, need_input_grad: bool = False, store=None) -> Dict:
     """Backward pass in reverse layer order.  Returns ``grad_in[name]`` (the
     gradient w.r.t. each layer's input), and ``dw[name]``/``db[name]`` for
     parametrised layers.  The first layer's input gradient is only computed
-    when ``need_input_grad`` is set (training never needs it)."""
+    when ``need_input_grad`` is set (training never needs it).  ``store`` is
+    applied to every activation gradient, as in ``forward``."""
+    keep = (lambda a: a) if store is None else store
     res = {"grad_in": {}, "dw": {}, "db": {}}
     pidx = {}
     pi = 0
@@ -106,19 +112,23 @@ def backward(layers, params: List, acts: Dict, dy_top=None, need_input_grad: boo
             g = dx.reshape(xin.shape)
         else:
             raise ValueError("unknown layer kind %s" % k)
+        if g is not None:
+            g = keep(g)
         res["grad_in"][l.name] = g
     return res
 
 
 def train_one_batch(layers, x, params: List, master: Optional[List] = None, labels=None, dy_top=None,
                     lr: float = 0.0, momentum: float = 0.0, wd: float = 0.0, velocity: Optional[List] = None,
-                    need_input_grad: bool = False) -> Dict:
+                    need_input_grad: bool = False, store=None) -> Dict:
     """Alg. 1 followed by the Updater.  ``params`` are the values the layers
     compute with; ``master`` (default: ``params``) are the values the Updater
     steps (for bf16 compute these are the fp32 master weights).  Returns the
-    forward dict, the backward dict and the updated (w, b) and momentum."""
-    acts = forward(layers, x, params, labels=labels)
-    grads = backward(layers, params, acts, dy_top=dy_top, need_input_grad=need_input_grad)
+    forward dict, the backward dict and the updated (w, b) and momentum.
+    ``store`` rounds stored activations and activation gradients (see
+    ``forward``); parameter gradients and the update stay in fp64."""
+    acts = forward(layers, x, params, labels=labels, store=store)
+    grads = backward(layers, params, acts, dy_top=dy_top, need_input_grad=need_input_grad, store=store)
     master = params if master is None else master
     names = [l.name for l in layers if _kind(l) in ("Conv", "FC")]
     new_params, new_vel = [], []

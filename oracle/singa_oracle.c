@@ -419,6 +419,29 @@ double oracle_softmax_ce(int64_t B, int64_t classes, const double* z,
     return total / (double)B;
 }
 
+/* ---------------------------------------------------- bf16 storage rounding */
+
+void oracle_round_bf16(int64_t n, double* x)
+{
+    for (int64_t i = 0; i < n; ++i) {
+        float f = (float)x[i]; /* C's conversion rounds to nearest even */
+        uint32_t u;
+        memcpy(&u, &f, sizeof u);
+        if ((u & 0x7fffffffu) > 0x7f800000u) { /* NaN stays NaN */
+            x[i] = (double)f;
+            continue;
+        }
+        /* keep the upper 16 bits, rounding the lower 16 to nearest, ties to even */
+        uint32_t lower = u & 0xffffu;
+        uint32_t upper = u >> 16;
+        if (lower > 0x8000u || (lower == 0x8000u && (upper & 1u)))
+            upper += 1u;
+        u = upper << 16;
+        memcpy(&f, &u, sizeof f);
+        x[i] = (double)f;
+    }
+}
+
 /* ---------------------------------------------------------------- updater */
 
 void oracle_sgd_momentum(int64_t n, double* w, const double* g, double* v,

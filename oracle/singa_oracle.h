@@ -129,6 +129,13 @@ void oracle_relu_bwd(int64_t n, const double* y, const double* dy, double* dx);
 double oracle_softmax_ce(int64_t B, int64_t classes, const double* z,
                          const int32_t* label, double* dz);
 
+/* Storage rounding of a bf16 layer boundary, in place: each value is rounded
+ * to binary32 (round to nearest even) and then to bfloat16 (round to nearest
+ * even on the 16 discarded mantissa bits), i.e. the value a bf16 tensor would
+ * hold after an fp32 computation.  Used to take the ReLU and max-pooling
+ * decisions on the same stored values as a bf16 pipeline. */
+void oracle_round_bf16(int64_t n, double* x);
+
 /* Updater (Sec. 4.1.4): one step of SGD with momentum and weight decay,
  * in place on w and v:
  *   g' = g + wd * w;  v = momentum * v + lr * g';  w = w - v. */

@@ -52,6 +52,11 @@ int conv_geometry(const singa_shape4* x, const singa_filter4* w, const singa_con
 inline size_t act_bytes(const ConvShape& s, int dt) { return (size_t)s.N * s.H * s.W * s.C * dt_size(dt); }
 inline size_t out_bytes(const ConvShape& s, int dt) { return (size_t)s.N * s.P * s.Q * s.K * dt_size(dt); }
 inline size_t filt_bytes(const ConvShape& s, int dt) { return (size_t)s.K * s.R * s.S * s.C * dt_size(dt); }
+// Algorithmic flops of one pass of a convolution layer: 2 x the multiply-adds
+// of the direct definition, padded taps included (the same for all 3 passes).
+inline double conv_flops(const ConvShape& s) {
+  return 2.0 * s.N * (double)s.P * s.Q * s.K * (double)s.C * s.R * s.S;
+}
 
 // Backward-data through the forward GEMM needs a transposed filter copy:
 // dense "fully connected" geometry, or unit stride (flipped filter).
@@ -206,10 +211,11 @@ int singa_conv_fwd(singa_dtype dtype, singa_layout layout, const singa_shape4* x
   if (need > 0 && (!ws || ws_bytes < need)) return SINGA_ERR_WORKSPACE;
   carve_fwd(s, dtype, layout, ws, &o);
   hipStream_t st = (hipStream_t)stream;
-  if (layout == SINGA_NHWC) return hip_status(launch_conv_fwd(dtype, s, x_ptr, w_ptr, bias, y_ptr, fuse_relu, st));
+  if (layout == SINGA_NHWC)
+    return hip_status(launch_conv_fwd(dtype, s, x_ptr, w_ptr, bias, y_ptr, fuse_relu, 0, conv_flops(s), st));
   hipError_t e = launch_nchw_to_nhwc(dtype, x_ptr, o.x, s.N, s.C, s.H, s.W, st);
   if (e == hipSuccess) e = kcrs_to_krsc(dtype, s, w_ptr, o.w, st);
-  if (e == hipSuccess) e = launch_conv_fwd(dtype, s, o.x, o.w, bias, o.y, fuse_relu, st);
+  if (e == hipSuccess) e = launch_conv_fwd(dtype, s, o.x, o.w, bias, o.y, fuse_relu, 0, conv_flops(s), st);
   if (e == hipSuccess) e = launch_nhwc_to_nchw(dtype, o.y, y_ptr, s.N, s.K, s.P, s.Q, st);
   return hip_status(e);
 }
@@ -249,13 +255,13 @@ int singa_conv_bwd_data(singa_dtype dtype, singa_layout layout, const singa_shap
       const int J = RS * s.C;
       e = launch_transpose(dtype, wk, o.wt, 1, s.K, J, 0, J, 0, s.K, 0, st);
       ConvShape g{s.N, 1, 1, s.K, J, 1, 1, 1, 1, 0, 0, 1, 1};
-      if (e == hipSuccess) e = launch_conv_fwd(dtype, g, dy, o.wt, nullptr, dx, 0, st);
+      if (e == hipSuccess) e = launch_conv_fwd(dtype, g, dy, o.wt, nullptr, dx, 0, 1, conv_flops(s), st);
     } else if (s.sh == 1 && s.sw == 1) {
       // unit stride: dx = conv(dy, flip(w)^T) with padding R-1-ph, S-1-pw, where
       // wt[c][r'][s'][k] = w[k][R-1-r'][S-1-s'][c]
       e = launch_transpose(dtype, wk, o.wt, RS, s.K, s.C, s.C, (long)RS * s.C, s.K, (long)RS * s.K, 1, st);
       ConvShape g{s.N, s.P, s.Q, s.K, s.C, s.R, s.S, s.H, s.W, s.R - 1 - s.ph, s.S - 1 - s.pw, 1, 1};
-      if (e == hipSuccess) e = launch_conv_fwd(dtype, g, dy, o.wt, nullptr, dx, 0, st);
+      if (e == hipSuccess) e = launch_conv_fwd(dtype, g, dy, o.wt, nullptr, dx, 0, 1, conv_flops(s), st);
     } else {
       e = launch_conv_bwd_data_direct(dtype, s, dy, wk, dx, st);
     }

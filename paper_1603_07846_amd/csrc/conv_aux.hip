@@ -77,28 +77,69 @@ __global__ __launch_bounds__(256) void bwd_data_direct_kernel(ConvShape s, const
   }
 }
 
-// Pass 1: partial[chunk][col] = sum of rows [chunk*RC, (chunk+1)*RC) in row order.
-constexpr int COLSUM_RC = 256;
-template <typename T>
+// Bias gradient db[col] = sum over rows of a[row][col], in two passes with a
+// fixed summation order (no atomics, bitwise reproducible).
+// Pass 1: chunk b of COLSUM_RC rows.  The 256 threads form TC column lanes
+// (each VEC consecutive columns) x TR row lanes; row lane r sums rows
+// r, r + TR, ... of the chunk, then the TR lanes are added in lane order.
+constexpr int COLSUM_RC = 1024;
+template <typename T, int VEC>
 __global__ __launch_bounds__(256) void colsum_partial_kernel(const T* __restrict__ a, int rows, int cols,
                                                              float* __restrict__ partial) {
-  const int chunk = blockIdx.x;
-  const int r0 = chunk * COLSUM_RC, r1 = min(rows, r0 + COLSUM_RC);
-  for (int c = threadIdx.x; c < cols; c += blockDim.x) {
-    float s = 0.f;
-    for (int r = r0; r < r1; ++r) s += ld_f<T>(a + (long)r * cols + c);
-    partial[(long)chunk * cols + c] = s;
+  __shared__ float red[256 * VEC];
+  const int nvec = cols / VEC;                 // column vectors in a row
+  const int TC = nvec < 256 ? nvec : 256;      // column lanes
+  const int TR = 256 / TC;                     // row lanes
+  const int tc = threadIdx.x % TC, tr = threadIdx.x / TC;
+  const int r0 = blockIdx.x * COLSUM_RC, r1 = min(rows, r0 + COLSUM_RC);
+  for (int cv0 = 0; cv0 < nvec; cv0 += TC) {
+    const int cv = cv0 + tc;
+    float acc[VEC];
+#pragma unroll
+    for (int j = 0; j < VEC; ++j) acc[j] = 0.f;
+    if (tr < TR && cv < nvec) {
+      for (int r = r0 + tr; r < r1; r += TR) {
+        const T* src = a + (long)r * cols + (long)cv * VEC;
+        if constexpr (VEC == 1) {
+          acc[0] += ld_f<T>(src);
+        } else {
+          union { uint4 u; T e[VEC]; } v;
+          v.u = *(const uint4*)src;
+#pragma unroll
+          for (int j = 0; j < VEC; ++j) acc[j] += ld_f<T>(&v.e[j]);
+        }
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < VEC; ++j) red[threadIdx.x * VEC + j] = acc[j];
+    __syncthreads();
+    if (threadIdx.x < TC && cv < nvec) {
+#pragma unroll
+      for (int j = 0; j < VEC; ++j) {
+        float t = 0.f;
+        for (int l = 0; l < TR; ++l) t += red[(l * TC + threadIdx.x) * VEC + j];
+        partial[(long)blockIdx.x * cols + (long)cv * VEC + j] = t;
+      }
+    }
+    __syncthreads();
   }
 }
 
-// Pass 2: out[col] = (accumulate ? out : 0) + sum of the chunks in chunk order.
+// Pass 2: one block per column; thread t sums chunks t, t + 256, ... in order,
+// then a fixed-shape tree adds the 256 thread sums.
 __global__ __launch_bounds__(256) void colsum_final_kernel(const float* __restrict__ partial, int chunks, int cols,
                                                            float* __restrict__ out, int accumulate) {
-  const int c = blockIdx.x * blockDim.x + threadIdx.x;
-  if (c >= cols) return;
+  __shared__ float red[256];
+  const int c = blockIdx.x;
   float s = 0.f;
-  for (int k = 0; k < chunks; ++k) s += partial[(long)k * cols + c];
-  out[c] = (accumulate ? out[c] : 0.f) + s;
+  for (int k = threadIdx.x; k < chunks; k += 256) s += partial[(long)k * cols + c];
+  red[threadIdx.x] = s;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if (threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) out[c] = (accumulate ? out[c] : 0.f) + red[0];
 }
 
 template <typename T>
@@ -168,6 +209,7 @@ unsigned grid_for(long total, int block = 256, long cap = 65536) {
 hipError_t launch_transpose(int dt, const void* in, void* out, int batch, int rows, int cols, long in_bstride,
                             long in_rstride, long out_bstride, long out_rstride, int flip, hipStream_t st) {
   dim3 grid((cols + 31) / 32, (rows + 31) / 32, batch), block(256);
+  TraceScope ts("transpose_kernel", st, 2.0 * batch * (double)rows * cols * dt_size(dt), WORK_BYTE);
   if (dt == BF16)
     hipLaunchKernelGGL(transpose_kernel<bf16_t>, grid, block, 0, st, (const bf16_t*)in, (bf16_t*)out, batch, rows,
                        cols, in_bstride, in_rstride, out_bstride, out_rstride, flip);
@@ -181,6 +223,8 @@ hipError_t launch_conv_bwd_data_direct(int dt, const ConvShape& s, const void* d
                                        hipStream_t st) {
   const long total = (long)s.N * s.H * s.W * s.C;
   const unsigned g = grid_for(total);
+  TraceScope ts("bwd_data_direct_kernel", st,
+                2.0 * s.N * (double)s.P * s.Q * s.K * (double)s.C * s.R * s.S, WORK_FLOP);
   if (dt == BF16)
     hipLaunchKernelGGL(bwd_data_direct_kernel<bf16_t>, dim3(g), dim3(256), 0, st, s, (const bf16_t*)dy,
                        (const bf16_t*)w, (bf16_t*)dx, total);
@@ -198,22 +242,38 @@ size_t colsum_partial_bytes(int rows, int cols) {
 hipError_t launch_colsum(int dt, const void* a, int rows, int cols, float* partial, float* out, int accumulate,
                          hipStream_t st) {
   const int chunks = (rows + COLSUM_RC - 1) / COLSUM_RC;
-  if (dt == BF16)
-    hipLaunchKernelGGL(colsum_partial_kernel<bf16_t>, dim3(chunks), dim3(256), 0, st, (const bf16_t*)a, rows, cols,
-                       partial);
-  else
-    hipLaunchKernelGGL(colsum_partial_kernel<float>, dim3(chunks), dim3(256), 0, st, (const float*)a, rows, cols,
-                       partial);
+  const size_t es = dt_size(dt);
+  const int vec = (int)(16 / es);
+  const bool v = (cols % vec) == 0 && ((uintptr_t)a % 16) == 0;
+  {
+    TraceScope ts("colsum_partial_kernel", st, (double)rows * cols * es + 4.0 * chunks * cols, WORK_BYTE);
+    if (dt == BF16) {
+      if (v)
+        hipLaunchKernelGGL((colsum_partial_kernel<bf16_t, 8>), dim3(chunks), dim3(256), 0, st, (const bf16_t*)a,
+                           rows, cols, partial);
+      else
+        hipLaunchKernelGGL((colsum_partial_kernel<bf16_t, 1>), dim3(chunks), dim3(256), 0, st, (const bf16_t*)a,
+                           rows, cols, partial);
+    } else {
+      if (v)
+        hipLaunchKernelGGL((colsum_partial_kernel<float, 4>), dim3(chunks), dim3(256), 0, st, (const float*)a,
+                           rows, cols, partial);
+      else
+        hipLaunchKernelGGL((colsum_partial_kernel<float, 1>), dim3(chunks), dim3(256), 0, st, (const float*)a,
+                           rows, cols, partial);
+    }
+  }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(colsum_final_kernel, dim3((cols + 255) / 256), dim3(256), 0, st, partial, chunks, cols, out,
-                     accumulate);
+  TraceScope ts("colsum_final_kernel", st, 4.0 * chunks * cols + 4.0 * cols * (accumulate ? 2 : 1), WORK_BYTE);
+  hipLaunchKernelGGL(colsum_final_kernel, dim3(cols), dim3(256), 0, st, partial, chunks, cols, out, accumulate);
   return hipGetLastError();
 }
 
 hipError_t launch_nchw_to_nhwc(int dt, const void* in, void* out, int N, int C, int H, int W, hipStream_t st) {
   const int HW = H * W;
   dim3 grid((HW + 31) / 32, (C + 31) / 32, N), block(256);
+  TraceScope ts("nchw_to_nhwc_kernel", st, 2.0 * N * (double)C * HW * dt_size(dt), WORK_BYTE);
   if (dt == BF16)
     hipLaunchKernelGGL(nchw_to_nhwc_kernel<bf16_t>, grid, block, 0, st, (const bf16_t*)in, (bf16_t*)out, C, HW);
   else
@@ -224,6 +284,7 @@ hipError_t launch_nchw_to_nhwc(int dt, const void* in, void* out, int N, int C, 
 hipError_t launch_nhwc_to_nchw(int dt, const void* in, void* out, int N, int C, int H, int W, hipStream_t st) {
   const int HW = H * W;
   dim3 grid((C + 31) / 32, (HW + 31) / 32, N), block(256);
+  TraceScope ts("nhwc_to_nchw_kernel", st, 2.0 * N * (double)C * HW * dt_size(dt), WORK_BYTE);
   if (dt == BF16)
     hipLaunchKernelGGL(nhwc_to_nchw_kernel<bf16_t>, grid, block, 0, st, (const bf16_t*)in, (bf16_t*)out, C, HW);
   else
@@ -234,6 +295,7 @@ hipError_t launch_nhwc_to_nchw(int dt, const void* in, void* out, int N, int C, 
 hipError_t launch_krsc_to_kcrs_f32(const float* in, float* out, int K, int C, int R, int S, int accumulate,
                                    hipStream_t st) {
   const long total = (long)K * C * R * S;
+  TraceScope ts("krsc_to_kcrs_kernel", st, 4.0 * total * (accumulate ? 3 : 2), WORK_BYTE);
   hipLaunchKernelGGL(krsc_to_kcrs_kernel, dim3(grid_for(total)), dim3(256), 0, st, in, out, K, C, R * S,
                      accumulate);
   return hipGetLastError();

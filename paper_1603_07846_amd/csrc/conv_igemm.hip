@@ -108,8 +108,9 @@ struct FwdArgs {
 };
 
 // VA: A taps are loaded as 16-byte vectors (C % VEC == 0); otherwise element
-// by element.  VB: likewise for the filter rows (Kg % VEC == 0).
-template <typename T, bool VA, bool VB>
+// by element.  VB: likewise for the filter rows (Kg % VEC == 0).  BWD only
+// names the instance that serves backward-data, so profiles tell them apart.
+template <typename T, bool VA, bool VB, bool BWD>
 __global__ __launch_bounds__(NT) void conv_fwd_kernel(FwdArgs a) {
   constexpr int VEC = KT<T>::VEC;
   constexpr int BK = KT<T>::BK;
@@ -438,9 +439,45 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restr
   }
 }
 
+template <typename T> constexpr const char* tname();
+template <> constexpr const char* tname<float>() { return "f32"; }
+template <> constexpr const char* tname<bf16_t>() { return "bf16"; }
+
+// "conv_fwd_kernel<dtype,vecA,vecB,bwd>" for each instance
+template <typename T, bool VA, bool VB, bool BWD> const char* fwd_name() {
+  static const char* names[2][2][2] = {
+      {{"conv_fwd_kernel<%s,0,0,0>", "conv_fwd_kernel<%s,0,0,1>"},
+       {"conv_fwd_kernel<%s,0,1,0>", "conv_fwd_kernel<%s,0,1,1>"}},
+      {{"conv_fwd_kernel<%s,1,0,0>", "conv_fwd_kernel<%s,1,0,1>"},
+       {"conv_fwd_kernel<%s,1,1,0>", "conv_fwd_kernel<%s,1,1,1>"}}};
+  static char buf[2][2][2][48];
+  static bool init = false;
+  if (!init) {
+    for (int i = 0; i < 2; ++i)
+      for (int j = 0; j < 2; ++j)
+        for (int k = 0; k < 2; ++k) snprintf(buf[i][j][k], sizeof buf[i][j][k], names[i][j][k], tname<T>());
+    init = true;
+  }
+  return buf[VA][VB][BWD];
+}
+
+template <typename T, bool VA, bool VB, bool BWD>
+void launch_fwd_instance(const FwdArgs& a, dim3 grid, double flops, hipStream_t st) {
+  TraceScope ts(fwd_name<T, VA, VB, BWD>(), st, flops, WORK_FLOP);
+  hipLaunchKernelGGL((conv_fwd_kernel<T, VA, VB, BWD>), grid, dim3(NT), 0, st, a);
+}
+
+template <typename T, bool BWD>
+void launch_fwd_variant(bool va, bool vb, const FwdArgs& a, dim3 grid, double flops, hipStream_t st) {
+  if (va && vb) launch_fwd_instance<T, true, true, BWD>(a, grid, flops, st);
+  else if (vb) launch_fwd_instance<T, false, true, BWD>(a, grid, flops, st);
+  else if (va) launch_fwd_instance<T, true, false, BWD>(a, grid, flops, st);
+  else launch_fwd_instance<T, false, false, BWD>(a, grid, flops, st);
+}
+
 template <typename T>
 hipError_t conv_fwd_dispatch(const ConvShape& s, const void* x, const void* w, const float* bias, void* y,
-                             int relu, hipStream_t st) {
+                             int relu, int bwd, double flops, hipStream_t st) {
   constexpr int VEC = KT<T>::VEC;
   FwdArgs a;
   a.x = x; a.w = w; a.bias = bias; a.y = y;
@@ -456,18 +493,30 @@ hipError_t conv_fwd_dispatch(const ConvShape& s, const void* x, const void* w, c
   a.relu = relu;
   const int tiles_m = (a.M + BM - 1) / BM;
   a.tiles_n = (a.Nn + BN - 1) / BN;
-  dim3 grid(tiles_m * a.tiles_n), block(NT);
+  dim3 grid(tiles_m * a.tiles_n);
   const bool va = (s.C % VEC) == 0 && ((uintptr_t)x % 16) == 0;
   const bool vb = (a.Kg % VEC) == 0 && ((uintptr_t)w % 16) == 0;
-  if (va && vb)
-    hipLaunchKernelGGL((conv_fwd_kernel<T, true, true>), grid, block, 0, st, a);
-  else if (vb)
-    hipLaunchKernelGGL((conv_fwd_kernel<T, false, true>), grid, block, 0, st, a);
-  else if (va)
-    hipLaunchKernelGGL((conv_fwd_kernel<T, true, false>), grid, block, 0, st, a);
+  if (bwd)
+    launch_fwd_variant<T, true>(va, vb, a, grid, flops, st);
   else
-    hipLaunchKernelGGL((conv_fwd_kernel<T, false, false>), grid, block, 0, st, a);
+    launch_fwd_variant<T, false>(va, vb, a, grid, flops, st);
   return hipGetLastError();
+}
+
+template <typename T, bool VA, bool VB> const char* wgrad_name() {
+  static char buf[48];
+  static bool init = false;
+  if (!init) {
+    snprintf(buf, sizeof buf, "conv_wgrad_kernel<%s,%d,%d>", tname<T>(), (int)VA, (int)VB);
+    init = true;
+  }
+  return buf;
+}
+
+template <typename T, bool VA, bool VB>
+void launch_wgrad_instance(const WgradArgs& a, dim3 grid, double flops, hipStream_t st) {
+  TraceScope ts(wgrad_name<T, VA, VB>(), st, flops, WORK_FLOP);
+  hipLaunchKernelGGL((conv_wgrad_kernel<T, VA, VB>), grid, dim3(NT), 0, st, a);
 }
 
 template <typename T>
@@ -489,26 +538,27 @@ hipError_t conv_wgrad_dispatch(const ConvShape& s, const void* x, const void* dy
   a.nkt = (a.T + BK - 1) / BK;
   const int splits = wgrad_splits(s);
   a.kt_per_split = (a.nkt + splits - 1) / splits;
-  dim3 grid(tiles_m * a.tiles_n, splits), block(NT);
+  dim3 grid(tiles_m * a.tiles_n, splits);
   const bool va = (a.M % 4) == 0 && ((uintptr_t)dy % (4 * sizeof(T))) == 0;
   const bool vb = (s.C % 4) == 0 && ((uintptr_t)x % (4 * sizeof(T))) == 0;
+  const double flops = 2.0 * a.M * (double)a.Nn * (double)a.T;
   if (va && vb)
-    hipLaunchKernelGGL((conv_wgrad_kernel<T, true, true>), grid, block, 0, st, a);
+    launch_wgrad_instance<T, true, true>(a, grid, flops, st);
   else if (va)
-    hipLaunchKernelGGL((conv_wgrad_kernel<T, true, false>), grid, block, 0, st, a);
+    launch_wgrad_instance<T, true, false>(a, grid, flops, st);
   else if (vb)
-    hipLaunchKernelGGL((conv_wgrad_kernel<T, false, true>), grid, block, 0, st, a);
+    launch_wgrad_instance<T, false, true>(a, grid, flops, st);
   else
-    hipLaunchKernelGGL((conv_wgrad_kernel<T, false, false>), grid, block, 0, st, a);
+    launch_wgrad_instance<T, false, false>(a, grid, flops, st);
   return hipGetLastError();
 }
 
 }  // namespace
 
 hipError_t launch_conv_fwd(int dt, const ConvShape& s, const void* x, const void* w, const float* bias, void* y,
-                           int relu, hipStream_t st) {
-  if (dt == BF16) return conv_fwd_dispatch<bf16_t>(s, x, w, bias, y, relu, st);
-  return conv_fwd_dispatch<float>(s, x, w, bias, y, relu, st);
+                           int relu, int bwd, double flops, hipStream_t st) {
+  if (dt == BF16) return conv_fwd_dispatch<bf16_t>(s, x, w, bias, y, relu, bwd, flops, st);
+  return conv_fwd_dispatch<float>(s, x, w, bias, y, relu, bwd, flops, st);
 }
 
 int wgrad_splits(const ConvShape& s) {
@@ -538,6 +588,7 @@ hipError_t launch_splitk_reduce(const float* partial, int splits, size_t n, floa
                                 hipStream_t st) {
   size_t blocks = (n + 255) / 256;
   if (blocks > 4096) blocks = 4096;
+  TraceScope ts("splitk_reduce_kernel", st, (double)n * 4.0 * (splits + 1 + (accumulate ? 1 : 0)), WORK_BYTE);
   hipLaunchKernelGGL(splitk_reduce_kernel, dim3((unsigned)blocks), dim3(256), 0, st, partial, splits, n, dw,
                      accumulate);
   return hipGetLastError();

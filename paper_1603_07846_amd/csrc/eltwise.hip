@@ -143,6 +143,128 @@ __global__ __launch_bounds__(256) void pool_bwd_kernel(PoolGeom g, int mode, con
   }
 }
 
+// NHWC pooling over 16-byte channel vectors: one thread per (output pixel,
+// VEC consecutive channels).  Same window scan and first-maximum rule as the
+// scalar kernel, applied per channel; the VEC argmax bytes are stored together.
+template <typename T, int VEC>
+__global__ __launch_bounds__(256) void pool_fwd_nhwc_vec_kernel(PoolGeom g, int mode, const T* __restrict__ x,
+                                                                T* __restrict__ y, uint8_t* __restrict__ argmax,
+                                                                long total) {
+  const int CV = g.C / VEC;
+  for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += (long)gridDim.x * blockDim.x) {
+    const int cv = (int)(i % CV);
+    long t = i / CV;
+    const int q = (int)(t % g.Q);
+    t /= g.Q;
+    const int p = (int)(t % g.P);
+    const int n = (int)(t / g.P);
+    const int h0 = p * g.sh - g.ph, w0 = q * g.sw - g.pw;
+    float best[VEC];
+    uint8_t cell[VEC];
+#pragma unroll
+    for (int j = 0; j < VEC; ++j) {
+      best[j] = 0.f;
+      cell[j] = 0;
+    }
+    bool found = false;
+    for (int r = 0; r < g.kh; ++r) {
+      const int h = h0 + r;
+      if ((unsigned)h >= (unsigned)g.H) continue;
+      for (int s = 0; s < g.kw; ++s) {
+        const int w = w0 + s;
+        if ((unsigned)w >= (unsigned)g.W) continue;
+        union { uint4 u; T e[VEC]; } v;
+        v.u = *(const uint4*)(x + (((long)n * g.H + h) * g.W + w) * g.C + (long)cv * VEC);
+#pragma unroll
+        for (int j = 0; j < VEC; ++j) {
+          const float f = ld_f<T>(&v.e[j]);
+          if (mode == 0) {
+            if (!found || f > best[j]) {
+              best[j] = f;
+              cell[j] = (uint8_t)(r * g.kw + s);
+            }
+          } else {
+            best[j] += f;
+          }
+        }
+        found = true;
+      }
+    }
+    union { uint4 u; T e[VEC]; } o;
+    const float inv = mode == 0 ? 1.f : 1.f / (float)pool_divisor(g, p, q);
+#pragma unroll
+    for (int j = 0; j < VEC; ++j) st_f<T>(&o.e[j], mode == 0 ? best[j] : best[j] * inv);
+    *(uint4*)(y + i * VEC) = o.u;
+    if (mode == 0) {
+      if constexpr (VEC == 8) {
+        uint2 a;
+        a.x = cell[0] | (cell[1] << 8) | (cell[2] << 16) | ((uint32_t)cell[3] << 24);
+        a.y = cell[4] | (cell[5] << 8) | (cell[6] << 16) | ((uint32_t)cell[7] << 24);
+        *(uint2*)(argmax + i * VEC) = a;
+      } else {
+        *(uint32_t*)(argmax + i * VEC) = cell[0] | (cell[1] << 8) | (cell[2] << 16) | ((uint32_t)cell[3] << 24);
+      }
+    }
+  }
+}
+
+template <typename T, int VEC>
+__global__ __launch_bounds__(256) void pool_bwd_nhwc_vec_kernel(PoolGeom g, int mode, const T* __restrict__ dy,
+                                                                const uint8_t* __restrict__ argmax,
+                                                                T* __restrict__ dx, long total) {
+  const int CV = g.C / VEC;
+  for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += (long)gridDim.x * blockDim.x) {
+    const int cv = (int)(i % CV);
+    long t = i / CV;
+    const int w = (int)(t % g.W);
+    t /= g.W;
+    const int h = (int)(t % g.H);
+    const int n = (int)(t / g.H);
+    const int hn = h + g.ph - g.kh + 1, wn = w + g.pw - g.kw + 1;
+    const int p_lo = hn <= 0 ? 0 : (hn + g.sh - 1) / g.sh;
+    const int q_lo = wn <= 0 ? 0 : (wn + g.sw - 1) / g.sw;
+    const int p_hi = min(g.P - 1, (h + g.ph) / g.sh);
+    const int q_hi = min(g.Q - 1, (w + g.pw) / g.sw);
+    float acc[VEC];
+#pragma unroll
+    for (int j = 0; j < VEC; ++j) acc[j] = 0.f;
+    for (int p = p_lo; p <= p_hi; ++p) {
+      for (int q = q_lo; q <= q_hi; ++q) {
+        const long o = (((long)n * g.P + p) * g.Q + q) * g.C + (long)cv * VEC;
+        union { uint4 u; T e[VEC]; } v;
+        v.u = *(const uint4*)(dy + o);
+        if (mode == 0) {
+          const int cell = (h - (p * g.sh - g.ph)) * g.kw + (w - (q * g.sw - g.pw));
+          uint8_t am[VEC];
+          if constexpr (VEC == 8) {
+            const uint2 a = *(const uint2*)(argmax + o);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+              am[j] = (uint8_t)(a.x >> (8 * j));
+              am[4 + j] = (uint8_t)(a.y >> (8 * j));
+            }
+          } else {
+            const uint32_t a = *(const uint32_t*)(argmax + o);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) am[j] = (uint8_t)(a >> (8 * j));
+          }
+#pragma unroll
+          for (int j = 0; j < VEC; ++j)
+            if (am[j] == cell) acc[j] += ld_f<T>(&v.e[j]);
+        } else {
+          const float inv = 1.f / (float)pool_divisor(g, p, q);
+#pragma unroll
+          for (int j = 0; j < VEC; ++j) acc[j] += ld_f<T>(&v.e[j]) * inv;
+        }
+      }
+    }
+    union { uint4 u; T e[VEC]; } out;
+#pragma unroll
+    for (int j = 0; j < VEC; ++j) st_f<T>(&out.e[j], acc[j]);
+    *(uint4*)(dx + i * VEC) = out.u;
+  }
+}
+
 // ReLU over 16-byte vectors; the scalar tail goes to the first threads.
 template <typename T>
 __global__ __launch_bounds__(256) void relu_fwd_kernel(const T* x, T* y, size_t n) {
@@ -190,43 +312,55 @@ __device__ __forceinline__ float wave_sum(float v) {
   return v;
 }
 
-// One workgroup of 16 waves; wave w takes rows w, w+16, ...  Each wave keeps
-// its rows' losses in row order and the waves are summed in wave order, so
-// the loss does not depend on timing.
-constexpr int CE_WAVES = 16;
+// One wave per row.  The row's maximum and the sum of exp(z - max) are
+// built in one pass with the running-max rescaling of the sum; a second pass
+// writes the gradient.  The row's loss goes to loss[1 + row].
 template <typename T>
-__global__ __launch_bounds__(64 * CE_WAVES) void softmax_ce_kernel(int B, int classes, const T* __restrict__ z,
-                                                                   const int32_t* __restrict__ labels,
-                                                                   float* __restrict__ loss, T* __restrict__ dz) {
-  __shared__ float wave_loss[CE_WAVES];
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const float invB = 1.f / (float)B;
-  float my_loss = 0.f;
-  for (int row = wave; row < B; row += CE_WAVES) {
-    const T* zr = z + (size_t)row * classes;
-    float m = -INFINITY;
-    for (int j = lane; j < classes; j += 64) m = fmaxf(m, ld_f<T>(zr + j));
-    m = wave_max(m);
-    float s = 0.f;
-    for (int j = lane; j < classes; j += 64) s += expf(ld_f<T>(zr + j) - m);
-    s = wave_sum(s);
-    const float lse = m + logf(s);
-    const int lab = labels[row];
-    const bool lab_ok = lab >= 0 && lab < classes;
-    if (lab_ok) my_loss += lse - ld_f<T>(zr + lab);
-    T* dr = dz + (size_t)row * classes;
-    for (int j = lane; j < classes; j += 64) {
-      const float prob = expf(ld_f<T>(zr + j) - lse);
-      st_f<T>(dr + j, (prob - (j == lab ? 1.f : 0.f)) * invB);
+__global__ __launch_bounds__(256) void softmax_ce_rows_kernel(int B, int classes, const T* __restrict__ z,
+                                                              const int32_t* __restrict__ labels,
+                                                              float* __restrict__ loss, T* __restrict__ dz) {
+  const int lane = threadIdx.x & 63;
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= B) return;
+  const T* zr = z + (size_t)row * classes;
+  float m = -INFINITY, s = 0.f;
+  for (int j = lane; j < classes; j += 64) {
+    const float v = ld_f<T>(zr + j);
+    if (v > m) {
+      s = s * expf(m - v) + 1.f;
+      m = v;
+    } else {
+      s += expf(v - m);
     }
   }
-  if (lane == 0) wave_loss[wave] = my_loss;
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    float t = 0.f;
-    for (int w = 0; w < CE_WAVES; ++w) t += wave_loss[w];
-    *loss = t * invB;
+  // combine the lanes' (max, sum) pairs
+  const float mw = wave_max(m);
+  s = (m == -INFINITY) ? 0.f : s * expf(m - mw);
+  s = wave_sum(s);
+  const float lse = mw + logf(s);
+  const int lab = labels[row];
+  const float invB = 1.f / (float)B;
+  T* dr = dz + (size_t)row * classes;
+  for (int j = lane; j < classes; j += 64) {
+    const float prob = expf(ld_f<T>(zr + j) - lse);
+    st_f<T>(dr + j, (prob - (j == lab ? 1.f : 0.f)) * invB);
   }
+  if (lane == 0) loss[1 + row] = (lab >= 0 && lab < classes) ? lse - ld_f<T>(zr + lab) : 0.f;
+}
+
+// loss[0] = mean of loss[1..B]: thread t adds rows t, t + 256, ... in order,
+// then a fixed-shape tree adds the thread sums.
+__global__ __launch_bounds__(256) void softmax_ce_mean_kernel(int B, float* __restrict__ loss) {
+  __shared__ float red[256];
+  float s = 0.f;
+  for (int r = threadIdx.x; r < B; r += 256) s += loss[1 + r];
+  red[threadIdx.x] = s;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if (threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) loss[0] = red[0] / (float)B;
 }
 
 __global__ __launch_bounds__(256) void sgd_kernel(size_t n, float* __restrict__ w, const float* __restrict__ g,
@@ -271,6 +405,21 @@ hipError_t launch_pool_fwd(int dt, int mode, int N, int C, int H, int W, int P, 
                            int ph, int pw, const void* x, void* y, uint8_t* argmax, int nchw, hipStream_t st) {
   PoolGeom g{N, C, H, W, P, Q, kh, kw, sh, sw, ph, pw};
   const long total = (long)N * C * P * Q;
+  const int vec = dt == BF16 ? 8 : 4;
+  const bool v = !nchw && C % vec == 0 && (uintptr_t)x % 16 == 0 && (uintptr_t)y % 16 == 0 &&
+                 (mode != 0 || (uintptr_t)argmax % vec == 0);
+  TraceScope ts(mode == 0 ? "pool_fwd_kernel<max>" : "pool_fwd_kernel<avg>", st,
+                (double)N * C * H * W * dt_size(dt) + (double)total * (dt_size(dt) + (mode == 0 ? 1 : 0)), WORK_BYTE);
+  if (v) {
+    const unsigned grid = grid_for((size_t)(total / vec));
+    if (dt == BF16)
+      hipLaunchKernelGGL((pool_fwd_nhwc_vec_kernel<bf16_t, 8>), dim3(grid), dim3(256), 0, st, g, mode,
+                         (const bf16_t*)x, (bf16_t*)y, argmax, total / vec);
+    else
+      hipLaunchKernelGGL((pool_fwd_nhwc_vec_kernel<float, 4>), dim3(grid), dim3(256), 0, st, g, mode,
+                         (const float*)x, (float*)y, argmax, total / vec);
+    return hipGetLastError();
+  }
   const unsigned grid = grid_for((size_t)total);
 #define POOL_FWD(T, L) \
   hipLaunchKernelGGL((pool_fwd_kernel<T, L>), dim3(grid), dim3(256), 0, st, g, mode, (const T*)x, (T*)y, argmax, total)
@@ -287,6 +436,21 @@ hipError_t launch_pool_bwd(int dt, int mode, int N, int C, int H, int W, int P, 
                            int ph, int pw, const void* dy, const uint8_t* argmax, void* dx, int nchw, hipStream_t st) {
   PoolGeom g{N, C, H, W, P, Q, kh, kw, sh, sw, ph, pw};
   const long total = (long)N * C * H * W;
+  const int vec = dt == BF16 ? 8 : 4;
+  const bool v = !nchw && C % vec == 0 && (uintptr_t)dy % 16 == 0 && (uintptr_t)dx % 16 == 0 &&
+                 (mode != 0 || (uintptr_t)argmax % vec == 0);
+  TraceScope ts(mode == 0 ? "pool_bwd_kernel<max>" : "pool_bwd_kernel<avg>", st,
+                (double)N * C * P * Q * (dt_size(dt) + (mode == 0 ? 1 : 0)) + (double)total * dt_size(dt), WORK_BYTE);
+  if (v) {
+    const unsigned grid = grid_for((size_t)(total / vec));
+    if (dt == BF16)
+      hipLaunchKernelGGL((pool_bwd_nhwc_vec_kernel<bf16_t, 8>), dim3(grid), dim3(256), 0, st, g, mode,
+                         (const bf16_t*)dy, argmax, (bf16_t*)dx, total / vec);
+    else
+      hipLaunchKernelGGL((pool_bwd_nhwc_vec_kernel<float, 4>), dim3(grid), dim3(256), 0, st, g, mode,
+                         (const float*)dy, argmax, (float*)dx, total / vec);
+    return hipGetLastError();
+  }
   const unsigned grid = grid_for((size_t)total);
 #define POOL_BWD(T, L) \
   hipLaunchKernelGGL((pool_bwd_kernel<T, L>), dim3(grid), dim3(256), 0, st, g, mode, (const T*)dy, argmax, (T*)dx, total)
@@ -302,6 +466,7 @@ hipError_t launch_pool_bwd(int dt, int mode, int N, int C, int H, int W, int P, 
 hipError_t launch_relu_fwd(int dt, size_t n, const void* x, void* y, hipStream_t st) {
   const size_t vec = dt == BF16 ? 8 : 4;
   const unsigned grid = grid_for(n / vec + 1, 256, 8192);
+  TraceScope ts("relu_fwd_kernel", st, 2.0 * n * dt_size(dt), WORK_BYTE);
   if (dt == BF16)
     hipLaunchKernelGGL(relu_fwd_kernel<bf16_t>, dim3(grid), dim3(256), 0, st, (const bf16_t*)x, (bf16_t*)y, n);
   else
@@ -312,6 +477,7 @@ hipError_t launch_relu_fwd(int dt, size_t n, const void* x, void* y, hipStream_t
 hipError_t launch_relu_bwd(int dt, size_t n, const void* y, const void* dy, void* dx, hipStream_t st) {
   const size_t vec = dt == BF16 ? 8 : 4;
   const unsigned grid = grid_for(n / vec + 1, 256, 8192);
+  TraceScope ts("relu_bwd_kernel", st, 3.0 * n * dt_size(dt), WORK_BYTE);
   if (dt == BF16)
     hipLaunchKernelGGL(relu_bwd_kernel<bf16_t>, dim3(grid), dim3(256), 0, st, (const bf16_t*)y, (const bf16_t*)dy,
                        (bf16_t*)dx, n);
@@ -323,18 +489,27 @@ hipError_t launch_relu_bwd(int dt, size_t n, const void* y, const void* dy, void
 
 hipError_t launch_softmax_ce(int dt, int B, int classes, const void* z, const int32_t* labels, float* loss, void* dz,
                              hipStream_t st) {
-  if (dt == BF16)
-    hipLaunchKernelGGL(softmax_ce_kernel<bf16_t>, dim3(1), dim3(64 * CE_WAVES), 0, st, B, classes, (const bf16_t*)z,
-                       labels, loss, (bf16_t*)dz);
-  else
-    hipLaunchKernelGGL(softmax_ce_kernel<float>, dim3(1), dim3(64 * CE_WAVES), 0, st, B, classes, (const float*)z,
-                       labels, loss, (float*)dz);
+  {
+    TraceScope ts("softmax_ce_rows_kernel", st, 2.0 * B * (double)classes * dt_size(dt) + 8.0 * B, WORK_BYTE);
+    const unsigned grid = (unsigned)((B + 3) / 4);
+    if (dt == BF16)
+      hipLaunchKernelGGL(softmax_ce_rows_kernel<bf16_t>, dim3(grid), dim3(256), 0, st, B, classes, (const bf16_t*)z,
+                         labels, loss, (bf16_t*)dz);
+    else
+      hipLaunchKernelGGL(softmax_ce_rows_kernel<float>, dim3(grid), dim3(256), 0, st, B, classes, (const float*)z,
+                         labels, loss, (float*)dz);
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  TraceScope ts("softmax_ce_mean_kernel", st, 4.0 * B + 4.0, WORK_BYTE);
+  hipLaunchKernelGGL(softmax_ce_mean_kernel, dim3(1), dim3(256), 0, st, B, loss);
   return hipGetLastError();
 }
 
 hipError_t launch_sgd(size_t n, float* w, const float* g, float* v, uint16_t* wb, float lr, float mom, float wd,
                       hipStream_t st) {
   const unsigned grid = grid_for(n / 4 + 1, 256, 8192);
+  TraceScope ts("sgd_kernel", st, (double)n * (20.0 + (wb ? 2.0 : 0.0)), WORK_BYTE);
   hipLaunchKernelGGL(sgd_kernel, dim3(grid), dim3(256), 0, st, n, w, g, v, wb, lr, mom, wd);
   return hipGetLastError();
 }

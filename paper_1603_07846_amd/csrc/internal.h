@@ -14,6 +14,22 @@ enum Dt { F32 = 0, BF16 = 1 };
 
 inline size_t dt_size(int dt) { return dt == BF16 ? 2 : 4; }
 
+// Per-kernel timing (trace.cpp): while the trace is enabled, a TraceScope
+// brackets one kernel launch with timing events on its stream and tags it with
+// the kernel's algorithmic work.
+enum { WORK_FLOP = 0, WORK_BYTE = 1 };
+class TraceScope {
+ public:
+  TraceScope(const char* name, hipStream_t st, double work, int unit);
+  ~TraceScope();
+  TraceScope(const TraceScope&) = delete;
+  TraceScope& operator=(const TraceScope&) = delete;
+
+ private:
+  hipStream_t st_;
+  long idx_;
+};
+
 // Geometry of one convolution: input N x H x W x C, K filters R x S x C,
 // output N x P x Q x K.
 struct ConvShape {
@@ -21,9 +37,10 @@ struct ConvShape {
 };
 
 // Implicit-GEMM forward convolution (also used for stride-1 backward-data over
-// a flipped filter copy): y = act(conv(x, w) + bias).
+// a flipped filter copy, bwd != 0): y = act(conv(x, w) + bias).  `flops` is
+// the algorithmic work of the layer pass this launch carries out.
 hipError_t launch_conv_fwd(int dt, const ConvShape& s, const void* x, const void* w, const float* bias,
-                           void* y, int relu, hipStream_t st);
+                           void* y, int relu, int bwd, double flops, hipStream_t st);
 
 // Split-K implicit-GEMM filter gradient.  Number of K-splits used for a shape
 // and the fp32 partial-sum buffer it needs.

@@ -144,7 +144,7 @@ class SoftmaxCELayer(Layer):
     def __init__(self, net, spec, in_shape):
         self.name = spec.name
         self.in_shape = tuple(in_shape)
-        self.loss = torch.empty((1,), dtype=torch.float32, device=net.device)
+        self.loss = torch.empty((in_shape[0] + 1,), dtype=torch.float32, device=net.device)  # mean, then rows
         self.dz = torch.empty(self.in_shape, dtype=net.dtype, device=net.device)
         self.labels = None
         self.out_shape = (1,)

@@ -31,7 +31,8 @@ OP_FWD, OP_BWD_DATA, OP_BWD_FILTER = 0, 1, 2
 # every exported symbol of the C ABI (checked by the CPU tests against the header)
 EXPORTS = ["singa_strerror", "singa_conv_out_shape", "singa_pool_out_shape", "singa_conv_workspace_bytes",
            "singa_conv_fwd", "singa_conv_bwd_data", "singa_conv_bwd_filter", "singa_pool_fwd", "singa_pool_bwd",
-           "singa_relu_fwd", "singa_relu_bwd", "singa_softmax_ce", "singa_sgd_momentum_update"]
+           "singa_relu_fwd", "singa_relu_bwd", "singa_softmax_ce", "singa_sgd_momentum_update",
+           "singa_trace_enable", "singa_trace_count", "singa_trace_get"]
 
 
 class Shape4(ctypes.Structure):
@@ -87,6 +88,10 @@ def _lib():
         lib.singa_softmax_ce.argtypes = [i32, i32, i32, vp, vp, vp, vp, vp]
         lib.singa_sgd_momentum_update.argtypes = [sz, vp, vp, vp, vp, ctypes.c_float, ctypes.c_float,
                                                   ctypes.c_float, vp]
+        lib.singa_trace_enable.argtypes = [i32]
+        lib.singa_trace_count.argtypes = []
+        lib.singa_trace_get.argtypes = [i32, ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(ctypes.c_double),
+                                        ctypes.POINTER(ctypes.c_double), ctypes.POINTER(i32)]
         for name in EXPORTS:
             if name != "singa_strerror":
                 getattr(lib, name).restype = i32
@@ -286,9 +291,10 @@ def relu_bwd(y, dy, out=None):
 
 
 def softmax_ce(z, labels, loss=None, dz=None):
-    """Softmax cross-entropy over rows of z (batch, classes); returns (loss[1] fp32 tensor, dz)."""
+    """Softmax cross-entropy over rows of z (batch, classes); returns (loss, dz) where
+    loss is an fp32 tensor of batch + 1 values: the mean, then each row's loss."""
     B, classes = z.shape[0], z[0].numel()
-    loss = torch.empty((1,), dtype=torch.float32, device=z.device) if loss is None else loss
+    loss = torch.empty((B + 1,), dtype=torch.float32, device=z.device) if loss is None else loss
     dz = torch.empty_like(z) if dz is None else dz
     _check("singa_softmax_ce", _lib().singa_softmax_ce(_dt(z), B, classes, _ptr(z), _ptr(labels), _ptr(loss),
                                                        _ptr(dz), _stream()))
@@ -301,6 +307,23 @@ def sgd_momentum_update(w, g, v, w_bf16=None, lr=0.01, momentum=0.9, weight_deca
         w.numel(), _ptr(w), _ptr(g), _ptr(v), _ptr(w_bf16), float(lr), float(momentum), float(weight_decay),
         _stream()))
     return w, v
+
+
+def trace_enable(on: bool = True):
+    """Start (clearing) or stop the library's per-kernel timing trace."""
+    _lib().singa_trace_enable(int(bool(on)))
+
+
+def trace_records():
+    """[(kernel name, ms, work, unit)] of the recorded launches; synchronize first."""
+    out = []
+    name, ms, work, unit = ctypes.c_char_p(), ctypes.c_double(), ctypes.c_double(), ctypes.c_int()
+    for i in range(_lib().singa_trace_count()):
+        rc = _lib().singa_trace_get(i, ctypes.byref(name), ctypes.byref(ms), ctypes.byref(work), ctypes.byref(unit))
+        if rc != 0:
+            raise RuntimeError("singa_trace_get(%d) failed: %d" % (i, rc))
+        out.append((name.value.decode(), ms.value, work.value, "flop" if unit.value == 0 else "byte"))
+    return out
 
 
 # Import-time load: the product path fails loudly when the HIP library is missing.

@@ -197,8 +197,11 @@ def test_softmax_ce(shape, dt):
     zd = torch.from_numpy(z).cuda().to(torch.bfloat16 if dt == "bf16" else torch.float32)
     loss, dz = singa.softmax_ce(zd, torch.from_numpy(lab).cuda())
     torch.cuda.synchronize()
-    assert abs(loss.item() - ref_loss) <= 1e-5 * max(1.0, abs(ref_loss))
+    assert abs(loss[0].item() - ref_loss) <= 1e-5 * max(1.0, abs(ref_loss))
     assert rel_l2(dz.float().cpu().numpy(), ref_dz) <= TOL[dt]
+    # per-row losses: the oracle's loss of each row as a batch of one
+    rows = np.array([oracle.softmax_ce(z[n:n + 1], lab[n:n + 1])[0] for n in range(B)])
+    assert rel_l2(loss[1:].cpu().numpy(), rows) <= 1e-5
 
 
 @pytest.mark.parametrize("n", [1, 5, 2400, 89578, 1 << 20])

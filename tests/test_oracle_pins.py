@@ -407,6 +407,19 @@ def test_softmax_ce_closed_forms_and_torch():
         assert abs(fd - dz[idx]) < 1e-8
 
 
+# ------------------------------------------------------ bf16 storage rounding
+
+def test_round_bf16_against_torch():
+    rng = _rng(81)
+    x = rng.standard_normal(200000) * np.exp(rng.uniform(-40, 40, 200000))
+    x[:6] = [0.0, -0.0, 1.0, -1.5, 1.0 + 2.0 ** -8, 1.0 + 3 * 2.0 ** -8]  # exact and tie cases
+    ref = torch.tensor(x).float().bfloat16().double().numpy()
+    np.testing.assert_array_equal(oracle.round_bf16(x), ref)
+    # ties go to even: 1 + 2^-8 is halfway between 1 and 1 + 2^-7
+    assert oracle.round_bf16(np.array([1.0 + 2.0 ** -8]))[0] == 1.0
+    assert oracle.round_bf16(np.array([1.0 + 3 * 2.0 ** -8]))[0] == 1.0 + 2.0 ** -6
+
+
 # --------------------------------------------------------------- SGD pins
 
 def test_sgd_momentum_closed_forms():
