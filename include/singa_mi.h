@@ -28,7 +28,11 @@
  *     patterns, uint16).  bf16 arithmetic accumulates in fp32 and rounds to
  *     nearest even when it stores bf16.  Parameter gradients, biases, master
  *     weights and momentum are always fp32.
- *   - Every device pointer must be 16-byte aligned (SINGA_ERR_ALIGN).
+ *   - Alignment (SINGA_ERR_ALIGN): tensor pointers must be aligned to their
+ *     element size; the ReLU and update calls need 16-byte alignment.  The
+ *     convolution and pooling kernels take 16-byte vector paths when the
+ *     pointers are 16-byte aligned and the channel count allows, and
+ *     element-wise paths otherwise (same results).
  *   - Calls are asynchronous on `stream` (a hipStream_t; NULL is the legacy
  *     null stream).  The library never synchronizes.  A kernel fault shows
  *     up at the caller's next synchronization.
@@ -53,7 +57,7 @@ extern "C" {
 #define SINGA_ERR_SHAPE (-2)       /* non-positive or inconsistent sizes, empty output */
 #define SINGA_ERR_UNSUPPORTED (-3) /* dtype/layout/parameter combination not provided */
 #define SINGA_ERR_WORKSPACE (-4)   /* workspace smaller than singa_conv_workspace_bytes() */
-#define SINGA_ERR_ALIGN (-5)       /* a device pointer is not 16-byte aligned */
+#define SINGA_ERR_ALIGN (-5)       /* a device pointer is misaligned (see below) */
 #define SINGA_ERR_HIP (-6)         /* the HIP runtime rejected a launch */
 
 typedef enum { SINGA_F32 = 0, SINGA_BF16 = 1 } singa_dtype;

@@ -20,9 +20,9 @@
  *
  * Parity status: every routine is pinned by the CPU tests (hand-worked
  * examples, brute-force operator matrices, adjoint identities, finite
- * differences, closed forms and library routines).  No routine is "parity
- * unpinned" except the avg-pool divisor on clipped ceil-mode edge windows,
- * where the paper says nothing and the reading follows Caffe's pooling.
+ * differences, closed forms and library routines).  The avg-pool divisor on
+ * clipped ceil-mode edge windows, where the paper says nothing, follows
+ * Caffe's pooling and is pinned by the same rule in torch's avg_pool2d.
  */
 #ifndef SINGA_ORACLE_H
 #define SINGA_ORACLE_H
