@@ -38,9 +38,9 @@ int conv_geometry(const singa_shape4* x, const singa_filter4* w, const singa_con
   if (hs < 0 || ws < 0) return SINGA_ERR_SHAPE;
   const long long P = hs / d->stride_h + 1, Q = ws / d->stride_w + 1;
   // every index the kernels form must fit a signed 32-bit integer
-  if (!fits_i32((long long)x->n * x->h * x->w * x->c) || !fits_i32((long long)x->n * P * Q * w->k) ||
-      !fits_i32((long long)w->k * w->r * w->s * w->c) || !fits_i32((long long)x->n * P * Q) ||
-      !fits_i32((long long)x->h * x->w * x->c * 2))
+  // every operand must stay below 2^31 bytes in fp32 (32-bit buffer offsets)
+  if (!fits_i32(4LL * x->n * x->h * x->w * x->c) || !fits_i32(4LL * x->n * P * Q * w->k) ||
+      !fits_i32(4LL * w->k * w->r * w->s * w->c))
     return SINGA_ERR_UNSUPPORTED;
   s->N = x->n; s->H = x->h; s->W = x->w; s->C = x->c;
   s->K = w->k; s->R = w->r; s->S = w->s;
@@ -65,6 +65,16 @@ bool bwd_data_fc(const ConvShape& s) {
 }
 bool bwd_data_gemm(const ConvShape& s) { return bwd_data_fc(s) || (s.sh == 1 && s.sw == 1); }
 
+// The forward convolution that carries out a GEMM-style backward-data:
+// dense FC geometry: dx[n][(r,s,c)] = sum_k dy[n][k] w[k][(r,s,c)], a 1x1
+//   "convolution" of dy (N x 1 x 1 x K) with wt[(r,s,c)][k];
+// unit stride: dx = conv(dy, wt) with wt[c][r'][s'][k] = w[k][R-1-r'][S-1-s'][c]
+//   and padding R-1-ph, S-1-pw.
+ConvShape bwd_data_inner(const ConvShape& s) {
+  if (bwd_data_fc(s)) return ConvShape{s.N, 1, 1, s.K, s.R * s.S * s.C, 1, 1, 1, 1, 0, 0, 1, 1};
+  return ConvShape{s.N, s.P, s.Q, s.K, s.C, s.R, s.S, s.H, s.W, s.R - 1 - s.ph, s.S - 1 - s.pw, 1, 1};
+}
+
 // Workspace carving: a list of sub-buffers, each 256-byte aligned.
 struct Carve {
   char* base;
@@ -77,32 +87,73 @@ struct Carve {
   }
 };
 
+// Forward convolutions whose channel count is not a multiple of the 16-byte
+// vector width (the first layer's 3 colour channels) run on zero-padded
+// copies of the input and the filter, so that every operand load is a 16-byte
+// vector; the extra zero taps cost at most 3x the multiply-adds of the layer
+// (8/3 for C = 3 in bf16).
+inline int padded_channels(const ConvShape& s, int dt) {
+  const int vec = dt == BF16 ? 8 : 4;
+  if (s.C % vec == 0) return 0;
+  const int cp = (s.C + vec - 1) / vec * vec;
+  return cp <= 3 * s.C ? cp : 0;
+}
+
 // One function computes both the size and the layout of every workspace, so
 // the two can never disagree.
-struct FwdWs { void *x, *w, *y; };
-struct BwdDataWs { void *dy, *w, *wt, *dx; };
+struct FwdWs { void *x, *w, *y, *xp, *wp; float* partial; };
+struct BwdDataWs { void *dy, *w, *wt, *dx; float* partial; };
 struct BwdFilterWs { void *x, *dy; float *dw, *partial, *colsum; };
 
 size_t carve_fwd(const ConvShape& s, int dt, int layout, void* ws, FwdWs* o) {
   Carve c(ws);
-  o->x = o->w = o->y = nullptr;
+  o->x = o->w = o->y = o->xp = o->wp = nullptr;
+  o->partial = nullptr;
   if (layout == SINGA_NCHW) {
     o->x = c.take(act_bytes(s, dt));
     o->w = c.take(filt_bytes(s, dt));
     o->y = c.take(out_bytes(s, dt));
   }
+  const int cp = padded_channels(s, dt);
+  ConvShape g = s;
+  if (cp) {
+    o->xp = c.take((size_t)s.N * s.H * s.W * cp * dt_size(dt));
+    o->wp = c.take((size_t)s.K * s.R * s.S * cp * dt_size(dt));
+    g.C = cp;
+  }
+  const size_t pb = fwd_partial_bytes(g, dt);
+  if (pb) o->partial = (float*)c.take(pb);
   return c.used;
+}
+
+// NHWC forward on (x, w): through zero-padded channel copies when the channel
+// count needs it.
+hipError_t conv_fwd_nhwc(int dt, const ConvShape& s, const void* x, const void* w, const float* bias, void* y,
+                         int relu, const FwdWs& o, hipStream_t st) {
+  const int cp = padded_channels(s, dt);
+  if (!cp) return launch_conv_fwd(dt, s, x, w, bias, y, relu, 0, conv_flops(s), o.partial, st);
+  hipError_t e = launch_pad_channels(dt, x, o.xp, (long)s.N * s.H * s.W, s.C, cp, st);
+  if (e == hipSuccess) e = launch_pad_channels(dt, w, o.wp, (long)s.K * s.R * s.S, s.C, cp, st);
+  ConvShape g = s;
+  g.C = cp;
+  if (e == hipSuccess) e = launch_conv_fwd(dt, g, o.xp, o.wp, bias, y, relu, 0, conv_flops(s), o.partial, st);
+  return e;
 }
 
 size_t carve_bwd_data(const ConvShape& s, int dt, int layout, void* ws, BwdDataWs* o) {
   Carve c(ws);
   o->dy = o->w = o->wt = o->dx = nullptr;
+  o->partial = nullptr;
   if (layout == SINGA_NCHW) {
     o->dy = c.take(out_bytes(s, dt));
     o->w = c.take(filt_bytes(s, dt));
     o->dx = c.take(act_bytes(s, dt));
   }
-  if (bwd_data_gemm(s)) o->wt = c.take(filt_bytes(s, dt));
+  if (bwd_data_gemm(s)) {
+    o->wt = c.take(filt_bytes(s, dt));
+    const size_t pb = fwd_partial_bytes(bwd_data_inner(s), dt);
+    if (pb) o->partial = (float*)c.take(pb);
+  }
   return c.used;
 }
 
@@ -115,7 +166,8 @@ size_t carve_bwd_filter(const ConvShape& s, int dt, int layout, void* ws, BwdFil
     o->dy = c.take(out_bytes(s, dt));
     o->dw = (float*)c.take((size_t)s.K * s.R * s.S * s.C * sizeof(float));
   }
-  o->partial = (float*)c.take(wgrad_partial_bytes(s));
+  if (wgrad_splits(s, dt) > 1) o->partial = (float*)c.take(wgrad_partial_bytes(s, dt));
+  else o->partial = nullptr;
   o->colsum = (float*)c.take(colsum_partial_bytes(s.N * s.P * s.Q, s.K));
   return c.used;
 }
@@ -211,11 +263,10 @@ int singa_conv_fwd(singa_dtype dtype, singa_layout layout, const singa_shape4* x
   if (need > 0 && (!ws || ws_bytes < need)) return SINGA_ERR_WORKSPACE;
   carve_fwd(s, dtype, layout, ws, &o);
   hipStream_t st = (hipStream_t)stream;
-  if (layout == SINGA_NHWC)
-    return hip_status(launch_conv_fwd(dtype, s, x_ptr, w_ptr, bias, y_ptr, fuse_relu, 0, conv_flops(s), st));
+  if (layout == SINGA_NHWC) return hip_status(conv_fwd_nhwc(dtype, s, x_ptr, w_ptr, bias, y_ptr, fuse_relu, o, st));
   hipError_t e = launch_nchw_to_nhwc(dtype, x_ptr, o.x, s.N, s.C, s.H, s.W, st);
   if (e == hipSuccess) e = kcrs_to_krsc(dtype, s, w_ptr, o.w, st);
-  if (e == hipSuccess) e = launch_conv_fwd(dtype, s, o.x, o.w, bias, o.y, fuse_relu, 0, conv_flops(s), st);
+  if (e == hipSuccess) e = conv_fwd_nhwc(dtype, s, o.x, o.w, bias, o.y, fuse_relu, o, st);
   if (e == hipSuccess) e = launch_nhwc_to_nchw(dtype, o.y, y_ptr, s.N, s.K, s.P, s.Q, st);
   return hip_status(e);
 }
@@ -249,19 +300,15 @@ int singa_conv_bwd_data(singa_dtype dtype, singa_layout layout, const singa_shap
   }
   const int RS = s.R * s.S;
   if (e == hipSuccess) {
-    if (bwd_data_fc(s)) {
-      // dx[n][(r,s,c)] = sum_k dy[n][k] w[k][(r,s,c)]: a 1x1 "convolution" of dy
-      // with the transposed filter wt[(r,s,c)][k].
-      const int J = RS * s.C;
-      e = launch_transpose(dtype, wk, o.wt, 1, s.K, J, 0, J, 0, s.K, 0, st);
-      ConvShape g{s.N, 1, 1, s.K, J, 1, 1, 1, 1, 0, 0, 1, 1};
-      if (e == hipSuccess) e = launch_conv_fwd(dtype, g, dy, o.wt, nullptr, dx, 0, 1, conv_flops(s), st);
-    } else if (s.sh == 1 && s.sw == 1) {
-      // unit stride: dx = conv(dy, flip(w)^T) with padding R-1-ph, S-1-pw, where
-      // wt[c][r'][s'][k] = w[k][R-1-r'][S-1-s'][c]
-      e = launch_transpose(dtype, wk, o.wt, RS, s.K, s.C, s.C, (long)RS * s.C, s.K, (long)RS * s.K, 1, st);
-      ConvShape g{s.N, s.P, s.Q, s.K, s.C, s.R, s.S, s.H, s.W, s.R - 1 - s.ph, s.S - 1 - s.pw, 1, 1};
-      if (e == hipSuccess) e = launch_conv_fwd(dtype, g, dy, o.wt, nullptr, dx, 0, 1, conv_flops(s), st);
+    if (bwd_data_gemm(s)) {
+      if (bwd_data_fc(s)) {
+        const int J = RS * s.C;  // wt[(r,s,c)][k] = w[k][(r,s,c)]
+        e = launch_transpose(dtype, wk, o.wt, 1, s.K, J, 0, J, 0, s.K, 0, st);
+      } else {  // wt[c][r'][s'][k] = w[k][R-1-r'][S-1-s'][c]
+        e = launch_transpose(dtype, wk, o.wt, RS, s.K, s.C, s.C, (long)RS * s.C, s.K, (long)RS * s.K, 1, st);
+      }
+      if (e == hipSuccess)
+        e = launch_conv_fwd(dtype, bwd_data_inner(s), dy, o.wt, nullptr, dx, 0, 1, conv_flops(s), o.partial, st);
     } else {
       e = launch_conv_bwd_data_direct(dtype, s, dy, wk, dx, st);
     }
@@ -297,15 +344,12 @@ int singa_conv_bwd_filter(singa_dtype dtype, singa_layout layout, const singa_sh
     dy = o.dy;
   }
   const size_t nw = (size_t)s.K * s.R * s.S * s.C;
-  if (e == hipSuccess) e = launch_conv_wgrad(dtype, s, xx, dy, o.partial, st);
-  if (e == hipSuccess) {
-    if (layout == SINGA_NHWC) {
-      e = launch_splitk_reduce(o.partial, wgrad_splits(s), nw, dw, accumulate, st);
-    } else {
-      e = launch_splitk_reduce(o.partial, wgrad_splits(s), nw, o.dw, 0, st);
-      if (e == hipSuccess) e = launch_krsc_to_kcrs_f32(o.dw, dw, s.K, s.C, s.R, s.S, accumulate, st);
-    }
-  }
+  const int splits = wgrad_splits(s, dtype);
+  float* target = layout == SINGA_NHWC ? dw : o.dw;  // KRSC result
+  const int acc = layout == SINGA_NHWC ? accumulate : 0;
+  if (e == hipSuccess) e = launch_conv_wgrad(dtype, s, xx, dy, o.partial, target, acc, st);
+  if (e == hipSuccess && splits > 1) e = launch_splitk_reduce(o.partial, splits, nw, target, acc, st);
+  if (e == hipSuccess && layout == SINGA_NCHW) e = launch_krsc_to_kcrs_f32(o.dw, dw, s.K, s.C, s.R, s.S, accumulate, st);
   if (e == hipSuccess && db) e = launch_colsum(dtype, dy, s.N * s.P * s.Q, s.K, o.colsum, db, accumulate, st);
   return hip_status(e);
 }

@@ -92,6 +92,38 @@ __device__ __forceinline__ void mma_tile(const char* As, const char* Bs, f32x16 
   }
 }
 
+// ------------------------------------------------------------ global loads
+//
+// Operands are read with raw buffer loads: a tap outside the input (padding,
+// ragged tails) gets the offset OOB, past the end of every tensor, and the
+// hardware returns zeros for it.  No branch, no select on the loaded data.
+constexpr uint32_t OOB = 0x80000000u;
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, 0x00020000);
+}
+__device__ __forceinline__ uint4 ld16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0));
+}
+__device__ __forceinline__ uint2 ld8(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(r, (int)off, 0, 0));
+}
+template <typename T> __device__ __forceinline__ T ld_elem(__amdgpu_buffer_rsrc_t r, uint32_t off);
+template <> __device__ __forceinline__ float ld_elem<float>(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, (int)off, 0, 0));
+}
+template <> __device__ __forceinline__ bf16_t ld_elem<bf16_t>(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return (bf16_t)__builtin_amdgcn_raw_buffer_load_b16(r, (int)off, 0, 0);
+}
+
+// Workgroups are dealt to the 8 XCDs round-robin; give each XCD a contiguous
+// run of tiles so neighbouring tiles (shared input rows, shared filters) meet
+// in the same L2.
+__device__ __forceinline__ int xcd_remap(int b, int G) {
+  const int q = G >> 3, r = G & 7, x = b & 7, l = b >> 3;
+  return x * q + min(x, r) + l;
+}
+
 // ------------------------------------------------------------------ forward
 
 struct FwdArgs {
@@ -99,12 +131,15 @@ struct FwdArgs {
   const void* w;
   const float* bias;
   void* y;
+  uint32_t x_bytes, w_bytes;
   int M, Nn, Kg;
   int H, W, C, S, P, Q;
   int sh, sw, ph, pw;
   FastDiv dPQ, dQ, dC, dS;
   int relu;
-  int tiles_n;
+  int tiles, tiles_n;
+  float* partial;  // split-K: fp32 partial tiles [split][M][Nn] instead of y
+  int kt_per_split;
 };
 
 // VA: A taps are loaded as 16-byte vectors (C % VEC == 0); otherwise element
@@ -114,88 +149,92 @@ template <typename T, bool VA, bool VB, bool BWD>
 __global__ __launch_bounds__(NT) void conv_fwd_kernel(FwdArgs a) {
   constexpr int VEC = KT<T>::VEC;
   constexpr int BK = KT<T>::BK;
+  constexpr uint32_t ES = sizeof(T);
   __shared__ __attribute__((aligned(16))) char smem[SMEM];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int tm = blockIdx.x / a.tiles_n, tn = blockIdx.x - tm * a.tiles_n;
+  const int L = xcd_remap(blockIdx.x, gridDim.x);
+  const int split = L / a.tiles, tile = L - split * a.tiles;
+  const int tm = tile / a.tiles_n, tn = tile - tm * a.tiles_n;
   const int m0 = tm * BM, n0 = tn * BN;
-  const T* __restrict__ xp = (const T*)a.x;
-  const T* __restrict__ wp = (const T*)a.w;
+  const __amdgpu_buffer_rsrc_t xr = make_rsrc(a.x, a.x_bytes);
+  const __amdgpu_buffer_rsrc_t wr = make_rsrc(a.w, a.w_bytes);
 
   // Each thread fills one 16-byte column (cv) of 4 rows (rl + 32 i) of each operand.
   const int cv = tid & 7, rl = tid >> 3;
-  int abase[4], ah0[4], aw0[4];
+  int apix[4], ah0[4], aw0[4];  // element offset of input pixel (n, h0, w0); window origin
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    int m = m0 + rl + 32 * i;
+    const int m = m0 + rl + 32 * i;
     if (m < a.M) {
-      int n = (int)fdiv((uint32_t)m, a.dPQ);
-      int pq = m - n * a.P * a.Q;
-      int p = (int)fdiv((uint32_t)pq, a.dQ);
-      int q = pq - p * a.Q;
-      abase[i] = n * a.H * a.W * a.C;
+      const int n = (int)fdiv((uint32_t)m, a.dPQ);
+      const int pq = m - n * a.P * a.Q;
+      const int p = (int)fdiv((uint32_t)pq, a.dQ);
+      const int q = pq - p * a.Q;
       ah0[i] = p * a.sh - a.ph;
       aw0[i] = q * a.sw - a.pw;
+      apix[i] = ((n * a.H + ah0[i]) * a.W + aw0[i]) * a.C;
     } else {
-      abase[i] = 0;
       ah0[i] = -(1 << 28);  // fails every bounds check
       aw0[i] = 0;
+      apix[i] = 0;
     }
   }
-  int brow[4];
+  int brow[4];  // element offset of the filter row, or -1
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    int n = n0 + rl + 32 * i;
-    brow[i] = n < a.Nn ? n : -1;
+    const int n = n0 + rl + 32 * i;
+    brow[i] = n < a.Nn ? n * a.Kg : -1;
   }
 
-  V16 ra[4], rb[4];
-  auto load_tile = [&](int k0) {
+  auto load_tile = [&](int k0, V16 (&ra)[4], V16 (&rb)[4]) {
     const int kk = k0 + cv * VEC;
     if constexpr (VA) {
       const bool kin = kk < a.Kg;
-      int rs = (int)fdiv((uint32_t)kk, a.dC);
-      int c = kk - rs * a.C;
-      int r = (int)fdiv((uint32_t)rs, a.dS);
-      int s = rs - r * a.S;
+      const int rs = (int)fdiv((uint32_t)kk, a.dC);
+      const int c = kk - rs * a.C;
+      const int r = (int)fdiv((uint32_t)rs, a.dS);
+      const int s = rs - r * a.S;
+      const int tap = (r * a.W + s) * a.C + c;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        int h = ah0[i] + r, w = aw0[i] + s;
-        bool ok = kin && (unsigned)h < (unsigned)a.H && (unsigned)w < (unsigned)a.W;
-        ra[i].u = ok ? *(const uint4*)(xp + abase[i] + (h * a.W + w) * a.C + c) : make_uint4(0, 0, 0, 0);
+        const int h = ah0[i] + r, w = aw0[i] + s;
+        const bool ok = kin && (unsigned)h < (unsigned)a.H && (unsigned)w < (unsigned)a.W;
+        ra[i].u = ld16(xr, ok ? (uint32_t)(apix[i] + tap) * ES : OOB);
       }
     } else {
 #pragma unroll
       for (int j = 0; j < VEC; ++j) {
-        int kj = kk + j;
+        const int kj = kk + j;
         const bool kin = kj < a.Kg;
-        int rs = (int)fdiv((uint32_t)kj, a.dC);
-        int c = kj - rs * a.C;
-        int r = (int)fdiv((uint32_t)rs, a.dS);
-        int s = rs - r * a.S;
+        const int rs = (int)fdiv((uint32_t)kj, a.dC);
+        const int c = kj - rs * a.C;
+        const int r = (int)fdiv((uint32_t)rs, a.dS);
+        const int s = rs - r * a.S;
+        const int tap = (r * a.W + s) * a.C + c;
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          int h = ah0[i] + r, w = aw0[i] + s;
-          bool ok = kin && (unsigned)h < (unsigned)a.H && (unsigned)w < (unsigned)a.W;
-          set_elem<T>(ra[i], j, ok ? xp[abase[i] + (h * a.W + w) * a.C + c] : zero_elem<T>());
+          const int h = ah0[i] + r, w = aw0[i] + s;
+          const bool ok = kin && (unsigned)h < (unsigned)a.H && (unsigned)w < (unsigned)a.W;
+          set_elem<T>(ra[i], j, ld_elem<T>(xr, ok ? (uint32_t)(apix[i] + tap) * ES : OOB));
         }
       }
     }
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       if constexpr (VB) {
-        bool ok = brow[i] >= 0 && kk < a.Kg;
-        rb[i].u = ok ? *(const uint4*)(wp + (size_t)brow[i] * a.Kg + kk) : make_uint4(0, 0, 0, 0);
+        const bool ok = brow[i] >= 0 && kk < a.Kg;
+        rb[i].u = ld16(wr, ok ? (uint32_t)(brow[i] + kk) * ES : OOB);
       } else {
 #pragma unroll
         for (int j = 0; j < VEC; ++j) {
-          bool ok = brow[i] >= 0 && kk + j < a.Kg;
-          set_elem<T>(rb[i], j, ok ? wp[(size_t)brow[i] * a.Kg + kk + j] : zero_elem<T>());
+          const bool ok = brow[i] >= 0 && kk + j < a.Kg;
+          set_elem<T>(rb[i], j, ld_elem<T>(wr, ok ? (uint32_t)(brow[i] + kk + j) * ES : OOB));
         }
       }
     }
   };
-  auto store_tile = [&](int stage) {
+  auto store_tile = [&](int stage, const V16 (&ra)[4], const V16 (&rb)[4]) {
     char* As = smem + stage * 2 * TILE;
     char* Bs = As + TILE;
 #pragma unroll
@@ -213,23 +252,50 @@ __global__ __launch_bounds__(NT) void conv_fwd_kernel(FwdArgs a) {
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
+  // Two LDS stages and two register sets: the global loads of tile k+2 are in
+  // flight while tile k is multiplied and tile k+1 goes from registers to LDS.
   const int wm = wave >> 1, wn = wave & 1;
-  const int nkt = (a.Kg + BK - 1) / BK;
-  load_tile(0);
-  store_tile(0);
+  const int nkt_all = (a.Kg + BK - 1) / BK;
+  const int kbase = split * a.kt_per_split * BK;                   // first tap of this split
+  const int nkt = min(a.kt_per_split, nkt_all - split * a.kt_per_split);  // K-tiles of this split (>= 1)
+  V16 a0[4], b0[4], a1[4], b1[4];
+  load_tile(kbase, a0, b0);
+  if (nkt > 1) load_tile(kbase + BK, a1, b1);
+  store_tile(0, a0, b0);
   __syncthreads();
-  for (int kt = 0; kt < nkt; ++kt) {
-    const bool more = kt + 1 < nkt;
-    if (more) load_tile((kt + 1) * BK);
-    const char* As = smem + (kt & 1) * 2 * TILE;
-    mma_tile<T>(As, As + TILE, acc, wm, wn, lane);
-    if (more) store_tile((kt + 1) & 1);
+  int kt = 0;
+  for (; kt + 1 < nkt; kt += 2) {  // tiles kt (stage 0) and kt + 1 (stage 1)
+    if (kt + 2 < nkt) load_tile(kbase + (kt + 2) * BK, a0, b0);
+    mma_tile<T>(smem, smem + TILE, acc, wm, wn, lane);
+    store_tile(1, a1, b1);
+    __syncthreads();
+    if (kt + 3 < nkt) load_tile(kbase + (kt + 3) * BK, a1, b1);
+    mma_tile<T>(smem + 2 * TILE, smem + 3 * TILE, acc, wm, wn, lane);
+    if (kt + 2 < nkt) store_tile(0, a0, b0);
     __syncthreads();
   }
+  if (kt < nkt) mma_tile<T>(smem, smem + TILE, acc, wm, wn, lane);  // odd count: last tile is in stage 0
 
   // Epilogue: lane holds column li of each 32x32 block, rows 8*(v/4) + 4*lh + v%4.
-  T* __restrict__ yp = (T*)a.y;
   const int li = lane & 31, lh = lane >> 5;
+  if (a.partial) {
+    float* __restrict__ out = a.partial + (size_t)split * a.M * a.Nn;
+#pragma unroll
+    for (int bn = 0; bn < 2; ++bn) {
+      const int col = n0 + wn * 64 + bn * 32 + li;
+      if (col >= a.Nn) continue;
+#pragma unroll
+      for (int bm = 0; bm < 2; ++bm) {
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int row = m0 + wm * 64 + bm * 32 + (v >> 2) * 8 + lh * 4 + (v & 3);
+          if (row < a.M) out[(size_t)row * a.Nn + col] = acc[bm][bn][v];
+        }
+      }
+    }
+    return;
+  }
+  T* __restrict__ yp = (T*)a.y;
 #pragma unroll
   for (int bn = 0; bn < 2; ++bn) {
     const int col = n0 + wn * 64 + bn * 32 + li;
@@ -251,141 +317,209 @@ __global__ __launch_bounds__(NT) void conv_fwd_kernel(FwdArgs a) {
 }
 
 // ----------------------------------------------------------- filter gradient
+//
+// dW[i][j] = sum_t dy[t][i] * x^[t][j], i = filter, j = tap (r, s, c),
+// t = output pixel of one image.  The order of the reduction is free: t runs
+// over (p, q) with the image n fastest, t = (p*Q + q)*N + n.  When N is a
+// multiple of the K-tile, all rows of a K-tile share one output pixel (p, q):
+// the bounds check of a tap is the same for every row and a row's address is
+// n times the image stride.  Both operand tiles sit in LDS exactly as loaded,
+// t-major rows of 128 consecutive filters / taps.  For bf16 the MFMA fragment
+// (8 consecutive t of one filter or tap) comes from ds_read_b64_tr_b16, which
+// hands each lane of a 16-lane group one column of the 4 rows the group
+// addresses; for fp32 (v_mfma_f32_32x32x2_f32) a lane needs a single value and
+// reads it directly.
+
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+
+template <typename T> struct WG;
+template <> struct WG<bf16_t> {
+  static constexpr int BK = 64;     // t per K-tile
+  static constexpr int PITCH = 320;  // 256 B row + 64 B: a tr-read group's 4 rows hit disjoint banks
+};
+template <> struct WG<float> {
+  static constexpr int BK = 32;
+  static constexpr int PITCH = 640;  // 512 B row + 128 B: the 2 rows of a fragment read hit disjoint banks
+};
+constexpr int WSMEM = 2 * 2 * 64 * 320;  // 2 stages x 2 operands (equal for both dtypes)
 
 struct WgradArgs {
   const void* x;
   const void* dy;
-  float* partial;  // [splits][M][Nn]
-  int M, Nn, T;    // M = K filters, Nn = R*S*C, T = N*P*Q
-  int H, W, C, S, P, Q;
+  float* out;  // partial tiles [splits][M][Nn], or dw itself when direct
+  uint32_t x_bytes, dy_bytes;
+  int M, Nn, T;  // M = K filters, Nn = R*S*C taps, T = N*P*Q
+  int N, H, W, C, S, P, Q;
   int sh, sw, ph, pw;
-  FastDiv dPQ, dQ, dC, dS;
-  int tiles_n, kt_per_split, nkt;
+  FastDiv dN, dQ, dC, dS;
+  int tiles, tiles_n, kt_per_split, nkt;
+  int direct, accumulate;
 };
 
-// Rows of the thread's (TR x 4) block: TR = VEC taps of t, 4 columns.
-// VA: dy columns loaded 4 at a time (M % 4 == 0); VB: x columns 4 at a time (C % 4 == 0).
-template <typename T, bool VA, bool VB>
+__device__ __forceinline__ v4i16 lds_tr16(const char* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) v4i16*)(__attribute__((address_space(3))) char*)p);
+}
+
+// One K-tile of t-major operand rows: acc[bm][bn] += A(rows) * B(cols)^T.
+template <typename T>
+__device__ __forceinline__ void mma_tile_tmajor(const char* As, const char* Bs, f32x16 (&acc)[2][2], int wm, int wn,
+                                                int lane) {
+  constexpr int BK = WG<T>::BK, PIT = WG<T>::PITCH;
+  if constexpr (sizeof(T) == 2) {
+    // lane l: column (l & 15) of a 16-column group, t rows 8*(l >> 5) + 0..7 of the 16-t step
+    const int g = lane >> 4, s = lane & 15;
+    const int row = 8 * (g >> 1) + (s >> 2);
+    const int colb = 2 * (16 * (g & 1) + 4 * (s & 3));  // byte offset within a 32-column block
+    const char* ab = As + row * PIT + 2 * (wm * 64) + colb;
+    const char* bb = Bs + row * PIT + 2 * (wn * 64) + colb;
+#pragma unroll
+    for (int kc = 0; kc < BK / 16; ++kc) {
+      bf16x8 af[2], bfr[2];
+#pragma unroll
+      for (int b = 0; b < 2; ++b) {
+        const v4i16 alo = lds_tr16(ab + kc * 16 * PIT + b * 64);
+        const v4i16 ahi = lds_tr16(ab + (kc * 16 + 4) * PIT + b * 64);
+        const v4i16 blo = lds_tr16(bb + kc * 16 * PIT + b * 64);
+        const v4i16 bhi = lds_tr16(bb + (kc * 16 + 4) * PIT + b * 64);
+        af[b] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(alo, ahi, 0, 1, 2, 3, 4, 5, 6, 7));
+        bfr[b] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(blo, bhi, 0, 1, 2, 3, 4, 5, 6, 7));
+      }
+      acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[0], bfr[0], acc[0][0], 0, 0, 0);
+      acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[0], bfr[1], acc[0][1], 0, 0, 0);
+      acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[1], bfr[0], acc[1][0], 0, 0, 0);
+      acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[1], bfr[1], acc[1][1], 0, 0, 0);
+    }
+  } else {
+    // lane l: column (l & 31) of a 32-column block, t row (l >> 5) of the 2-t step
+    const int li = lane & 31, lh = lane >> 5;
+    const char* ab = As + lh * PIT + 4 * (wm * 64 + li);
+    const char* bb = Bs + lh * PIT + 4 * (wn * 64 + li);
+#pragma unroll
+    for (int kc = 0; kc < BK / 2; ++kc) {
+      const float a0 = *(const float*)(ab + 2 * kc * PIT);
+      const float a1 = *(const float*)(ab + 2 * kc * PIT + 128);
+      const float b0 = *(const float*)(bb + 2 * kc * PIT);
+      const float b1 = *(const float*)(bb + 2 * kc * PIT + 128);
+      acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a0, b0, acc[0][0], 0, 0, 0);
+      acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a0, b1, acc[0][1], 0, 0, 0);
+      acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1, b0, acc[1][0], 0, 0, 0);
+      acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1, b1, acc[1][1], 0, 0, 0);
+    }
+  }
+}
+
+// VA: the 16-byte filter chunks of dy are whole vectors (M % VEC == 0); VB:
+// likewise the tap chunks of x (C % VEC == 0); otherwise element loads.
+// NFAST: N % BK == 0, so a K-tile's rows share one output pixel.
+template <typename T, bool VA, bool VB, bool NFAST>
 __global__ __launch_bounds__(NT) void conv_wgrad_kernel(WgradArgs a) {
-  constexpr int TR = KT<T>::VEC;  // t-rows per block = elements per 16-byte LDS write
-  constexpr int BK = KT<T>::BK;
-  __shared__ __attribute__((aligned(16))) char smem[SMEM];
+  constexpr int VEC = 16 / (int)sizeof(T);
+  constexpr int CH = 128 / VEC;  // 16-byte chunks per tile row
+  constexpr int RPP = NT / CH;   // rows covered by one pass of the 256 threads
+  constexpr int BK = WG<T>::BK;
+  constexpr int PIT = WG<T>::PITCH;
+  constexpr int OPB = BK * PIT;  // bytes of one operand tile
+  constexpr uint32_t ES = sizeof(T);
+  static_assert(BK == 4 * RPP, "four passes fill a K-tile");
+  static_assert(2 * 2 * OPB == WSMEM, "LDS budget");
+  __shared__ __attribute__((aligned(16))) char smem[WSMEM];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int tm = blockIdx.x / a.tiles_n, tn = blockIdx.x - tm * a.tiles_n;
+  const int L = xcd_remap(blockIdx.x, gridDim.x);
+  const int split = L / a.tiles, tile = L - split * a.tiles;
+  const int tm = tile / a.tiles_n, tn = tile - tm * a.tiles_n;
   const int m0 = tm * BM, n0 = tn * BN;
-  const int split = blockIdx.y;
   const int kt_begin = split * a.kt_per_split;
-  const int kt_end = min(a.nkt, kt_begin + a.kt_per_split);
-  const T* __restrict__ xp = (const T*)a.x;
-  const T* __restrict__ dyp = (const T*)a.dy;
+  const int nk = min(a.nkt, kt_begin + a.kt_per_split) - kt_begin;
+  const __amdgpu_buffer_rsrc_t xr = make_rsrc(a.x, a.x_bytes);
+  const __amdgpu_buffer_rsrc_t dyr = make_rsrc(a.dy, a.dy_bytes);
 
-  // thread -> (t-block tb, 4-column block cb); the same mapping serves A and B
-  const int tb = tid & 7, cb = tid >> 3;
-  const int i0 = m0 + cb * 4;  // first dy column (filter) of this thread
-  const int j0 = n0 + cb * 4;  // first tap column of this thread
-  // Taps of the four B columns (fixed for the whole reduction).
-  int br[4], bs[4], bc[4];
-  bool bok[4];
+  const int ch = tid % CH, r0 = tid / CH;  // this thread's chunk column and first row
+  const int i0 = m0 + ch * VEC;            // first filter of its dy chunk
+  const int j0 = n0 + ch * VEC;            // first tap of its x chunk
+  const int PQ = a.P * a.Q;
+  const int ystride = PQ * a.M;            // dy elements per image
+  const int xstride = a.H * a.W * a.C;     // x elements per image
+  // taps of the x chunk, fixed for the whole reduction
+  int br[VEC], bs[VEC], btap[VEC];
+  bool bok[VEC];
 #pragma unroll
-  for (int u = 0; u < 4; ++u) {
-    int j = j0 + u;
-    bok[u] = j < a.Nn;
-    int jj = bok[u] ? j : 0;
-    int rs = (int)fdiv((uint32_t)jj, a.dC);
-    bc[u] = jj - rs * a.C;
-    br[u] = (int)fdiv((uint32_t)rs, a.dS);
-    bs[u] = rs - br[u] * a.S;
+  for (int e = 0; e < VEC; ++e) {
+    const int j = j0 + e;
+    bok[e] = j < a.Nn;
+    const int jj = bok[e] ? j : 0;
+    const int rs = (int)fdiv((uint32_t)jj, a.dC);
+    const int c = jj - rs * a.C;
+    br[e] = (int)fdiv((uint32_t)rs, a.dS);
+    bs[e] = rs - br[e] * a.S;
+    btap[e] = (br[e] * a.W + bs[e]) * a.C + c;
+    if (VB) break;  // one chunk = one tap (r, s) and VEC consecutive channels
   }
 
-  V16 ra[4], rb[4];
-  auto load_tile = [&](int kt) {
-    const int t0 = kt * BK + tb * TR;
-    // decompose the first t of the block, then step along q
-    int n = (int)fdiv((uint32_t)t0, a.dPQ);
-    int pq = t0 - n * a.P * a.Q;
-    int p = (int)fdiv((uint32_t)pq, a.dQ);
-    int q = pq - p * a.Q;
-    T av[TR][4], bv[TR][4];
-#pragma unroll
-    for (int e = 0; e < TR; ++e) {
-      const int t = t0 + e;
-      const bool tin = t < a.T;
-      // A: dy[t][i0 .. i0+3]
-      if constexpr (VA) {
-        if (tin && i0 < a.M) {
-          const T* src = dyp + (size_t)t * a.M + i0;
-          if constexpr (sizeof(T) == 4) {
-            float4 v = *(const float4*)src;
-            av[e][0] = v.x; av[e][1] = v.y; av[e][2] = v.z; av[e][3] = v.w;
-          } else {
-            uint2 v = *(const uint2*)src;
-            av[e][0] = (bf16_t)(v.x & 0xffffu); av[e][1] = (bf16_t)(v.x >> 16);
-            av[e][2] = (bf16_t)(v.y & 0xffffu); av[e][3] = (bf16_t)(v.y >> 16);
-          }
-        } else {
-#pragma unroll
-          for (int u = 0; u < 4; ++u) av[e][u] = zero_elem<T>();
-        }
-      } else {
-#pragma unroll
-        for (int u = 0; u < 4; ++u)
-          av[e][u] = (tin && i0 + u < a.M) ? dyp[(size_t)t * a.M + i0 + u] : zero_elem<T>();
-      }
-      // B: x[n, p*sh-ph+r, q*sw-pw+s, c] for the four tap columns
-      const int hb = p * a.sh - a.ph, wb = q * a.sw - a.pw;
-      const int xbase = n * a.H * a.W * a.C;
-      if constexpr (VB) {
-        const int h = hb + br[0], w = wb + bs[0];
-        const bool ok = tin && bok[0] && (unsigned)h < (unsigned)a.H && (unsigned)w < (unsigned)a.W;
-        if (ok) {
-          const T* src = xp + xbase + (h * a.W + w) * a.C + bc[0];
-          if constexpr (sizeof(T) == 4) {
-            float4 v = *(const float4*)src;
-            bv[e][0] = v.x; bv[e][1] = v.y; bv[e][2] = v.z; bv[e][3] = v.w;
-          } else {
-            uint2 v = *(const uint2*)src;
-            bv[e][0] = (bf16_t)(v.x & 0xffffu); bv[e][1] = (bf16_t)(v.x >> 16);
-            bv[e][2] = (bf16_t)(v.y & 0xffffu); bv[e][3] = (bf16_t)(v.y >> 16);
-          }
-        } else {
-#pragma unroll
-          for (int u = 0; u < 4; ++u) bv[e][u] = zero_elem<T>();
-        }
-      } else {
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const int h = hb + br[u], w = wb + bs[u];
-          const bool ok = tin && bok[u] && (unsigned)h < (unsigned)a.H && (unsigned)w < (unsigned)a.W;
-          bv[e][u] = ok ? xp[xbase + (h * a.W + w) * a.C + bc[u]] : zero_elem<T>();
-        }
-      }
-      // step to the next output pixel
-      if (++q == a.Q) {
-        q = 0;
-        if (++p == a.P) {
-          p = 0;
-          ++n;
-        }
-      }
+  // Row d of the K-tile starting at t0: dy offset and x pixel (n, hb, wb).
+  auto load_tile = [&](int kt, V16 (&ra)[4], V16 (&rb)[4]) {
+    const int t0 = kt * BK;
+    int pq = 0, nb = 0, hb = 0, wb = 0;
+    if constexpr (NFAST) {
+      pq = (int)fdiv((uint32_t)t0, a.dN);
+      nb = t0 - pq * a.N;
+      const int p = (int)fdiv((uint32_t)pq, a.dQ);
+      hb = p * a.sh - a.ph;
+      wb = (pq - p * a.Q) * a.sw - a.pw;
     }
-    // transpose: LDS row = column u, 16 bytes = the TR t-values
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
+    for (int v = 0; v < 4; ++v) {
+      const int d = r0 + RPP * v;
+      int n, rpq, h0, w0;
+      bool tin;
+      if constexpr (NFAST) {
+        n = nb + d;
+        rpq = pq;
+        h0 = hb;
+        w0 = wb;
+        tin = true;  // T is a multiple of BK
+      } else {
+        const int t = t0 + d;
+        tin = t < a.T;
+        rpq = (int)fdiv((uint32_t)t, a.dN);
+        n = t - rpq * a.N;
+        const int p = (int)fdiv((uint32_t)rpq, a.dQ);
+        h0 = p * a.sh - a.ph;
+        w0 = (rpq - p * a.Q) * a.sw - a.pw;
+      }
+      // A: dy[n][p][q][i0 .. i0 + VEC)
+      const int aoff = n * ystride + rpq * a.M + i0;
+      if constexpr (VA) {
+        ra[v].u = ld16(dyr, (tin && i0 < a.M) ? (uint32_t)aoff * ES : OOB);
+      } else {
 #pragma unroll
-      for (int e = 0; e < TR; ++e) {
-        set_elem<T>(ra[u], e, av[e][u]);
-        set_elem<T>(rb[u], e, bv[e][u]);
+        for (int e = 0; e < VEC; ++e)
+          set_elem<T>(ra[v], e, ld_elem<T>(dyr, (tin && i0 + e < a.M) ? (uint32_t)(aoff + e) * ES : OOB));
+      }
+      // B: x[n][h0 + r][w0 + s][c .. c + VEC)
+      const int xpix = n * xstride + (h0 * a.W + w0) * a.C;
+      if constexpr (VB) {
+        const int h = h0 + br[0], w = w0 + bs[0];
+        const bool ok = tin && bok[0] && (unsigned)h < (unsigned)a.H && (unsigned)w < (unsigned)a.W;
+        rb[v].u = ld16(xr, ok ? (uint32_t)(xpix + btap[0]) * ES : OOB);
+      } else {
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) {
+          const int h = h0 + br[e], w = w0 + bs[e];
+          const bool ok = tin && bok[e] && (unsigned)h < (unsigned)a.H && (unsigned)w < (unsigned)a.W;
+          set_elem<T>(rb[v], e, ld_elem<T>(xr, ok ? (uint32_t)(xpix + btap[e]) * ES : OOB));
+        }
       }
     }
   };
-  auto store_tile = [&](int stage) {
-    char* As = smem + stage * 2 * TILE;
-    char* Bs = As + TILE;
+  auto store_tile = [&](int stage, const V16 (&ra)[4], const V16 (&rb)[4]) {
+    char* As = smem + stage * 2 * OPB;
+    char* Bs = As + OPB;
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      *(uint4*)(As + (cb * 4 + u) * PITCH + tb * 16) = ra[u].u;
-      *(uint4*)(Bs + (cb * 4 + u) * PITCH + tb * 16) = rb[u].u;
+    for (int v = 0; v < 4; ++v) {
+      *(uint4*)(As + (r0 + RPP * v) * PIT + ch * 16) = ra[v].u;
+      *(uint4*)(Bs + (r0 + RPP * v) * PIT + ch * 16) = rb[v].u;
     }
   };
 
@@ -398,21 +532,27 @@ __global__ __launch_bounds__(NT) void conv_wgrad_kernel(WgradArgs a) {
       for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
   const int wm = wave >> 1, wn = wave & 1;
-  if (kt_begin < kt_end) {
-    load_tile(kt_begin);
-    store_tile(0);
+  if (nk > 0) {
+    V16 a0[4], b0[4], a1[4], b1[4];
+    load_tile(kt_begin, a0, b0);
+    if (nk > 1) load_tile(kt_begin + 1, a1, b1);
+    store_tile(0, a0, b0);
     __syncthreads();
-    for (int kt = kt_begin; kt < kt_end; ++kt) {
-      const bool more = kt + 1 < kt_end;
-      if (more) load_tile(kt + 1);
-      const char* As = smem + ((kt - kt_begin) & 1) * 2 * TILE;
-      mma_tile<T>(As, As + TILE, acc, wm, wn, lane);
-      if (more) store_tile((kt + 1 - kt_begin) & 1);
+    int k = 0;
+    for (; k + 1 < nk; k += 2) {  // tiles k (stage 0) and k + 1 (stage 1)
+      if (k + 2 < nk) load_tile(kt_begin + k + 2, a0, b0);
+      mma_tile_tmajor<T>(smem, smem + OPB, acc, wm, wn, lane);
+      store_tile(1, a1, b1);
+      __syncthreads();
+      if (k + 3 < nk) load_tile(kt_begin + k + 3, a1, b1);
+      mma_tile_tmajor<T>(smem + 2 * OPB, smem + 3 * OPB, acc, wm, wn, lane);
+      if (k + 2 < nk) store_tile(0, a0, b0);
       __syncthreads();
     }
+    if (k < nk) mma_tile_tmajor<T>(smem, smem + OPB, acc, wm, wn, lane);  // odd count: last tile in stage 0
   }
 
-  float* __restrict__ out = a.partial + (size_t)split * a.M * a.Nn;
+  float* __restrict__ out = a.direct ? a.out : a.out + (size_t)split * a.M * a.Nn;
   const int li = lane & 31, lh = lane >> 5;
 #pragma unroll
   for (int bn = 0; bn < 2; ++bn) {
@@ -423,19 +563,48 @@ __global__ __launch_bounds__(NT) void conv_wgrad_kernel(WgradArgs a) {
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
         const int row = m0 + wm * 64 + bm * 32 + (v >> 2) * 8 + lh * 4 + (v & 3);
-        if (row < a.M) out[(size_t)row * a.Nn + col] = acc[bm][bn][v];
+        if (row < a.M) {
+          float* o = out + (size_t)row * a.Nn + col;
+          *o = (a.direct && a.accumulate) ? *o + acc[bm][bn][v] : acc[bm][bn][v];
+        }
       }
     }
   }
 }
 
+// dw[i] (+)= sum over splits of partial[split][i].  A block owns 64
+// consecutive elements; its 4 waves each sum every 4th split (coalesced 256 B
+// rows), then wave 0 adds the 4 partial sums in a fixed order, so the result
+// does not depend on timing.
 __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restrict__ partial, int splits,
                                                             size_t n, float* __restrict__ dw, int accumulate) {
+  __shared__ float part[4][64];
+  const int g = threadIdx.x >> 6, l = threadIdx.x & 63;
+  const size_t i = (size_t)blockIdx.x * 64 + l;
+  float t = 0.f;
+  if (i < n)
+    for (int k = g; k < splits; k += 4) t += partial[(size_t)k * n + i];
+  part[g][l] = t;
+  __syncthreads();
+  if (g == 0 && i < n) {
+    const float sum = (part[0][l] + part[1][l]) + (part[2][l] + part[3][l]);
+    dw[i] = accumulate ? dw[i] + sum : sum;
+  }
+}
+
+// Split-K forward: y[i] = act(sum over splits of partial[split][i] + bias[col]),
+// splits added in order.
+template <typename T>
+__global__ __launch_bounds__(256) void splitk_epilogue_kernel(const float* __restrict__ partial, int splits, int M,
+                                                              int Nn, const float* __restrict__ bias, int relu,
+                                                              T* __restrict__ y) {
+  const size_t n = (size_t)M * Nn;
   for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x) {
-    float s = accumulate ? dw[i] : 0.f;
     float t = 0.f;
     for (int k = 0; k < splits; ++k) t += partial[(size_t)k * n + i];
-    dw[i] = s + t;
+    if (bias) t += bias[i % Nn];
+    if (relu) t = fmaxf(t, 0.f);
+    store_out<T>(y + i, t);
   }
 }
 
@@ -467,6 +636,20 @@ void launch_fwd_instance(const FwdArgs& a, dim3 grid, double flops, hipStream_t 
   hipLaunchKernelGGL((conv_fwd_kernel<T, VA, VB, BWD>), grid, dim3(NT), 0, st, a);
 }
 
+// Reduction splits of a forward-style launch: split the taps when the output
+// tiles alone cannot give every CU two workgroups.
+int fwd_splits_for(long M, long Nn, long Kg, long bk) {
+  const long tiles = ((M + BM - 1) / BM) * ((Nn + BN - 1) / BN);
+  const long nkt = (Kg + bk - 1) / bk;
+  if (tiles >= 256 || nkt < 8) return 1;
+  long splits = (512 + tiles - 1) / tiles;
+  if (splits > nkt / 4) splits = nkt / 4;
+  if (splits > 16) splits = 16;
+  if (splits < 2) return 1;
+  const long per = (nkt + splits - 1) / splits;
+  return (int)((nkt + per - 1) / per);  // every split gets at least one K-tile
+}
+
 template <typename T, bool BWD>
 void launch_fwd_variant(bool va, bool vb, const FwdArgs& a, dim3 grid, double flops, hipStream_t st) {
   if (va && vb) launch_fwd_instance<T, true, true, BWD>(a, grid, flops, st);
@@ -477,10 +660,12 @@ void launch_fwd_variant(bool va, bool vb, const FwdArgs& a, dim3 grid, double fl
 
 template <typename T>
 hipError_t conv_fwd_dispatch(const ConvShape& s, const void* x, const void* w, const float* bias, void* y,
-                             int relu, int bwd, double flops, hipStream_t st) {
+                             int relu, int bwd, double flops, float* partial, hipStream_t st) {
   constexpr int VEC = KT<T>::VEC;
   FwdArgs a;
   a.x = x; a.w = w; a.bias = bias; a.y = y;
+  a.x_bytes = (uint32_t)((size_t)s.N * s.H * s.W * s.C * sizeof(T));
+  a.w_bytes = (uint32_t)((size_t)s.K * s.R * s.S * s.C * sizeof(T));
   a.M = s.N * s.P * s.Q;
   a.Nn = s.K;
   a.Kg = s.R * s.S * s.C;
@@ -493,101 +678,135 @@ hipError_t conv_fwd_dispatch(const ConvShape& s, const void* x, const void* w, c
   a.relu = relu;
   const int tiles_m = (a.M + BM - 1) / BM;
   a.tiles_n = (a.Nn + BN - 1) / BN;
-  dim3 grid(tiles_m * a.tiles_n);
+  a.tiles = tiles_m * a.tiles_n;
+  constexpr int BK = KT<T>::BK;
+  const int nkt = (a.Kg + BK - 1) / BK;
+  const int splits = partial ? fwd_splits_for(a.M, a.Nn, a.Kg, BK) : 1;
+  a.partial = splits > 1 ? partial : nullptr;
+  a.kt_per_split = (nkt + splits - 1) / splits;
+  dim3 grid(a.tiles * splits);
   const bool va = (s.C % VEC) == 0 && ((uintptr_t)x % 16) == 0;
   const bool vb = (a.Kg % VEC) == 0 && ((uintptr_t)w % 16) == 0;
   if (bwd)
     launch_fwd_variant<T, true>(va, vb, a, grid, flops, st);
   else
     launch_fwd_variant<T, false>(va, vb, a, grid, flops, st);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || splits == 1) return e;
+  const size_t n = (size_t)a.M * a.Nn;
+  size_t blocks = (n + 255) / 256;
+  if (blocks > 8192) blocks = 8192;
+  TraceScope ts("splitk_epilogue_kernel", st, (double)n * (4.0 * splits + sizeof(T)), WORK_BYTE);
+  hipLaunchKernelGGL(splitk_epilogue_kernel<T>, dim3((unsigned)blocks), dim3(256), 0, st, partial, splits, a.M,
+                     a.Nn, bias, relu, (T*)y);
   return hipGetLastError();
 }
 
-template <typename T, bool VA, bool VB> const char* wgrad_name() {
+template <typename T, bool VA, bool VB, bool NF> const char* wgrad_name() {
   static char buf[48];
   static bool init = false;
   if (!init) {
-    snprintf(buf, sizeof buf, "conv_wgrad_kernel<%s,%d,%d>", tname<T>(), (int)VA, (int)VB);
+    snprintf(buf, sizeof buf, "conv_wgrad_kernel<%s,%d,%d,%d>", tname<T>(), (int)VA, (int)VB, (int)NF);
     init = true;
   }
   return buf;
 }
 
-template <typename T, bool VA, bool VB>
+template <typename T, bool VA, bool VB, bool NF>
 void launch_wgrad_instance(const WgradArgs& a, dim3 grid, double flops, hipStream_t st) {
-  TraceScope ts(wgrad_name<T, VA, VB>(), st, flops, WORK_FLOP);
-  hipLaunchKernelGGL((conv_wgrad_kernel<T, VA, VB>), grid, dim3(NT), 0, st, a);
+  TraceScope ts(wgrad_name<T, VA, VB, NF>(), st, flops, WORK_FLOP);
+  hipLaunchKernelGGL((conv_wgrad_kernel<T, VA, VB, NF>), grid, dim3(NT), 0, st, a);
+}
+
+template <typename T, bool NF>
+void launch_wgrad_variant(bool va, bool vb, const WgradArgs& a, dim3 grid, double flops, hipStream_t st) {
+  if (va && vb) launch_wgrad_instance<T, true, true, NF>(a, grid, flops, st);
+  else if (va) launch_wgrad_instance<T, true, false, NF>(a, grid, flops, st);
+  else if (vb) launch_wgrad_instance<T, false, true, NF>(a, grid, flops, st);
+  else launch_wgrad_instance<T, false, false, NF>(a, grid, flops, st);
 }
 
 template <typename T>
-hipError_t conv_wgrad_dispatch(const ConvShape& s, const void* x, const void* dy, float* partial, hipStream_t st) {
+hipError_t conv_wgrad_dispatch(const ConvShape& s, const void* x, const void* dy, float* partial, float* dw,
+                               int accumulate, hipStream_t st) {
+  constexpr int VEC = 16 / (int)sizeof(T);
+  constexpr int BK = WG<T>::BK;
   WgradArgs a;
-  a.x = x; a.dy = dy; a.partial = partial;
+  a.x = x; a.dy = dy;
+  a.x_bytes = (uint32_t)((size_t)s.N * s.H * s.W * s.C * sizeof(T));
+  a.dy_bytes = (uint32_t)((size_t)s.N * s.P * s.Q * s.K * sizeof(T));
   a.M = s.K;
   a.Nn = s.R * s.S * s.C;
   a.T = s.N * s.P * s.Q;
-  a.H = s.H; a.W = s.W; a.C = s.C; a.S = s.S; a.P = s.P; a.Q = s.Q;
+  a.N = s.N; a.H = s.H; a.W = s.W; a.C = s.C; a.S = s.S; a.P = s.P; a.Q = s.Q;
   a.sh = s.sh; a.sw = s.sw; a.ph = s.ph; a.pw = s.pw;
-  a.dPQ = make_fastdiv((uint32_t)(s.P * s.Q));
+  a.dN = make_fastdiv((uint32_t)s.N);
   a.dQ = make_fastdiv((uint32_t)s.Q);
   a.dC = make_fastdiv((uint32_t)s.C);
   a.dS = make_fastdiv((uint32_t)s.S);
   const int tiles_m = (a.M + BM - 1) / BM;
   a.tiles_n = (a.Nn + BN - 1) / BN;
-  constexpr int BK = KT<T>::BK;
+  a.tiles = tiles_m * a.tiles_n;
   a.nkt = (a.T + BK - 1) / BK;
-  const int splits = wgrad_splits(s);
+  const int splits = wgrad_splits(s, sizeof(T) == 2 ? BF16 : F32);
   a.kt_per_split = (a.nkt + splits - 1) / splits;
-  dim3 grid(tiles_m * a.tiles_n, splits);
-  const bool va = (a.M % 4) == 0 && ((uintptr_t)dy % (4 * sizeof(T))) == 0;
-  const bool vb = (s.C % 4) == 0 && ((uintptr_t)x % (4 * sizeof(T))) == 0;
+  a.direct = splits == 1;
+  a.accumulate = accumulate;
+  a.out = a.direct ? dw : partial;
+  dim3 grid(a.tiles * splits);
+  const bool va = (a.M % VEC) == 0 && ((uintptr_t)dy % 16) == 0;
+  const bool vb = (s.C % VEC) == 0 && ((uintptr_t)x % 16) == 0;
   const double flops = 2.0 * a.M * (double)a.Nn * (double)a.T;
-  if (va && vb)
-    launch_wgrad_instance<T, true, true>(a, grid, flops, st);
-  else if (va)
-    launch_wgrad_instance<T, true, false>(a, grid, flops, st);
-  else if (vb)
-    launch_wgrad_instance<T, false, true>(a, grid, flops, st);
+  if (s.N % BK == 0)
+    launch_wgrad_variant<T, true>(va, vb, a, grid, flops, st);
   else
-    launch_wgrad_instance<T, false, false>(a, grid, flops, st);
+    launch_wgrad_variant<T, false>(va, vb, a, grid, flops, st);
   return hipGetLastError();
 }
 
 }  // namespace
 
 hipError_t launch_conv_fwd(int dt, const ConvShape& s, const void* x, const void* w, const float* bias, void* y,
-                           int relu, int bwd, double flops, hipStream_t st) {
-  if (dt == BF16) return conv_fwd_dispatch<bf16_t>(s, x, w, bias, y, relu, bwd, flops, st);
-  return conv_fwd_dispatch<float>(s, x, w, bias, y, relu, bwd, flops, st);
+                           int relu, int bwd, double flops, float* partial, hipStream_t st) {
+  if (dt == BF16) return conv_fwd_dispatch<bf16_t>(s, x, w, bias, y, relu, bwd, flops, partial, st);
+  return conv_fwd_dispatch<float>(s, x, w, bias, y, relu, bwd, flops, partial, st);
 }
 
-int wgrad_splits(const ConvShape& s) {
+size_t fwd_partial_bytes(const ConvShape& s, int dt) {
+  const long M = (long)s.N * s.P * s.Q, Nn = s.K, Kg = (long)s.R * s.S * s.C;
+  const int splits = fwd_splits_for(M, Nn, Kg, dt == BF16 ? KT<bf16_t>::BK : KT<float>::BK);
+  return splits > 1 ? (size_t)splits * M * Nn * sizeof(float) : 0;
+}
+
+int wgrad_splits(const ConvShape& s, int dt) {
   const long M = s.K, Nn = (long)s.R * s.S * s.C, T = (long)s.N * s.P * s.Q;
   const long tiles = ((M + BM - 1) / BM) * ((Nn + BN - 1) / BN);
-  const long nkt = (T + 31) / 32;  // fp32 K-tiles (bf16 tiles are twice as long)
+  const long bk = dt == BF16 ? WG<bf16_t>::BK : WG<float>::BK;
+  const long nkt = (T + bk - 1) / bk;
   // aim for about 4 workgroups per CU on 256 CUs, at least 8 K-tiles per split
   long splits = (1024 + tiles - 1) / tiles;
-  long max_by_len = nkt / 8;
+  const long max_by_len = nkt / 8;
   if (splits > max_by_len) splits = max_by_len;
   if (splits < 1) splits = 1;
   if (splits > 256) splits = 256;
-  return (int)splits;
+  // every split gets at least one K-tile
+  const long per = (nkt + splits - 1) / splits;
+  return (int)((nkt + per - 1) / per);
 }
 
-size_t wgrad_partial_bytes(const ConvShape& s) {
-  return (size_t)wgrad_splits(s) * s.K * s.R * s.S * s.C * sizeof(float);
+size_t wgrad_partial_bytes(const ConvShape& s, int dt) {
+  return (size_t)wgrad_splits(s, dt) * s.K * s.R * s.S * s.C * sizeof(float);
 }
 
-hipError_t launch_conv_wgrad(int dt, const ConvShape& s, const void* x, const void* dy, float* partial,
-                             hipStream_t st) {
-  if (dt == BF16) return conv_wgrad_dispatch<bf16_t>(s, x, dy, partial, st);
-  return conv_wgrad_dispatch<float>(s, x, dy, partial, st);
+hipError_t launch_conv_wgrad(int dt, const ConvShape& s, const void* x, const void* dy, float* partial, float* dw,
+                             int accumulate, hipStream_t st) {
+  if (dt == BF16) return conv_wgrad_dispatch<bf16_t>(s, x, dy, partial, dw, accumulate, st);
+  return conv_wgrad_dispatch<float>(s, x, dy, partial, dw, accumulate, st);
 }
 
 hipError_t launch_splitk_reduce(const float* partial, int splits, size_t n, float* dw, int accumulate,
                                 hipStream_t st) {
-  size_t blocks = (n + 255) / 256;
-  if (blocks > 4096) blocks = 4096;
+  const size_t blocks = (n + 63) / 64;
   TraceScope ts("splitk_reduce_kernel", st, (double)n * 4.0 * (splits + 1 + (accumulate ? 1 : 0)), WORK_BYTE);
   hipLaunchKernelGGL(splitk_reduce_kernel, dim3((unsigned)blocks), dim3(256), 0, st, partial, splits, n, dw,
                      accumulate);

@@ -1,7 +1,8 @@
 // internal.h -- launchers shared between the ABI layer and the kernel files.
 // Everything here works on NHWC activations and KRSC filters; the ABI layer
 // validates arguments before calling in, so launchers assume consistent
-// shapes, 16-byte aligned pointers and 32-bit-indexable tensors.
+// shapes, element-aligned pointers and tensors of fewer than 2^31 bytes (the
+// convolution kernels address operands with 32-bit buffer offsets).
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -38,16 +39,22 @@ struct ConvShape {
 
 // Implicit-GEMM forward convolution (also used for stride-1 backward-data over
 // a flipped filter copy, bwd != 0): y = act(conv(x, w) + bias).  `flops` is
-// the algorithmic work of the layer pass this launch carries out.
+// the algorithmic work of the layer pass this launch carries out.  When the
+// output tiles cannot fill the GPU and `partial` (fwd_partial_bytes() of
+// workspace) is given, the taps are split across workgroups and a second
+// kernel adds the fp32 partial tiles in a fixed order.
 hipError_t launch_conv_fwd(int dt, const ConvShape& s, const void* x, const void* w, const float* bias,
-                           void* y, int relu, int bwd, double flops, hipStream_t st);
+                           void* y, int relu, int bwd, double flops, float* partial, hipStream_t st);
+size_t fwd_partial_bytes(const ConvShape& s, int dt);
 
 // Split-K implicit-GEMM filter gradient.  Number of K-splits used for a shape
-// and the fp32 partial-sum buffer it needs.
-int wgrad_splits(const ConvShape& s);
-size_t wgrad_partial_bytes(const ConvShape& s);
-hipError_t launch_conv_wgrad(int dt, const ConvShape& s, const void* x, const void* dy, float* partial,
-                             hipStream_t st);
+// and the fp32 partial-sum buffer it needs.  With one split the kernel writes
+// (or, with accumulate, adds into) dw directly; otherwise it writes the
+// partial tiles and launch_splitk_reduce adds them into dw.
+int wgrad_splits(const ConvShape& s, int dt);
+size_t wgrad_partial_bytes(const ConvShape& s, int dt);
+hipError_t launch_conv_wgrad(int dt, const ConvShape& s, const void* x, const void* dy, float* partial, float* dw,
+                             int accumulate, hipStream_t st);
 // dw = (accumulate ? dw : 0) + sum over splits of partial, in split order.
 hipError_t launch_splitk_reduce(const float* partial, int splits, size_t n, float* dw, int accumulate,
                                 hipStream_t st);
@@ -68,6 +75,10 @@ hipError_t launch_transpose(int dt, const void* in, void* out, int batch, int ro
 // Direct (gather) backward-data for any stride: dx = conv^T(dy, w).
 hipError_t launch_conv_bwd_data_direct(int dt, const ConvShape& s, const void* dy, const void* w, void* dx,
                                        hipStream_t st);
+
+// Zero-pad the innermost (channel) dimension: in [rows][C] -> out [rows][Cp],
+// Cp a multiple of the 16-byte vector width.
+hipError_t launch_pad_channels(int dt, const void* in, void* out, long rows, int C, int Cp, hipStream_t st);
 
 // NCHW <-> NHWC permutations for the NCHW entry points.
 hipError_t launch_nchw_to_nhwc(int dt, const void* in, void* out, int N, int C, int H, int W, hipStream_t st);

@@ -40,6 +40,9 @@ CONV_CASES = [
     (7, 40, 1, 1, 20, 1, 1, 0, 1),       # 1x1 on 1x1 (FC)
     (1, 16, 6, 5, 12, 1, 1, 0, 1),       # 1x1, non-square
     (2, 12, 8, 8, 9, 3, 3, 2, 1),        # pad 2 with a 3x3 kernel
+    (4, 64, 4, 4, 200, 4, 4, 0, 1),      # FC, few rows, long reduction: split-K forward
+    (5, 256, 2, 2, 520, 2, 2, 0, 1),     # FC: split-K forward and split-K backward-data
+    (3, 5, 9, 9, 16, 3, 3, 1, 1),        # C=5: zero-padded channels in the forward pass
 ]
 
 
