@@ -12,9 +12,12 @@ Inputs are seeded synthetic tensors resident in HBM before timing starts.
 
 Timing follows the paper's protocol by default (Sec. 6.2.2: run 100
 iterations, average iterations 30-80): 30 warm-up steps, then 50 timed steps
-between two device synchronizations.  During the timed steps the library's
-kernel trace brackets every launch with HIP events on its own stream; the
-per-kernel figures (and the roofline of the dominant kernel) come from those.
+between two device synchronizations.  The timed steps are replays of a HIP
+graph holding one whole step (--eager launches them one by one instead; the
+eager rate is reported beside it).  Then the same number of steps runs
+eagerly with the library's kernel trace on, which brackets every launch with
+HIP events on the launch's own stream; the per-kernel figures (and the
+roofline of the dominant kernel) come from those.
 
 Prints one JSON line.
 """
@@ -39,6 +42,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=30)
     ap.add_argument("--workload", type=int, default=5, help="workload index (5 = AlexNet-shaped training step)")
+    ap.add_argument("--eager", action="store_true", help="time eager launches instead of graph replays")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-images", type=int, default=8, help="images in the oracle's timed sample")
     return ap.parse_args()
@@ -99,19 +103,36 @@ def main():
         net.train_one_batch(x, labels=labels, dy_top=dy)
     torch.cuda.synchronize()
 
-    singa.trace_enable(True)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
+    def timed(step):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            step()
+        torch.cuda.synchronize()
+        return (time.perf_counter() - t0) * 1e3 / args.steps
+
+    def eager_step():
         net.train_one_batch(x, labels=labels, dy_top=dy)
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
+
+    # timed region: K steps replayed from a HIP graph of one step (or eager)
+    if args.eager:
+        ms_per_step = timed(eager_step)
+        eager_ms = ms_per_step
+    else:
+        graph = net.capture(x, labels=labels, dy_top=dy)
+        for _ in range(3):
+            graph.replay()
+        ms_per_step = timed(graph.replay)
+        eager_ms = timed(eager_step)
+    loss = float(net.layers[-1].loss[0].item()) if w.classes else None
+    images_per_s = net.batch / (ms_per_step / 1e3)
+
+    # per-kernel pass: the same K steps launched eagerly, every launch
+    # bracketed by HIP events on its own stream
+    singa.trace_enable(True)
+    traced_ms = timed(eager_step)
     singa.trace_enable(False)
     recs = singa.trace_records()
-    loss = float(net.layers[-1].loss[0].item()) if w.classes else None
-
-    ms_per_step = (t1 - t0) * 1e3 / args.steps
-    images_per_s = net.batch / (ms_per_step / 1e3)
 
     # per-kernel aggregates over the timed steps
     agg = {}
@@ -178,6 +199,9 @@ def main():
         "conv_gflop_per_step": round(conv_flops / args.steps / 1e9, 2),
         "conv_ms_per_step": round(conv_ms / args.steps, 4),
         "kernel_ms_per_step": round(kernel_ms / args.steps, 4),
+        "launch": "eager" if args.eager else "hip_graph",
+        "eager_ms_per_step": round(eager_ms, 4),
+        "traced_eager_ms_per_step": round(traced_ms, 4),
         "loss": loss,
         "roofline": roof,
         "update": update,

@@ -272,6 +272,22 @@ class Net:
             self.update()
         return gx
 
+    def capture(self, x, labels=None, dy_top=None, need_input_grad=False) -> torch.cuda.CUDAGraph:
+        """Record one train_one_batch on (x, labels, dy_top) into a HIP graph.
+
+        A step launches some 75 kernels whose host-side launch cost is
+        comparable to the shorter ones; replaying the graph issues them all at
+        once.  Every buffer a step touches was allocated when the net was
+        built and the library allocates nothing and records no memset, so the
+        graph holds exactly the step's kernels.  Capturing runs nothing;
+        each ``replay()`` performs one full step (forward, backward, update)
+        on whatever the captured input, label and gradient tensors hold then.
+        """
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            self.train_one_batch(x, labels, dy_top, need_input_grad)
+        return g
+
     def layer(self, name: str) -> Layer:
         for l in self.layers:
             if l.name == name:

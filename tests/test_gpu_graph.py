@@ -1,0 +1,51 @@
+"""A training step replayed from a HIP graph against the same step run eagerly.
+
+Two nets start from the same parameters.  One runs train_one_batch eagerly,
+the other replays a graph captured from its own train_one_batch.  Between
+replays the program does eager work of its own (the eager net's step, a copy
+into the captured input, synchronizations), and after every replay the
+graph's loss, updated master weights, momentum and bf16 shadow must equal the
+eager net's bit for bit: both run the same kernels, whose reductions have a
+fixed order.  A fresh input is copied into the captured tensor before the
+third replay to show that a replay reads the tensor's current contents.
+"""
+import numpy as np
+import pytest
+import torch
+
+from paper_1603_07846_amd import workloads as wl
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.mark.parametrize("index,batch", [(2, 16), (5, 8)])
+def test_graph_replay_matches_eager(index, batch):
+    from paper_1603_07846_amd import net as gnet
+    w = wl.WORKLOADS[index]
+    inp = wl.make_inputs(w, batch=batch, seed_offset=31)
+    inp2 = wl.make_inputs(w, batch=batch, seed_offset=32)
+    eager = gnet.Net(w, batch=batch, device="cuda:0")
+    graphed = gnet.Net(w, batch=batch, device="cuda:0")
+    for n in (eager, graphed):
+        n.load_params(inp.params)
+    xe = eager.to_device_input(inp.x)
+    xg = graphed.to_device_input(inp.x)
+    lab = torch.from_numpy(inp.labels).cuda()
+    torch.cuda.synchronize()
+    g = graphed.capture(xg, labels=lab)
+    torch.cuda.synchronize()
+    for step in range(4):
+        if step == 2:
+            fresh = eager.to_device_input(inp2.x)
+            xe.copy_(fresh)
+            xg.copy_(fresh)
+        eager.train_one_batch(xe, labels=lab)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(graphed.layers[-1].loss, eager.layers[-1].loss), step
+        assert torch.equal(graphed.w_flat, eager.w_flat), step
+        assert torch.equal(graphed.v_flat, eager.v_flat), step
+        if eager.wb_flat is not None:
+            assert torch.equal(graphed.wb_flat, eager.wb_flat), step
+        assert np.isfinite(float(eager.layers[-1].loss[0]))
