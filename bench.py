@@ -32,8 +32,9 @@ sys.path.insert(0, ROOT)
 
 PEAK = {"bf16_tflops": 2516.6, "f32_tflops": 157.3, "hbm_gbs": 8000.0}
 METRIC = "conv fwd+bwd TFLOP/s (% MFMA peak) and training images/sec, 1×MI355X"
-CONV_KERNELS = ("conv_fwd_kernel", "conv_wgrad_kernel", "bwd_data_direct_kernel")
-CONV_HELPERS = ("transpose_kernel", "splitk_reduce_kernel", "colsum_partial_kernel", "colsum_final_kernel")
+CONV_KERNELS = ("conv_fwd_kernel", "conv_fwd_large_kernel", "conv_wgrad_kernel", "bwd_data_direct_kernel")
+CONV_HELPERS = ("transpose_kernel", "splitk_reduce_kernel", "splitk_epilogue_kernel", "colsum_partial_kernel",
+                "colsum_final_kernel", "pad_channels_kernel", "unpad_channels_f32_kernel")
 
 
 def parse():

@@ -87,23 +87,24 @@ struct Carve {
   }
 };
 
-// Forward convolutions whose channel count is not a multiple of the 16-byte
-// vector width (the first layer's 3 colour channels) run on zero-padded
-// copies of the input and the filter, so that every operand load is a 16-byte
-// vector; the extra zero taps cost at most 3x the multiply-adds of the layer
-// (8/3 for C = 3 in bf16).
+// Convolutions whose channel count is not a multiple of 4 (the first layer's
+// 3 colour channels) run their forward and filter-gradient passes on copies of
+// the input (and, forward, the filter) zero-padded to a multiple of 4
+// channels, so that every tap load is a vector: 16 bytes for fp32, two 8-byte
+// halves for bf16 (16-byte loads need 8 bf16 channels).  The padded taps are
+// zeros: 4/3 of the layer's multiply-adds for C = 3.
 inline int padded_channels(const ConvShape& s, int dt) {
-  const int vec = dt == BF16 ? 8 : 4;
-  if (s.C % vec == 0) return 0;
-  const int cp = (s.C + vec - 1) / vec * vec;
-  return cp <= 3 * s.C ? cp : 0;
+  (void)dt;
+  if (s.C % 4 == 0) return 0;
+  const int cp = (s.C + 3) / 4 * 4;
+  return cp <= 2 * s.C ? cp : 0;
 }
 
 // One function computes both the size and the layout of every workspace, so
 // the two can never disagree.
 struct FwdWs { void *x, *w, *y, *xp, *wp; float* partial; };
 struct BwdDataWs { void *dy, *w, *wt, *dx; float* partial; };
-struct BwdFilterWs { void *x, *dy; float *dw, *partial, *colsum; };
+struct BwdFilterWs { void *x, *dy, *xp; float *dw, *dwp, *partial, *colsum; };
 
 size_t carve_fwd(const ConvShape& s, int dt, int layout, void* ws, FwdWs* o) {
   Carve c(ws);
@@ -159,14 +160,21 @@ size_t carve_bwd_data(const ConvShape& s, int dt, int layout, void* ws, BwdDataW
 
 size_t carve_bwd_filter(const ConvShape& s, int dt, int layout, void* ws, BwdFilterWs* o) {
   Carve c(ws);
-  o->x = o->dy = nullptr;
-  o->dw = nullptr;
+  o->x = o->dy = o->xp = nullptr;
+  o->dw = o->dwp = nullptr;
   if (layout == SINGA_NCHW) {
     o->x = c.take(act_bytes(s, dt));
     o->dy = c.take(out_bytes(s, dt));
     o->dw = (float*)c.take((size_t)s.K * s.R * s.S * s.C * sizeof(float));
   }
-  if (wgrad_splits(s, dt) > 1) o->partial = (float*)c.take(wgrad_partial_bytes(s, dt));
+  const int cp = padded_channels(s, dt);
+  ConvShape g = s;
+  if (cp) {
+    g.C = cp;
+    o->xp = c.take((size_t)s.N * s.H * s.W * cp * dt_size(dt));
+    o->dwp = (float*)c.take((size_t)s.K * s.R * s.S * cp * sizeof(float));
+  }
+  if (wgrad_splits(g, dt) > 1) o->partial = (float*)c.take(wgrad_partial_bytes(g, dt));
   else o->partial = nullptr;
   o->colsum = (float*)c.take(colsum_partial_bytes(s.N * s.P * s.Q, s.K));
   return c.used;
@@ -343,12 +351,23 @@ int singa_conv_bwd_filter(singa_dtype dtype, singa_layout layout, const singa_sh
     xx = o.x;
     dy = o.dy;
   }
-  const size_t nw = (size_t)s.K * s.R * s.S * s.C;
-  const int splits = wgrad_splits(s, dtype);
-  float* target = layout == SINGA_NHWC ? dw : o.dw;  // KRSC result
+  // g: the GEMM's geometry (channels zero-padded when padded_channels says so)
+  const int cp = padded_channels(s, dtype);
+  ConvShape g = s;
+  if (cp) {
+    g.C = cp;
+    if (e == hipSuccess) e = launch_pad_channels(dtype, xx, o.xp, (long)s.N * s.H * s.W, s.C, cp, st);
+    xx = o.xp;
+  }
+  const size_t nw = (size_t)g.K * g.R * g.S * g.C;
+  const int splits = wgrad_splits(g, dtype);
+  float* krsc = layout == SINGA_NHWC ? dw : o.dw;  // KRSC result
   const int acc = layout == SINGA_NHWC ? accumulate : 0;
-  if (e == hipSuccess) e = launch_conv_wgrad(dtype, s, xx, dy, o.partial, target, acc, st);
-  if (e == hipSuccess && splits > 1) e = launch_splitk_reduce(o.partial, splits, nw, target, acc, st);
+  float* target = cp ? o.dwp : krsc;  // the GEMM's (K, R, S, g.C) result
+  const int tacc = cp ? 0 : acc;
+  if (e == hipSuccess) e = launch_conv_wgrad(dtype, g, xx, dy, o.partial, target, tacc, st);
+  if (e == hipSuccess && splits > 1) e = launch_splitk_reduce(o.partial, splits, nw, target, tacc, st);
+  if (e == hipSuccess && cp) e = launch_unpad_channels_f32(o.dwp, krsc, (long)s.K * s.R * s.S, cp, s.C, acc, st);
   if (e == hipSuccess && layout == SINGA_NCHW) e = launch_krsc_to_kcrs_f32(o.dw, dw, s.K, s.C, s.R, s.S, accumulate, st);
   if (e == hipSuccess && db) e = launch_colsum(dtype, dy, s.N * s.P * s.Q, s.K, o.colsum, db, accumulate, st);
   return hip_status(e);

@@ -4,6 +4,8 @@
 //   * direct gather backward-data for strides above one,
 //   * bias-gradient column sums in a fixed order,
 //   * NCHW <-> NHWC permutations for the NCHW entry points.
+#include <type_traits>
+
 #include "common.h"
 #include "internal.h"
 
@@ -205,19 +207,35 @@ __global__ __launch_bounds__(256) void krsc_to_kcrs_kernel(const float* __restri
 
 // out[r][c] = c < C ? in[r][c] : 0 for c < Cp: one thread per 16-byte output
 // vector (Cp is a multiple of the vector width).
+// out[r][c] = in[r][c] for c < C, 0 for C <= c < Cp (Cp % 4 == 0): one
+// thread per 4-channel chunk of an output row, stored as one vector.
 template <typename T>
 __global__ __launch_bounds__(256) void pad_channels_kernel(const T* __restrict__ in, T* __restrict__ out, long rows,
                                                            int C, int Cp) {
-  constexpr int VEC = 16 / sizeof(T);
-  const int nv = Cp / VEC;
+  typedef typename std::conditional<sizeof(T) == 2, uint2, uint4>::type V4;
+  const int nv = Cp / 4;
   const long total = rows * nv;
   for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += (long)gridDim.x * blockDim.x) {
     const long r = i / nv;
-    const int c0 = (int)(i - r * nv) * VEC;
-    union { uint4 u; T e[VEC]; } v;
+    const int c0 = (int)(i - r * nv) * 4;
+    union { V4 u; T e[4]; } v;
 #pragma unroll
-    for (int j = 0; j < VEC; ++j) v.e[j] = (c0 + j < C) ? in[r * C + c0 + j] : (T)0;
-    *(uint4*)(out + r * Cp + c0) = v.u;
+    for (int j = 0; j < 4; ++j) v.e[j] = (c0 + j < C) ? in[r * C + c0 + j] : (T)0;
+    *(V4*)(out + r * Cp + c0) = v.u;
+  }
+}
+
+// out[r][c] (+)= in[r][c] for c < C: drops the zero-padded channels of an
+// fp32 filter gradient computed on a channel-padded input.
+__global__ __launch_bounds__(256) void unpad_channels_f32_kernel(const float* __restrict__ in,
+                                                                 float* __restrict__ out, long rows, int Cp, int C,
+                                                                 int accumulate) {
+  const long total = rows * C;
+  for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += (long)gridDim.x * blockDim.x) {
+    const long r = i / C;
+    const int c = (int)(i - r * C);
+    const float v = in[r * Cp + c];
+    out[i] = accumulate ? out[i] + v : v;
   }
 }
 
@@ -299,8 +317,8 @@ hipError_t launch_colsum(int dt, const void* a, int rows, int cols, float* parti
 }
 
 hipError_t launch_pad_channels(int dt, const void* in, void* out, long rows, int C, int Cp, hipStream_t st) {
-  const int vec = dt == BF16 ? 8 : 4;
-  const long total = rows * (Cp / vec);
+  if (Cp % 4 != 0 || C > Cp) return hipErrorInvalidValue;
+  const long total = rows * (Cp / 4);
   TraceScope ts("pad_channels_kernel", st, (double)rows * (C + Cp) * dt_size(dt), WORK_BYTE);
   if (dt == BF16)
     hipLaunchKernelGGL(pad_channels_kernel<bf16_t>, dim3(grid_for(total)), dim3(256), 0, st, (const bf16_t*)in,
@@ -308,6 +326,15 @@ hipError_t launch_pad_channels(int dt, const void* in, void* out, long rows, int
   else
     hipLaunchKernelGGL(pad_channels_kernel<float>, dim3(grid_for(total)), dim3(256), 0, st, (const float*)in,
                        (float*)out, rows, C, Cp);
+  return hipGetLastError();
+}
+
+hipError_t launch_unpad_channels_f32(const float* in, float* out, long rows, int Cp, int C, int accumulate,
+                                     hipStream_t st) {
+  const long total = rows * C;
+  TraceScope ts("unpad_channels_f32_kernel", st, (double)rows * (C * (accumulate ? 12.0 : 8.0)), WORK_BYTE);
+  hipLaunchKernelGGL(unpad_channels_f32_kernel, dim3(grid_for(total)), dim3(256), 0, st, in, out, rows, Cp, C,
+                     accumulate);
   return hipGetLastError();
 }
 

@@ -142,10 +142,16 @@ struct FwdArgs {
   int kt_per_split;
 };
 
-// VA: A taps are loaded as 16-byte vectors (C % VEC == 0); otherwise element
-// by element.  VB: likewise for the filter rows (Kg % VEC == 0).  BWD only
-// names the instance that serves backward-data, so profiles tell them apart.
-template <typename T, bool VA, bool VB, bool BWD>
+// Operand load modes.  VEC16: 16-byte vectors of VEC taps (C % VEC == 0 for
+// the input, Kg % VEC == 0 for the filter rows).  VEC8 (bf16 only): two 8-byte
+// halves of 4 taps each, for channel counts that are a multiple of 4 but not
+// of 8 (the first layer's colour channels padded to 4).  ELEM: one element at
+// a time.
+constexpr int ELEM = 0, VEC8 = 1, VEC16 = 2;
+
+// AM / BMD: load mode of the input taps / filter rows.  BWD only names the
+// instance that serves backward-data, so profiles tell them apart.
+template <typename T, int AM, int BMD, bool BWD>
 __global__ __launch_bounds__(NT) void conv_fwd_kernel(FwdArgs a) {
   constexpr int VEC = KT<T>::VEC;
   constexpr int BK = KT<T>::BK;
@@ -189,7 +195,7 @@ __global__ __launch_bounds__(NT) void conv_fwd_kernel(FwdArgs a) {
 
   auto load_tile = [&](int k0, V16 (&ra)[4], V16 (&rb)[4]) {
     const int kk = k0 + cv * VEC;
-    if constexpr (VA) {
+    if constexpr (AM == VEC16) {
       const bool kin = kk < a.Kg;
       const int rs = (int)fdiv((uint32_t)kk, a.dC);
       const int c = kk - rs * a.C;
@@ -201,6 +207,28 @@ __global__ __launch_bounds__(NT) void conv_fwd_kernel(FwdArgs a) {
         const int h = ah0[i] + r, w = aw0[i] + s;
         const bool ok = kin && (unsigned)h < (unsigned)a.H && (unsigned)w < (unsigned)a.W;
         ra[i].u = ld16(xr, ok ? (uint32_t)(apix[i] + tap) * ES : OOB);
+      }
+    } else if constexpr (AM == VEC8) {
+      // taps kk..kk+3 at (r0, s0, c0..c0+3), kk+4..kk+7 at (r1, s1, c1..c1+3)
+      const int rs0 = (int)fdiv((uint32_t)kk, a.dC);
+      const int c0 = kk - rs0 * a.C;
+      const int r0 = (int)fdiv((uint32_t)rs0, a.dS);
+      const int s0 = rs0 - r0 * a.S;
+      const bool wrap = c0 + 4 >= a.C;
+      const int c1 = wrap ? c0 + 4 - a.C : c0 + 4;
+      const bool snext = wrap && s0 + 1 == a.S;
+      const int s1 = wrap ? (snext ? 0 : s0 + 1) : s0;
+      const int r1 = snext ? r0 + 1 : r0;
+      const int tap0 = (r0 * a.W + s0) * a.C + c0, tap1 = (r1 * a.W + s1) * a.C + c1;
+      const bool kin0 = kk < a.Kg, kin1 = kk + 4 < a.Kg;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int h0 = ah0[i] + r0, w0 = aw0[i] + s0, h1 = ah0[i] + r1, w1 = aw0[i] + s1;
+        const bool ok0 = kin0 & ((unsigned)h0 < (unsigned)a.H) & ((unsigned)w0 < (unsigned)a.W);
+        const bool ok1 = kin1 & ((unsigned)h1 < (unsigned)a.H) & ((unsigned)w1 < (unsigned)a.W);
+        const uint2 lo = ld8(xr, ok0 ? (uint32_t)(apix[i] + tap0) * ES : OOB);
+        const uint2 hi = ld8(xr, ok1 ? (uint32_t)(apix[i] + tap1) * ES : OOB);
+        ra[i].u = make_uint4(lo.x, lo.y, hi.x, hi.y);
       }
     } else {
 #pragma unroll
@@ -222,9 +250,14 @@ __global__ __launch_bounds__(NT) void conv_fwd_kernel(FwdArgs a) {
     }
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      if constexpr (VB) {
+      if constexpr (BMD == VEC16) {
         const bool ok = brow[i] >= 0 && kk < a.Kg;
         rb[i].u = ld16(wr, ok ? (uint32_t)(brow[i] + kk) * ES : OOB);
+      } else if constexpr (BMD == VEC8) {
+        const bool ok0 = (brow[i] >= 0) & (kk < a.Kg), ok1 = (brow[i] >= 0) & (kk + 4 < a.Kg);
+        const uint2 lo = ld8(wr, ok0 ? (uint32_t)(brow[i] + kk) * ES : OOB);
+        const uint2 hi = ld8(wr, ok1 ? (uint32_t)(brow[i] + kk + 4) * ES : OOB);
+        rb[i].u = make_uint4(lo.x, lo.y, hi.x, hi.y);
       } else {
 #pragma unroll
         for (int j = 0; j < VEC; ++j) {
@@ -313,6 +346,234 @@ __global__ __launch_bounds__(NT) void conv_fwd_kernel(FwdArgs a) {
         }
       }
     }
+  }
+}
+
+// ------------------------------------------------- forward, large bf16 tiles
+//
+// The same implicit GEMM for bf16 operands whose taps and filter rows are
+// whole 16-byte vectors (C % 8 == 0), with a 256 x 128 output tile: each of
+// the 4 waves owns a 128 x 64 quadrant (4 x 2 blocks of 32 x 32), so one
+// 16-byte fragment read feeds more MFMAs than in the 128 x 128 kernel.
+// Global data goes straight from the buffer loads into LDS (each load
+// instruction writes 64 consecutive 16-byte slots, i.e. 8 rows of 128 bytes),
+// with no register staging.  Three LDS stages: the loads of K-tile k+2 are in
+// flight while tile k is multiplied; one barrier per K-tile.
+//
+// LDS rows are 128 bytes without padding; slot s of row r holds the 16-byte
+// tap chunk s ^ ((r >> 1) & 7).  A fragment read (16 lanes, 16 consecutive
+// rows, one chunk) then touches 16 distinct 16-byte bank groups.
+constexpr int L_BM = 256;
+constexpr int L_STAGES = 3;
+constexpr int L_ATILE = L_BM * ROWB;           // 32 KB
+constexpr int L_BTILE = BN * ROWB;             // 16 KB
+constexpr int L_STAGE = L_ATILE + L_BTILE;
+constexpr int L_SMEM = L_STAGES * L_STAGE;     // 144 KB
+
+typedef __attribute__((address_space(3))) void* lds_ptr;
+
+// One 16-byte buffer load per lane into LDS slot (base + 16 * lane); base is
+// wave-uniform.
+__device__ __forceinline__ void ld_lds16(__amdgpu_buffer_rsrc_t r, uint32_t off, char* base) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_ptr)base, 16, off, 0, 0, 0);
+}
+
+// s_waitcnt vmcnt(n) (n < 64), leaving the other counters alone.
+template <int N> __device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+__device__ __forceinline__ void block_barrier() { asm volatile("s_barrier" ::: "memory"); }
+
+template <bool BWD>
+__global__ __launch_bounds__(NT) void conv_fwd_large_kernel(FwdArgs a) {
+  constexpr int BK = 64;
+  constexpr int LOADS = L_BM / 32 + BN / 32;  // 16-byte loads per thread per K-tile
+  __shared__ __attribute__((aligned(16))) char smem[L_SMEM];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int L = xcd_remap(blockIdx.x, gridDim.x);
+  const int split = L / a.tiles, tile = L - split * a.tiles;
+  const int tm = tile / a.tiles_n, tn = tile - tm * a.tiles_n;
+  const int m0 = tm * L_BM, n0 = tn * BN;
+  const __amdgpu_buffer_rsrc_t xr = make_rsrc(a.x, a.x_bytes);
+  const __amdgpu_buffer_rsrc_t wr = make_rsrc(a.w, a.w_bytes);
+
+  // Loader: instruction i of this wave fills rows 8i .. 8i+7 of the wave's
+  // 64-row (A) / 32-row (B) band; this lane owns row 8i + lane/8, slot
+  // lane % 8, which holds chunk (lane % 8) ^ (4 (i & 1) + lane / 16).
+  const int lrow = lane >> 3;
+  int cpar[2];
+#pragma unroll
+  for (int p = 0; p < 2; ++p) cpar[p] = (lane & 7) ^ (4 * p + (lane >> 4));
+  int apix[8], ah0[8], aw0[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int m = m0 + 64 * wave + 8 * i + lrow;
+    if (m < a.M) {
+      const int n = (int)fdiv((uint32_t)m, a.dPQ);
+      const int pq = m - n * a.P * a.Q;
+      const int p = (int)fdiv((uint32_t)pq, a.dQ);
+      const int q = pq - p * a.Q;
+      ah0[i] = p * a.sh - a.ph;
+      aw0[i] = q * a.sw - a.pw;
+      apix[i] = ((n * a.H + ah0[i]) * a.W + aw0[i]) * a.C;
+    } else {
+      ah0[i] = -(1 << 28);
+      aw0[i] = 0;
+      apix[i] = 0;
+    }
+  }
+  int brow[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int n = n0 + 32 * wave + 8 * i + lrow;
+    brow[i] = n < a.Nn ? n * a.Kg : -1;
+  }
+
+  // Tap decomposition of this lane's two chunks (even / odd instructions) of
+  // the K-tile at k0; a K-tile past the end gives OOB everywhere.
+  struct Taps {
+    int tap[2], r[2], s[2];
+    bool kin[2];
+    int kk[2];
+  };
+  auto taps = [&](int k0) {
+    Taps t;
+#pragma unroll
+    for (int p = 0; p < 2; ++p) {
+      const int kk = k0 + 8 * cpar[p];
+      t.kk[p] = kk;
+      t.kin[p] = kk < a.Kg;
+      const int rs = (int)fdiv((uint32_t)kk, a.dC);
+      const int c = kk - rs * a.C;
+      t.r[p] = (int)fdiv((uint32_t)rs, a.dS);
+      t.s[p] = rs - t.r[p] * a.S;
+      t.tap[p] = (t.r[p] * a.W + t.s[p]) * a.C + c;
+    }
+    return t;
+  };
+  auto issue_a = [&](const Taps& t, char* As, int i) {
+    const int p = i & 1;
+    const int h = ah0[i] + t.r[p], w = aw0[i] + t.s[p];
+    const bool ok = t.kin[p] & ((unsigned)h < (unsigned)a.H) & ((unsigned)w < (unsigned)a.W);
+    ld_lds16(xr, ok ? (uint32_t)(apix[i] + t.tap[p]) * 2u : OOB, As + (64 * wave + 8 * i) * ROWB);
+  };
+  auto issue_b = [&](const Taps& t, char* Bs, int i) {
+    const int p = i & 1;
+    const bool ok = (brow[i] >= 0) & t.kin[p];
+    ld_lds16(wr, ok ? (uint32_t)(brow[i] + t.kk[p]) * 2u : OOB, Bs + (32 * wave + 8 * i) * ROWB);
+  };
+  auto issue = [&](int k0, int stage) {
+    char* As = smem + stage * L_STAGE;
+    const Taps t = taps(k0);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) issue_a(t, As, i);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) issue_b(t, As + L_ATILE, i);
+  };
+
+  f32x16 acc[4][2];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+
+  const int wm = wave >> 1, wn = wave & 1;
+  const int li = lane & 31, lh = lane >> 5;
+  const int tsw = (lh ^ ((li >> 1) & 7)) << 4;  // chunk of k-step kc sits at byte (32 kc) ^ tsw
+  const int aoff = (wm * 128 + li) * ROWB, boff = L_ATILE + (wn * 64 + li) * ROWB;
+  struct Frags {
+    bf16x8 a[4], b[2];
+  };
+  auto frags = [&](const char* S, int kc) {
+    Frags f;
+    const int co = (32 * kc) ^ tsw;
+#pragma unroll
+    for (int b = 0; b < 4; ++b) f.a[b] = *(const bf16x8*)(S + aoff + b * 32 * ROWB + co);
+#pragma unroll
+    for (int b = 0; b < 2; ++b) f.b[b] = *(const bf16x8*)(S + boff + b * 32 * ROWB + co);
+    return f;
+  };
+  auto mma = [&](const Frags& f) {
+#pragma unroll
+    for (int bm = 0; bm < 4; ++bm)
+#pragma unroll
+      for (int bn = 0; bn < 2; ++bn)
+        acc[bm][bn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[bm], f.b[bn], acc[bm][bn], 0, 0, 0);
+  };
+
+  const int nkt_all = (a.Kg + BK - 1) / BK;
+  const int kbase = split * a.kt_per_split * BK;
+  const int nkt = min(a.kt_per_split, nkt_all - split * a.kt_per_split);
+  const int kend = kbase + nkt * BK;  // K-tiles from here on are issued as all-OOB (zeros, no traffic)
+  issue(kbase, 0);
+  issue(nkt > 1 ? kbase + BK : a.Kg, 1);
+  int stage = 0;
+  for (int kt = 0; kt < nkt; ++kt) {
+    wait_vmcnt<LOADS>();  // this thread's loads of tile kt have landed (tile kt+1's may be in flight)
+    block_barrier();      // ... and everyone's; everyone is also done with tile kt-1
+    const int nstage = stage == 0 ? 2 : stage - 1;
+    char* Ns = smem + nstage * L_STAGE;
+    const int knext = kbase + (kt + 2) * BK;
+    const Taps t = taps(knext < kend ? knext : a.Kg);
+    const char* S = smem + stage * L_STAGE;
+    // Fragments one k-step ahead; the loads of tile kt+2 are spread over the
+    // k-steps so their address arithmetic overlaps the MFMAs.
+    Frags f0 = frags(S, 0);
+    Frags f1 = frags(S, 1);
+    mma(f0);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) issue_a(t, Ns, i);
+    f0 = frags(S, 2);
+    mma(f1);
+#pragma unroll
+    for (int i = 4; i < 8; ++i) issue_a(t, Ns, i);
+    f1 = frags(S, 3);
+    mma(f0);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) issue_b(t, Ns + L_ATILE, i);
+    mma(f1);
+    stage = stage == 2 ? 0 : stage + 1;
+  }
+  wait_vmcnt<0>();  // the trailing all-OOB loads still write LDS
+
+  if (a.partial) {
+    float* __restrict__ out = a.partial + (size_t)split * a.M * a.Nn;
+#pragma unroll
+    for (int bn = 0; bn < 2; ++bn) {
+      const int col = n0 + wn * 64 + bn * 32 + li;
+      if (col >= a.Nn) continue;
+#pragma unroll
+      for (int bm = 0; bm < 4; ++bm)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int row = m0 + wm * 128 + bm * 32 + (v >> 2) * 8 + lh * 4 + (v & 3);
+          if (row < a.M) out[(size_t)row * a.Nn + col] = acc[bm][bn][v];
+        }
+    }
+    return;
+  }
+  bf16_t* __restrict__ yp = (bf16_t*)a.y;
+#pragma unroll
+  for (int bn = 0; bn < 2; ++bn) {
+    const int col = n0 + wn * 64 + bn * 32 + li;
+    if (col >= a.Nn) continue;
+    const float bv = a.bias ? a.bias[col] : 0.f;
+#pragma unroll
+    for (int bm = 0; bm < 4; ++bm)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int row = m0 + wm * 128 + bm * 32 + (v >> 2) * 8 + lh * 4 + (v & 3);
+        if (row < a.M) {
+          float val = acc[bm][bn][v] + bv;
+          if (a.relu) val = fmaxf(val, 0.f);
+          yp[(size_t)row * a.Nn + col] = f32_to_bf16(val);
+        }
+      }
   }
 }
 
@@ -409,10 +670,11 @@ __device__ __forceinline__ void mma_tile_tmajor(const char* As, const char* Bs, 
   }
 }
 
-// VA: the 16-byte filter chunks of dy are whole vectors (M % VEC == 0); VB:
-// likewise the tap chunks of x (C % VEC == 0); otherwise element loads.
+// VA: the 16-byte filter chunks of dy are whole vectors (M % VEC == 0),
+// otherwise element loads.  BMD: load mode of the tap chunks of x (VEC16 for
+// C % VEC == 0, VEC8 for bf16 with C % 4 == 0, else ELEM).
 // NFAST: N % BK == 0, so a K-tile's rows share one output pixel.
-template <typename T, bool VA, bool VB, bool NFAST>
+template <typename T, bool VA, int BMD, bool NFAST>
 __global__ __launch_bounds__(NT) void conv_wgrad_kernel(WgradArgs a) {
   constexpr int VEC = 16 / (int)sizeof(T);
   constexpr int CH = 128 / VEC;  // 16-byte chunks per tile row
@@ -441,12 +703,15 @@ __global__ __launch_bounds__(NT) void conv_wgrad_kernel(WgradArgs a) {
   const int PQ = a.P * a.Q;
   const int ystride = PQ * a.M;            // dy elements per image
   const int xstride = a.H * a.W * a.C;     // x elements per image
-  // taps of the x chunk, fixed for the whole reduction
-  int br[VEC], bs[VEC], btap[VEC];
-  bool bok[VEC];
+  // taps of the x chunk, fixed for the whole reduction: NG groups of GS
+  // consecutive channels of one tap (r, s) each
+  constexpr int NG = BMD == VEC16 ? 1 : BMD == VEC8 ? 2 : VEC;
+  constexpr int GS = VEC / NG;
+  int br[NG], bs[NG], btap[NG];
+  bool bok[NG];
 #pragma unroll
-  for (int e = 0; e < VEC; ++e) {
-    const int j = j0 + e;
+  for (int e = 0; e < NG; ++e) {
+    const int j = j0 + e * GS;
     bok[e] = j < a.Nn;
     const int jj = bok[e] ? j : 0;
     const int rs = (int)fdiv((uint32_t)jj, a.dC);
@@ -454,7 +719,6 @@ __global__ __launch_bounds__(NT) void conv_wgrad_kernel(WgradArgs a) {
     br[e] = (int)fdiv((uint32_t)rs, a.dS);
     bs[e] = rs - br[e] * a.S;
     btap[e] = (br[e] * a.W + bs[e]) * a.C + c;
-    if (VB) break;  // one chunk = one tap (r, s) and VEC consecutive channels
   }
 
   // Row d of the K-tile starting at t0: dy offset and x pixel (n, hb, wb).
@@ -499,10 +763,19 @@ __global__ __launch_bounds__(NT) void conv_wgrad_kernel(WgradArgs a) {
       }
       // B: x[n][h0 + r][w0 + s][c .. c + VEC)
       const int xpix = n * xstride + (h0 * a.W + w0) * a.C;
-      if constexpr (VB) {
+      if constexpr (BMD == VEC16) {
         const int h = h0 + br[0], w = w0 + bs[0];
         const bool ok = tin && bok[0] && (unsigned)h < (unsigned)a.H && (unsigned)w < (unsigned)a.W;
         rb[v].u = ld16(xr, ok ? (uint32_t)(xpix + btap[0]) * ES : OOB);
+      } else if constexpr (BMD == VEC8) {
+        uint2 half[2];
+#pragma unroll
+        for (int e = 0; e < 2; ++e) {
+          const int h = h0 + br[e], w = w0 + bs[e];
+          const bool ok = tin & bok[e] & ((unsigned)h < (unsigned)a.H) & ((unsigned)w < (unsigned)a.W);
+          half[e] = ld8(xr, ok ? (uint32_t)(xpix + btap[e]) * ES : OOB);
+        }
+        rb[v].u = make_uint4(half[0].x, half[0].y, half[1].x, half[1].y);
       } else {
 #pragma unroll
         for (int e = 0; e < VEC; ++e) {
@@ -612,32 +885,39 @@ template <typename T> constexpr const char* tname();
 template <> constexpr const char* tname<float>() { return "f32"; }
 template <> constexpr const char* tname<bf16_t>() { return "bf16"; }
 
-// "conv_fwd_kernel<dtype,vecA,vecB,bwd>" for each instance
-template <typename T, bool VA, bool VB, bool BWD> const char* fwd_name() {
-  static const char* names[2][2][2] = {
-      {{"conv_fwd_kernel<%s,0,0,0>", "conv_fwd_kernel<%s,0,0,1>"},
-       {"conv_fwd_kernel<%s,0,1,0>", "conv_fwd_kernel<%s,0,1,1>"}},
-      {{"conv_fwd_kernel<%s,1,0,0>", "conv_fwd_kernel<%s,1,0,1>"},
-       {"conv_fwd_kernel<%s,1,1,0>", "conv_fwd_kernel<%s,1,1,1>"}}};
-  static char buf[2][2][2][48];
+// "conv_fwd_kernel<dtype,modeA,modeB,bwd>" for each instance
+template <typename T, int AM, int BMD, bool BWD> const char* fwd_name() {
+  static char buf[48];
   static bool init = false;
   if (!init) {
-    for (int i = 0; i < 2; ++i)
-      for (int j = 0; j < 2; ++j)
-        for (int k = 0; k < 2; ++k) snprintf(buf[i][j][k], sizeof buf[i][j][k], names[i][j][k], tname<T>());
+    snprintf(buf, sizeof buf, "conv_fwd_kernel<%s,%d,%d,%d>", tname<T>(), AM, BMD, (int)BWD);
     init = true;
   }
-  return buf[VA][VB][BWD];
+  return buf;
 }
 
-template <typename T, bool VA, bool VB, bool BWD>
+template <typename T, int AM, int BMD, bool BWD>
 void launch_fwd_instance(const FwdArgs& a, dim3 grid, double flops, hipStream_t st) {
-  TraceScope ts(fwd_name<T, VA, VB, BWD>(), st, flops, WORK_FLOP);
-  hipLaunchKernelGGL((conv_fwd_kernel<T, VA, VB, BWD>), grid, dim3(NT), 0, st, a);
+  TraceScope ts(fwd_name<T, AM, BMD, BWD>(), st, flops, WORK_FLOP);
+  hipLaunchKernelGGL((conv_fwd_kernel<T, AM, BMD, BWD>), grid, dim3(NT), 0, st, a);
 }
 
-// Reduction splits of a forward-style launch: split the taps when the output
-// tiles alone cannot give every CU two workgroups.
+template <bool BWD> const char* fwd_large_name() {
+  return BWD ? "conv_fwd_large_kernel<bf16,1>" : "conv_fwd_large_kernel<bf16,0>";
+}
+
+// Workgroups of the 256 x 128 kernel per full round of the chip (one per CU)
+// against those of the 128 x 128 kernel (two per CU): the large tile is used
+// when it does not leave a much emptier last round.
+bool use_large_fwd(long M, long Nn) {
+  const long big = ((M + L_BM - 1) / L_BM) * ((Nn + BN - 1) / BN);
+  const long small = ((M + BM - 1) / BM) * ((Nn + BN - 1) / BN);
+  if (big < 256) return false;
+  const double eff_big = (double)big / (double)(((big + 255) / 256) * 256);
+  const double eff_small = (double)small / (double)(((small + 511) / 512) * 512);
+  return eff_big >= 0.85 * eff_small;
+}
+
 int fwd_splits_for(long M, long Nn, long Kg, long bk) {
   const long tiles = ((M + BM - 1) / BM) * ((Nn + BN - 1) / BN);
   const long nkt = (Kg + bk - 1) / bk;
@@ -650,12 +930,27 @@ int fwd_splits_for(long M, long Nn, long Kg, long bk) {
   return (int)((nkt + per - 1) / per);  // every split gets at least one K-tile
 }
 
+template <typename T, int AM, bool BWD>
+void launch_fwd_bmode(int bm, const FwdArgs& a, dim3 grid, double flops, hipStream_t st) {
+  if (bm == VEC16) launch_fwd_instance<T, AM, VEC16, BWD>(a, grid, flops, st);
+  else if (sizeof(T) == 2 && bm == VEC8) launch_fwd_instance<T, AM, sizeof(T) == 2 ? VEC8 : ELEM, BWD>(a, grid, flops, st);
+  else launch_fwd_instance<T, AM, ELEM, BWD>(a, grid, flops, st);
+}
+
 template <typename T, bool BWD>
-void launch_fwd_variant(bool va, bool vb, const FwdArgs& a, dim3 grid, double flops, hipStream_t st) {
-  if (va && vb) launch_fwd_instance<T, true, true, BWD>(a, grid, flops, st);
-  else if (vb) launch_fwd_instance<T, false, true, BWD>(a, grid, flops, st);
-  else if (va) launch_fwd_instance<T, true, false, BWD>(a, grid, flops, st);
-  else launch_fwd_instance<T, false, false, BWD>(a, grid, flops, st);
+void launch_fwd_variant(int am, int bm, const FwdArgs& a, dim3 grid, double flops, hipStream_t st) {
+  if (am == VEC16) launch_fwd_bmode<T, VEC16, BWD>(bm, a, grid, flops, st);
+  else if (sizeof(T) == 2 && am == VEC8) launch_fwd_bmode<T, sizeof(T) == 2 ? VEC8 : ELEM, BWD>(bm, a, grid, flops, st);
+  else launch_fwd_bmode<T, ELEM, BWD>(bm, a, grid, flops, st);
+}
+
+// Load mode for rows of `len` contiguous elements starting at multiples of
+// `len` from base pointer p.
+template <typename T> int load_mode(long len, const void* p) {
+  constexpr int VEC = 16 / (int)sizeof(T);
+  if (len % VEC == 0 && ((uintptr_t)p % 16) == 0) return VEC16;
+  if (sizeof(T) == 2 && len % 4 == 0 && ((uintptr_t)p % 8) == 0) return VEC8;
+  return ELEM;
 }
 
 template <typename T>
@@ -685,12 +980,24 @@ hipError_t conv_fwd_dispatch(const ConvShape& s, const void* x, const void* w, c
   a.partial = splits > 1 ? partial : nullptr;
   a.kt_per_split = (nkt + splits - 1) / splits;
   dim3 grid(a.tiles * splits);
-  const bool va = (s.C % VEC) == 0 && ((uintptr_t)x % 16) == 0;
-  const bool vb = (a.Kg % VEC) == 0 && ((uintptr_t)w % 16) == 0;
+  const int am = load_mode<T>(s.C, x);
+  const int bm = load_mode<T>(a.Kg, w);
+  if (sizeof(T) == 2 && am == VEC16 && bm == VEC16 && splits == 1 && use_large_fwd(a.M, a.Nn)) {
+    a.tiles_n = (a.Nn + BN - 1) / BN;
+    a.tiles = ((a.M + L_BM - 1) / L_BM) * a.tiles_n;
+    a.partial = nullptr;
+    a.kt_per_split = nkt;
+    TraceScope ts(bwd ? fwd_large_name<true>() : fwd_large_name<false>(), st, flops, WORK_FLOP);
+    if (bwd)
+      hipLaunchKernelGGL(conv_fwd_large_kernel<true>, dim3(a.tiles), dim3(NT), 0, st, a);
+    else
+      hipLaunchKernelGGL(conv_fwd_large_kernel<false>, dim3(a.tiles), dim3(NT), 0, st, a);
+    return hipGetLastError();
+  }
   if (bwd)
-    launch_fwd_variant<T, true>(va, vb, a, grid, flops, st);
+    launch_fwd_variant<T, true>(am, bm, a, grid, flops, st);
   else
-    launch_fwd_variant<T, false>(va, vb, a, grid, flops, st);
+    launch_fwd_variant<T, false>(am, bm, a, grid, flops, st);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || splits == 1) return e;
   const size_t n = (size_t)a.M * a.Nn;
@@ -702,28 +1009,34 @@ hipError_t conv_fwd_dispatch(const ConvShape& s, const void* x, const void* w, c
   return hipGetLastError();
 }
 
-template <typename T, bool VA, bool VB, bool NF> const char* wgrad_name() {
+template <typename T, bool VA, int BMD, bool NF> const char* wgrad_name() {
   static char buf[48];
   static bool init = false;
   if (!init) {
-    snprintf(buf, sizeof buf, "conv_wgrad_kernel<%s,%d,%d,%d>", tname<T>(), (int)VA, (int)VB, (int)NF);
+    snprintf(buf, sizeof buf, "conv_wgrad_kernel<%s,%d,%d,%d>", tname<T>(), (int)VA, BMD, (int)NF);
     init = true;
   }
   return buf;
 }
 
-template <typename T, bool VA, bool VB, bool NF>
+template <typename T, bool VA, int BMD, bool NF>
 void launch_wgrad_instance(const WgradArgs& a, dim3 grid, double flops, hipStream_t st) {
-  TraceScope ts(wgrad_name<T, VA, VB, NF>(), st, flops, WORK_FLOP);
-  hipLaunchKernelGGL((conv_wgrad_kernel<T, VA, VB, NF>), grid, dim3(NT), 0, st, a);
+  TraceScope ts(wgrad_name<T, VA, BMD, NF>(), st, flops, WORK_FLOP);
+  hipLaunchKernelGGL((conv_wgrad_kernel<T, VA, BMD, NF>), grid, dim3(NT), 0, st, a);
+}
+
+template <typename T, bool VA, bool NF>
+void launch_wgrad_bmode(int bm, const WgradArgs& a, dim3 grid, double flops, hipStream_t st) {
+  if (bm == VEC16) launch_wgrad_instance<T, VA, VEC16, NF>(a, grid, flops, st);
+  else if (sizeof(T) == 2 && bm == VEC8)
+    launch_wgrad_instance<T, VA, sizeof(T) == 2 ? VEC8 : ELEM, NF>(a, grid, flops, st);
+  else launch_wgrad_instance<T, VA, ELEM, NF>(a, grid, flops, st);
 }
 
 template <typename T, bool NF>
-void launch_wgrad_variant(bool va, bool vb, const WgradArgs& a, dim3 grid, double flops, hipStream_t st) {
-  if (va && vb) launch_wgrad_instance<T, true, true, NF>(a, grid, flops, st);
-  else if (va) launch_wgrad_instance<T, true, false, NF>(a, grid, flops, st);
-  else if (vb) launch_wgrad_instance<T, false, true, NF>(a, grid, flops, st);
-  else launch_wgrad_instance<T, false, false, NF>(a, grid, flops, st);
+void launch_wgrad_variant(bool va, int bm, const WgradArgs& a, dim3 grid, double flops, hipStream_t st) {
+  if (va) launch_wgrad_bmode<T, true, NF>(bm, a, grid, flops, st);
+  else launch_wgrad_bmode<T, false, NF>(bm, a, grid, flops, st);
 }
 
 template <typename T>
@@ -755,7 +1068,7 @@ hipError_t conv_wgrad_dispatch(const ConvShape& s, const void* x, const void* dy
   a.out = a.direct ? dw : partial;
   dim3 grid(a.tiles * splits);
   const bool va = (a.M % VEC) == 0 && ((uintptr_t)dy % 16) == 0;
-  const bool vb = (s.C % VEC) == 0 && ((uintptr_t)x % 16) == 0;
+  const int vb = load_mode<T>(s.C, x);
   const double flops = 2.0 * a.M * (double)a.Nn * (double)a.T;
   if (s.N % BK == 0)
     launch_wgrad_variant<T, true>(va, vb, a, grid, flops, st);

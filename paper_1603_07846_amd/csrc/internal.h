@@ -79,6 +79,8 @@ hipError_t launch_conv_bwd_data_direct(int dt, const ConvShape& s, const void* d
 // Zero-pad the innermost (channel) dimension: in [rows][C] -> out [rows][Cp],
 // Cp a multiple of the 16-byte vector width.
 hipError_t launch_pad_channels(int dt, const void* in, void* out, long rows, int C, int Cp, hipStream_t st);
+hipError_t launch_unpad_channels_f32(const float* in, float* out, long rows, int Cp, int C, int accumulate,
+                                     hipStream_t st);
 
 // NCHW <-> NHWC permutations for the NCHW entry points.
 hipError_t launch_nchw_to_nhwc(int dt, const void* in, void* out, int N, int C, int H, int W, hipStream_t st);

@@ -43,6 +43,8 @@ CONV_CASES = [
     (4, 64, 4, 4, 200, 4, 4, 0, 1),      # FC, few rows, long reduction: split-K forward
     (5, 256, 2, 2, 520, 2, 2, 0, 1),     # FC: split-K forward and split-K backward-data
     (3, 5, 9, 9, 16, 3, 3, 1, 1),        # C=5: zero-padded channels in the forward pass
+    (2, 12, 10, 10, 24, 3, 3, 1, 1),     # C=12: bf16 8-byte tap halves that wrap to the next tap
+    (3, 4, 19, 19, 16, 5, 5, 2, 2),      # C=4, filter rows of 100 taps: 8-byte halves for both operands
 ]
 
 
@@ -240,3 +242,35 @@ def test_abi_errors_launch_nothing():
     with pytest.raises(singa.SingaError) as e:
         singa.relu_fwd(x.view(-1)[1:])
     assert e.value.status == -5
+
+
+# Shapes big enough that the bf16 forward / backward-data passes take the
+# 256 x 128 direct-to-LDS kernel (checked through the kernel trace), with
+# ragged M, N and K tails and stride 2; compared element by element.
+LARGE_CASES = [
+    ("fwd", (10, 40, 47, 47, 300, 3, 3, 1, 1)),
+    ("bwd_data", (16, 200, 47, 47, 64, 3, 3, 1, 1)),
+    ("fwd", (40, 64, 59, 59, 136, 3, 3, 1, 2)),
+]
+
+
+@pytest.mark.parametrize("op,case", LARGE_CASES, ids=[o + "-" + "x".join(map(str, c)) for o, c in LARGE_CASES])
+def test_conv_large_tile_path(op, case):
+    N, C, H, W, K, R, S, pad, stride = case
+    x, w, b, dy = _conv_inputs(case, "bf16", 50)
+    singa.trace_enable(True)
+    if op == "fwd":
+        out = singa.conv_fwd(nchw_to_dev(x, "bf16"), kcrs_to_dev(w, "bf16"), torch.from_numpy(b).cuda(), pad, stride,
+                             relu=True)
+    else:
+        out = singa.conv_bwd_data(nchw_to_dev(dy, "bf16"), kcrs_to_dev(w, "bf16"), phys(x.shape), pad, stride)
+    torch.cuda.synchronize()
+    names = [r[0] for r in singa.trace_records()]
+    singa.trace_enable(False)
+    assert any(n.startswith("conv_fwd_large_kernel") for n in names), names
+    if op == "fwd":
+        ref = oracle.relu_fwd(oracle.conv_fwd(x, w, b, pad=pad, stride=stride))
+    else:
+        ref = oracle.conv_bwd_data(dy, w, x.shape, pad=pad, stride=stride)
+    err = rel_l2(dev_to_nchw(out), ref)
+    assert err <= TOL["bf16"], (case, err)
