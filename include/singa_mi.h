@@ -122,14 +122,19 @@ int singa_conv_fwd(singa_dtype dtype, singa_layout layout,
  *                 of W[k,c,r,s] * dy[n,k,p,q]
  *   x      : shape of the layer's input (the shape of dx)
  *   dy_ptr : dtype, shape singa_conv_out_shape()    (read)
+ *   relu_y : NULL, or dtype, shape *x (read): the output of a ReLU layer that
+ *            is this layer's source.  Then dx is the gradient at that ReLU's
+ *            input instead: dx[i] = relu_y[i] > 0 ? (the sum above) : 0, the
+ *            ReLU layer's ComputeGradient folded into this call.  NCHW callers
+ *            must pass 16-byte aligned relu_y and dx_ptr.
  *   dx_ptr : dtype, shape *x                        (overwritten)
  * Stride 1 (and dense "fully connected" geometry) runs as an implicit GEMM on
  * MFMA over a flipped, transposed copy of W in the workspace; other strides
  * run a gather kernel. */
 int singa_conv_bwd_data(singa_dtype dtype, singa_layout layout,
                         const singa_shape4* x, const singa_filter4* w, const void* w_ptr,
-                        const singa_conv_desc* d, const void* dy_ptr, void* dx_ptr,
-                        void* ws, size_t ws_bytes, singa_stream stream);
+                        const singa_conv_desc* d, const void* dy_ptr, const void* relu_y,
+                        void* dx_ptr, void* ws, size_t ws_bytes, singa_stream stream);
 
 /* Convolution ComputeGradient, Param gradients (Sec. 4.1.2):
  *   dW[k,c,r,s] = sum_{n,p,q} dy[n,k,p,q] * x[n,c,p*sh-ph+r, q*sw-pw+s]
@@ -163,11 +168,16 @@ int singa_pool_fwd(singa_dtype dtype, singa_layout layout,
 
 /* Pooling ComputeGradient: every input cell gathers, from each window that
  * covers it, dy[o] if it is that window's argmax (MAX) or dy[o]/divisor(o)
- * (AVG).  dx_ptr (shape *x) is overwritten; no atomics. */
+ * (AVG).  dx_ptr (shape *x) is overwritten; no atomics.
+ *   relu_y : NULL, or (MAX only) the pooling's forward output y_ptr, when the
+ *            pooling's input is the output of a ReLU layer.  Then dx is the
+ *            gradient at that ReLU's input: a window routes dy[o] only when
+ *            y[o] > 0.  This is exact: the arg-max cell holds y[o], so it is
+ *            the ReLU's output there.  AVG with relu_y is SINGA_ERR_UNSUPPORTED. */
 int singa_pool_bwd(singa_dtype dtype, singa_layout layout,
                    const singa_shape4* x, const singa_pool_desc* d,
-                   const void* dy_ptr, const uint8_t* argmax, void* dx_ptr,
-                   singa_stream stream);
+                   const void* dy_ptr, const uint8_t* argmax, const void* relu_y,
+                   void* dx_ptr, singa_stream stream);
 
 /* --------------------------------------------------------------------- ReLU */
 

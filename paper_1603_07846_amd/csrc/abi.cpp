@@ -132,12 +132,13 @@ size_t carve_fwd(const ConvShape& s, int dt, int layout, void* ws, FwdWs* o) {
 hipError_t conv_fwd_nhwc(int dt, const ConvShape& s, const void* x, const void* w, const float* bias, void* y,
                          int relu, const FwdWs& o, hipStream_t st) {
   const int cp = padded_channels(s, dt);
-  if (!cp) return launch_conv_fwd(dt, s, x, w, bias, y, relu, 0, conv_flops(s), o.partial, st);
+  if (!cp) return launch_conv_fwd(dt, s, x, w, bias, y, relu, 0, conv_flops(s), o.partial, nullptr, st);
   hipError_t e = launch_pad_channels(dt, x, o.xp, (long)s.N * s.H * s.W, s.C, cp, st);
   if (e == hipSuccess) e = launch_pad_channels(dt, w, o.wp, (long)s.K * s.R * s.S, s.C, cp, st);
   ConvShape g = s;
   g.C = cp;
-  if (e == hipSuccess) e = launch_conv_fwd(dt, g, o.xp, o.wp, bias, y, relu, 0, conv_flops(s), o.partial, st);
+  if (e == hipSuccess)
+    e = launch_conv_fwd(dt, g, o.xp, o.wp, bias, y, relu, 0, conv_flops(s), o.partial, nullptr, st);
   return e;
 }
 
@@ -280,15 +281,19 @@ int singa_conv_fwd(singa_dtype dtype, singa_layout layout, const singa_shape4* x
 }
 
 int singa_conv_bwd_data(singa_dtype dtype, singa_layout layout, const singa_shape4* x, const singa_filter4* w,
-                        const void* w_ptr, const singa_conv_desc* d, const void* dy_ptr, void* dx_ptr, void* ws,
-                        size_t ws_bytes, singa_stream stream) {
+                        const void* w_ptr, const singa_conv_desc* d, const void* dy_ptr, const void* relu_y,
+                        void* dx_ptr, void* ws, size_t ws_bytes, singa_stream stream) {
   if (!dtype_ok(dtype) || !layout_ok(layout)) return SINGA_ERR_UNSUPPORTED;
   ConvShape s;
   int rc = conv_geometry(x, w, d, &s);
   if (rc != SINGA_OK) return rc;
   if (!w_ptr || !dy_ptr || !dx_ptr) return SINGA_ERR_NULL;
   const size_t es = dt_size(dtype);
-  if (!aligned_to(w_ptr, es) || !aligned_to(dy_ptr, es) || !aligned_to(dx_ptr, es) || !aligned_to(ws, 16))
+  if (!aligned_to(w_ptr, es) || !aligned_to(dy_ptr, es) || !aligned_to(dx_ptr, es) || !aligned_to(ws, 16) ||
+      !aligned_to(relu_y, es))
+    return SINGA_ERR_ALIGN;
+  // NCHW applies the ReLU mask with the vectorized ReLU-backward kernel
+  if (relu_y && layout == SINGA_NCHW && (!aligned_to(relu_y, 16) || !aligned_to(dx_ptr, 16)))
     return SINGA_ERR_ALIGN;
   BwdDataWs o;
   const size_t need = carve_bwd_data(s, dtype, layout, nullptr, &o);
@@ -299,6 +304,7 @@ int singa_conv_bwd_data(singa_dtype dtype, singa_layout layout, const singa_shap
   const void* dy = dy_ptr;
   const void* wk = w_ptr;  // KRSC filter
   void* dx = dx_ptr;
+  const void* nhwc_mask = layout == SINGA_NHWC ? relu_y : nullptr;  // folded into the producing kernel
   if (layout == SINGA_NCHW) {
     e = launch_nchw_to_nhwc(dtype, dy_ptr, o.dy, s.N, s.K, s.P, s.Q, st);
     if (e == hipSuccess) e = kcrs_to_krsc(dtype, s, w_ptr, o.w, st);
@@ -316,12 +322,16 @@ int singa_conv_bwd_data(singa_dtype dtype, singa_layout layout, const singa_shap
         e = launch_transpose(dtype, wk, o.wt, RS, s.K, s.C, s.C, (long)RS * s.C, s.K, (long)RS * s.K, 1, st);
       }
       if (e == hipSuccess)
-        e = launch_conv_fwd(dtype, bwd_data_inner(s), dy, o.wt, nullptr, dx, 0, 1, conv_flops(s), o.partial, st);
+        e = launch_conv_fwd(dtype, bwd_data_inner(s), dy, o.wt, nullptr, dx, 0, 1, conv_flops(s), o.partial,
+                            nhwc_mask, st);
     } else {
-      e = launch_conv_bwd_data_direct(dtype, s, dy, wk, dx, st);
+      e = launch_conv_bwd_data_direct(dtype, s, dy, wk, dx, nhwc_mask, st);
     }
   }
-  if (e == hipSuccess && layout == SINGA_NCHW) e = launch_nhwc_to_nchw(dtype, dx, dx_ptr, s.N, s.C, s.H, s.W, st);
+  if (e == hipSuccess && layout == SINGA_NCHW) {
+    e = launch_nhwc_to_nchw(dtype, dx, dx_ptr, s.N, s.C, s.H, s.W, st);
+    if (e == hipSuccess && relu_y) e = launch_relu_bwd(dtype, act_bytes(s, dtype) / es, relu_y, dx_ptr, dx_ptr, st);
+  }
   return hip_status(e);
 }
 
@@ -389,17 +399,19 @@ int singa_pool_fwd(singa_dtype dtype, singa_layout layout, const singa_shape4* x
 }
 
 int singa_pool_bwd(singa_dtype dtype, singa_layout layout, const singa_shape4* x, const singa_pool_desc* d,
-                   const void* dy_ptr, const uint8_t* argmax, void* dx_ptr, singa_stream stream) {
+                   const void* dy_ptr, const uint8_t* argmax, const void* relu_y, void* dx_ptr,
+                   singa_stream stream) {
   if (!dtype_ok(dtype) || !layout_ok(layout)) return SINGA_ERR_UNSUPPORTED;
   singa_shape4 y;
   int rc = singa_pool_out_shape(x, d, &y);
   if (rc != SINGA_OK) return rc;
   if (!dy_ptr || !dx_ptr || (d->mode == SINGA_POOL_MAX && !argmax)) return SINGA_ERR_NULL;
+  if (relu_y && d->mode != SINGA_POOL_MAX) return SINGA_ERR_UNSUPPORTED;
   const size_t es = dt_size(dtype);
-  if (!aligned_to(dy_ptr, es) || !aligned_to(dx_ptr, es)) return SINGA_ERR_ALIGN;
+  if (!aligned_to(dy_ptr, es) || !aligned_to(dx_ptr, es) || !aligned_to(relu_y, es)) return SINGA_ERR_ALIGN;
   return hip_status(launch_pool_bwd(dtype, d->mode, x->n, x->c, x->h, x->w, y.h, y.w, d->kh, d->kw, d->stride_h,
-                                    d->stride_w, d->pad_h, d->pad_w, dy_ptr, argmax, dx_ptr, layout == SINGA_NCHW,
-                                    (hipStream_t)stream));
+                                    d->stride_w, d->pad_h, d->pad_w, dy_ptr, argmax, relu_y, dx_ptr,
+                                    layout == SINGA_NCHW, (hipStream_t)stream));
 }
 
 int singa_relu_fwd(singa_dtype dtype, size_t n, const void* x, void* y, singa_stream stream) {

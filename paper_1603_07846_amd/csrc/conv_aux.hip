@@ -49,7 +49,8 @@ __global__ __launch_bounds__(256) void transpose_kernel(const T* __restrict__ in
 // multiple of the stride, and over k, of w[k,r,s,c] * dy[n,p,q,k].
 template <typename T>
 __global__ __launch_bounds__(256) void bwd_data_direct_kernel(ConvShape s, const T* __restrict__ dy,
-                                                              const T* __restrict__ w, T* __restrict__ dx,
+                                                              const T* __restrict__ w,
+                                                              const T* __restrict__ mask, T* __restrict__ dx,
                                                               long total) {
   for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += (long)gridDim.x * blockDim.x) {
     const int c = (int)(i % s.C);
@@ -75,6 +76,7 @@ __global__ __launch_bounds__(256) void bwd_data_direct_kernel(ConvShape s, const
         for (int k = 0; k < s.K; ++k) acc += ld_f<T>(wr + k * wk) * ld_f<T>(dyr + k);
       }
     }
+    if (mask && !(ld_f<T>(mask + i) > 0.f)) acc = 0.f;
     st_f<T>(dx + i, acc);
   }
 }
@@ -262,17 +264,17 @@ hipError_t launch_transpose(int dt, const void* in, void* out, int batch, int ro
 }
 
 hipError_t launch_conv_bwd_data_direct(int dt, const ConvShape& s, const void* dy, const void* w, void* dx,
-                                       hipStream_t st) {
+                                       const void* mask, hipStream_t st) {
   const long total = (long)s.N * s.H * s.W * s.C;
   const unsigned g = grid_for(total);
   TraceScope ts("bwd_data_direct_kernel", st,
                 2.0 * s.N * (double)s.P * s.Q * s.K * (double)s.C * s.R * s.S, WORK_FLOP);
   if (dt == BF16)
     hipLaunchKernelGGL(bwd_data_direct_kernel<bf16_t>, dim3(g), dim3(256), 0, st, s, (const bf16_t*)dy,
-                       (const bf16_t*)w, (bf16_t*)dx, total);
+                       (const bf16_t*)w, (const bf16_t*)mask, (bf16_t*)dx, total);
   else
     hipLaunchKernelGGL(bwd_data_direct_kernel<float>, dim3(g), dim3(256), 0, st, s, (const float*)dy,
-                       (const float*)w, (float*)dx, total);
+                       (const float*)w, (const float*)mask, (float*)dx, total);
   return hipGetLastError();
 }
 

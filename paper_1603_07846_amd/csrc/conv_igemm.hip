@@ -23,6 +23,8 @@
 // rows are padded to 144 bytes so the 16-byte fragment reads of 16
 // consecutive rows hit distinct banks.  Two LDS stages: global loads of tile
 // k+1 are in flight while tile k is multiplied.
+#include <cstdlib>
+
 #include "common.h"
 #include "internal.h"
 
@@ -60,6 +62,18 @@ template <> __device__ __forceinline__ bf16_t zero_elem<bf16_t>() { return (bf16
 template <typename T> __device__ __forceinline__ void store_out(T* p, float v);
 template <> __device__ __forceinline__ void store_out<float>(float* p, float v) { *p = v; }
 template <> __device__ __forceinline__ void store_out<bf16_t>(bf16_t* p, float v) { *p = f32_to_bf16(v); }
+
+__device__ __forceinline__ float elem_f(float v) { return v; }
+__device__ __forceinline__ float elem_f(bf16_t v) { return bf16_to_f32(v); }
+
+// ReLU backward folded into an epilogue: keep v where the ReLU's output is > 0.
+template <typename T> __device__ __forceinline__ bool mask_pass(const void* m, size_t i);
+template <> __device__ __forceinline__ bool mask_pass<float>(const void* m, size_t i) {
+  return ((const float*)m)[i] > 0.f;
+}
+template <> __device__ __forceinline__ bool mask_pass<bf16_t>(const void* m, size_t i) {
+  return bf16_to_f32(((const bf16_t*)m)[i]) > 0.f;
+}
 
 // Multiply one K-tile held in LDS: acc[bm][bn] += A(rows) * B(cols)^T.
 template <typename T>
@@ -124,6 +138,86 @@ __device__ __forceinline__ int xcd_remap(int b, int G) {
   return x * q + min(x, r) + l;
 }
 
+// ------------------------------------------------------------ epilogue
+//
+// y[row][col] = act(acc + bias[col]), optionally zeroed where mask <= 0, for
+// one wave's (32 FM) x 64 quadrant of the output tile.  The accumulators hold
+// one column per lane (rows 8 (v / 4) + 4 (lane / 32) + v % 4 of each 32 x 32
+// block); they go through the wave's own LDS region as T so that the global
+// stores (and the mask loads) are 16-byte vectors of consecutive columns.
+// Needs (32 FM) * (64 * sizeof(T) + 16) bytes of LDS at `lds`; the caller
+// has finished with the operand tiles there (barrier).  `vec`: y, mask and Nn
+// allow 16-byte vectors; otherwise the staged values are stored one by one.
+template <typename T, int FM>
+__device__ __forceinline__ void store_quadrant(const f32x16 (&acc)[FM][2], char* lds, int lane, int row0, int col0,
+                                               int M, int Nn, const float* bias, int relu, const void* mask,
+                                               T* __restrict__ y, bool vec) {
+  constexpr int ES = (int)sizeof(T);
+  constexpr int PIT = 64 * ES + 16;
+  constexpr int VEC = 16 / ES;
+  constexpr int CPR = 64 / VEC;      // 16-byte chunks per row
+  constexpr int RPS = 64 / CPR;      // rows per pass of the wave
+  const int li = lane & 31, lh = lane >> 5;
+#pragma unroll
+  for (int bn = 0; bn < 2; ++bn) {
+    const int c = bn * 32 + li;
+    const float bv = (bias && col0 + c < Nn) ? bias[col0 + c] : 0.f;
+#pragma unroll
+    for (int bm = 0; bm < FM; ++bm)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        float val = acc[bm][bn][v] + bv;
+        if (relu) val = fmaxf(val, 0.f);
+        const int r = bm * 32 + (v >> 2) * 8 + lh * 4 + (v & 3);
+        store_out<T>((T*)(lds + r * PIT + c * ES), val);
+      }
+  }
+  __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's LDS writes are done
+  __builtin_amdgcn_wave_barrier();
+  const int cc = lane % CPR, rr = lane / CPR;
+  const int col = col0 + cc * VEC;
+  const T* __restrict__ mk = (const T*)mask;
+  if (vec) {
+#pragma unroll
+    for (int pass = 0; pass < FM * 32 / RPS; ++pass) {
+      const int r = pass * RPS + rr;
+      const int row = row0 + r;
+      union { uint4 u; T e[VEC]; } val, mv;
+      val.u = *(const uint4*)(lds + r * PIT + cc * 16);
+      if (row < M && col < Nn) {
+        const size_t o = (size_t)row * Nn + col;
+        if (mk) {
+          mv.u = *(const uint4*)(mk + o);
+#pragma unroll
+          for (int j = 0; j < VEC; ++j)
+            if (!(elem_f(mv.e[j]) > 0.f)) val.e[j] = T(0);
+        }
+        *(uint4*)(y + o) = val.u;
+      }
+    }
+  } else {
+#pragma unroll
+    for (int pass = 0; pass < FM * 32 / RPS; ++pass) {
+      const int r = pass * RPS + rr;
+      const int row = row0 + r;
+      union { uint4 u; T e[VEC]; } val;
+      val.u = *(const uint4*)(lds + r * PIT + cc * 16);
+      if (row < M) {
+#pragma unroll
+        for (int j = 0; j < VEC; ++j) {
+          const int cj = col + j;
+          if (cj < Nn) {
+            const size_t o = (size_t)row * Nn + cj;
+            T e = val.e[j];
+            if (mk && !(elem_f(mk[o]) > 0.f)) e = T(0);
+            y[o] = e;
+          }
+        }
+      }
+    }
+  }
+}
+
 // ------------------------------------------------------------------ forward
 
 struct FwdArgs {
@@ -140,6 +234,7 @@ struct FwdArgs {
   int tiles, tiles_n;
   float* partial;  // split-K: fp32 partial tiles [split][M][Nn] instead of y
   int kt_per_split;
+  const void* mask;  // optional [M][Nn] tensor: an output is zeroed where mask <= 0
 };
 
 // Operand load modes.  VEC16: 16-byte vectors of VEC taps (C % VEC == 0 for
@@ -328,25 +423,10 @@ __global__ __launch_bounds__(NT) void conv_fwd_kernel(FwdArgs a) {
     }
     return;
   }
-  T* __restrict__ yp = (T*)a.y;
-#pragma unroll
-  for (int bn = 0; bn < 2; ++bn) {
-    const int col = n0 + wn * 64 + bn * 32 + li;
-    if (col >= a.Nn) continue;
-    const float bv = a.bias ? a.bias[col] : 0.f;
-#pragma unroll
-    for (int bm = 0; bm < 2; ++bm) {
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int row = m0 + wm * 64 + bm * 32 + (v >> 2) * 8 + lh * 4 + (v & 3);
-        if (row < a.M) {
-          float val = acc[bm][bn][v] + bv;
-          if (a.relu) val = fmaxf(val, 0.f);
-          store_out<T>(yp + (size_t)row * a.Nn + col, val);
-        }
-      }
-    }
-  }
+  __syncthreads();  // every wave is done with the operand tiles
+  const bool vec = a.Nn % VEC == 0 && (((uintptr_t)a.y | (uintptr_t)a.mask) % 16) == 0;
+  store_quadrant<T, 2>(acc, smem + wave * 64 * (64 * (int)sizeof(T) + 16), lane, m0 + wm * 64, n0 + wn * 64, a.M,
+                       a.Nn, a.bias, a.relu, a.mask, (T*)a.y, vec);
 }
 
 // ------------------------------------------------- forward, large bf16 tiles
@@ -557,24 +637,10 @@ __global__ __launch_bounds__(NT) void conv_fwd_large_kernel(FwdArgs a) {
     }
     return;
   }
-  bf16_t* __restrict__ yp = (bf16_t*)a.y;
-#pragma unroll
-  for (int bn = 0; bn < 2; ++bn) {
-    const int col = n0 + wn * 64 + bn * 32 + li;
-    if (col >= a.Nn) continue;
-    const float bv = a.bias ? a.bias[col] : 0.f;
-#pragma unroll
-    for (int bm = 0; bm < 4; ++bm)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int row = m0 + wm * 128 + bm * 32 + (v >> 2) * 8 + lh * 4 + (v & 3);
-        if (row < a.M) {
-          float val = acc[bm][bn][v] + bv;
-          if (a.relu) val = fmaxf(val, 0.f);
-          yp[(size_t)row * a.Nn + col] = f32_to_bf16(val);
-        }
-      }
-  }
+  __syncthreads();  // every wave is done with the operand tiles
+  const bool vec = a.Nn % 8 == 0 && (((uintptr_t)a.y | (uintptr_t)a.mask) % 16) == 0;
+  store_quadrant<bf16_t, 4>(acc, smem + wave * 128 * (64 * 2 + 16), lane, m0 + wm * 128, n0 + wn * 64, a.M, a.Nn,
+                            a.bias, a.relu, a.mask, (bf16_t*)a.y, vec);
 }
 
 // ----------------------------------------------------------- filter gradient
@@ -870,13 +936,14 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restr
 template <typename T>
 __global__ __launch_bounds__(256) void splitk_epilogue_kernel(const float* __restrict__ partial, int splits, int M,
                                                               int Nn, const float* __restrict__ bias, int relu,
-                                                              T* __restrict__ y) {
+                                                              const void* mask, T* __restrict__ y) {
   const size_t n = (size_t)M * Nn;
   for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x) {
     float t = 0.f;
     for (int k = 0; k < splits; ++k) t += partial[(size_t)k * n + i];
     if (bias) t += bias[i % Nn];
     if (relu) t = fmaxf(t, 0.f);
+    if (mask && !mask_pass<T>(mask, i)) t = 0.f;
     store_out<T>(y + i, t);
   }
 }
@@ -909,7 +976,19 @@ template <bool BWD> const char* fwd_large_name() {
 // Workgroups of the 256 x 128 kernel per full round of the chip (one per CU)
 // against those of the 128 x 128 kernel (two per CU): the large tile is used
 // when it does not leave a much emptier last round.
+// SINGA_CONV_TILE=128 or =256 in the environment forces the tile choice
+// (read once; anything else, or unset, keeps the automatic rule).
+int forced_tile() {
+  static const int v = [] {
+    const char* e = getenv("SINGA_CONV_TILE");
+    return e ? atoi(e) : 0;
+  }();
+  return v;
+}
+
 bool use_large_fwd(long M, long Nn) {
+  if (forced_tile() == 128) return false;
+  if (forced_tile() == 256) return ((M + L_BM - 1) / L_BM) * ((Nn + BN - 1) / BN) > 0;
   const long big = ((M + L_BM - 1) / L_BM) * ((Nn + BN - 1) / BN);
   const long small = ((M + BM - 1) / BM) * ((Nn + BN - 1) / BN);
   if (big < 256) return false;
@@ -955,10 +1034,10 @@ template <typename T> int load_mode(long len, const void* p) {
 
 template <typename T>
 hipError_t conv_fwd_dispatch(const ConvShape& s, const void* x, const void* w, const float* bias, void* y,
-                             int relu, int bwd, double flops, float* partial, hipStream_t st) {
+                             int relu, int bwd, double flops, float* partial, const void* mask, hipStream_t st) {
   constexpr int VEC = KT<T>::VEC;
   FwdArgs a;
-  a.x = x; a.w = w; a.bias = bias; a.y = y;
+  a.x = x; a.w = w; a.bias = bias; a.y = y; a.mask = mask;
   a.x_bytes = (uint32_t)((size_t)s.N * s.H * s.W * s.C * sizeof(T));
   a.w_bytes = (uint32_t)((size_t)s.K * s.R * s.S * s.C * sizeof(T));
   a.M = s.N * s.P * s.Q;
@@ -1005,7 +1084,7 @@ hipError_t conv_fwd_dispatch(const ConvShape& s, const void* x, const void* w, c
   if (blocks > 8192) blocks = 8192;
   TraceScope ts("splitk_epilogue_kernel", st, (double)n * (4.0 * splits + sizeof(T)), WORK_BYTE);
   hipLaunchKernelGGL(splitk_epilogue_kernel<T>, dim3((unsigned)blocks), dim3(256), 0, st, partial, splits, a.M,
-                     a.Nn, bias, relu, (T*)y);
+                     a.Nn, bias, relu, mask, (T*)y);
   return hipGetLastError();
 }
 
@@ -1080,9 +1159,9 @@ hipError_t conv_wgrad_dispatch(const ConvShape& s, const void* x, const void* dy
 }  // namespace
 
 hipError_t launch_conv_fwd(int dt, const ConvShape& s, const void* x, const void* w, const float* bias, void* y,
-                           int relu, int bwd, double flops, float* partial, hipStream_t st) {
-  if (dt == BF16) return conv_fwd_dispatch<bf16_t>(s, x, w, bias, y, relu, bwd, flops, partial, st);
-  return conv_fwd_dispatch<float>(s, x, w, bias, y, relu, bwd, flops, partial, st);
+                           int relu, int bwd, double flops, float* partial, const void* mask, hipStream_t st) {
+  if (dt == BF16) return conv_fwd_dispatch<bf16_t>(s, x, w, bias, y, relu, bwd, flops, partial, mask, st);
+  return conv_fwd_dispatch<float>(s, x, w, bias, y, relu, bwd, flops, partial, mask, st);
 }
 
 size_t fwd_partial_bytes(const ConvShape& s, int dt) {

@@ -102,7 +102,8 @@ __global__ __launch_bounds__(256) void pool_fwd_kernel(PoolGeom g, int mode, con
 // that cover it (in window order) and takes what they route to it.
 template <typename T, bool NCHW>
 __global__ __launch_bounds__(256) void pool_bwd_kernel(PoolGeom g, int mode, const T* __restrict__ dy,
-                                                       const uint8_t* __restrict__ argmax, T* __restrict__ dx,
+                                                       const uint8_t* __restrict__ argmax,
+                                                       const T* __restrict__ ymask, T* __restrict__ dx,
                                                        long total) {
   for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += (long)gridDim.x * blockDim.x) {
     int n, c, h, w;
@@ -133,7 +134,7 @@ __global__ __launch_bounds__(256) void pool_bwd_kernel(PoolGeom g, int mode, con
         const long o = off4<NCHW>(g, n, c, p, q, g.P, g.Q);
         if (mode == 0) {
           const int cell = (h - (p * g.sh - g.ph)) * g.kw + (w - (q * g.sw - g.pw));
-          if (argmax[o] == cell) acc += ld_f<T>(dy + o);
+          if (argmax[o] == cell && (!ymask || ld_f<T>(ymask + o) > 0.f)) acc += ld_f<T>(dy + o);
         } else {
           acc += ld_f<T>(dy + o) / (float)pool_divisor(g, p, q);
         }
@@ -208,18 +209,22 @@ __global__ __launch_bounds__(256) void pool_fwd_nhwc_vec_kernel(PoolGeom g, int 
   }
 }
 
-template <typename T, int VEC>
-__global__ __launch_bounds__(256) void pool_bwd_nhwc_vec_kernel(PoolGeom g, int mode, const T* __restrict__ dy,
+// One thread per (input pixel, VEC consecutive channels), 32-bit index math
+// (every pooled tensor has fewer than 2^31 elements).
+template <typename T, int VEC, bool MASK>
+__global__ __launch_bounds__(256) void pool_bwd_nhwc_vec_kernel(PoolGeom g, FastDiv dCV, FastDiv dW, FastDiv dH,
+                                                                int mode, const T* __restrict__ dy,
                                                                 const uint8_t* __restrict__ argmax,
-                                                                T* __restrict__ dx, long total) {
+                                                                const T* __restrict__ ymask, T* __restrict__ dx,
+                                                                int total) {
   const int CV = g.C / VEC;
-  for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += (long)gridDim.x * blockDim.x) {
-    const int cv = (int)(i % CV);
-    long t = i / CV;
-    const int w = (int)(t % g.W);
-    t /= g.W;
-    const int h = (int)(t % g.H);
-    const int n = (int)(t / g.H);
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < total; i += gridDim.x * blockDim.x) {
+    const int t1 = (int)fdiv((uint32_t)i, dCV);
+    const int cv = i - t1 * CV;
+    const int t2 = (int)fdiv((uint32_t)t1, dW);
+    const int w = t1 - t2 * g.W;
+    const int n = (int)fdiv((uint32_t)t2, dH);
+    const int h = t2 - n * g.H;
     const int hn = h + g.ph - g.kh + 1, wn = w + g.pw - g.kw + 1;
     const int p_lo = hn <= 0 ? 0 : (hn + g.sh - 1) / g.sh;
     const int q_lo = wn <= 0 ? 0 : (wn + g.sw - 1) / g.sw;
@@ -230,7 +235,7 @@ __global__ __launch_bounds__(256) void pool_bwd_nhwc_vec_kernel(PoolGeom g, int 
     for (int j = 0; j < VEC; ++j) acc[j] = 0.f;
     for (int p = p_lo; p <= p_hi; ++p) {
       for (int q = q_lo; q <= q_hi; ++q) {
-        const long o = (((long)n * g.P + p) * g.Q + q) * g.C + (long)cv * VEC;
+        const int o = ((n * g.P + p) * g.Q + q) * g.C + cv * VEC;
         union { uint4 u; T e[VEC]; } v;
         v.u = *(const uint4*)(dy + o);
         if (mode == 0) {
@@ -248,9 +253,14 @@ __global__ __launch_bounds__(256) void pool_bwd_nhwc_vec_kernel(PoolGeom g, int 
 #pragma unroll
             for (int j = 0; j < 4; ++j) am[j] = (uint8_t)(a >> (8 * j));
           }
+          union { uint4 u; T e[VEC]; } ym;
+          if constexpr (MASK) ym.u = *(const uint4*)(ymask + o);
 #pragma unroll
-          for (int j = 0; j < VEC; ++j)
-            if (am[j] == cell) acc[j] += ld_f<T>(&v.e[j]);
+          for (int j = 0; j < VEC; ++j) {
+            bool take = am[j] == cell;
+            if constexpr (MASK) take = take && ld_f<T>(&ym.e[j]) > 0.f;
+            if (take) acc[j] += ld_f<T>(&v.e[j]);
+          }
         } else {
           const float inv = 1.f / (float)pool_divisor(g, p, q);
 #pragma unroll
@@ -261,7 +271,7 @@ __global__ __launch_bounds__(256) void pool_bwd_nhwc_vec_kernel(PoolGeom g, int 
     union { uint4 u; T e[VEC]; } out;
 #pragma unroll
     for (int j = 0; j < VEC; ++j) st_f<T>(&out.e[j], acc[j]);
-    *(uint4*)(dx + i * VEC) = out.u;
+    *(uint4*)(dx + (size_t)i * VEC) = out.u;
   }
 }
 
@@ -433,27 +443,38 @@ hipError_t launch_pool_fwd(int dt, int mode, int N, int C, int H, int W, int P, 
 }
 
 hipError_t launch_pool_bwd(int dt, int mode, int N, int C, int H, int W, int P, int Q, int kh, int kw, int sh, int sw,
-                           int ph, int pw, const void* dy, const uint8_t* argmax, void* dx, int nchw, hipStream_t st) {
+                           int ph, int pw, const void* dy, const uint8_t* argmax, const void* ymask, void* dx,
+                           int nchw, hipStream_t st) {
   PoolGeom g{N, C, H, W, P, Q, kh, kw, sh, sw, ph, pw};
   const long total = (long)N * C * H * W;
   const int vec = dt == BF16 ? 8 : 4;
+  if (mode != 0) ymask = nullptr;
   const bool v = !nchw && C % vec == 0 && (uintptr_t)dy % 16 == 0 && (uintptr_t)dx % 16 == 0 &&
-                 (mode != 0 || (uintptr_t)argmax % vec == 0);
+                 (mode != 0 || (uintptr_t)argmax % vec == 0) && (uintptr_t)ymask % 16 == 0;
   TraceScope ts(mode == 0 ? "pool_bwd_kernel<max>" : "pool_bwd_kernel<avg>", st,
-                (double)N * C * P * Q * (dt_size(dt) + (mode == 0 ? 1 : 0)) + (double)total * dt_size(dt), WORK_BYTE);
+                (double)N * C * P * Q * (dt_size(dt) * (ymask ? 2 : 1) + (mode == 0 ? 1 : 0)) +
+                    (double)total * dt_size(dt),
+                WORK_BYTE);
   if (v) {
-    const unsigned grid = grid_for((size_t)(total / vec));
-    if (dt == BF16)
-      hipLaunchKernelGGL((pool_bwd_nhwc_vec_kernel<bf16_t, 8>), dim3(grid), dim3(256), 0, st, g, mode,
-                         (const bf16_t*)dy, argmax, (bf16_t*)dx, total / vec);
-    else
-      hipLaunchKernelGGL((pool_bwd_nhwc_vec_kernel<float, 4>), dim3(grid), dim3(256), 0, st, g, mode,
-                         (const float*)dy, argmax, (float*)dx, total / vec);
+    const int tv = (int)(total / vec);
+    const unsigned grid = grid_for((size_t)tv);
+    const FastDiv dCV = make_fastdiv((uint32_t)(C / vec)), dW = make_fastdiv((uint32_t)W),
+                  dH = make_fastdiv((uint32_t)H);
+#define POOL_BWD_VEC(T, VV, M)                                                                                   \
+  hipLaunchKernelGGL((pool_bwd_nhwc_vec_kernel<T, VV, M>), dim3(grid), dim3(256), 0, st, g, dCV, dW, dH, mode, \
+                     (const T*)dy, argmax, (const T*)ymask, (T*)dx, tv)
+    if (dt == BF16) {
+      if (ymask) POOL_BWD_VEC(bf16_t, 8, true); else POOL_BWD_VEC(bf16_t, 8, false);
+    } else {
+      if (ymask) POOL_BWD_VEC(float, 4, true); else POOL_BWD_VEC(float, 4, false);
+    }
+#undef POOL_BWD_VEC
     return hipGetLastError();
   }
   const unsigned grid = grid_for((size_t)total);
-#define POOL_BWD(T, L) \
-  hipLaunchKernelGGL((pool_bwd_kernel<T, L>), dim3(grid), dim3(256), 0, st, g, mode, (const T*)dy, argmax, (T*)dx, total)
+#define POOL_BWD(T, L)                                                                                           \
+  hipLaunchKernelGGL((pool_bwd_kernel<T, L>), dim3(grid), dim3(256), 0, st, g, mode, (const T*)dy, argmax,      \
+                     (const T*)ymask, (T*)dx, total)
   if (dt == BF16) {
     if (nchw) POOL_BWD(bf16_t, true); else POOL_BWD(bf16_t, false);
   } else {

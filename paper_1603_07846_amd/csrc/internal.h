@@ -42,9 +42,12 @@ struct ConvShape {
 // the algorithmic work of the layer pass this launch carries out.  When the
 // output tiles cannot fill the GPU and `partial` (fwd_partial_bytes() of
 // workspace) is given, the taps are split across workgroups and a second
-// kernel adds the fp32 partial tiles in a fixed order.
+// kernel adds the fp32 partial tiles in a fixed order.  `mask` (optional, the
+// shape of y) zeroes each output whose mask value is <= 0: the backward of a
+// ReLU whose output is `mask`, folded into the store.
 hipError_t launch_conv_fwd(int dt, const ConvShape& s, const void* x, const void* w, const float* bias,
-                           void* y, int relu, int bwd, double flops, float* partial, hipStream_t st);
+                           void* y, int relu, int bwd, double flops, float* partial, const void* mask,
+                           hipStream_t st);
 size_t fwd_partial_bytes(const ConvShape& s, int dt);
 
 // Split-K implicit-GEMM filter gradient.  Number of K-splits used for a shape
@@ -74,7 +77,7 @@ hipError_t launch_transpose(int dt, const void* in, void* out, int batch, int ro
 
 // Direct (gather) backward-data for any stride: dx = conv^T(dy, w).
 hipError_t launch_conv_bwd_data_direct(int dt, const ConvShape& s, const void* dy, const void* w, void* dx,
-                                       hipStream_t st);
+                                       const void* mask, hipStream_t st);
 
 // Zero-pad the innermost (channel) dimension: in [rows][C] -> out [rows][Cp],
 // Cp a multiple of the 16-byte vector width.
@@ -93,9 +96,12 @@ hipError_t launch_krsc_to_kcrs_f32(const float* in, float* out, int K, int C, in
 hipError_t launch_pool_fwd(int dt, int mode, int N, int C, int H, int W, int P, int Q, int kh, int kw, int sh,
                            int sw, int ph, int pw, const void* x, void* y, uint8_t* argmax, int nchw,
                            hipStream_t st);
+// ymask (MAX only, optional): the pooling's forward output; a window routes
+// its gradient only when its maximum is > 0 (ReLU backward on the pooling's
+// input folded in: the input equals the maximum at the arg-max cell).
 hipError_t launch_pool_bwd(int dt, int mode, int N, int C, int H, int W, int P, int Q, int kh, int kw, int sh,
-                           int sw, int ph, int pw, const void* dy, const uint8_t* argmax, void* dx, int nchw,
-                           hipStream_t st);
+                           int sw, int ph, int pw, const void* dy, const uint8_t* argmax, const void* ymask,
+                           void* dx, int nchw, hipStream_t st);
 hipError_t launch_relu_fwd(int dt, size_t n, const void* x, void* y, hipStream_t st);
 hipError_t launch_relu_bwd(int dt, size_t n, const void* y, const void* dy, void* dx, hipStream_t st);
 hipError_t launch_softmax_ce(int dt, int B, int classes, const void* z, const int32_t* labels, float* loss,

@@ -70,6 +70,7 @@ class ConvLayer(Layer):
         self.w_shape = (self.K, self.R, self.S, C)
         self.out_shape = singa.conv_out_shape(self.in_shape, self.w_shape, self.pad, self.stride)
         self.relu = False  # set when a ReLU layer directly follows and is fused
+        self.relu_src = None  # the ReLU layer feeding this one, whose backward bwd-data folds in
         dev, dt = net.device, net.dtype
         self.y = torch.empty(self.out_shape, dtype=dt, device=dev)
         self.dx = torch.empty(self.in_shape, dtype=dt, device=dev)
@@ -93,7 +94,8 @@ class ConvLayer(Layer):
         if not need_dx:
             return None
         singa.conv_bwd_data(dy, self.w_compute, self.in_shape, self.pad, self.stride, out=self.dx,
-                            workspace=self.net.workspace)
+                            workspace=self.net.workspace,
+                            relu_y=None if self.relu_src is None else self.relu_src.y)
         return self.dx
 
 
@@ -108,6 +110,7 @@ class PoolLayer(Layer):
         self.y = torch.empty(self.out_shape, dtype=dt, device=dev)
         self.argmax = torch.empty(self.out_shape, dtype=torch.uint8, device=dev) if self.mode == "max" else None
         self.dx = torch.empty(self.in_shape, dtype=dt, device=dev)
+        self.relu_src = None  # the ReLU layer feeding this max pooling, whose backward folds in
 
     def compute_feature(self, x):
         singa.pool_fwd(x, self.mode, self.k, self.stride, self.pad, self.ceil, out=self.y, argmax=self.argmax)
@@ -115,7 +118,7 @@ class PoolLayer(Layer):
 
     def compute_gradient(self, dy, need_dx=True):
         singa.pool_bwd(dy, self.argmax, self.in_shape, self.mode, self.k, self.stride, self.pad, self.ceil,
-                       out=self.dx)
+                       out=self.dx, relu_y=None if self.relu_src is None else self.y)
         return self.dx
 
 
@@ -123,6 +126,7 @@ class ReluLayer(Layer):
     def __init__(self, net, spec, in_shape, fused_into: Optional[ConvLayer]):
         self.name = spec.name
         self.fused = fused_into
+        self.folded = False  # backward done by the consuming layer (set by Net)
         self.out_shape = tuple(in_shape)
         self.y = None
         if fused_into is None:
@@ -136,6 +140,8 @@ class ReluLayer(Layer):
         return self.y
 
     def compute_gradient(self, dy, need_dx=True):
+        if self.folded:
+            return dy  # the consuming layer already produced the gradient at this ReLU's input
         # in place on the incoming gradient buffer
         return singa.relu_bwd(self.y, dy, out=dy)
 
@@ -187,6 +193,12 @@ class Net:
                 layer = SoftmaxCELayer(self, spec, shape)
             else:
                 raise TypeError(spec)
+            # a convolution's backward-data or a max pooling's backward can
+            # also apply the backward of the ReLU that feeds it
+            if isinstance(prev, ReluLayer) and (isinstance(layer, ConvLayer) or
+                                               (isinstance(layer, PoolLayer) and layer.mode == "max")):
+                layer.relu_src = prev
+                prev.folded = True
             self.layers.append(layer)
             shape = layer.out_shape
             prev = layer

@@ -79,10 +79,10 @@ def _lib():
         lib.singa_pool_out_shape.argtypes = [S4, PD, S4]
         lib.singa_conv_workspace_bytes.argtypes = [i32, i32, i32, S4, F4, CD, ctypes.POINTER(sz)]
         lib.singa_conv_fwd.argtypes = [i32, i32, S4, vp, F4, vp, vp, CD, vp, i32, vp, sz, vp]
-        lib.singa_conv_bwd_data.argtypes = [i32, i32, S4, F4, vp, CD, vp, vp, vp, sz, vp]
+        lib.singa_conv_bwd_data.argtypes = [i32, i32, S4, F4, vp, CD, vp, vp, vp, vp, sz, vp]
         lib.singa_conv_bwd_filter.argtypes = [i32, i32, S4, vp, F4, CD, vp, vp, vp, i32, vp, sz, vp]
         lib.singa_pool_fwd.argtypes = [i32, i32, S4, vp, PD, vp, vp, vp]
-        lib.singa_pool_bwd.argtypes = [i32, i32, S4, PD, vp, vp, vp, vp]
+        lib.singa_pool_bwd.argtypes = [i32, i32, S4, PD, vp, vp, vp, vp, vp]
         lib.singa_relu_fwd.argtypes = [i32, sz, vp, vp, vp]
         lib.singa_relu_bwd.argtypes = [i32, sz, vp, vp, vp, vp]
         lib.singa_softmax_ce.argtypes = [i32, i32, i32, vp, vp, vp, vp, vp]
@@ -215,16 +215,20 @@ def conv_fwd(x, w, bias=None, pad=0, stride=1, relu=False, layout="NHWC", out=No
     return y
 
 
-def conv_bwd_data(dy, w, x_shape, pad=0, stride=1, layout="NHWC", out=None, workspace=None):
-    """Convolution ComputeGradient, gradient w.r.t. the source layer's blob."""
+def conv_bwd_data(dy, w, x_shape, pad=0, stride=1, layout="NHWC", out=None, workspace=None, relu_y=None):
+    """Convolution ComputeGradient, gradient w.r.t. the source layer's blob.
+
+    relu_y: the output of a ReLU that is the source layer (shape x_shape); the
+    result is then the gradient at that ReLU's input (its ComputeGradient
+    folded into this call)."""
     lay = _layout(layout)
     dx = torch.empty(tuple(x_shape), dtype=dy.dtype, device=dy.device) if out is None else out
     nbytes = conv_workspace_bytes(OP_BWD_DATA, _dt(dy), tuple(x_shape), tuple(w.shape), pad, stride, lay)
     ws = _workspace(nbytes, dy.device, workspace)
     _check("singa_conv_bwd_data", _lib().singa_conv_bwd_data(
         _dt(dy), lay, ctypes.byref(_act_shape4(x_shape, lay)), ctypes.byref(_filt4(w.shape, lay)), _ptr(w),
-        ctypes.byref(_cdesc(pad, stride)), _ptr(dy), _ptr(dx), _ptr(ws), 0 if ws is None else ws.numel(),
-        _stream()))
+        ctypes.byref(_cdesc(pad, stride)), _ptr(dy), _ptr(relu_y), _ptr(dx), _ptr(ws),
+        0 if ws is None else ws.numel(), _stream()))
     return dx
 
 
@@ -268,13 +272,16 @@ def pool_fwd(x, mode, k=3, stride=2, pad=0, ceil_mode=True, layout="NHWC", out=N
     return y, (argmax if d.mode == POOL_MAX else None)
 
 
-def pool_bwd(dy, argmax, x_shape, mode, k=3, stride=2, pad=0, ceil_mode=True, layout="NHWC", out=None):
+def pool_bwd(dy, argmax, x_shape, mode, k=3, stride=2, pad=0, ceil_mode=True, layout="NHWC", out=None, relu_y=None):
+    """Pooling ComputeGradient.  relu_y (max pooling): the pooling's own output,
+    when its input is a ReLU's output; the result is then the gradient at that
+    ReLU's input."""
     lay = _layout(layout)
     d = _pdesc(mode, k, stride, pad, ceil_mode)
     dx = torch.empty(tuple(x_shape), dtype=dy.dtype, device=dy.device) if out is None else out
     _check("singa_pool_bwd", _lib().singa_pool_bwd(
         _dt(dy), lay, ctypes.byref(_act_shape4(x_shape, lay)), ctypes.byref(d), _ptr(dy),
-        _ptr(argmax if d.mode == POOL_MAX else None), _ptr(dx), _stream()))
+        _ptr(argmax if d.mode == POOL_MAX else None), _ptr(relu_y), _ptr(dx), _stream()))
     return dx
 
 

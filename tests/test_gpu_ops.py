@@ -174,6 +174,79 @@ def test_pool(case, layout, dt):
     assert rel_l2(dev_to_nchw(dx, layout), ref_dx) <= TOL[dt]
 
 
+# ReLU backward folded into the pooling backward: the pooling's input is a
+# ReLU output (many zeros, hence all-zero windows whose maximum is 0).
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("layout", ["NHWC", "NCHW"])
+@pytest.mark.parametrize("case", [c for c in POOL_CASES if c[4] == "max"], ids=_ids([c for c in POOL_CASES
+                                                                                      if c[4] == "max"]))
+def test_pool_bwd_relu_folded(case, layout, dt):
+    N, C, H, W, mode, k, s, p = case
+    x = np.maximum(wl.random_array((N, C, H, W), 62, "normal", 1.0, dt), 0.0)
+    ref_y, ref_am = oracle.pool_fwd(x, oracle.MAX, k, s, p, True)
+    y, am = singa.pool_fwd(nchw_to_dev(x, dt, layout), mode, k, s, p, True, layout=layout)
+    dy = wl.random_array(ref_y.shape, 63, "normal", 1.0, dt)
+    dx = singa.pool_bwd(nchw_to_dev(dy, dt, layout), am, phys(x.shape, layout), mode, k, s, p, True, layout=layout,
+                        relu_y=y)
+    torch.cuda.synchronize()
+    ref_dx = oracle.relu_bwd(x, oracle.pool_bwd(dy, ref_am, x.shape, oracle.MAX, k, s, p, True))
+    got = dev_to_nchw(dx, layout)
+    np.testing.assert_array_equal(got[x <= 0], 0.0)
+    assert rel_l2(got, ref_dx) <= TOL[dt]
+
+
+def test_pool_bwd_relu_folded_rejects_avg():
+    x = nchw_to_dev(np.ones((1, 8, 5, 5)), "f32")
+    y, _ = singa.pool_fwd(x, "avg", 3, 2, 0, True)
+    with pytest.raises(singa.SingaError):
+        singa.pool_bwd(y, None, tuple(x.shape), "avg", 3, 2, 0, True, relu_y=y)
+
+
+# ReLU backward folded into the backward-data pass: the layer's input is a
+# ReLU output.  Covers the GEMM path (3x3 and 1x1), the dense geometry with
+# split-K, the strided gather kernel and the 256 x 128 bf16 kernel.
+RELU_FOLD_CASES = [
+    (2, 12, 9, 9, 20, 3, 3, 1, 1),
+    (5, 256, 2, 2, 520, 2, 2, 0, 1),
+    (3, 32, 17, 17, 40, 3, 3, 1, 2),
+    (2, 16, 6, 5, 12, 1, 1, 0, 1),
+]
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("layout", ["NHWC", "NCHW"])
+@pytest.mark.parametrize("case", RELU_FOLD_CASES, ids=_ids(RELU_FOLD_CASES))
+def test_conv_bwd_data_relu_folded(case, layout, dt):
+    N, C, H, W, K, R, S, pad, stride = case
+    x, w, b, dy = _conv_inputs(case, dt, 90)
+    xr = np.maximum(x, 0.0)
+    ref = oracle.relu_bwd(xr, oracle.conv_bwd_data(dy, w, x.shape, pad=pad, stride=stride))
+    dx = singa.conv_bwd_data(nchw_to_dev(dy, dt, layout), kcrs_to_dev(w, dt, layout), phys(x.shape, layout),
+                             pad, stride, layout=layout, relu_y=nchw_to_dev(xr, dt, layout))
+    torch.cuda.synchronize()
+    got = dev_to_nchw(dx, layout)
+    np.testing.assert_array_equal(got[xr <= 0], 0.0)
+    assert rel_l2(got, ref) <= TOL[dt], case
+
+
+def test_conv_bwd_data_relu_folded_large_tile():
+    case = (16, 200, 47, 47, 64, 3, 3, 1, 1)
+    N, C, H, W, K, R, S, pad, stride = case
+    x, w, b, dy = _conv_inputs(case, "bf16", 91)
+    xr = np.maximum(x, 0.0)
+    singa.trace_enable(True)
+    dx = singa.conv_bwd_data(nchw_to_dev(dy, "bf16"), kcrs_to_dev(w, "bf16"), phys(x.shape), pad, stride,
+                             relu_y=nchw_to_dev(xr, "bf16"))
+    torch.cuda.synchronize()
+    names = [r[0] for r in singa.trace_records()]
+    singa.trace_enable(False)
+    assert any(n.startswith("conv_fwd_large_kernel") for n in names), names
+    ref = oracle.relu_bwd(xr, oracle.conv_bwd_data(dy, w, x.shape, pad=pad, stride=stride))
+    got = dev_to_nchw(dx)
+    np.testing.assert_array_equal(got[xr <= 0], 0.0)
+    assert rel_l2(got, ref) <= TOL["bf16"]
+
+
 @pytest.mark.parametrize("dt", ["f32", "bf16"])
 @pytest.mark.parametrize("n", [1, 7, 8, 1000, 4099, 1 << 20])
 def test_relu(n, dt):

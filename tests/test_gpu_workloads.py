@@ -275,13 +275,20 @@ def test_backward_teacher_forced(index, batch):
             np.testing.assert_array_equal(_nhwc_to_nchw(got),
                                           grads["grad_in"][spec.name].astype(np.float32).astype(np.float64))
             continue
+        below_relu = li > 0 and isinstance(layers[li - 1], wl.Relu)
         if isinstance(spec, wl.Pool):
             shape = (xin.shape[0], xin.shape[2], xin.shape[3], xin.shape[1])
-            _, am = singa.pool_fwd(_dev(xin, dt), spec.mode, spec.kernel, spec.stride, spec.pad, spec.ceil_mode)
+            yp, am = singa.pool_fwd(_dev(xin, dt), spec.mode, spec.kernel, spec.stride, spec.pad, spec.ceil_mode)
             got = singa.pool_bwd(_dev(up, dt), am, shape, spec.mode, spec.kernel, spec.stride, spec.pad,
                                  spec.ceil_mode)
             torch.cuda.synchronize()
             errs["dx:" + spec.name] = rel_l2(_nhwc_to_nchw(got), grads["grad_in"][spec.name])
+            if below_relu and spec.mode == "max":
+                # the ReLU below folded in: the gradient at the ReLU's input
+                got = singa.pool_bwd(_dev(up, dt), am, shape, spec.mode, spec.kernel, spec.stride, spec.pad,
+                                     spec.ceil_mode, relu_y=yp)
+                torch.cuda.synchronize()
+                errs["dx+relu:" + spec.name] = rel_l2(_nhwc_to_nchw(got), grads["grad_in"][layers[li - 1].name])
             continue
         wk, bk = params[pi[spec.name]]
         if isinstance(spec, wl.FC):
@@ -303,6 +310,12 @@ def test_backward_teacher_forced(index, batch):
         rdx = grads["grad_in"][spec.name]
         if rdx is not None:
             errs["dx:" + spec.name] = rel_l2(_nhwc_to_nchw(dx), rdx.reshape(xin.shape))
+        if below_relu:
+            # the ReLU below folded in (its output is this layer's input)
+            dxr = singa.conv_bwd_data(upd, wd, tuple(xd.shape), pad, stride, relu_y=xd)
+            torch.cuda.synchronize()
+            rr = grads["grad_in"][layers[li - 1].name]
+            errs["dx+relu:" + spec.name] = rel_l2(_nhwc_to_nchw(dxr), rr.reshape(xin.shape))
     bad = {k: v for k, v in errs.items() if not v <= TOL[dt]}
     print("workload %d teacher-forced worst rel-L2: %s" % (index, max(errs.items(), key=lambda kv: kv[1])))
     assert not bad, bad
