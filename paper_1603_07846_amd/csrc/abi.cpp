@@ -104,7 +104,7 @@ inline int padded_channels(const ConvShape& s, int dt) {
 // the two can never disagree.
 struct FwdWs { void *x, *w, *y, *xp, *wp; float* partial; };
 struct BwdDataWs { void *dy, *w, *wt, *dx; float* partial; };
-struct BwdFilterWs { void *x, *dy, *xp; float *dw, *dwp, *partial, *colsum; };
+struct BwdFilterWs { void *x, *dy, *xp; float *dw, *dwp, *partial; };
 
 size_t carve_fwd(const ConvShape& s, int dt, int layout, void* ws, FwdWs* o) {
   Carve c(ws);
@@ -159,7 +159,7 @@ size_t carve_bwd_data(const ConvShape& s, int dt, int layout, void* ws, BwdDataW
   return c.used;
 }
 
-size_t carve_bwd_filter(const ConvShape& s, int dt, int layout, void* ws, BwdFilterWs* o) {
+size_t carve_bwd_filter(const ConvShape& s, int dt, int layout, bool bias, void* ws, BwdFilterWs* o) {
   Carve c(ws);
   o->x = o->dy = o->xp = nullptr;
   o->dw = o->dwp = nullptr;
@@ -175,9 +175,8 @@ size_t carve_bwd_filter(const ConvShape& s, int dt, int layout, void* ws, BwdFil
     o->xp = c.take((size_t)s.N * s.H * s.W * cp * dt_size(dt));
     o->dwp = (float*)c.take((size_t)s.K * s.R * s.S * cp * sizeof(float));
   }
-  if (wgrad_splits(g, dt) > 1) o->partial = (float*)c.take(wgrad_partial_bytes(g, dt));
+  if (wgrad_splits(g, dt, bias) > 1) o->partial = (float*)c.take(wgrad_partial_bytes(g, dt, bias));
   else o->partial = nullptr;
-  o->colsum = (float*)c.take(colsum_partial_bytes(s.N * s.P * s.Q, s.K));
   return c.used;
 }
 
@@ -249,7 +248,7 @@ int singa_conv_workspace_bytes(int op, singa_dtype dtype, singa_layout layout, c
   switch (op) {
     case SINGA_OP_FWD: { FwdWs o; *bytes = carve_fwd(s, dtype, layout, nullptr, &o); break; }
     case SINGA_OP_BWD_DATA: { BwdDataWs o; *bytes = carve_bwd_data(s, dtype, layout, nullptr, &o); break; }
-    case SINGA_OP_BWD_FILTER: { BwdFilterWs o; *bytes = carve_bwd_filter(s, dtype, layout, nullptr, &o); break; }
+    case SINGA_OP_BWD_FILTER: { BwdFilterWs o; *bytes = carve_bwd_filter(s, dtype, layout, true, nullptr, &o); break; }
     default: return SINGA_ERR_UNSUPPORTED;
   }
   return SINGA_OK;
@@ -348,9 +347,10 @@ int singa_conv_bwd_filter(singa_dtype dtype, singa_layout layout, const singa_sh
       !aligned_to(ws, 16))
     return SINGA_ERR_ALIGN;
   BwdFilterWs o;
-  const size_t need = carve_bwd_filter(s, dtype, layout, nullptr, &o);
-  if (!ws || ws_bytes < need) return SINGA_ERR_WORKSPACE;
-  carve_bwd_filter(s, dtype, layout, ws, &o);
+  const bool bias = db != nullptr;
+  const size_t need = carve_bwd_filter(s, dtype, layout, bias, nullptr, &o);
+  if (need > 0 && (!ws || ws_bytes < need)) return SINGA_ERR_WORKSPACE;
+  carve_bwd_filter(s, dtype, layout, bias, ws, &o);
   hipStream_t st = (hipStream_t)stream;
   hipError_t e = hipSuccess;
   const void* xx = x_ptr;
@@ -369,17 +369,17 @@ int singa_conv_bwd_filter(singa_dtype dtype, singa_layout layout, const singa_sh
     if (e == hipSuccess) e = launch_pad_channels(dtype, xx, o.xp, (long)s.N * s.H * s.W, s.C, cp, st);
     xx = o.xp;
   }
-  const size_t nw = (size_t)g.K * g.R * g.S * g.C;
-  const int splits = wgrad_splits(g, dtype);
+  const int splits = wgrad_splits(g, dtype, bias);
   float* krsc = layout == SINGA_NHWC ? dw : o.dw;  // KRSC result
   const int acc = layout == SINGA_NHWC ? accumulate : 0;
   float* target = cp ? o.dwp : krsc;  // the GEMM's (K, R, S, g.C) result
   const int tacc = cp ? 0 : acc;
-  if (e == hipSuccess) e = launch_conv_wgrad(dtype, g, xx, dy, o.partial, target, tacc, st);
-  if (e == hipSuccess && splits > 1) e = launch_splitk_reduce(o.partial, splits, nw, target, tacc, st);
+  // db is written in place by the GEMM's bias column, with the caller's accumulate
+  if (e == hipSuccess) e = launch_conv_wgrad(dtype, g, xx, dy, o.partial, target, db, tacc, accumulate, st);
+  if (e == hipSuccess && splits > 1)
+    e = launch_splitk_reduce(o.partial, splits, g, bias, target, db, tacc, accumulate, st);
   if (e == hipSuccess && cp) e = launch_unpad_channels_f32(o.dwp, krsc, (long)s.K * s.R * s.S, cp, s.C, acc, st);
   if (e == hipSuccess && layout == SINGA_NCHW) e = launch_krsc_to_kcrs_f32(o.dw, dw, s.K, s.C, s.R, s.S, accumulate, st);
-  if (e == hipSuccess && db) e = launch_colsum(dtype, dy, s.N * s.P * s.Q, s.K, o.colsum, db, accumulate, st);
   return hip_status(e);
 }
 

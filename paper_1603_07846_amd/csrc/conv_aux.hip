@@ -81,77 +81,6 @@ __global__ __launch_bounds__(256) void bwd_data_direct_kernel(ConvShape s, const
   }
 }
 
-// Bias gradient db[col] = sum over rows of a[row][col], in two passes with a
-// fixed summation order (no atomics, bitwise reproducible).
-// Pass 1: block (bx, by) takes rows [bx*rc, (bx+1)*rc) and column vectors
-// [by*256, by*256 + 256).  Its threads form TC column lanes (each VEC
-// consecutive columns) x TR row lanes; row lane r sums rows r, r + TR, ...
-// of the chunk, then the TR lanes are added in lane order.
-template <typename T, int VEC>
-__global__ __launch_bounds__(256) void colsum_partial_kernel(const T* __restrict__ a, int rows, int cols, int rc,
-                                                             float* __restrict__ partial) {
-  __shared__ float red[256 * VEC];
-  const int nvec = cols / VEC;                       // column vectors in a row
-  const int cv0 = blockIdx.y * 256;
-  const int ncv = min(256, nvec - cv0);              // column vectors of this block
-  const int TC = ncv;                                // column lanes
-  const int TR = 256 / TC;                           // row lanes
-  const int tc = threadIdx.x % TC, tr = threadIdx.x / TC;
-  const int r0 = blockIdx.x * rc, r1 = min(rows, r0 + rc);
-  const int cv = cv0 + tc;
-  float acc[VEC];
-#pragma unroll
-  for (int j = 0; j < VEC; ++j) acc[j] = 0.f;
-  if (tr < TR) {
-    for (int r = r0 + tr; r < r1; r += TR) {
-      const T* src = a + (long)r * cols + (long)cv * VEC;
-      if constexpr (VEC == 1) {
-        acc[0] += ld_f<T>(src);
-      } else {
-        union { uint4 u; T e[VEC]; } v;
-        v.u = *(const uint4*)src;
-#pragma unroll
-        for (int j = 0; j < VEC; ++j) acc[j] += ld_f<T>(&v.e[j]);
-      }
-    }
-  }
-#pragma unroll
-  for (int j = 0; j < VEC; ++j) red[threadIdx.x * VEC + j] = acc[j];
-  __syncthreads();
-  if (threadIdx.x < TC) {
-#pragma unroll
-    for (int j = 0; j < VEC; ++j) {
-      float t = 0.f;
-      for (int l = 0; l < TR; ++l) t += red[(l * TC + threadIdx.x) * VEC + j];
-      partial[(long)blockIdx.x * cols + (long)cv * VEC + j] = t;
-    }
-  }
-}
-
-// Rows per pass-1 chunk: about 64K elements per block, 16 to 1024 rows.
-int colsum_rows_per_chunk(int cols) {
-  int rc = 1024;
-  while (rc > 16 && (long)rc * cols > 65536) rc >>= 1;
-  return rc;
-}
-
-// Pass 2: one block per column; thread t sums chunks t, t + 256, ... in order,
-// then a fixed-shape tree adds the 256 thread sums.
-__global__ __launch_bounds__(256) void colsum_final_kernel(const float* __restrict__ partial, int chunks, int cols,
-                                                           float* __restrict__ out, int accumulate) {
-  __shared__ float red[256];
-  const int c = blockIdx.x;
-  float s = 0.f;
-  for (int k = threadIdx.x; k < chunks; k += 256) s += partial[(long)k * cols + c];
-  red[threadIdx.x] = s;
-  __syncthreads();
-  for (int w = 128; w > 0; w >>= 1) {
-    if (threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
-    __syncthreads();
-  }
-  if (threadIdx.x == 0) out[c] = (accumulate ? out[c] : 0.f) + red[0];
-}
-
 template <typename T>
 __global__ __launch_bounds__(256) void nchw_to_nhwc_kernel(const T* __restrict__ in, T* __restrict__ out, int C,
                                                            int HW) {
@@ -207,8 +136,6 @@ __global__ __launch_bounds__(256) void krsc_to_kcrs_kernel(const float* __restri
   }
 }
 
-// out[r][c] = c < C ? in[r][c] : 0 for c < Cp: one thread per 16-byte output
-// vector (Cp is a multiple of the vector width).
 // out[r][c] = in[r][c] for c < C, 0 for C <= c < Cp (Cp % 4 == 0): one
 // thread per 4-channel chunk of an output row, stored as one vector.
 template <typename T>
@@ -275,46 +202,6 @@ hipError_t launch_conv_bwd_data_direct(int dt, const ConvShape& s, const void* d
   else
     hipLaunchKernelGGL(bwd_data_direct_kernel<float>, dim3(g), dim3(256), 0, st, s, (const float*)dy,
                        (const float*)w, (const float*)mask, (float*)dx, total);
-  return hipGetLastError();
-}
-
-size_t colsum_partial_bytes(int rows, int cols) {
-  const int rc = colsum_rows_per_chunk(cols);
-  const size_t chunks = ((size_t)rows + rc - 1) / rc;
-  return chunks * (size_t)cols * sizeof(float);
-}
-
-hipError_t launch_colsum(int dt, const void* a, int rows, int cols, float* partial, float* out, int accumulate,
-                         hipStream_t st) {
-  const int rc = colsum_rows_per_chunk(cols);
-  const int chunks = (rows + rc - 1) / rc;
-  const size_t es = dt_size(dt);
-  const int vec = (int)(16 / es);
-  const bool v = (cols % vec) == 0 && ((uintptr_t)a % 16) == 0;
-  const int nvec = v ? cols / vec : cols;
-  const dim3 grid(chunks, (nvec + 255) / 256);
-  {
-    TraceScope ts("colsum_partial_kernel", st, (double)rows * cols * es + 4.0 * chunks * cols, WORK_BYTE);
-    if (dt == BF16) {
-      if (v)
-        hipLaunchKernelGGL((colsum_partial_kernel<bf16_t, 8>), grid, dim3(256), 0, st, (const bf16_t*)a, rows, cols,
-                           rc, partial);
-      else
-        hipLaunchKernelGGL((colsum_partial_kernel<bf16_t, 1>), grid, dim3(256), 0, st, (const bf16_t*)a, rows, cols,
-                           rc, partial);
-    } else {
-      if (v)
-        hipLaunchKernelGGL((colsum_partial_kernel<float, 4>), grid, dim3(256), 0, st, (const float*)a, rows, cols, rc,
-                           partial);
-      else
-        hipLaunchKernelGGL((colsum_partial_kernel<float, 1>), grid, dim3(256), 0, st, (const float*)a, rows, cols, rc,
-                           partial);
-    }
-  }
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  TraceScope ts("colsum_final_kernel", st, 4.0 * chunks * cols + 4.0 * cols * (accumulate ? 2 : 1), WORK_BYTE);
-  hipLaunchKernelGGL(colsum_final_kernel, dim3(cols), dim3(256), 0, st, partial, chunks, cols, out, accumulate);
   return hipGetLastError();
 }
 

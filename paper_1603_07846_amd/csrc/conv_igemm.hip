@@ -55,6 +55,10 @@ template <typename T> __device__ __forceinline__ void set_elem(V16& v, int j, T 
 template <> __device__ __forceinline__ void set_elem<float>(V16& v, int j, float e) { v.f[j] = e; }
 template <> __device__ __forceinline__ void set_elem<bf16_t>(V16& v, int j, bf16_t e) { v.h[j] = e; }
 
+template <typename T> __device__ __forceinline__ T one_elem();
+template <> __device__ __forceinline__ float one_elem<float>() { return 1.f; }
+template <> __device__ __forceinline__ bf16_t one_elem<bf16_t>() { return (bf16_t)0x3f80; }
+
 template <typename T> __device__ __forceinline__ T zero_elem();
 template <> __device__ __forceinline__ float zero_elem<float>() { return 0.f; }
 template <> __device__ __forceinline__ bf16_t zero_elem<bf16_t>() { return (bf16_t)0; }
@@ -670,17 +674,21 @@ template <> struct WG<float> {
 };
 constexpr int WSMEM = 2 * 2 * 64 * 320;  // 2 stages x 2 operands (equal for both dtypes)
 
+// With a bias, the GEMM gets one more column, Ng = Nn + 1, whose operand is
+// 1 for every reduction index: its results are db[k] = sum_t dy[t][k].
 struct WgradArgs {
   const void* x;
   const void* dy;
-  float* out;  // partial tiles [splits][M][Nn], or dw itself when direct
+  float* out;  // partial tiles [splits][M][Ng], or dw itself when direct
+  float* db;   // direct: the bias gradient (column Nn); NULL without bias
   uint32_t x_bytes, dy_bytes;
-  int M, Nn, T;  // M = K filters, Nn = R*S*C taps, T = N*P*Q
+  int M, Nn, Ng, T;  // M = K filters, Nn = R*S*C taps, Ng = Nn (+1 with bias), T = N*P*Q
+  int ldp;           // row stride of the partial tiles: Ng rounded up to 64 (256-byte rows)
   int N, H, W, C, S, P, Q;
   int sh, sw, ph, pw;
   FastDiv dN, dQ, dC, dS;
   int tiles, tiles_n, kt_per_split, nkt;
-  int direct, accumulate;
+  int direct, acc_dw, acc_db;
 };
 
 __device__ __forceinline__ v4i16 lds_tr16(const char* p) {
@@ -769,6 +777,12 @@ __global__ __launch_bounds__(NT) void conv_wgrad_kernel(WgradArgs a) {
   const int PQ = a.P * a.Q;
   const int ystride = PQ * a.M;            // dy elements per image
   const int xstride = a.H * a.W * a.C;     // x elements per image
+  // position of the bias column Nn in this thread's chunk, or -1, and the
+  // chunk with a 1 there (static indexing: no register array in scratch)
+  const int ones = (a.Ng > a.Nn && j0 <= a.Nn && a.Nn < j0 + VEC) ? a.Nn - j0 : -1;
+  V16 onesv;
+#pragma unroll
+  for (int e = 0; e < VEC; ++e) set_elem<T>(onesv, e, e == ones ? one_elem<T>() : zero_elem<T>());
   // taps of the x chunk, fixed for the whole reduction: NG groups of GS
   // consecutive channels of one tap (r, s) each
   constexpr int NG = BMD == VEC16 ? 1 : BMD == VEC8 ? 2 : VEC;
@@ -852,13 +866,22 @@ __global__ __launch_bounds__(NT) void conv_wgrad_kernel(WgradArgs a) {
       }
     }
   };
+  // The bias column is OR-ed in as the tile goes to LDS (its element was
+  // loaded as an out-of-range zero), not at load time, so the loads stay in
+  // flight across the MFMAs.  Rows past the end hold dy = 0, so the column
+  // can be 1 there too.
   auto store_tile = [&](int stage, const V16 (&ra)[4], const V16 (&rb)[4]) {
     char* As = smem + stage * 2 * OPB;
     char* Bs = As + OPB;
 #pragma unroll
     for (int v = 0; v < 4; ++v) {
       *(uint4*)(As + (r0 + RPP * v) * PIT + ch * 16) = ra[v].u;
-      *(uint4*)(Bs + (r0 + RPP * v) * PIT + ch * 16) = rb[v].u;
+      uint4 b = rb[v].u;
+      b.x |= onesv.u.x;
+      b.y |= onesv.u.y;
+      b.z |= onesv.u.z;
+      b.w |= onesv.u.w;
+      *(uint4*)(Bs + (r0 + RPP * v) * PIT + ch * 16) = b;
     }
   };
 
@@ -891,43 +914,69 @@ __global__ __launch_bounds__(NT) void conv_wgrad_kernel(WgradArgs a) {
     if (k < nk) mma_tile_tmajor<T>(smem, smem + OPB, acc, wm, wn, lane);  // odd count: last tile in stage 0
   }
 
-  float* __restrict__ out = a.direct ? a.out : a.out + (size_t)split * a.M * a.Nn;
   const int li = lane & 31, lh = lane >> 5;
+  if (!a.direct) {
+    float* __restrict__ out = a.out + (size_t)split * a.M * a.ldp;
+#pragma unroll
+    for (int bn = 0; bn < 2; ++bn) {
+      const int col = n0 + wn * 64 + bn * 32 + li;
+      if (col >= a.Ng) continue;
+#pragma unroll
+      for (int bm = 0; bm < 2; ++bm)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int row = m0 + wm * 64 + bm * 32 + (v >> 2) * 8 + lh * 4 + (v & 3);
+          if (row < a.M) out[(size_t)row * a.ldp + col] = acc[bm][bn][v];
+        }
+    }
+    return;
+  }
 #pragma unroll
   for (int bn = 0; bn < 2; ++bn) {
     const int col = n0 + wn * 64 + bn * 32 + li;
-    if (col >= a.Nn) continue;
+    if (col >= a.Ng) continue;
+    const bool is_db = col == a.Nn;
+    float* __restrict__ base = is_db ? a.db : a.out + col;
+    const size_t stride = is_db ? 1 : (size_t)a.Nn;
+    const int accum = is_db ? a.acc_db : a.acc_dw;
 #pragma unroll
-    for (int bm = 0; bm < 2; ++bm) {
+    for (int bm = 0; bm < 2; ++bm)
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
         const int row = m0 + wm * 64 + bm * 32 + (v >> 2) * 8 + lh * 4 + (v & 3);
         if (row < a.M) {
-          float* o = out + (size_t)row * a.Nn + col;
-          *o = (a.direct && a.accumulate) ? *o + acc[bm][bn][v] : acc[bm][bn][v];
+          float* o = base + (size_t)row * stride;
+          *o = accum ? *o + acc[bm][bn][v] : acc[bm][bn][v];
         }
       }
-    }
   }
 }
 
-// dw[i] (+)= sum over splits of partial[split][i].  A block owns 64
-// consecutive elements; its 4 waves each sum every 4th split (coalesced 256 B
-// rows), then wave 0 adds the 4 partial sums in a fixed order, so the result
-// does not depend on timing.
-__global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restrict__ partial, int splits,
-                                                            size_t n, float* __restrict__ dw, int accumulate) {
+// Filter-gradient split-K reduction over partial[split][M][Ng]: element
+// (row, col) goes to dw[row][col] for col < Nn and to db[row] for col == Nn
+// (the bias column), each added to or overwriting its target.  A block owns
+// 64 consecutive elements; its 4 waves each sum every 4th split (coalesced
+// 256 B rows), then wave 0 adds the 4 partial sums in a fixed order, so the
+// result does not depend on timing.
+__global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restrict__ partial, int splits, int M,
+                                                            int ldp, int Ng, int Nn, float* __restrict__ dw,
+                                                            float* __restrict__ db, int acc_dw, int acc_db) {
   __shared__ float part[4][64];
+  const size_t n = (size_t)M * ldp;  // ldp % 64 == 0: a block covers 64 columns of one row
   const int g = threadIdx.x >> 6, l = threadIdx.x & 63;
   const size_t i = (size_t)blockIdx.x * 64 + l;
+  const int row = (int)(i / (size_t)ldp);
+  const int col = (int)(i - (size_t)row * ldp);
+  if (col - l >= Ng) return;  // the whole block is in the row padding
   float t = 0.f;
-  if (i < n)
+  if (col < Ng)
     for (int k = g; k < splits; k += 4) t += partial[(size_t)k * n + i];
   part[g][l] = t;
   __syncthreads();
-  if (g == 0 && i < n) {
+  if (g == 0 && col < Ng) {
     const float sum = (part[0][l] + part[1][l]) + (part[2][l] + part[3][l]);
-    dw[i] = accumulate ? dw[i] + sum : sum;
+    float* o = col < Nn ? dw + (size_t)row * Nn + col : db + row;
+    *o = (col < Nn ? acc_dw : acc_db) ? *o + sum : sum;
   }
 }
 
@@ -1120,7 +1169,7 @@ void launch_wgrad_variant(bool va, int bm, const WgradArgs& a, dim3 grid, double
 
 template <typename T>
 hipError_t conv_wgrad_dispatch(const ConvShape& s, const void* x, const void* dy, float* partial, float* dw,
-                               int accumulate, hipStream_t st) {
+                               float* db, int acc_dw, int acc_db, hipStream_t st) {
   constexpr int VEC = 16 / (int)sizeof(T);
   constexpr int BK = WG<T>::BK;
   WgradArgs a;
@@ -1129,6 +1178,8 @@ hipError_t conv_wgrad_dispatch(const ConvShape& s, const void* x, const void* dy
   a.dy_bytes = (uint32_t)((size_t)s.N * s.P * s.Q * s.K * sizeof(T));
   a.M = s.K;
   a.Nn = s.R * s.S * s.C;
+  a.Ng = a.Nn + (db ? 1 : 0);
+  a.ldp = (a.Ng + 63) / 64 * 64;
   a.T = s.N * s.P * s.Q;
   a.N = s.N; a.H = s.H; a.W = s.W; a.C = s.C; a.S = s.S; a.P = s.P; a.Q = s.Q;
   a.sh = s.sh; a.sw = s.sw; a.ph = s.ph; a.pw = s.pw;
@@ -1137,14 +1188,16 @@ hipError_t conv_wgrad_dispatch(const ConvShape& s, const void* x, const void* dy
   a.dC = make_fastdiv((uint32_t)s.C);
   a.dS = make_fastdiv((uint32_t)s.S);
   const int tiles_m = (a.M + BM - 1) / BM;
-  a.tiles_n = (a.Nn + BN - 1) / BN;
+  a.tiles_n = (a.Ng + BN - 1) / BN;
   a.tiles = tiles_m * a.tiles_n;
   a.nkt = (a.T + BK - 1) / BK;
-  const int splits = wgrad_splits(s, sizeof(T) == 2 ? BF16 : F32);
+  const int splits = wgrad_splits(s, sizeof(T) == 2 ? BF16 : F32, db != nullptr);
   a.kt_per_split = (a.nkt + splits - 1) / splits;
   a.direct = splits == 1;
-  a.accumulate = accumulate;
+  a.acc_dw = acc_dw;
+  a.acc_db = acc_db;
   a.out = a.direct ? dw : partial;
+  a.db = db;
   dim3 grid(a.tiles * splits);
   const bool va = (a.M % VEC) == 0 && ((uintptr_t)dy % 16) == 0;
   const int vb = load_mode<T>(s.C, x);
@@ -1170,9 +1223,9 @@ size_t fwd_partial_bytes(const ConvShape& s, int dt) {
   return splits > 1 ? (size_t)splits * M * Nn * sizeof(float) : 0;
 }
 
-int wgrad_splits(const ConvShape& s, int dt) {
-  const long M = s.K, Nn = (long)s.R * s.S * s.C, T = (long)s.N * s.P * s.Q;
-  const long tiles = ((M + BM - 1) / BM) * ((Nn + BN - 1) / BN);
+int wgrad_splits(const ConvShape& s, int dt, bool bias) {
+  const long M = s.K, Ng = (long)s.R * s.S * s.C + (bias ? 1 : 0), T = (long)s.N * s.P * s.Q;
+  const long tiles = ((M + BM - 1) / BM) * ((Ng + BN - 1) / BN);
   const long bk = dt == BF16 ? WG<bf16_t>::BK : WG<float>::BK;
   const long nkt = (T + bk - 1) / bk;
   // aim for about 4 workgroups per CU on 256 CUs, at least 8 K-tiles per split
@@ -1186,22 +1239,26 @@ int wgrad_splits(const ConvShape& s, int dt) {
   return (int)((nkt + per - 1) / per);
 }
 
-size_t wgrad_partial_bytes(const ConvShape& s, int dt) {
-  return (size_t)wgrad_splits(s, dt) * s.K * s.R * s.S * s.C * sizeof(float);
+size_t wgrad_partial_bytes(const ConvShape& s, int dt, bool bias) {
+  const size_t Ng = (size_t)s.R * s.S * s.C + (bias ? 1 : 0);
+  const size_t ldp = (Ng + 63) / 64 * 64;
+  return (size_t)wgrad_splits(s, dt, bias) * s.K * ldp * sizeof(float);
 }
 
 hipError_t launch_conv_wgrad(int dt, const ConvShape& s, const void* x, const void* dy, float* partial, float* dw,
-                             int accumulate, hipStream_t st) {
-  if (dt == BF16) return conv_wgrad_dispatch<bf16_t>(s, x, dy, partial, dw, accumulate, st);
-  return conv_wgrad_dispatch<float>(s, x, dy, partial, dw, accumulate, st);
+                             float* db, int acc_dw, int acc_db, hipStream_t st) {
+  if (dt == BF16) return conv_wgrad_dispatch<bf16_t>(s, x, dy, partial, dw, db, acc_dw, acc_db, st);
+  return conv_wgrad_dispatch<float>(s, x, dy, partial, dw, db, acc_dw, acc_db, st);
 }
 
-hipError_t launch_splitk_reduce(const float* partial, int splits, size_t n, float* dw, int accumulate,
-                                hipStream_t st) {
-  const size_t blocks = (n + 63) / 64;
-  TraceScope ts("splitk_reduce_kernel", st, (double)n * 4.0 * (splits + 1 + (accumulate ? 1 : 0)), WORK_BYTE);
-  hipLaunchKernelGGL(splitk_reduce_kernel, dim3((unsigned)blocks), dim3(256), 0, st, partial, splits, n, dw,
-                     accumulate);
+hipError_t launch_splitk_reduce(const float* partial, int splits, const ConvShape& s, bool bias, float* dw,
+                                float* db, int acc_dw, int acc_db, hipStream_t st) {
+  const int Nn = s.R * s.S * s.C, Ng = Nn + (bias ? 1 : 0), ldp = (Ng + 63) / 64 * 64;
+  const size_t n = (size_t)s.K * ldp;
+  const size_t blocks = n / 64;
+  TraceScope ts("splitk_reduce_kernel", st, (double)s.K * Ng * 4.0 * (splits + 1 + (acc_dw ? 1 : 0)), WORK_BYTE);
+  hipLaunchKernelGGL(splitk_reduce_kernel, dim3((unsigned)blocks), dim3(256), 0, st, partial, splits, s.K, ldp, Ng,
+                     Nn, dw, db, acc_dw, acc_db);
   return hipGetLastError();
 }
 

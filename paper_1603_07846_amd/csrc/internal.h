@@ -51,22 +51,18 @@ hipError_t launch_conv_fwd(int dt, const ConvShape& s, const void* x, const void
 size_t fwd_partial_bytes(const ConvShape& s, int dt);
 
 // Split-K implicit-GEMM filter gradient.  Number of K-splits used for a shape
-// and the fp32 partial-sum buffer it needs.  With one split the kernel writes
-// (or, with accumulate, adds into) dw directly; otherwise it writes the
-// partial tiles and launch_splitk_reduce adds them into dw.
-int wgrad_splits(const ConvShape& s, int dt);
-size_t wgrad_partial_bytes(const ConvShape& s, int dt);
+// and the fp32 partial-sum buffer it needs.  With `bias` the GEMM carries one
+// more column, a reduction against ones, that yields db.  With one split the
+// kernel writes (or, with acc_dw / acc_db, adds into) dw and db directly;
+// otherwise it writes the partial tiles and launch_splitk_reduce adds them.
+int wgrad_splits(const ConvShape& s, int dt, bool bias);
+size_t wgrad_partial_bytes(const ConvShape& s, int dt, bool bias);
 hipError_t launch_conv_wgrad(int dt, const ConvShape& s, const void* x, const void* dy, float* partial, float* dw,
-                             int accumulate, hipStream_t st);
-// dw = (accumulate ? dw : 0) + sum over splits of partial, in split order.
-hipError_t launch_splitk_reduce(const float* partial, int splits, size_t n, float* dw, int accumulate,
-                                hipStream_t st);
-
-// Column sums of a [rows][cols] matrix (bias gradient): two passes through a
-// fixed-order partial buffer of colsum_partial_bytes().
-size_t colsum_partial_bytes(int rows, int cols);
-hipError_t launch_colsum(int dt, const void* a, int rows, int cols, float* partial, float* out,
-                         int accumulate, hipStream_t st);
+                             float* db, int acc_dw, int acc_db, hipStream_t st);
+// dw (and db, the bias column) = (accumulate ? old : 0) + the sum over splits
+// of the partial tiles, in a fixed order.
+hipError_t launch_splitk_reduce(const float* partial, int splits, const ConvShape& s, bool bias, float* dw,
+                                float* db, int acc_dw, int acc_db, hipStream_t st);
 
 // Batched 2-D transpose: for b in [0, batch): out(b)[c][r] = in(b)[r][c] with
 // in(b) = in + in_base(b), out(b) = out + out_base(b), where

@@ -128,6 +128,37 @@ def test_conv_bwd_filter_accumulate_shards(dt):
     assert rel_l2(dw.cpu().numpy(), full_dw.cpu().numpy()) <= 1e-6
 
 
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("case", [(16, 16, 24, 24, 24, 3, 3, 1, 1), (8, 3, 35, 35, 8, 11, 11, 0, 4)],
+                         ids=["split-K", "padded-channels"])
+def test_conv_bwd_filter_accumulate_split(case, dt):
+    # accumulate through the split-K reduction (and the channel-padded path)
+    N, C, H, W, K, R, S, pad, stride = case
+    x, w, b, dy = _conv_inputs(case, dt, 41)
+    ref_dw, ref_db = oracle.conv_bwd_filter(x, dy, w.shape, pad=pad, stride=stride)
+    xd, dyd = nchw_to_dev(x, dt), nchw_to_dev(dy, dt)
+    h = N // 2
+    dw, db = singa.conv_bwd_filter(xd[:h], dyd[:h], fphys(w.shape), pad, stride)
+    singa.conv_bwd_filter(xd[h:], dyd[h:], fphys(w.shape), pad, stride, dw=dw, db=db, accumulate=True)
+    torch.cuda.synchronize()
+    assert rel_l2(filt_to_kcrs(dw), ref_dw) <= TOL["f32"]
+    assert rel_l2(db.cpu().numpy(), ref_db) <= TOL["f32"]
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("layout", ["NHWC", "NCHW"])
+def test_conv_bwd_filter_without_bias(layout, dt):
+    case = (4, 8, 11, 11, 16, 3, 3, 1, 1)
+    N, C, H, W, K, R, S, pad, stride = case
+    x, w, b, dy = _conv_inputs(case, dt, 42)
+    ref_dw, _ = oracle.conv_bwd_filter(x, dy, w.shape, pad=pad, stride=stride)
+    dw, db = singa.conv_bwd_filter(nchw_to_dev(x, dt, layout), nchw_to_dev(dy, dt, layout), fphys(w.shape, layout),
+                                   pad, stride, layout=layout, with_bias=False)
+    torch.cuda.synchronize()
+    assert db is None
+    assert rel_l2(filt_to_kcrs(dw, layout), ref_dw) <= TOL["f32"]
+
+
 def test_conv_bwd_filter_deterministic():
     case = (4, 32, 15, 15, 48, 3, 3, 1, 1)
     x, w, b, dy = _conv_inputs(case, "f32", 50)
@@ -309,8 +340,9 @@ def test_abi_errors_launch_nothing():
         singa.conv_fwd(x, torch.zeros((4, 3, 3, 5), device="cuda"))
     assert e.value.status == -2
     ws = torch.zeros(16, dtype=torch.uint8, device="cuda")
+    xs = torch.zeros((16, 24, 24, 16), device="cuda")  # long reduction: split-K partial sums need workspace
     with pytest.raises(singa.SingaError) as e:
-        singa.conv_bwd_filter(x, torch.zeros((2, 8, 8, 4), device="cuda"), (4, 3, 3, 4), 1, 1, workspace=ws)
+        singa.conv_bwd_filter(xs, torch.zeros((16, 24, 24, 4), device="cuda"), (4, 3, 3, 16), 1, 1, workspace=ws)
     assert e.value.status == -4
     with pytest.raises(singa.SingaError) as e:
         singa.relu_fwd(x.view(-1)[1:])
