@@ -45,6 +45,44 @@ __global__ __launch_bounds__(256) void transpose_kernel(const T* __restrict__ in
   }
 }
 
+// Vector form for 16-byte aligned rows: a 64 x 64 tile, read as 16-byte row
+// vectors into LDS and written as 16-byte vectors of the transposed rows
+// (every stride, size and base a multiple of the vector width).
+template <typename T>
+__global__ __launch_bounds__(256) void transpose_vec_kernel(const T* __restrict__ in, T* __restrict__ out, int batch,
+                                                            int rows, int cols, long in_bstride, long in_rstride,
+                                                            long out_bstride, long out_rstride, int flip) {
+  constexpr int VEC = 16 / (int)sizeof(T);
+  constexpr int TPR = 64 / VEC;   // threads per 64-element row
+  constexpr int RPP = 256 / TPR;  // rows per pass
+  __shared__ T tile[64][64 + 2];
+  const int b = blockIdx.z;
+  const int r0 = blockIdx.y * 64, c0 = blockIdx.x * 64;
+  const T* src = in + (long)b * in_bstride;
+  T* dst = out + (long)(flip ? batch - 1 - b : b) * out_bstride;
+  const int tc = threadIdx.x % TPR, tr = threadIdx.x / TPR;
+#pragma unroll
+  for (int k = 0; k < 64; k += RPP) {
+    const int r = r0 + tr + k, c = c0 + tc * VEC;
+    union { uint4 u; T e[VEC]; } v;
+    if (r < rows && c < cols) v.u = *(const uint4*)(src + (long)r * in_rstride + c);
+    else v.u = make_uint4(0, 0, 0, 0);
+#pragma unroll
+    for (int j = 0; j < VEC; ++j) tile[tr + k][tc * VEC + j] = v.e[j];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < 64; k += RPP) {
+    const int c = c0 + tr + k, r = r0 + tc * VEC;  // output row c, output columns r .. r + VEC - 1
+    if (c < cols && r < rows) {
+      union { uint4 u; T e[VEC]; } v;
+#pragma unroll
+      for (int j = 0; j < VEC; ++j) v.e[j] = tile[tc * VEC + j][tr + k];
+      *(uint4*)(dst + (long)c * out_rstride + r) = v.u;
+    }
+  }
+}
+
 // dx[n,h,w,c] = sum over taps (r,s) whose output pixel (p,q) lands on a whole
 // multiple of the stride, and over k, of w[k,r,s,c] * dy[n,p,q,k].
 template <typename T>
@@ -154,6 +192,30 @@ __global__ __launch_bounds__(256) void pad_channels_kernel(const T* __restrict__
   }
 }
 
+// The same for C = 3, Cp = 4 (colour images): one thread per 8 rows, read as
+// 3 (bf16) / 6 (fp32) 16-byte vectors and written as 4 / 8.
+template <typename T>
+__global__ __launch_bounds__(256) void pad_3to4_kernel(const T* __restrict__ in, T* __restrict__ out, long groups) {
+  constexpr int NI = 24 * (int)sizeof(T) / 16, NO = 32 * (int)sizeof(T) / 16;
+  for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < groups; i += (long)gridDim.x * blockDim.x) {
+    union { uint4 u[NI]; T e[24]; } a;
+    union { uint4 u[NO]; T e[32]; } b;
+    const uint4* src = (const uint4*)(in + i * 24);
+#pragma unroll
+    for (int k = 0; k < NI; ++k) a.u[k] = src[k];
+#pragma unroll
+    for (int p = 0; p < 8; ++p) {
+      b.e[4 * p] = a.e[3 * p];
+      b.e[4 * p + 1] = a.e[3 * p + 1];
+      b.e[4 * p + 2] = a.e[3 * p + 2];
+      b.e[4 * p + 3] = T(0);
+    }
+    uint4* dst = (uint4*)(out + i * 32);
+#pragma unroll
+    for (int k = 0; k < NO; ++k) dst[k] = b.u[k];
+  }
+}
+
 // out[r][c] (+)= in[r][c] for c < C: drops the zero-padded channels of an
 // fp32 filter gradient computed on a channel-padded input.
 __global__ __launch_bounds__(256) void unpad_channels_f32_kernel(const float* __restrict__ in,
@@ -179,8 +241,20 @@ unsigned grid_for(long total, int block = 256, long cap = 65536) {
 
 hipError_t launch_transpose(int dt, const void* in, void* out, int batch, int rows, int cols, long in_bstride,
                             long in_rstride, long out_bstride, long out_rstride, int flip, hipStream_t st) {
-  dim3 grid((cols + 31) / 32, (rows + 31) / 32, batch), block(256);
   TraceScope ts("transpose_kernel", st, 2.0 * batch * (double)rows * cols * dt_size(dt), WORK_BYTE);
+  const long vec = 16 / (long)dt_size(dt);
+  if (rows % vec == 0 && cols % vec == 0 && in_rstride % vec == 0 && out_rstride % vec == 0 &&
+      in_bstride % vec == 0 && out_bstride % vec == 0 && (uintptr_t)in % 16 == 0 && (uintptr_t)out % 16 == 0) {
+    dim3 g64((cols + 63) / 64, (rows + 63) / 64, batch);
+    if (dt == BF16)
+      hipLaunchKernelGGL(transpose_vec_kernel<bf16_t>, g64, dim3(256), 0, st, (const bf16_t*)in, (bf16_t*)out, batch,
+                         rows, cols, in_bstride, in_rstride, out_bstride, out_rstride, flip);
+    else
+      hipLaunchKernelGGL(transpose_vec_kernel<float>, g64, dim3(256), 0, st, (const float*)in, (float*)out, batch,
+                         rows, cols, in_bstride, in_rstride, out_bstride, out_rstride, flip);
+    return hipGetLastError();
+  }
+  dim3 grid((cols + 31) / 32, (rows + 31) / 32, batch), block(256);
   if (dt == BF16)
     hipLaunchKernelGGL(transpose_kernel<bf16_t>, grid, block, 0, st, (const bf16_t*)in, (bf16_t*)out, batch, rows,
                        cols, in_bstride, in_rstride, out_bstride, out_rstride, flip);
@@ -207,8 +281,24 @@ hipError_t launch_conv_bwd_data_direct(int dt, const ConvShape& s, const void* d
 
 hipError_t launch_pad_channels(int dt, const void* in, void* out, long rows, int C, int Cp, hipStream_t st) {
   if (Cp % 4 != 0 || C > Cp) return hipErrorInvalidValue;
-  const long total = rows * (Cp / 4);
   TraceScope ts("pad_channels_kernel", st, (double)rows * (C + Cp) * dt_size(dt), WORK_BYTE);
+  const long groups = rows / 8;
+  if (C == 3 && Cp == 4 && groups > 0 && (uintptr_t)in % 16 == 0 && (uintptr_t)out % 16 == 0) {
+    // vector body over whole groups of 8 rows, generic kernel for the tail
+    if (dt == BF16)
+      hipLaunchKernelGGL(pad_3to4_kernel<bf16_t>, dim3(grid_for(groups)), dim3(256), 0, st, (const bf16_t*)in,
+                         (bf16_t*)out, groups);
+    else
+      hipLaunchKernelGGL(pad_3to4_kernel<float>, dim3(grid_for(groups)), dim3(256), 0, st, (const float*)in,
+                         (float*)out, groups);
+    const long done = groups * 8;
+    if (done == rows) return hipGetLastError();
+    const size_t es = dt_size(dt);
+    in = (const char*)in + done * C * es;
+    out = (char*)out + done * Cp * es;
+    rows -= done;
+  }
+  const long total = rows * (Cp / 4);
   if (dt == BF16)
     hipLaunchKernelGGL(pad_channels_kernel<bf16_t>, dim3(grid_for(total)), dim3(256), 0, st, (const bf16_t*)in,
                        (bf16_t*)out, rows, C, Cp);

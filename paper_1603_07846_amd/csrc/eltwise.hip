@@ -148,17 +148,18 @@ __global__ __launch_bounds__(256) void pool_bwd_kernel(PoolGeom g, int mode, con
 // VEC consecutive channels).  Same window scan and first-maximum rule as the
 // scalar kernel, applied per channel; the VEC argmax bytes are stored together.
 template <typename T, int VEC>
-__global__ __launch_bounds__(256) void pool_fwd_nhwc_vec_kernel(PoolGeom g, int mode, const T* __restrict__ x,
+__global__ __launch_bounds__(256) void pool_fwd_nhwc_vec_kernel(PoolGeom g, FastDiv dCV, FastDiv dQ, FastDiv dP,
+                                                                int mode, const T* __restrict__ x,
                                                                 T* __restrict__ y, uint8_t* __restrict__ argmax,
-                                                                long total) {
+                                                                int total) {
   const int CV = g.C / VEC;
-  for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += (long)gridDim.x * blockDim.x) {
-    const int cv = (int)(i % CV);
-    long t = i / CV;
-    const int q = (int)(t % g.Q);
-    t /= g.Q;
-    const int p = (int)(t % g.P);
-    const int n = (int)(t / g.P);
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < total; i += gridDim.x * blockDim.x) {
+    const int t1 = (int)fdiv((uint32_t)i, dCV);
+    const int cv = i - t1 * CV;
+    const int t2 = (int)fdiv((uint32_t)t1, dQ);
+    const int q = t1 - t2 * g.Q;
+    const int n = (int)fdiv((uint32_t)t2, dP);
+    const int p = t2 - n * g.P;
     const int h0 = p * g.sh - g.ph, w0 = q * g.sw - g.pw;
     float best[VEC];
     uint8_t cell[VEC];
@@ -175,7 +176,7 @@ __global__ __launch_bounds__(256) void pool_fwd_nhwc_vec_kernel(PoolGeom g, int 
         const int w = w0 + s;
         if ((unsigned)w >= (unsigned)g.W) continue;
         union { uint4 u; T e[VEC]; } v;
-        v.u = *(const uint4*)(x + (((long)n * g.H + h) * g.W + w) * g.C + (long)cv * VEC);
+        v.u = *(const uint4*)(x + ((n * g.H + h) * g.W + w) * g.C + cv * VEC);
 #pragma unroll
         for (int j = 0; j < VEC; ++j) {
           const float f = ld_f<T>(&v.e[j]);
@@ -195,15 +196,15 @@ __global__ __launch_bounds__(256) void pool_fwd_nhwc_vec_kernel(PoolGeom g, int 
     const float inv = mode == 0 ? 1.f : 1.f / (float)pool_divisor(g, p, q);
 #pragma unroll
     for (int j = 0; j < VEC; ++j) st_f<T>(&o.e[j], mode == 0 ? best[j] : best[j] * inv);
-    *(uint4*)(y + i * VEC) = o.u;
+    *(uint4*)(y + (size_t)i * VEC) = o.u;
     if (mode == 0) {
       if constexpr (VEC == 8) {
         uint2 a;
         a.x = cell[0] | (cell[1] << 8) | (cell[2] << 16) | ((uint32_t)cell[3] << 24);
         a.y = cell[4] | (cell[5] << 8) | (cell[6] << 16) | ((uint32_t)cell[7] << 24);
-        *(uint2*)(argmax + i * VEC) = a;
+        *(uint2*)(argmax + (size_t)i * VEC) = a;
       } else {
-        *(uint32_t*)(argmax + i * VEC) = cell[0] | (cell[1] << 8) | (cell[2] << 16) | ((uint32_t)cell[3] << 24);
+        *(uint32_t*)(argmax + (size_t)i * VEC) = cell[0] | (cell[1] << 8) | (cell[2] << 16) | ((uint32_t)cell[3] << 24);
       }
     }
   }
@@ -272,6 +273,94 @@ __global__ __launch_bounds__(256) void pool_bwd_nhwc_vec_kernel(PoolGeom g, Fast
 #pragma unroll
     for (int j = 0; j < VEC; ++j) st_f<T>(&out.e[j], acc[j]);
     *(uint4*)(dx + (size_t)i * VEC) = out.u;
+  }
+}
+
+// Max pooling backward for 3x3 windows, stride 2, no padding (NHWC, VEC
+// channels per thread): a thread owns the 2 x 2 input block (2 hb + dh,
+// 2 wb + dw), which windows (hb - 1 .. hb) x (wb - 1 .. wb) cover, so each
+// window's dy / arg-max / mask vectors are read once for four input pixels
+// instead of once per pixel.  Same window order per pixel as the generic
+// kernel: windows p ascending, then q ascending.
+template <typename T, int VEC, bool MASK>
+__global__ __launch_bounds__(256) void pool_bwd_k3s2_kernel(PoolGeom g, FastDiv dCV, FastDiv dWB, FastDiv dHB,
+                                                            int HB, int WB, const T* __restrict__ dy,
+                                                            const uint8_t* __restrict__ argmax,
+                                                            const T* __restrict__ ymask, T* __restrict__ dx,
+                                                            int total) {
+  const int CV = g.C / VEC;
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < total; i += gridDim.x * blockDim.x) {
+    const int t1 = (int)fdiv((uint32_t)i, dCV);
+    const int cv = i - t1 * CV;
+    const int t2 = (int)fdiv((uint32_t)t1, dWB);
+    const int wb = t1 - t2 * WB;
+    const int n = (int)fdiv((uint32_t)t2, dHB);
+    const int hb = t2 - n * HB;
+    float acc[2][2][VEC];
+#pragma unroll
+    for (int a = 0; a < 2; ++a)
+#pragma unroll
+      for (int b = 0; b < 2; ++b)
+#pragma unroll
+        for (int j = 0; j < VEC; ++j) acc[a][b][j] = 0.f;
+#pragma unroll
+    for (int pi = 0; pi < 2; ++pi) {
+      const int p = hb - 1 + pi;
+      if (p < 0 || p >= g.P) continue;
+#pragma unroll
+      for (int qi = 0; qi < 2; ++qi) {
+        const int q = wb - 1 + qi;
+        if (q < 0 || q >= g.Q) continue;
+        const int o = ((n * g.P + p) * g.Q + q) * g.C + cv * VEC;
+        union { uint4 u; T e[VEC]; } v, ym;
+        v.u = *(const uint4*)(dy + o);
+        if constexpr (MASK) ym.u = *(const uint4*)(ymask + o);
+        uint8_t am[VEC];
+        if constexpr (VEC == 8) {
+          const uint2 a = *(const uint2*)(argmax + o);
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            am[j] = (uint8_t)(a.x >> (8 * j));
+            am[4 + j] = (uint8_t)(a.y >> (8 * j));
+          }
+        } else {
+          const uint32_t a = *(const uint32_t*)(argmax + o);
+#pragma unroll
+          for (int j = 0; j < 4; ++j) am[j] = (uint8_t)(a >> (8 * j));
+        }
+        // input (2 hb + dh, 2 wb + dw) sits at cell (2 hb + dh - 2 p) * 3 + (2 wb + dw - 2 q) of this window;
+        // window p = hb - 1 covers only dh = 0 (cell row 2), p = hb covers dh = 0, 1 (rows 0, 1)
+#pragma unroll
+        for (int dh = 0; dh < 2; ++dh) {
+          if (pi == 0 && dh == 1) continue;
+#pragma unroll
+          for (int dw = 0; dw < 2; ++dw) {
+            if (qi == 0 && dw == 1) continue;
+            const int cell = (2 * (1 - pi) + dh) * 3 + (2 * (1 - qi) + dw);
+#pragma unroll
+            for (int j = 0; j < VEC; ++j) {
+              bool take = am[j] == cell;
+              if constexpr (MASK) take = take && ld_f<T>(&ym.e[j]) > 0.f;
+              if (take) acc[dh][dw][j] += ld_f<T>(&v.e[j]);
+            }
+          }
+        }
+      }
+    }
+#pragma unroll
+    for (int dh = 0; dh < 2; ++dh) {
+      const int h = 2 * hb + dh;
+      if (h >= g.H) continue;
+#pragma unroll
+      for (int dw = 0; dw < 2; ++dw) {
+        const int w = 2 * wb + dw;
+        if (w >= g.W) continue;
+        union { uint4 u; T e[VEC]; } out;
+#pragma unroll
+        for (int j = 0; j < VEC; ++j) st_f<T>(&out.e[j], acc[dh][dw][j]);
+        *(uint4*)(dx + (size_t)((n * g.H + h) * g.W + w) * g.C + cv * VEC) = out.u;
+      }
+    }
   }
 }
 
@@ -421,13 +510,16 @@ hipError_t launch_pool_fwd(int dt, int mode, int N, int C, int H, int W, int P, 
   TraceScope ts(mode == 0 ? "pool_fwd_kernel<max>" : "pool_fwd_kernel<avg>", st,
                 (double)N * C * H * W * dt_size(dt) + (double)total * (dt_size(dt) + (mode == 0 ? 1 : 0)), WORK_BYTE);
   if (v) {
-    const unsigned grid = grid_for((size_t)(total / vec));
+    const int tv = (int)(total / vec);
+    const unsigned grid = grid_for((size_t)tv);
+    const FastDiv dCV = make_fastdiv((uint32_t)(C / vec)), dQ = make_fastdiv((uint32_t)Q),
+                  dP = make_fastdiv((uint32_t)P);
     if (dt == BF16)
-      hipLaunchKernelGGL((pool_fwd_nhwc_vec_kernel<bf16_t, 8>), dim3(grid), dim3(256), 0, st, g, mode,
-                         (const bf16_t*)x, (bf16_t*)y, argmax, total / vec);
+      hipLaunchKernelGGL((pool_fwd_nhwc_vec_kernel<bf16_t, 8>), dim3(grid), dim3(256), 0, st, g, dCV, dQ, dP, mode,
+                         (const bf16_t*)x, (bf16_t*)y, argmax, tv);
     else
-      hipLaunchKernelGGL((pool_fwd_nhwc_vec_kernel<float, 4>), dim3(grid), dim3(256), 0, st, g, mode,
-                         (const float*)x, (float*)y, argmax, total / vec);
+      hipLaunchKernelGGL((pool_fwd_nhwc_vec_kernel<float, 4>), dim3(grid), dim3(256), 0, st, g, dCV, dQ, dP, mode,
+                         (const float*)x, (float*)y, argmax, tv);
     return hipGetLastError();
   }
   const unsigned grid = grid_for((size_t)total);
@@ -455,6 +547,23 @@ hipError_t launch_pool_bwd(int dt, int mode, int N, int C, int H, int W, int P, 
                 (double)N * C * P * Q * (dt_size(dt) * (ymask ? 2 : 1) + (mode == 0 ? 1 : 0)) +
                     (double)total * dt_size(dt),
                 WORK_BYTE);
+  if (v && mode == 0 && kh == 3 && kw == 3 && sh == 2 && sw == 2 && ph == 0 && pw == 0) {
+    const int HB = (H + 1) / 2, WB = (W + 1) / 2;
+    const int tb = N * HB * WB * (C / vec);
+    const unsigned grid = grid_for((size_t)tb);
+    const FastDiv dCV = make_fastdiv((uint32_t)(C / vec)), dWB = make_fastdiv((uint32_t)WB),
+                  dHB = make_fastdiv((uint32_t)HB);
+#define POOL_BWD_K3S2(T, VV, M)                                                                                  \
+  hipLaunchKernelGGL((pool_bwd_k3s2_kernel<T, VV, M>), dim3(grid), dim3(256), 0, st, g, dCV, dWB, dHB, HB, WB,   \
+                     (const T*)dy, argmax, (const T*)ymask, (T*)dx, tb)
+    if (dt == BF16) {
+      if (ymask) POOL_BWD_K3S2(bf16_t, 8, true); else POOL_BWD_K3S2(bf16_t, 8, false);
+    } else {
+      if (ymask) POOL_BWD_K3S2(float, 4, true); else POOL_BWD_K3S2(float, 4, false);
+    }
+#undef POOL_BWD_K3S2
+    return hipGetLastError();
+  }
   if (v) {
     const int tv = (int)(total / vec);
     const unsigned grid = grid_for((size_t)tv);
