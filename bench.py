@@ -49,6 +49,23 @@ def parse():
     return ap.parse_args()
 
 
+def measured_traffic(kernel):
+    """HBM bytes per launch of `kernel` from the committed counter summary
+    (profiles/traffic.json: FETCH_SIZE + WRITE_SIZE per dispatch, calibrated
+    against a copy of known size), or None when there is none for this kernel
+    or its source file has changed since the counters were taken."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    from paper_1603_07846_amd.profiling import sha256_of
+    with open(path) as f:
+        t = json.load(f)
+    src = os.path.join(ROOT, t.get("source", ""))
+    if t.get("kernel") != kernel or not os.path.exists(src) or sha256_of(src) != t.get("source_sha256"):
+        return None
+    return round(t["bytes_per_launch"])
+
+
 def cpu_baseline(w, n_images):
     """The oracle (fp64 C, OpenMP) on a bounded sample of the same step: the
     full forward/backward of `n_images` images of the workload plus the
@@ -161,7 +178,7 @@ def main():
         peak = PEAK["hbm_gbs"]
         roof = {"bound": "hbm", "unit": "GB/s"}
     roof.update({"kernel": dom_name, "achieved": round(achieved, 2), "peak": peak,
-                 "frac": round(achieved / peak, 4), "traffic": None,
+                 "frac": round(achieved / peak, 4), "traffic": measured_traffic(dom_name),
                  "avg_launch_ms": round(avg_ms, 4), "work_per_launch": per_launch,
                  "launches_per_step": dom["launches"] / args.steps})
 

@@ -1019,7 +1019,7 @@ void launch_fwd_instance(const FwdArgs& a, dim3 grid, double flops, hipStream_t 
 }
 
 template <bool BWD> const char* fwd_large_name() {
-  return BWD ? "conv_fwd_large_kernel<bf16,1>" : "conv_fwd_large_kernel<bf16,0>";
+  return BWD ? "conv_fwd_large_kernel<1>" : "conv_fwd_large_kernel<0>";
 }
 
 // Workgroups of the 256 x 128 kernel per full round of the chip (one per CU)
