@@ -650,11 +650,13 @@ __global__ __launch_bounds__(NT) void conv_fwd_large_kernel(FwdArgs a) {
 // ----------------------------------------------------------- filter gradient
 //
 // dW[i][j] = sum_t dy[t][i] * x^[t][j], i = filter, j = tap (r, s, c),
-// t = output pixel of one image.  The order of the reduction is free: t runs
-// over (p, q) with the image n fastest, t = (p*Q + q)*N + n.  When N is a
-// multiple of the K-tile, all rows of a K-tile share one output pixel (p, q):
-// the bounds check of a tap is the same for every row and a row's address is
-// n times the image stride.  Both operand tiles sit in LDS exactly as loaded,
+// t = output pixel of one image.  The order of the reduction is free.  NFAST
+// runs t over (p, q) with the image n fastest, t = (p*Q + q)*N + n: when N is
+// a multiple of the K-tile, all rows of a K-tile share one output pixel
+// (p, q), so the bounds check of a tap is the same for every row and a row's
+// address is n times the image stride.  Otherwise t is image-major,
+// t = n*P*Q + p*Q + q, which keeps a workgroup's input reads inside one image
+// (better L2 reuse when an image has many output pixels).  Both operand tiles sit in LDS exactly as loaded,
 // t-major rows of 128 consecutive filters / taps.  For bf16 the MFMA fragment
 // (8 consecutive t of one filter or tap) comes from ds_read_b64_tr_b16, which
 // hands each lane of a 16-lane group one column of the 4 rows the group
@@ -686,7 +688,7 @@ struct WgradArgs {
   int ldp;           // row stride of the partial tiles: Ng rounded up to 64 (256-byte rows)
   int N, H, W, C, S, P, Q;
   int sh, sw, ph, pw;
-  FastDiv dN, dQ, dC, dS;
+  FastDiv dN, dPQ, dQ, dC, dS;
   int tiles, tiles_n, kt_per_split, nkt;
   int direct, acc_dw, acc_db;
 };
@@ -823,11 +825,11 @@ __global__ __launch_bounds__(NT) void conv_wgrad_kernel(WgradArgs a) {
         h0 = hb;
         w0 = wb;
         tin = true;  // T is a multiple of BK
-      } else {
+      } else {  // image-major order: t = n P Q + p Q + q
         const int t = t0 + d;
         tin = t < a.T;
-        rpq = (int)fdiv((uint32_t)t, a.dN);
-        n = t - rpq * a.N;
+        n = (int)fdiv((uint32_t)t, a.dPQ);
+        rpq = t - n * PQ;
         const int p = (int)fdiv((uint32_t)rpq, a.dQ);
         h0 = p * a.sh - a.ph;
         w0 = (rpq - p * a.Q) * a.sw - a.pw;
@@ -1167,6 +1169,20 @@ void launch_wgrad_variant(bool va, int bm, const WgradArgs& a, dim3 grid, double
   else launch_wgrad_bmode<T, false, NF>(bm, a, grid, flops, st);
 }
 
+// Reduction order of the filter gradient: image fastest (needs N % BK == 0)
+// unless an image has many output pixels, where image-major keeps the input
+// reads of a workgroup local.  SINGA_WGRAD_ORDER=image|pixel forces one.
+bool use_image_fastest(const ConvShape& s, int bk) {
+  static const int forced = [] {
+    const char* e = getenv("SINGA_WGRAD_ORDER");
+    if (!e) return 0;
+    return e[0] == 'p' ? 1 : e[0] == 'i' ? 2 : 0;  // pixel-major (image fastest) / image-major
+  }();
+  if (s.N % bk != 0) return false;
+  if (forced) return forced == 1;
+  return s.P * s.Q < 1024;
+}
+
 template <typename T>
 hipError_t conv_wgrad_dispatch(const ConvShape& s, const void* x, const void* dy, float* partial, float* dw,
                                float* db, int acc_dw, int acc_db, hipStream_t st) {
@@ -1184,6 +1200,7 @@ hipError_t conv_wgrad_dispatch(const ConvShape& s, const void* x, const void* dy
   a.N = s.N; a.H = s.H; a.W = s.W; a.C = s.C; a.S = s.S; a.P = s.P; a.Q = s.Q;
   a.sh = s.sh; a.sw = s.sw; a.ph = s.ph; a.pw = s.pw;
   a.dN = make_fastdiv((uint32_t)s.N);
+  a.dPQ = make_fastdiv((uint32_t)(s.P * s.Q));
   a.dQ = make_fastdiv((uint32_t)s.Q);
   a.dC = make_fastdiv((uint32_t)s.C);
   a.dS = make_fastdiv((uint32_t)s.S);
@@ -1202,7 +1219,7 @@ hipError_t conv_wgrad_dispatch(const ConvShape& s, const void* x, const void* dy
   const bool va = (a.M % VEC) == 0 && ((uintptr_t)dy % 16) == 0;
   const int vb = load_mode<T>(s.C, x);
   const double flops = 2.0 * a.M * (double)a.Nn * (double)a.T;
-  if (s.N % BK == 0)
+  if (use_image_fastest(s, BK))
     launch_wgrad_variant<T, true>(va, vb, a, grid, flops, st);
   else
     launch_wgrad_variant<T, false>(va, vb, a, grid, flops, st);
