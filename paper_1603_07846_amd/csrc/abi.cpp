@@ -100,10 +100,62 @@ inline int padded_channels(const ConvShape& s, int dt) {
   return cp <= 2 * s.C ? cp : 0;
 }
 
+// Space-to-depth geometry of the strided convolution s: blocks of sh x sw
+// input pixels become channels, the filter shrinks to ceil(R/sh) x ceil(S/sw)
+// and the layer becomes a stride-1 convolution without padding with the same
+// output (the transforms are in conv_aux.hip).
+ConvShape s2d_shape(const ConvShape& s) {
+  ConvShape g = s;
+  g.R = (s.R + s.sh - 1) / s.sh;
+  g.S = (s.S + s.sw - 1) / s.sw;
+  g.C = s.C * s.sh * s.sw;
+  g.H = s.P + g.R - 1;
+  g.W = s.Q + g.S - 1;
+  g.ph = g.pw = 0;
+  g.sh = g.sw = 1;
+  return g;
+}
+bool s2d_fits(const ConvShape& g) {
+  return fits_i32(4LL * g.N * g.H * g.W * g.C) && fits_i32(4LL * g.K * g.R * g.S * g.C);
+}
+
+// Input rewrite of the forward and filter-gradient GEMMs, and the GEMM's
+// geometry g.  A strided layer whose channel count gives no 16-byte tap
+// vectors but whose space-to-depth channel count does is rewritten as that
+// stride-1 layer (the first layer, 11x11/4 on 3 channels, becomes 3x3/1 on
+// 48 channels: 432 taps instead of 484 padded ones, all vector loads); other
+// channel counts that are not a multiple of 4 are zero-padded.
+enum Rewrite { RW_NONE, RW_PAD, RW_S2D };
+Rewrite input_rewrite(const ConvShape& s, int dt, ConvShape* g) {
+  const int vec = dt == BF16 ? 8 : 4;
+  *g = s;
+  if (s.C % vec != 0 && (s.sh > 1 || s.sw > 1) && !bwd_data_fc(s)) {
+    const ConvShape t = s2d_shape(s);
+    if (t.C % vec == 0 && s2d_fits(t)) {
+      *g = t;
+      return RW_S2D;
+    }
+  }
+  const int cp = padded_channels(s, dt);
+  if (cp) {
+    g->C = cp;
+    return RW_PAD;
+  }
+  return RW_NONE;
+}
+
+// Backward-data of a strided, non-dense layer: the stride-1 GEMM on the
+// space-to-depth layer g, whose input gradient is then scattered back.
+bool bwd_data_s2d(const ConvShape& s, ConvShape* g) {
+  if (bwd_data_gemm(s)) return false;
+  *g = s2d_shape(s);
+  return s2d_fits(*g);
+}
+
 // One function computes both the size and the layout of every workspace, so
 // the two can never disagree.
 struct FwdWs { void *x, *w, *y, *xp, *wp; float* partial; };
-struct BwdDataWs { void *dy, *w, *wt, *dx; float* partial; };
+struct BwdDataWs { void *dy, *w, *wt, *dx, *ws, *dxs; float* partial; };
 struct BwdFilterWs { void *x, *dy, *xp; float *dw, *dwp, *partial; };
 
 size_t carve_fwd(const ConvShape& s, int dt, int layout, void* ws, FwdWs* o) {
@@ -115,28 +167,31 @@ size_t carve_fwd(const ConvShape& s, int dt, int layout, void* ws, FwdWs* o) {
     o->w = c.take(filt_bytes(s, dt));
     o->y = c.take(out_bytes(s, dt));
   }
-  const int cp = padded_channels(s, dt);
-  ConvShape g = s;
-  if (cp) {
-    o->xp = c.take((size_t)s.N * s.H * s.W * cp * dt_size(dt));
-    o->wp = c.take((size_t)s.K * s.R * s.S * cp * dt_size(dt));
-    g.C = cp;
+  ConvShape g;
+  if (input_rewrite(s, dt, &g) != RW_NONE) {
+    o->xp = c.take((size_t)g.N * g.H * g.W * g.C * dt_size(dt));
+    o->wp = c.take((size_t)g.K * g.R * g.S * g.C * dt_size(dt));
   }
   const size_t pb = fwd_partial_bytes(g, dt);
   if (pb) o->partial = (float*)c.take(pb);
   return c.used;
 }
 
-// NHWC forward on (x, w): through zero-padded channel copies when the channel
-// count needs it.
+// NHWC forward on (x, w): through the rewritten input and filter when
+// input_rewrite says so.
 hipError_t conv_fwd_nhwc(int dt, const ConvShape& s, const void* x, const void* w, const float* bias, void* y,
                          int relu, const FwdWs& o, hipStream_t st) {
-  const int cp = padded_channels(s, dt);
-  if (!cp) return launch_conv_fwd(dt, s, x, w, bias, y, relu, 0, conv_flops(s), o.partial, nullptr, st);
-  hipError_t e = launch_pad_channels(dt, x, o.xp, (long)s.N * s.H * s.W, s.C, cp, st);
-  if (e == hipSuccess) e = launch_pad_channels(dt, w, o.wp, (long)s.K * s.R * s.S, s.C, cp, st);
-  ConvShape g = s;
-  g.C = cp;
+  ConvShape g;
+  const Rewrite rw = input_rewrite(s, dt, &g);
+  if (rw == RW_NONE) return launch_conv_fwd(dt, s, x, w, bias, y, relu, 0, conv_flops(s), o.partial, nullptr, st);
+  hipError_t e;
+  if (rw == RW_PAD) {
+    e = launch_pad_channels(dt, x, o.xp, (long)s.N * s.H * s.W, s.C, g.C, st);
+    if (e == hipSuccess) e = launch_pad_channels(dt, w, o.wp, (long)s.K * s.R * s.S, s.C, g.C, st);
+  } else {
+    e = launch_space_to_depth(dt, s, g, x, o.xp, st);
+    if (e == hipSuccess) e = launch_filter_to_s2d(dt, s, g, w, o.wp, st);
+  }
   if (e == hipSuccess)
     e = launch_conv_fwd(dt, g, o.xp, o.wp, bias, y, relu, 0, conv_flops(s), o.partial, nullptr, st);
   return e;
@@ -144,16 +199,23 @@ hipError_t conv_fwd_nhwc(int dt, const ConvShape& s, const void* x, const void* 
 
 size_t carve_bwd_data(const ConvShape& s, int dt, int layout, void* ws, BwdDataWs* o) {
   Carve c(ws);
-  o->dy = o->w = o->wt = o->dx = nullptr;
+  o->dy = o->w = o->wt = o->dx = o->ws = o->dxs = nullptr;
   o->partial = nullptr;
   if (layout == SINGA_NCHW) {
     o->dy = c.take(out_bytes(s, dt));
     o->w = c.take(filt_bytes(s, dt));
     o->dx = c.take(act_bytes(s, dt));
   }
+  ConvShape g;
   if (bwd_data_gemm(s)) {
     o->wt = c.take(filt_bytes(s, dt));
     const size_t pb = fwd_partial_bytes(bwd_data_inner(s), dt);
+    if (pb) o->partial = (float*)c.take(pb);
+  } else if (bwd_data_s2d(s, &g)) {
+    o->ws = c.take(filt_bytes(g, dt));
+    o->wt = c.take(filt_bytes(g, dt));
+    o->dxs = c.take(act_bytes(g, dt));
+    const size_t pb = fwd_partial_bytes(bwd_data_inner(g), dt);
     if (pb) o->partial = (float*)c.take(pb);
   }
   return c.used;
@@ -168,12 +230,10 @@ size_t carve_bwd_filter(const ConvShape& s, int dt, int layout, bool bias, void*
     o->dy = c.take(out_bytes(s, dt));
     o->dw = (float*)c.take((size_t)s.K * s.R * s.S * s.C * sizeof(float));
   }
-  const int cp = padded_channels(s, dt);
-  ConvShape g = s;
-  if (cp) {
-    g.C = cp;
-    o->xp = c.take((size_t)s.N * s.H * s.W * cp * dt_size(dt));
-    o->dwp = (float*)c.take((size_t)s.K * s.R * s.S * cp * sizeof(float));
+  ConvShape g;
+  if (input_rewrite(s, dt, &g) != RW_NONE) {
+    o->xp = c.take((size_t)g.N * g.H * g.W * g.C * dt_size(dt));
+    o->dwp = (float*)c.take((size_t)g.K * g.R * g.S * g.C * sizeof(float));
   }
   if (wgrad_splits(g, dt, bias) > 1) o->partial = (float*)c.take(wgrad_partial_bytes(g, dt, bias));
   else o->partial = nullptr;
@@ -312,8 +372,19 @@ int singa_conv_bwd_data(singa_dtype dtype, singa_layout layout, const singa_shap
     dx = o.dx;
   }
   const int RS = s.R * s.S;
+  ConvShape g;
   if (e == hipSuccess) {
-    if (bwd_data_gemm(s)) {
+    if (!bwd_data_gemm(s) && bwd_data_s2d(s, &g)) {
+      // wt[c'][r'][s'][k] = w'[k][R'-1-r'][S'-1-s'][c'] of the space-to-depth layer g
+      const int RSg = g.R * g.S;
+      e = launch_filter_to_s2d(dtype, s, g, wk, o.ws, st);
+      if (e == hipSuccess)
+        e = launch_transpose(dtype, o.ws, o.wt, RSg, g.K, g.C, g.C, (long)RSg * g.C, g.K, (long)RSg * g.K, 1, st);
+      if (e == hipSuccess)
+        e = launch_conv_fwd(dtype, bwd_data_inner(g), dy, o.wt, nullptr, o.dxs, 0, 1, conv_flops(s), o.partial,
+                            nullptr, st);
+      if (e == hipSuccess) e = launch_depth_to_space(dtype, s, g, o.dxs, nhwc_mask, dx, st);
+    } else if (bwd_data_gemm(s)) {
       if (bwd_data_fc(s)) {
         const int J = RS * s.C;  // wt[(r,s,c)][k] = w[k][(r,s,c)]
         e = launch_transpose(dtype, wk, o.wt, 1, s.K, J, 0, J, 0, s.K, 0, st);
@@ -361,24 +432,24 @@ int singa_conv_bwd_filter(singa_dtype dtype, singa_layout layout, const singa_sh
     xx = o.x;
     dy = o.dy;
   }
-  // g: the GEMM's geometry (channels zero-padded when padded_channels says so)
-  const int cp = padded_channels(s, dtype);
-  ConvShape g = s;
-  if (cp) {
-    g.C = cp;
-    if (e == hipSuccess) e = launch_pad_channels(dtype, xx, o.xp, (long)s.N * s.H * s.W, s.C, cp, st);
-    xx = o.xp;
-  }
+  // g: the GEMM's geometry (input rewritten when input_rewrite says so)
+  ConvShape g;
+  const Rewrite rw = input_rewrite(s, dtype, &g);
+  if (rw == RW_PAD && e == hipSuccess) e = launch_pad_channels(dtype, xx, o.xp, (long)s.N * s.H * s.W, s.C, g.C, st);
+  if (rw == RW_S2D && e == hipSuccess) e = launch_space_to_depth(dtype, s, g, xx, o.xp, st);
+  if (rw != RW_NONE) xx = o.xp;
   const int splits = wgrad_splits(g, dtype, bias);
   float* krsc = layout == SINGA_NHWC ? dw : o.dw;  // KRSC result
   const int acc = layout == SINGA_NHWC ? accumulate : 0;
-  float* target = cp ? o.dwp : krsc;  // the GEMM's (K, R, S, g.C) result
-  const int tacc = cp ? 0 : acc;
+  float* target = rw != RW_NONE ? o.dwp : krsc;  // the GEMM's (K, g.R, g.S, g.C) result
+  const int tacc = rw != RW_NONE ? 0 : acc;
   // db is written in place by the GEMM's bias column, with the caller's accumulate
   if (e == hipSuccess) e = launch_conv_wgrad(dtype, g, xx, dy, o.partial, target, db, tacc, accumulate, st);
   if (e == hipSuccess && splits > 1)
     e = launch_splitk_reduce(o.partial, splits, g, bias, target, db, tacc, accumulate, st);
-  if (e == hipSuccess && cp) e = launch_unpad_channels_f32(o.dwp, krsc, (long)s.K * s.R * s.S, cp, s.C, acc, st);
+  if (e == hipSuccess && rw == RW_PAD)
+    e = launch_unpad_channels_f32(o.dwp, krsc, (long)s.K * s.R * s.S, g.C, s.C, acc, st);
+  if (e == hipSuccess && rw == RW_S2D) e = launch_s2d_to_filter_f32(s, g, o.dwp, krsc, acc, st);
   if (e == hipSuccess && layout == SINGA_NCHW) e = launch_krsc_to_kcrs_f32(o.dw, dw, s.K, s.C, s.R, s.S, accumulate, st);
   return hip_status(e);
 }

@@ -216,6 +216,104 @@ __global__ __launch_bounds__(256) void pad_3to4_kernel(const T* __restrict__ in,
   }
 }
 
+// Space-to-depth rewrite of a strided convolution (stride sh x sw, padding
+// ph, pw) as a stride-1 convolution without padding:
+//   x'[n][h'][w'][(dh*sw + dw)*C + c] = x[n][sh*h' + dh - ph][sw*w' + dw - pw][c]  (0 outside x)
+//   w'[k][r'][s'][(dh*sw + dw)*C + c] = w[k][sh*r' + dh][sw*s' + dw][c]           (0 past R, S)
+// so that y[n][p][q][k] = sum over (r', s', c') of w'[k][r'][s'][c'] x'[n][p + r'][q + s'][c'].
+// One thread per 16-byte chunk of x' (VEC channels of one rewritten pixel),
+// 32-bit index math with precomputed divisors.
+template <typename T>
+__global__ __launch_bounds__(256) void space_to_depth_kernel(const T* __restrict__ x, T* __restrict__ xs, int H,
+                                                             int W, int C, int Hs, int Ws, int sh, int sw, int ph,
+                                                             int pw, FastDiv dJ, FastDiv dWs, FastDiv dHs, FastDiv dC,
+                                                             FastDiv dSw, int total) {
+  constexpr int VEC = 16 / (int)sizeof(T);
+  const int J = (int)dJ.d;  // chunks per rewritten pixel
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < total; i += gridDim.x * blockDim.x) {
+    const int pix = (int)fdiv((uint32_t)i, dJ);
+    const int j = i - pix * J;
+    const int t = (int)fdiv((uint32_t)pix, dWs);
+    const int wq = pix - t * Ws;
+    const int n = (int)fdiv((uint32_t)t, dHs);
+    const int hq = t - n * Hs;
+    union { uint4 u; T e[VEC]; } v;
+#pragma unroll
+    for (int u = 0; u < VEC; ++u) {
+      const int e = j * VEC + u;
+      const int d = (int)fdiv((uint32_t)e, dC);
+      const int c = e - d * C;
+      const int dh = (int)fdiv((uint32_t)d, dSw);
+      const int dw = d - dh * sw;
+      const int h = sh * hq + dh - ph, w = sw * wq + dw - pw;
+      const bool ok = (unsigned)h < (unsigned)H && (unsigned)w < (unsigned)W;
+      v.e[u] = ok ? x[((n * H + h) * W + w) * C + c] : T(0);
+    }
+    *(uint4*)(xs + (size_t)i * VEC) = v.u;
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void filter_to_s2d_kernel(const T* __restrict__ w, T* __restrict__ ws, int K,
+                                                            int R, int S, int C, int Rs, int Ss, int sh, int sw,
+                                                            int total) {
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < total; i += gridDim.x * blockDim.x) {
+    const int Cs = sh * sw * C;
+    const int cs = i % Cs;
+    int t = i / Cs;
+    const int ss = t % Ss;
+    t /= Ss;
+    const int rs = t % Rs;
+    const int k = t / Rs;
+    const int c = cs % C, d = cs / C, dh = d / sw, dw = d % sw;
+    const int r = sh * rs + dh, s = sw * ss + dw;
+    ws[i] = (r < R && s < S) ? w[((k * R + r) * S + s) * C + c] : T(0);
+  }
+}
+
+// dw[k][r][s][c] (+)= dws[k][r / sh][s / sw][((r % sh)*sw + s % sw)*C + c] (fp32 filter gradients).
+__global__ __launch_bounds__(256) void s2d_to_filter_f32_kernel(const float* __restrict__ dws, float* __restrict__ dw,
+                                                                int K, int R, int S, int C, int Rs, int Ss, int sh,
+                                                                int sw, int accumulate, int total) {
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < total; i += gridDim.x * blockDim.x) {
+    const int c = i % C;
+    int t = i / C;
+    const int s = t % S;
+    t /= S;
+    const int r = t % R;
+    const int k = t / R;
+    const int Cs = sh * sw * C;
+    const float v = dws[((k * Rs + r / sh) * Ss + s / sw) * Cs + ((r % sh) * sw + s % sw) * C + c];
+    dw[i] = accumulate ? dw[i] + v : v;
+  }
+}
+
+// dx[n][h][w][c] = dxs[n][(h + ph) / sh][(w + pw) / sw][(((h + ph) % sh)*sw + (w + pw) % sw)*C + c]
+// (0 where that position lies outside dxs: no output window reads it), then
+// zeroed where mask <= 0 when a ReLU's output is given.
+template <typename T>
+__global__ __launch_bounds__(256) void depth_to_space_kernel(const T* __restrict__ dxs, const T* __restrict__ mask,
+                                                             T* __restrict__ dx, FastDiv dC, FastDiv dW, FastDiv dH,
+                                                             int H, int W, int C, int Hs, int Ws, int sh, int sw,
+                                                             int ph, int pw, int total) {
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < total; i += gridDim.x * blockDim.x) {
+    const int t1 = (int)fdiv((uint32_t)i, dC);
+    const int c = i - t1 * C;
+    const int t2 = (int)fdiv((uint32_t)t1, dW);
+    const int w = t1 - t2 * W;
+    const int n = (int)fdiv((uint32_t)t2, dH);
+    const int h = t2 - n * H;
+    const int hq = (h + ph) / sh, wq = (w + pw) / sw;
+    float v = 0.f;
+    if (hq < Hs && wq < Ws) {
+      const int Cs = sh * sw * C;
+      v = ld_f<T>(dxs + ((n * Hs + hq) * Ws + wq) * Cs + (((h + ph) % sh) * sw + (w + pw) % sw) * C + c);
+    }
+    if (mask && !(ld_f<T>(mask + i) > 0.f)) v = 0.f;
+    st_f<T>(dx + i, v);
+  }
+}
+
 // out[r][c] (+)= in[r][c] for c < C: drops the zero-padded channels of an
 // fp32 filter gradient computed on a channel-padded input.
 __global__ __launch_bounds__(256) void unpad_channels_f32_kernel(const float* __restrict__ in,
@@ -314,6 +412,63 @@ hipError_t launch_unpad_channels_f32(const float* in, float* out, long rows, int
   TraceScope ts("unpad_channels_f32_kernel", st, (double)rows * (C * (accumulate ? 12.0 : 8.0)), WORK_BYTE);
   hipLaunchKernelGGL(unpad_channels_f32_kernel, dim3(grid_for(total)), dim3(256), 0, st, in, out, rows, Cp, C,
                      accumulate);
+  return hipGetLastError();
+}
+
+hipError_t launch_space_to_depth(int dt, const ConvShape& s, const ConvShape& g, const void* x, void* xs,
+                                 hipStream_t st) {
+  const int vec = 16 / (int)dt_size(dt);
+  if (g.C % vec != 0 || (uintptr_t)xs % 16 != 0) return hipErrorInvalidValue;  // callers guarantee both
+  const int J = g.C / vec;
+  const int total = g.N * g.H * g.W * J;
+  TraceScope ts("space_to_depth_kernel", st,
+                ((double)s.N * s.H * s.W * s.C + (double)g.N * g.H * g.W * g.C) * dt_size(dt), WORK_BYTE);
+  const FastDiv dJ = make_fastdiv((uint32_t)J), dWs = make_fastdiv((uint32_t)g.W), dHs = make_fastdiv((uint32_t)g.H),
+                dC = make_fastdiv((uint32_t)s.C), dSw = make_fastdiv((uint32_t)s.sw);
+  if (dt == BF16)
+    hipLaunchKernelGGL(space_to_depth_kernel<bf16_t>, dim3(grid_for(total)), dim3(256), 0, st, (const bf16_t*)x,
+                       (bf16_t*)xs, s.H, s.W, s.C, g.H, g.W, s.sh, s.sw, s.ph, s.pw, dJ, dWs, dHs, dC, dSw, total);
+  else
+    hipLaunchKernelGGL(space_to_depth_kernel<float>, dim3(grid_for(total)), dim3(256), 0, st, (const float*)x,
+                       (float*)xs, s.H, s.W, s.C, g.H, g.W, s.sh, s.sw, s.ph, s.pw, dJ, dWs, dHs, dC, dSw, total);
+  return hipGetLastError();
+}
+
+hipError_t launch_filter_to_s2d(int dt, const ConvShape& s, const ConvShape& g, const void* w, void* ws,
+                                hipStream_t st) {
+  const int total = g.K * g.R * g.S * g.C;
+  TraceScope ts("filter_to_s2d_kernel", st, (double)total * 2 * dt_size(dt), WORK_BYTE);
+  if (dt == BF16)
+    hipLaunchKernelGGL(filter_to_s2d_kernel<bf16_t>, dim3(grid_for(total)), dim3(256), 0, st, (const bf16_t*)w,
+                       (bf16_t*)ws, s.K, s.R, s.S, s.C, g.R, g.S, s.sh, s.sw, total);
+  else
+    hipLaunchKernelGGL(filter_to_s2d_kernel<float>, dim3(grid_for(total)), dim3(256), 0, st, (const float*)w,
+                       (float*)ws, s.K, s.R, s.S, s.C, g.R, g.S, s.sh, s.sw, total);
+  return hipGetLastError();
+}
+
+hipError_t launch_s2d_to_filter_f32(const ConvShape& s, const ConvShape& g, const float* dws, float* dw,
+                                    int accumulate, hipStream_t st) {
+  const int total = s.K * s.R * s.S * s.C;
+  TraceScope ts("s2d_to_filter_f32_kernel", st, (double)total * (accumulate ? 12.0 : 8.0), WORK_BYTE);
+  hipLaunchKernelGGL(s2d_to_filter_f32_kernel, dim3(grid_for(total)), dim3(256), 0, st, dws, dw, s.K, s.R, s.S, s.C,
+                     g.R, g.S, s.sh, s.sw, accumulate, total);
+  return hipGetLastError();
+}
+
+hipError_t launch_depth_to_space(int dt, const ConvShape& s, const ConvShape& g, const void* dxs, const void* mask,
+                                 void* dx, hipStream_t st) {
+  const int total = s.N * s.H * s.W * s.C;
+  TraceScope ts("depth_to_space_kernel", st, (double)total * (mask ? 3 : 2) * dt_size(dt), WORK_BYTE);
+  const FastDiv dC = make_fastdiv((uint32_t)s.C), dW = make_fastdiv((uint32_t)s.W), dH = make_fastdiv((uint32_t)s.H);
+  if (dt == BF16)
+    hipLaunchKernelGGL(depth_to_space_kernel<bf16_t>, dim3(grid_for(total)), dim3(256), 0, st, (const bf16_t*)dxs,
+                       (const bf16_t*)mask, (bf16_t*)dx, dC, dW, dH, s.H, s.W, s.C, g.H, g.W, s.sh, s.sw, s.ph, s.pw,
+                       total);
+  else
+    hipLaunchKernelGGL(depth_to_space_kernel<float>, dim3(grid_for(total)), dim3(256), 0, st, (const float*)dxs,
+                       (const float*)mask, (float*)dx, dC, dW, dH, s.H, s.W, s.C, g.H, g.W, s.sh, s.sw, s.ph, s.pw,
+                       total);
   return hipGetLastError();
 }
 

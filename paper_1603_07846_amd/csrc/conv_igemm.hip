@@ -1037,9 +1037,12 @@ int forced_tile() {
   return v;
 }
 
-bool use_large_fwd(long M, long Nn) {
+bool use_large_fwd(long M, long Nn, long Kg) {
   if (forced_tile() == 128) return false;
   if (forced_tile() == 256) return ((M + L_BM - 1) / L_BM) * ((Nn + BN - 1) / BN) > 0;
+  // a short reduction leaves the one-block-per-CU kernel's prologue and
+  // epilogue exposed; the two-blocks-per-CU kernel overlaps them
+  if ((Kg + 63) / 64 < 16) return false;
   const long big = ((M + L_BM - 1) / L_BM) * ((Nn + BN - 1) / BN);
   const long small = ((M + BM - 1) / BM) * ((Nn + BN - 1) / BN);
   if (big < 256) return false;
@@ -1112,7 +1115,7 @@ hipError_t conv_fwd_dispatch(const ConvShape& s, const void* x, const void* w, c
   dim3 grid(a.tiles * splits);
   const int am = load_mode<T>(s.C, x);
   const int bm = load_mode<T>(a.Kg, w);
-  if (sizeof(T) == 2 && am == VEC16 && bm == VEC16 && splits == 1 && use_large_fwd(a.M, a.Nn)) {
+  if (sizeof(T) == 2 && am == VEC16 && bm == VEC16 && splits == 1 && use_large_fwd(a.M, a.Nn, a.Kg)) {
     a.tiles_n = (a.Nn + BN - 1) / BN;
     a.tiles = ((a.M + L_BM - 1) / L_BM) * a.tiles_n;
     a.partial = nullptr;

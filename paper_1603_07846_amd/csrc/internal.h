@@ -78,6 +78,18 @@ hipError_t launch_conv_bwd_data_direct(int dt, const ConvShape& s, const void* d
 // Zero-pad the innermost (channel) dimension: in [rows][C] -> out [rows][Cp],
 // Cp a multiple of the 16-byte vector width.
 hipError_t launch_pad_channels(int dt, const void* in, void* out, long rows, int C, int Cp, hipStream_t st);
+// Space-to-depth rewrite of the strided convolution s as the stride-1,
+// unpadded convolution g (H, W, C, R, S of g are the rewritten ones): input,
+// filter, filter gradient (fp32, optionally accumulated) and input gradient
+// (optionally masked by a ReLU output).
+hipError_t launch_space_to_depth(int dt, const ConvShape& s, const ConvShape& g, const void* x, void* xs,
+                                 hipStream_t st);
+hipError_t launch_filter_to_s2d(int dt, const ConvShape& s, const ConvShape& g, const void* w, void* ws,
+                                hipStream_t st);
+hipError_t launch_s2d_to_filter_f32(const ConvShape& s, const ConvShape& g, const float* dws, float* dw,
+                                    int accumulate, hipStream_t st);
+hipError_t launch_depth_to_space(int dt, const ConvShape& s, const ConvShape& g, const void* dxs, const void* mask,
+                                 void* dx, hipStream_t st);
 hipError_t launch_unpad_channels_f32(const float* in, float* out, long rows, int Cp, int C, int accumulate,
                                      hipStream_t st);
 

@@ -261,7 +261,7 @@ def test_conv_bwd_data_relu_folded(case, layout, dt):
 
 
 def test_conv_bwd_data_relu_folded_large_tile():
-    case = (16, 200, 47, 47, 64, 3, 3, 1, 1)
+    case = (15, 200, 47, 47, 128, 3, 3, 1, 1)
     N, C, H, W, K, R, S, pad, stride = case
     x, w, b, dy = _conv_inputs(case, "bf16", 91)
     xr = np.maximum(x, 0.0)
@@ -349,13 +349,14 @@ def test_abi_errors_launch_nothing():
     assert e.value.status == -5
 
 
-# Shapes big enough that the bf16 forward / backward-data passes take the
-# 256 x 128 direct-to-LDS kernel (checked through the kernel trace), with
-# ragged M, N and K tails and stride 2; compared element by element.
+# Shapes big enough (>= 256 tiles, >= 16 K-tiles) that the bf16 forward /
+# backward-data passes take the 256 x 128 direct-to-LDS kernel (checked
+# through the kernel trace), with ragged M, N and K tails and stride 2;
+# compared element by element.
 LARGE_CASES = [
-    ("fwd", (10, 40, 47, 47, 300, 3, 3, 1, 1)),
-    ("bwd_data", (16, 200, 47, 47, 64, 3, 3, 1, 1)),
-    ("fwd", (40, 64, 59, 59, 136, 3, 3, 1, 2)),
+    ("fwd", (10, 128, 47, 47, 300, 3, 3, 1, 1)),
+    ("bwd_data", (15, 200, 47, 47, 128, 3, 3, 1, 1)),
+    ("fwd", (40, 128, 59, 59, 136, 3, 3, 1, 2)),
 ]
 
 
