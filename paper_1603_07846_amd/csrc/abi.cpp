@@ -235,8 +235,8 @@ size_t carve_bwd_filter(const ConvShape& s, int dt, int layout, bool bias, void*
     o->xp = c.take((size_t)g.N * g.H * g.W * g.C * dt_size(dt));
     o->dwp = (float*)c.take((size_t)g.K * g.R * g.S * g.C * sizeof(float));
   }
-  if (wgrad_splits(g, dt, bias) > 1) o->partial = (float*)c.take(wgrad_partial_bytes(g, dt, bias));
-  else o->partial = nullptr;
+  const size_t pb = wgrad_partial_bytes(g, dt, bias);
+  o->partial = pb ? (float*)c.take(pb) : nullptr;
   return c.used;
 }
 
@@ -438,15 +438,12 @@ int singa_conv_bwd_filter(singa_dtype dtype, singa_layout layout, const singa_sh
   if (rw == RW_PAD && e == hipSuccess) e = launch_pad_channels(dtype, xx, o.xp, (long)s.N * s.H * s.W, s.C, g.C, st);
   if (rw == RW_S2D && e == hipSuccess) e = launch_space_to_depth(dtype, s, g, xx, o.xp, st);
   if (rw != RW_NONE) xx = o.xp;
-  const int splits = wgrad_splits(g, dtype, bias);
   float* krsc = layout == SINGA_NHWC ? dw : o.dw;  // KRSC result
   const int acc = layout == SINGA_NHWC ? accumulate : 0;
   float* target = rw != RW_NONE ? o.dwp : krsc;  // the GEMM's (K, g.R, g.S, g.C) result
   const int tacc = rw != RW_NONE ? 0 : acc;
   // db is written in place by the GEMM's bias column, with the caller's accumulate
   if (e == hipSuccess) e = launch_conv_wgrad(dtype, g, xx, dy, o.partial, target, db, tacc, accumulate, st);
-  if (e == hipSuccess && splits > 1)
-    e = launch_splitk_reduce(o.partial, splits, g, bias, target, db, tacc, accumulate, st);
   if (e == hipSuccess && rw == RW_PAD)
     e = launch_unpad_channels_f32(o.dwp, krsc, (long)s.K * s.R * s.S, g.C, s.C, acc, st);
   if (e == hipSuccess && rw == RW_S2D) e = launch_s2d_to_filter_f32(s, g, o.dwp, krsc, acc, st);

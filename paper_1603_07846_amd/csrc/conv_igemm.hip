@@ -23,6 +23,7 @@
 // rows are padded to 144 bytes so the 16-byte fragment reads of 16
 // consecutive rows hit distinct banks.  Two LDS stages: global loads of tile
 // k+1 are in flight while tile k is multiplied.
+#include <algorithm>
 #include <cstdlib>
 
 #include "common.h"
@@ -460,6 +461,19 @@ typedef __attribute__((address_space(3))) void* lds_ptr;
 // wave-uniform.
 __device__ __forceinline__ void ld_lds16(__amdgpu_buffer_rsrc_t r, uint32_t off, char* base) {
   __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_ptr)base, 16, off, 0, 0, 0);
+}
+
+// The same load issued from inline assembly.  The compiler then does not
+// know that the instruction writes LDS, so it adds no vmcnt wait in front of
+// later LDS reads (it does so for the transpose reads, which would serialize
+// every prefetch); the kernel orders the two itself with wait_vmcnt and a
+// barrier.  M0 carries the LDS address; no other code of these kernels uses
+// M0.
+__device__ __forceinline__ void ld_lds16_asm(__amdgpu_buffer_rsrc_t r, uint32_t off, char* base) {
+  const uint32_t lds = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)base;
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds" ::"s"(__builtin_amdgcn_readfirstlane(lds)),
+               "v"(off), "s"(r)
+               : "memory");
 }
 
 // s_waitcnt vmcnt(n) (n < 64), leaving the other counters alone.
@@ -954,31 +968,277 @@ __global__ __launch_bounds__(NT) void conv_wgrad_kernel(WgradArgs a) {
   }
 }
 
-// Filter-gradient split-K reduction over partial[split][M][Ng]: element
-// (row, col) goes to dw[row][col] for col < Nn and to db[row] for col == Nn
-// (the bias column), each added to or overwriting its target.  A block owns
-// 64 consecutive elements; its 4 waves each sum every 4th split (coalesced
-// 256 B rows), then wave 0 adds the 4 partial sums in a fixed order, so the
-// result does not depend on timing.
+// ----------------------------------------------- filter gradient, large tiles
+//
+// The same product for bf16 operands with whole 16-byte filter and tap chunks
+// (K % 8 == 0, C % 8 == 0), on a 128 (filters) x 256 (taps) tile: each of the
+// 4 waves owns 64 x 128 (2 x 4 blocks of 32 x 32), so one transpose read feeds
+// more MFMAs than in the 128 x 128 kernel.  Operands go from buffer loads
+// straight into LDS as t-major rows (256 bytes of filters, 512 bytes of taps
+// per reduction index); one load instruction fills 1 KB, i.e. 4 (A) or 2 (B)
+// rows.  Rows are unpadded and XOR-swizzled: the 16-byte chunk c of row r sits
+// in slot c ^ (4 (r & 3)), so the 4 rows x 2 column groups that 32 lanes of a
+// transpose read touch fall in 8 distinct 32-byte bank groups.  Three LDS stages; loads of K-tile k+2 are issued while k
+// is multiplied; one barrier per K-tile.  The bias column (tap index Nn) is
+// loaded as an out-of-range zero and set to 1 in the B fragments.
+constexpr int WL_BM = 128, WL_BN = 256, WL_BK = 32;  // BK: reduction rows per K-tile
+constexpr int WL_ARB = WL_BM * 2, WL_BRB = WL_BN * 2;  // row bytes
+constexpr int WL_AT = WL_BK * WL_ARB, WL_BT = WL_BK * WL_BRB;
+constexpr int WL_STAGE = WL_AT + WL_BT;
+constexpr int WL_SMEM = 3 * WL_STAGE;  // 72 KB: two workgroups per CU
+
+template <bool NFAST>
+__global__ __launch_bounds__(NT, 2) void conv_wgrad_large_kernel(WgradArgs a) {
+  constexpr uint32_t ES = 2;
+  constexpr int RPW = WL_BK / 4;    // K-tile rows loaded by each wave (of A and of B)
+  constexpr int AI = WL_BK / 16;    // A load instructions per wave (4 rows each)
+  constexpr int BI = WL_BK / 8;     // B load instructions per wave (2 rows each)
+  __shared__ __attribute__((aligned(16))) char smem[WL_SMEM];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int L = xcd_remap(blockIdx.x, gridDim.x);
+  const int split = L / a.tiles, tile = L - split * a.tiles;
+  const int tm = tile / a.tiles_n, tn = tile - tm * a.tiles_n;
+  const int m0 = tm * WL_BM, n0 = tn * WL_BN;
+  const int kt_begin = split * a.kt_per_split;
+  const int nk = min(a.nkt, kt_begin + a.kt_per_split) - kt_begin;
+  const __amdgpu_buffer_rsrc_t xr = make_rsrc(a.x, a.x_bytes);
+  const __amdgpu_buffer_rsrc_t dyr = make_rsrc(a.dy, a.dy_bytes);
+  const int PQ = a.P * a.Q;
+  const int ystride = PQ * a.M, xstride = a.H * a.W * a.C;
+
+  // A loads: instruction i fills rows 16 wave + 4 i + lane / 16; this lane's chunk
+  const int arow = lane >> 4;
+  const int i0 = m0 + 8 * ((lane & 15) ^ (4 * arow));
+  const bool aok = i0 < a.M;
+  // B loads: instruction i fills rows 16 wave + 2 i + lane / 32; chunk per parity of i
+  const int brow = lane >> 5;
+  int btap[2], br[2], bs[2];
+  bool bok[2];
+#pragma unroll
+  for (int p = 0; p < 2; ++p) {
+    const int j0 = n0 + 8 * ((lane & 31) ^ (4 * (2 * p + brow)));
+    bok[p] = j0 < a.Nn;
+    const int jj = bok[p] ? j0 : 0;
+    const int rs = (int)fdiv((uint32_t)jj, a.dC);
+    const int c = jj - rs * a.C;
+    br[p] = (int)fdiv((uint32_t)rs, a.dS);
+    bs[p] = rs - br[p] * a.S;
+    btap[p] = (br[p] * a.W + bs[p]) * a.C + c;
+  }
+
+  // row d of the K-tile starting at t0 -> (n, output pixel) and validity
+  auto row_pix = [&](int t0, int d, int& n, int& pq, bool& tin) {
+    if constexpr (NFAST) {
+      pq = (int)fdiv((uint32_t)t0, a.dN);
+      n = t0 - pq * a.N + d;
+      tin = true;
+    } else {
+      const int t = t0 + d;
+      tin = t < a.T;
+      n = (int)fdiv((uint32_t)t, a.dPQ);
+      pq = t - n * PQ;
+    }
+  };
+  auto issue = [&](int kt, int stage, int part) {  // part 0: A rows, 1 / 2: first / second half of the B rows
+    char* As = smem + stage * WL_STAGE;
+    char* Bs = As + WL_AT;
+    const int t0 = kt * WL_BK;
+    const bool live = kt < kt_begin + nk;
+    if (part == 0) {
+#pragma unroll
+      for (int i = 0; i < AI; ++i) {
+        const int d = RPW * wave + 4 * i + arow;
+        int n, pq;
+        bool tin;
+        row_pix(t0, d, n, pq, tin);
+        const bool ok = live & tin & aok;
+        ld_lds16_asm(dyr, ok ? (uint32_t)(n * ystride + pq * a.M + i0) * ES : OOB, As + (RPW * wave + 4 * i) * WL_ARB);
+      }
+    } else {
+#pragma unroll
+      for (int ii = 0; ii < BI / 2; ++ii) {
+        const int i = (part - 1) * (BI / 2) + ii;
+        const int p = i & 1;
+        const int d = RPW * wave + 2 * i + brow;
+        int n, pq;
+        bool tin;
+        row_pix(t0, d, n, pq, tin);
+        const int pr = (int)fdiv((uint32_t)pq, a.dQ);
+        const int h = pr * a.sh - a.ph + br[p], w = (pq - pr * a.Q) * a.sw - a.pw + bs[p];
+        const bool ok = live & tin & bok[p] & ((unsigned)h < (unsigned)a.H) & ((unsigned)w < (unsigned)a.W);
+        const int xoff = n * xstride + ((pr * a.sh - a.ph) * a.W + (pq - pr * a.Q) * a.sw - a.pw) * a.C + btap[p];
+        ld_lds16_asm(xr, ok ? (uint32_t)xoff * ES : OOB, Bs + (RPW * wave + 2 * i) * WL_BRB);
+      }
+    }
+  };
+
+  f32x16 acc[2][4];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+
+  // transpose-read addresses: lane -> column (lane & 31) of a 32-column block,
+  // reduction rows 8 (lane / 32) + 0..7 of a 16-row step
+  const int wm = wave >> 1, wn = wave & 1;
+  const int trow = 8 * (lane >> 5) + ((lane & 15) >> 2);
+  const int low = 2 * ((lane >> 4) & 1) + ((lane & 3) >> 1);  // chunk bits 0-1 within a 32-column block
+  const int rr = (lane & 15) >> 2;                                // row & 3 (same for every step)
+  const int off = 8 * (lane & 1);
+  int aaddr[2], baddr[4];
+#pragma unroll
+  for (int b = 0; b < 2; ++b) {
+    const int x32 = (wm * 64 + b * 32) / 32;  // chunk = 4 x32 + low, stored in slot chunk ^ (4 rr)
+    aaddr[b] = trow * WL_ARB + ((4 * (x32 ^ rr) + low) << 4) + off;
+  }
+#pragma unroll
+  for (int b = 0; b < 4; ++b) {
+    const int x32 = (wn * 128 + b * 32) / 32;
+    baddr[b] = WL_AT + trow * WL_BRB + ((4 * (x32 ^ rr) + low) << 4) + off;
+  }
+  // the bias column as ones in the B fragments of the wave that holds it
+  uint32_t onesm[4];
+  bool bias_wave = false;
+#pragma unroll
+  for (int b = 0; b < 4; ++b) {
+    const int cb = n0 + wn * 128 + b * 32;
+    onesm[b] = (a.Ng > a.Nn && cb + (lane & 31) == a.Nn) ? 0x3f803f80u : 0u;
+    bias_wave |= a.Ng > a.Nn && cb <= a.Nn && a.Nn < cb + 32;
+  }
+
+  auto compute = [&](const char* S) {
+#pragma unroll
+    for (int kc = 0; kc < WL_BK / 16; ++kc) {
+      bf16x8 af[2], bfr[4];
+#pragma unroll
+      for (int b = 0; b < 2; ++b) {
+        const v4i16 lo = lds_tr16(S + aaddr[b] + kc * 16 * WL_ARB);
+        const v4i16 hi = lds_tr16(S + aaddr[b] + (kc * 16 + 4) * WL_ARB);
+        af[b] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+      }
+#pragma unroll
+      for (int b = 0; b < 4; ++b) {
+        const v4i16 lo = lds_tr16(S + baddr[b] + kc * 16 * WL_BRB);
+        const v4i16 hi = lds_tr16(S + baddr[b] + (kc * 16 + 4) * WL_BRB);
+        bfr[b] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+      }
+      if (bias_wave) {
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+          uint4 u = __builtin_bit_cast(uint4, bfr[b]);
+          u.x |= onesm[b];
+          u.y |= onesm[b];
+          u.z |= onesm[b];
+          u.w |= onesm[b];
+          bfr[b] = __builtin_bit_cast(bf16x8, u);
+        }
+      }
+#pragma unroll
+      for (int bm = 0; bm < 2; ++bm)
+#pragma unroll
+        for (int bn = 0; bn < 4; ++bn)
+          acc[bm][bn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[bm], bfr[bn], acc[bm][bn], 0, 0, 0);
+    }
+  };
+
+  if (nk > 0) {
+    constexpr int LOADS = AI + BI;  // per thread per K-tile
+#pragma unroll
+    for (int part = 0; part < 3; ++part) issue(kt_begin, 0, part);
+#pragma unroll
+    for (int part = 0; part < 3; ++part) issue(kt_begin + 1, 1, part);
+    int stage = 0;
+    for (int k = 0; k < nk; ++k) {
+      wait_vmcnt<LOADS>();  // tile k has landed for this thread (tile k+1 may be in flight)
+      block_barrier();      // ... and for everyone; everyone is done with tile k-1
+      const int nstage = stage == 0 ? 2 : stage - 1;
+      const char* S = smem + stage * WL_STAGE;
+      issue(kt_begin + k + 2, nstage, 0);  // past the split's end: all-OOB, no traffic
+      compute(S);
+      issue(kt_begin + k + 2, nstage, 1);
+      issue(kt_begin + k + 2, nstage, 2);
+      stage = stage == 2 ? 0 : stage + 1;
+    }
+    wait_vmcnt<0>();
+  }
+
+  const int li = lane & 31, lh = lane >> 5;
+  if (!a.direct) {
+    float* __restrict__ out = a.out + (size_t)split * a.M * a.ldp;
+#pragma unroll
+    for (int bn = 0; bn < 4; ++bn) {
+      const int col = n0 + wn * 128 + bn * 32 + li;
+      if (col >= a.Ng) continue;
+#pragma unroll
+      for (int bm = 0; bm < 2; ++bm)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int row = m0 + wm * 64 + bm * 32 + (v >> 2) * 8 + lh * 4 + (v & 3);
+          if (row < a.M) out[(size_t)row * a.ldp + col] = acc[bm][bn][v];
+        }
+    }
+    return;
+  }
+#pragma unroll
+  for (int bn = 0; bn < 4; ++bn) {
+    const int col = n0 + wn * 128 + bn * 32 + li;
+    if (col >= a.Ng) continue;
+    const bool is_db = col == a.Nn;
+    float* __restrict__ base = is_db ? a.db : a.out + col;
+    const size_t stride = is_db ? 1 : (size_t)a.Nn;
+    const int accum = is_db ? a.acc_db : a.acc_dw;
+#pragma unroll
+    for (int bm = 0; bm < 2; ++bm)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int row = m0 + wm * 64 + bm * 32 + (v >> 2) * 8 + lh * 4 + (v & 3);
+        if (row < a.M) {
+          float* o = base + (size_t)row * stride;
+          *o = accum ? *o + acc[bm][bn][v] : acc[bm][bn][v];
+        }
+      }
+  }
+}
+
+// Filter-gradient split-K reduction over partial[split][M][Ng] (rows of ldp
+// floats, ldp % 64 == 0): element (row, col) goes to dw[row][col] for col < Nn
+// and to db[row] for col == Nn (the bias column), each added to or
+// overwriting its target.  A block owns 256 consecutive elements of one row
+// (ldp % 256 == 0 is not required: a block never straddles rows because it
+// covers 4 groups of 64 from the same 64-aligned start); its 4 waves each sum
+// every 4th split with 16-byte loads, then wave 0 adds the 4 partial sums in a
+// fixed order, so the result does not depend on timing.
 __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restrict__ partial, int splits, int M,
                                                             int ldp, int Ng, int Nn, float* __restrict__ dw,
                                                             float* __restrict__ db, int acc_dw, int acc_db) {
-  __shared__ float part[4][64];
-  const size_t n = (size_t)M * ldp;  // ldp % 64 == 0: a block covers 64 columns of one row
+  __shared__ float4 part[4][64];
+  const size_t n = (size_t)M * ldp;
   const int g = threadIdx.x >> 6, l = threadIdx.x & 63;
-  const size_t i = (size_t)blockIdx.x * 64 + l;
+  const size_t i = ((size_t)blockIdx.x * 64 + l) * 4;  // 4 consecutive elements of one row (ldp % 4 == 0)
   const int row = (int)(i / (size_t)ldp);
   const int col = (int)(i - (size_t)row * ldp);
-  if (col - l >= Ng) return;  // the whole block is in the row padding
-  float t = 0.f;
-  if (col < Ng)
-    for (int k = g; k < splits; k += 4) t += partial[(size_t)k * n + i];
+  float4 t = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (i < n && col < Ng) {
+    for (int k = g; k < splits; k += 4) {
+      const float4 v = *(const float4*)(partial + (size_t)k * n + i);
+      t.x += v.x; t.y += v.y; t.z += v.z; t.w += v.w;
+    }
+  }
   part[g][l] = t;
   __syncthreads();
-  if (g == 0 && col < Ng) {
-    const float sum = (part[0][l] + part[1][l]) + (part[2][l] + part[3][l]);
-    float* o = col < Nn ? dw + (size_t)row * Nn + col : db + row;
-    *o = (col < Nn ? acc_dw : acc_db) ? *o + sum : sum;
+  if (g == 0 && i < n) {
+    const float4 a = part[0][l], b = part[1][l], c = part[2][l], d = part[3][l];
+    const float s4[4] = {(a.x + b.x) + (c.x + d.x), (a.y + b.y) + (c.y + d.y), (a.z + b.z) + (c.z + d.z),
+                         (a.w + b.w) + (c.w + d.w)};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int ce = col + e;
+      if (ce >= Ng) break;
+      float* o = ce < Nn ? dw + (size_t)row * Nn + ce : db + row;
+      *o = (ce < Nn ? acc_dw : acc_db) ? *o + s4[e] : s4[e];
+    }
   }
 }
 
@@ -1186,11 +1446,42 @@ bool use_image_fastest(const ConvShape& s, int bk) {
   return s.P * s.Q < 1024;
 }
 
+// Split-K count of the filter gradient on `tiles` output tiles and `nkt`
+// K-tiles: about `target` workgroups, at least 8 K-tiles each, every split
+// non-empty.
+int wgrad_split_count(long tiles, long nkt, long target) {
+  long splits = (target + tiles - 1) / tiles;
+  const long max_by_len = nkt / 8;
+  if (splits > max_by_len) splits = max_by_len;
+  if (splits < 1) splits = 1;
+  if (splits > 256) splits = 256;
+  const long per = (nkt + splits - 1) / splits;
+  return (int)((nkt + per - 1) / per);
+}
+
+// The 128 x 256 kernel: bf16 with whole 16-byte filter and tap chunks
+// (SINGA_CONV_TILE=128 keeps the 128 x 128 kernel).
+bool wgrad_large_shape(const ConvShape& s, int dt) {
+  return dt == BF16 && s.K % 8 == 0 && s.C % 8 == 0 && forced_tile() != 128;
+}
+
+// Splits used by the kernel that runs shape s (large: the 128 x 256 kernel).
+int wgrad_splits_for(const ConvShape& s, int dt, bool bias, bool large) {
+  const long M = s.K, Ng = (long)s.R * s.S * s.C + (bias ? 1 : 0), T = (long)s.N * s.P * s.Q;
+  if (large) {
+    const long tiles = ((M + WL_BM - 1) / WL_BM) * ((Ng + WL_BN - 1) / WL_BN);
+    return wgrad_split_count(tiles, (T + WL_BK - 1) / WL_BK, 1024);  // two workgroups per CU: two rounds
+  }
+  const long tiles = ((M + BM - 1) / BM) * ((Ng + BN - 1) / BN);
+  const long bk = dt == BF16 ? WG<bf16_t>::BK : WG<float>::BK;
+  return wgrad_split_count(tiles, (T + bk - 1) / bk, 1024);  // about 4 workgroups per CU
+}
+
 template <typename T>
 hipError_t conv_wgrad_dispatch(const ConvShape& s, const void* x, const void* dy, float* partial, float* dw,
                                float* db, int acc_dw, int acc_db, hipStream_t st) {
   constexpr int VEC = 16 / (int)sizeof(T);
-  constexpr int BK = WG<T>::BK;
+  constexpr int DT = sizeof(T) == 2 ? BF16 : F32;
   WgradArgs a;
   a.x = x; a.dy = dy;
   a.x_bytes = (uint32_t)((size_t)s.N * s.H * s.W * s.C * sizeof(T));
@@ -1207,11 +1498,14 @@ hipError_t conv_wgrad_dispatch(const ConvShape& s, const void* x, const void* dy
   a.dQ = make_fastdiv((uint32_t)s.Q);
   a.dC = make_fastdiv((uint32_t)s.C);
   a.dS = make_fastdiv((uint32_t)s.S);
-  const int tiles_m = (a.M + BM - 1) / BM;
-  a.tiles_n = (a.Ng + BN - 1) / BN;
-  a.tiles = tiles_m * a.tiles_n;
-  a.nkt = (a.T + BK - 1) / BK;
-  const int splits = wgrad_splits(s, sizeof(T) == 2 ? BF16 : F32, db != nullptr);
+  const bool va = (a.M % VEC) == 0 && ((uintptr_t)dy % 16) == 0;
+  const int vb = load_mode<T>(s.C, x);
+  const bool large = wgrad_large_shape(s, DT) && va && vb == VEC16;
+  const int bm = large ? WL_BM : BM, bn = large ? WL_BN : BN, bk = large ? WL_BK : WG<T>::BK;
+  a.tiles_n = (a.Ng + bn - 1) / bn;
+  a.tiles = ((a.M + bm - 1) / bm) * a.tiles_n;
+  a.nkt = (a.T + bk - 1) / bk;
+  const int splits = wgrad_splits_for(s, DT, db != nullptr, large);
   a.kt_per_split = (a.nkt + splits - 1) / splits;
   a.direct = splits == 1;
   a.acc_dw = acc_dw;
@@ -1219,13 +1513,26 @@ hipError_t conv_wgrad_dispatch(const ConvShape& s, const void* x, const void* dy
   a.out = a.direct ? dw : partial;
   a.db = db;
   dim3 grid(a.tiles * splits);
-  const bool va = (a.M % VEC) == 0 && ((uintptr_t)dy % 16) == 0;
-  const int vb = load_mode<T>(s.C, x);
   const double flops = 2.0 * a.M * (double)a.Nn * (double)a.T;
-  if (use_image_fastest(s, BK))
+  const bool nf = use_image_fastest(s, bk);
+  if (large) {
+    TraceScope ts(nf ? "conv_wgrad_large_kernel<1>" : "conv_wgrad_large_kernel<0>", st, flops, WORK_FLOP);
+    if (nf)
+      hipLaunchKernelGGL(conv_wgrad_large_kernel<true>, grid, dim3(NT), 0, st, a);
+    else
+      hipLaunchKernelGGL(conv_wgrad_large_kernel<false>, grid, dim3(NT), 0, st, a);
+  } else if (nf) {
     launch_wgrad_variant<T, true>(va, vb, a, grid, flops, st);
-  else
+  } else {
     launch_wgrad_variant<T, false>(va, vb, a, grid, flops, st);
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || splits == 1) return e;
+  // fixed-order sum of the partial tiles into dw (and db)
+  const size_t n = (size_t)a.M * a.ldp;
+  TraceScope ts("splitk_reduce_kernel", st, (double)a.M * a.Ng * 4.0 * (splits + 1 + (acc_dw ? 1 : 0)), WORK_BYTE);
+  hipLaunchKernelGGL(splitk_reduce_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, partial, splits, a.M,
+                     a.ldp, a.Ng, a.Nn, dw, db, acc_dw, acc_db);
   return hipGetLastError();
 }
 
@@ -1243,43 +1550,19 @@ size_t fwd_partial_bytes(const ConvShape& s, int dt) {
   return splits > 1 ? (size_t)splits * M * Nn * sizeof(float) : 0;
 }
 
-int wgrad_splits(const ConvShape& s, int dt, bool bias) {
-  const long M = s.K, Ng = (long)s.R * s.S * s.C + (bias ? 1 : 0), T = (long)s.N * s.P * s.Q;
-  const long tiles = ((M + BM - 1) / BM) * ((Ng + BN - 1) / BN);
-  const long bk = dt == BF16 ? WG<bf16_t>::BK : WG<float>::BK;
-  const long nkt = (T + bk - 1) / bk;
-  // aim for about 4 workgroups per CU on 256 CUs, at least 8 K-tiles per split
-  long splits = (1024 + tiles - 1) / tiles;
-  const long max_by_len = nkt / 8;
-  if (splits > max_by_len) splits = max_by_len;
-  if (splits < 1) splits = 1;
-  if (splits > 256) splits = 256;
-  // every split gets at least one K-tile
-  const long per = (nkt + splits - 1) / splits;
-  return (int)((nkt + per - 1) / per);
-}
-
 size_t wgrad_partial_bytes(const ConvShape& s, int dt, bool bias) {
   const size_t Ng = (size_t)s.R * s.S * s.C + (bias ? 1 : 0);
   const size_t ldp = (Ng + 63) / 64 * 64;
-  return (size_t)wgrad_splits(s, dt, bias) * s.K * ldp * sizeof(float);
+  // either kernel may run (the large one also needs aligned pointers)
+  int splits = wgrad_splits_for(s, dt, bias, false);
+  if (wgrad_large_shape(s, dt)) splits = std::max(splits, wgrad_splits_for(s, dt, bias, true));
+  return splits > 1 ? (size_t)splits * s.K * ldp * sizeof(float) : 0;
 }
 
 hipError_t launch_conv_wgrad(int dt, const ConvShape& s, const void* x, const void* dy, float* partial, float* dw,
                              float* db, int acc_dw, int acc_db, hipStream_t st) {
   if (dt == BF16) return conv_wgrad_dispatch<bf16_t>(s, x, dy, partial, dw, db, acc_dw, acc_db, st);
   return conv_wgrad_dispatch<float>(s, x, dy, partial, dw, db, acc_dw, acc_db, st);
-}
-
-hipError_t launch_splitk_reduce(const float* partial, int splits, const ConvShape& s, bool bias, float* dw,
-                                float* db, int acc_dw, int acc_db, hipStream_t st) {
-  const int Nn = s.R * s.S * s.C, Ng = Nn + (bias ? 1 : 0), ldp = (Ng + 63) / 64 * 64;
-  const size_t n = (size_t)s.K * ldp;
-  const size_t blocks = n / 64;
-  TraceScope ts("splitk_reduce_kernel", st, (double)s.K * Ng * 4.0 * (splits + 1 + (acc_dw ? 1 : 0)), WORK_BYTE);
-  hipLaunchKernelGGL(splitk_reduce_kernel, dim3((unsigned)blocks), dim3(256), 0, st, partial, splits, s.K, ldp, Ng,
-                     Nn, dw, db, acc_dw, acc_db);
-  return hipGetLastError();
 }
 
 }  // namespace singa

@@ -50,19 +50,15 @@ hipError_t launch_conv_fwd(int dt, const ConvShape& s, const void* x, const void
                            hipStream_t st);
 size_t fwd_partial_bytes(const ConvShape& s, int dt);
 
-// Split-K implicit-GEMM filter gradient.  Number of K-splits used for a shape
-// and the fp32 partial-sum buffer it needs.  With `bias` the GEMM carries one
-// more column, a reduction against ones, that yields db.  With one split the
+// Split-K implicit-GEMM filter gradient, dw (K, R, S, C) and, with db, the
+// bias gradient from one more GEMM column against ones.  With one split the
 // kernel writes (or, with acc_dw / acc_db, adds into) dw and db directly;
-// otherwise it writes the partial tiles and launch_splitk_reduce adds them.
-int wgrad_splits(const ConvShape& s, int dt, bool bias);
+// otherwise it writes partial tiles into `partial` (wgrad_partial_bytes() of
+// workspace; NULL when that is 0) and a second kernel adds them in a fixed
+// order.
 size_t wgrad_partial_bytes(const ConvShape& s, int dt, bool bias);
 hipError_t launch_conv_wgrad(int dt, const ConvShape& s, const void* x, const void* dy, float* partial, float* dw,
                              float* db, int acc_dw, int acc_db, hipStream_t st);
-// dw (and db, the bias column) = (accumulate ? old : 0) + the sum over splits
-// of the partial tiles, in a fixed order.
-hipError_t launch_splitk_reduce(const float* partial, int splits, const ConvShape& s, bool bias, float* dw,
-                                float* db, int acc_dw, int acc_db, hipStream_t st);
 
 // Batched 2-D transpose: for b in [0, batch): out(b)[c][r] = in(b)[r][c] with
 // in(b) = in + in_base(b), out(b) = out + out_base(b), where

@@ -82,7 +82,10 @@ def test_workspace_sizes():
     assert singa.conv_workspace_bytes(singa.OP_FWD, singa.BF16, x, w, 2, 1) == 0
     # stride 1 backward-data keeps one flipped filter copy
     assert singa.conv_workspace_bytes(singa.OP_BWD_DATA, singa.BF16, x, w, 2, 1) >= 256 * 25 * 96 * 2
-    assert singa.conv_workspace_bytes(singa.OP_BWD_DATA, singa.F32, (2, 35, 35, 3), (8, 11, 11, 3), 0, 4) == 0
+    # strided backward-data: the space-to-depth filter, its flipped transpose and the rewritten input gradient
+    # (11x11/4 on 3 channels -> 3x3/1 on 48 channels, 9x9 rewritten input)
+    assert singa.conv_workspace_bytes(singa.OP_BWD_DATA, singa.F32, (2, 35, 35, 3), (8, 11, 11, 3), 0, 4) >= \
+        2 * (8 * 3 * 3 * 48 * 4) + 2 * 9 * 9 * 48 * 4
     assert singa.conv_workspace_bytes(singa.OP_BWD_FILTER, singa.F32, x, w, 2, 1) >= 256 * 25 * 96 * 4
     nchw = singa.conv_workspace_bytes(singa.OP_FWD, singa.F32, (2, 96, 27, 27), (256, 96, 5, 5), 2, 1,
                                       layout="NCHW")
