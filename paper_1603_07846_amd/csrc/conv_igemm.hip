@@ -441,19 +441,27 @@ __global__ __launch_bounds__(NT) void conv_fwd_kernel(FwdArgs a) {
 // the 4 waves owns a 128 x 64 quadrant (4 x 2 blocks of 32 x 32), so one
 // 16-byte fragment read feeds more MFMAs than in the 128 x 128 kernel.
 // Global data goes straight from the buffer loads into LDS (each load
-// instruction writes 64 consecutive 16-byte slots, i.e. 8 rows of 128 bytes),
-// with no register staging.  Three LDS stages: the loads of K-tile k+2 are in
-// flight while tile k is multiplied; one barrier per K-tile.
+// instruction writes 64 consecutive 16-byte slots) with no register staging.
+// Three LDS stages: the loads of K-tile k+2 are in flight while tile k is
+// multiplied; one barrier per K-tile.  LBK taps per K-tile: 64 (144 KB of
+// LDS, one workgroup per CU) or 32 (72 KB, two workgroups per CU).
 //
-// LDS rows are 128 bytes without padding; slot s of row r holds the 16-byte
-// tap chunk s ^ ((r >> 1) & 7).  A fragment read (16 lanes, 16 consecutive
-// rows, one chunk) then touches 16 distinct 16-byte bank groups.
+// LDS rows (LBK * 2 bytes) are unpadded and XOR-swizzled: slot s of row r
+// holds the 16-byte tap chunk s ^ ((r / RPW) % SL), with SL slots per row and
+// RPW rows per 256-byte bank window, so a fragment read (16 lanes, 16
+// consecutive rows, one chunk) touches 16 distinct 16-byte bank groups.
 constexpr int L_BM = 256;
 constexpr int L_STAGES = 3;
-constexpr int L_ATILE = L_BM * ROWB;           // 32 KB
-constexpr int L_BTILE = BN * ROWB;             // 16 KB
-constexpr int L_STAGE = L_ATILE + L_BTILE;
-constexpr int L_SMEM = L_STAGES * L_STAGE;     // 144 KB
+template <int LBK> struct LT {
+  static constexpr int RB = LBK * 2;                  // row bytes
+  static constexpr int SL = RB / 16;                  // 16-byte slots per row
+  static constexpr int RPI = 64 / SL;                 // rows per load instruction
+  static constexpr int RPW = 256 / RB;                // rows per 256-byte bank window
+  static constexpr int ATILE = L_BM * RB, BTILE = BN * RB, STAGE = ATILE + BTILE;
+  static constexpr int SMEM = L_STAGES * STAGE;
+  static constexpr int AI = L_BM / RPI / 4, BI = BN / RPI / 4;  // load instructions per wave
+  static constexpr int KS = LBK / 16;                 // MFMA k-steps per K-tile
+};
 
 typedef __attribute__((address_space(3))) void* lds_ptr;
 
@@ -484,11 +492,11 @@ template <int N> __device__ __forceinline__ void wait_vmcnt() {
 
 __device__ __forceinline__ void block_barrier() { asm volatile("s_barrier" ::: "memory"); }
 
-template <bool BWD>
-__global__ __launch_bounds__(NT) void conv_fwd_large_kernel(FwdArgs a) {
-  constexpr int BK = 64;
-  constexpr int LOADS = L_BM / 32 + BN / 32;  // 16-byte loads per thread per K-tile
-  __shared__ __attribute__((aligned(16))) char smem[L_SMEM];
+template <bool BWD, int LBK>
+__global__ __launch_bounds__(NT, LBK == 32 ? 2 : 1) void conv_fwd_large_kernel(FwdArgs a) {
+  typedef LT<LBK> G;
+  constexpr int LOADS = G::AI + G::BI;  // 16-byte loads per thread per K-tile
+  __shared__ __attribute__((aligned(16))) char smem[G::SMEM];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int L = xcd_remap(blockIdx.x, gridDim.x);
@@ -498,17 +506,19 @@ __global__ __launch_bounds__(NT) void conv_fwd_large_kernel(FwdArgs a) {
   const __amdgpu_buffer_rsrc_t xr = make_rsrc(a.x, a.x_bytes);
   const __amdgpu_buffer_rsrc_t wr = make_rsrc(a.w, a.w_bytes);
 
-  // Loader: instruction i of this wave fills rows 8i .. 8i+7 of the wave's
-  // 64-row (A) / 32-row (B) band; this lane owns row 8i + lane/8, slot
-  // lane % 8, which holds chunk (lane % 8) ^ (4 (i & 1) + lane / 16).
-  const int lrow = lane >> 3;
+  // Loader: instruction i of this wave fills rows RPI i .. RPI i + RPI - 1 of
+  // the wave's A (64 rows) / B (32 rows) band; this lane owns row RPI i +
+  // lane / SL, slot lane % SL, which holds chunk cpar[p] with p the parity of
+  // i for 128-byte rows (always 0 for 64-byte rows).
+  const int lrow = lane / G::SL;
   int cpar[2];
 #pragma unroll
-  for (int p = 0; p < 2; ++p) cpar[p] = (lane & 7) ^ (4 * p + (lane >> 4));
-  int apix[8], ah0[8], aw0[8];
+  for (int p = 0; p < 2; ++p) cpar[p] = (lane % G::SL) ^ ((4 * p * (G::SL == 8) + (lane >> 4)) % G::SL);
+  constexpr int NPAR = G::SL == 8 ? 2 : 1;
+  int apix[G::AI], ah0[G::AI], aw0[G::AI];
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    const int m = m0 + 64 * wave + 8 * i + lrow;
+  for (int i = 0; i < G::AI; ++i) {
+    const int m = m0 + 64 * wave + G::RPI * i + lrow;
     if (m < a.M) {
       const int n = (int)fdiv((uint32_t)m, a.dPQ);
       const int pq = m - n * a.P * a.Q;
@@ -523,15 +533,15 @@ __global__ __launch_bounds__(NT) void conv_fwd_large_kernel(FwdArgs a) {
       apix[i] = 0;
     }
   }
-  int brow[4];
+  int brow[G::BI];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int n = n0 + 32 * wave + 8 * i + lrow;
+  for (int i = 0; i < G::BI; ++i) {
+    const int n = n0 + 32 * wave + G::RPI * i + lrow;
     brow[i] = n < a.Nn ? n * a.Kg : -1;
   }
 
-  // Tap decomposition of this lane's two chunks (even / odd instructions) of
-  // the K-tile at k0; a K-tile past the end gives OOB everywhere.
+  // Tap decomposition of this lane's chunk(s) of the K-tile at k0; a K-tile
+  // past the end gives OOB everywhere.
   struct Taps {
     int tap[2], r[2], s[2];
     bool kin[2];
@@ -540,7 +550,7 @@ __global__ __launch_bounds__(NT) void conv_fwd_large_kernel(FwdArgs a) {
   auto taps = [&](int k0) {
     Taps t;
 #pragma unroll
-    for (int p = 0; p < 2; ++p) {
+    for (int p = 0; p < NPAR; ++p) {
       const int kk = k0 + 8 * cpar[p];
       t.kk[p] = kk;
       t.kin[p] = kk < a.Kg;
@@ -553,23 +563,25 @@ __global__ __launch_bounds__(NT) void conv_fwd_large_kernel(FwdArgs a) {
     return t;
   };
   auto issue_a = [&](const Taps& t, char* As, int i) {
-    const int p = i & 1;
+    const int p = NPAR == 2 ? (i & 1) : 0;
     const int h = ah0[i] + t.r[p], w = aw0[i] + t.s[p];
     const bool ok = t.kin[p] & ((unsigned)h < (unsigned)a.H) & ((unsigned)w < (unsigned)a.W);
-    ld_lds16(xr, ok ? (uint32_t)(apix[i] + t.tap[p]) * 2u : OOB, As + (64 * wave + 8 * i) * ROWB);
+    ld_lds16(xr, ok ? (uint32_t)(apix[i] + t.tap[p]) * 2u : OOB, As + (64 * wave + G::RPI * i) * G::RB);
   };
   auto issue_b = [&](const Taps& t, char* Bs, int i) {
-    const int p = i & 1;
+    const int p = NPAR == 2 ? (i & 1) : 0;
     const bool ok = (brow[i] >= 0) & t.kin[p];
-    ld_lds16(wr, ok ? (uint32_t)(brow[i] + t.kk[p]) * 2u : OOB, Bs + (32 * wave + 8 * i) * ROWB);
+    ld_lds16(wr, ok ? (uint32_t)(brow[i] + t.kk[p]) * 2u : OOB, Bs + (32 * wave + G::RPI * i) * G::RB);
   };
-  auto issue = [&](int k0, int stage) {
-    char* As = smem + stage * L_STAGE;
-    const Taps t = taps(k0);
+  // the j-th of KS slices of the K-tile's loads (spread over its k-steps)
+  auto issue_slice = [&](const Taps& t, char* St, int j) {
+    constexpr int TOT = G::AI + G::BI;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) issue_a(t, As, i);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) issue_b(t, As + L_ATILE, i);
+    for (int q = 0; q < TOT; ++q) {
+      if (q * G::KS / TOT != j) continue;
+      if (q < G::AI) issue_a(t, St, q);
+      else issue_b(t, St + G::ATILE, q - G::AI);
+    }
   };
 
   f32x16 acc[4][2];
@@ -582,8 +594,9 @@ __global__ __launch_bounds__(NT) void conv_fwd_large_kernel(FwdArgs a) {
 
   const int wm = wave >> 1, wn = wave & 1;
   const int li = lane & 31, lh = lane >> 5;
-  const int tsw = (lh ^ ((li >> 1) & 7)) << 4;  // chunk of k-step kc sits at byte (32 kc) ^ tsw
-  const int aoff = (wm * 128 + li) * ROWB, boff = L_ATILE + (wn * 64 + li) * ROWB;
+  // chunk 2 kc + lh of row r sits in slot (2 kc + lh) ^ ((r / RPW) % SL); r % 16 = li % 16
+  const int tsw = (lh ^ ((li / G::RPW) % G::SL)) << 4;
+  const int aoff = (wm * 128 + li) * G::RB, boff = G::ATILE + (wn * 64 + li) * G::RB;
   struct Frags {
     bf16x8 a[4], b[2];
   };
@@ -591,9 +604,9 @@ __global__ __launch_bounds__(NT) void conv_fwd_large_kernel(FwdArgs a) {
     Frags f;
     const int co = (32 * kc) ^ tsw;
 #pragma unroll
-    for (int b = 0; b < 4; ++b) f.a[b] = *(const bf16x8*)(S + aoff + b * 32 * ROWB + co);
+    for (int b = 0; b < 4; ++b) f.a[b] = *(const bf16x8*)(S + aoff + b * 32 * G::RB + co);
 #pragma unroll
-    for (int b = 0; b < 2; ++b) f.b[b] = *(const bf16x8*)(S + boff + b * 32 * ROWB + co);
+    for (int b = 0; b < 2; ++b) f.b[b] = *(const bf16x8*)(S + boff + b * 32 * G::RB + co);
     return f;
   };
   auto mma = [&](const Frags& f) {
@@ -604,37 +617,33 @@ __global__ __launch_bounds__(NT) void conv_fwd_large_kernel(FwdArgs a) {
         acc[bm][bn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[bm], f.b[bn], acc[bm][bn], 0, 0, 0);
   };
 
-  const int nkt_all = (a.Kg + BK - 1) / BK;
-  const int kbase = split * a.kt_per_split * BK;
+  const int nkt_all = (a.Kg + LBK - 1) / LBK;
+  const int kbase = split * a.kt_per_split * LBK;
   const int nkt = min(a.kt_per_split, nkt_all - split * a.kt_per_split);
-  const int kend = kbase + nkt * BK;  // K-tiles from here on are issued as all-OOB (zeros, no traffic)
-  issue(kbase, 0);
-  issue(nkt > 1 ? kbase + BK : a.Kg, 1);
+  const int kend = kbase + nkt * LBK;  // K-tiles from here on are issued as all-OOB (zeros, no traffic)
+#pragma unroll
+  for (int j = 0; j < G::KS; ++j) issue_slice(taps(kbase), smem, j);
+#pragma unroll
+  for (int j = 0; j < G::KS; ++j) issue_slice(taps(nkt > 1 ? kbase + LBK : a.Kg), smem + G::STAGE, j);
   int stage = 0;
   for (int kt = 0; kt < nkt; ++kt) {
     wait_vmcnt<LOADS>();  // this thread's loads of tile kt have landed (tile kt+1's may be in flight)
     block_barrier();      // ... and everyone's; everyone is also done with tile kt-1
     const int nstage = stage == 0 ? 2 : stage - 1;
-    char* Ns = smem + nstage * L_STAGE;
-    const int knext = kbase + (kt + 2) * BK;
+    char* Ns = smem + nstage * G::STAGE;
+    const int knext = kbase + (kt + 2) * LBK;
     const Taps t = taps(knext < kend ? knext : a.Kg);
-    const char* S = smem + stage * L_STAGE;
-    // Fragments one k-step ahead; the loads of tile kt+2 are spread over the
-    // k-steps so their address arithmetic overlaps the MFMAs.
-    Frags f0 = frags(S, 0);
-    Frags f1 = frags(S, 1);
-    mma(f0);
+    const char* S = smem + stage * G::STAGE;
+    // fragments one k-step ahead; the loads of tile kt+2 spread over the k-steps
+    Frags f = frags(S, 0);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) issue_a(t, Ns, i);
-    f0 = frags(S, 2);
-    mma(f1);
-#pragma unroll
-    for (int i = 4; i < 8; ++i) issue_a(t, Ns, i);
-    f1 = frags(S, 3);
-    mma(f0);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) issue_b(t, Ns + L_ATILE, i);
-    mma(f1);
+    for (int kc = 0; kc < G::KS; ++kc) {
+      Frags g;
+      if (kc + 1 < G::KS) g = frags(S, kc + 1);
+      mma(f);
+      issue_slice(t, Ns, kc);
+      if (kc + 1 < G::KS) f = g;
+    }
     stage = stage == 2 ? 0 : stage + 1;
   }
   wait_vmcnt<0>();  // the trailing all-OOB loads still write LDS
@@ -1297,6 +1306,19 @@ int forced_tile() {
   return v;
 }
 
+// K-tile depth of the 256 x 128 forward kernel: 32 taps (two workgroups per
+// CU, more latency hiding) unless the reduction is very long, where 64 (one
+// workgroup per CU, half the barriers) measured faster.  SINGA_FWD_BK=32|64
+// forces one.
+int fwd_large_bk(long Kg) {
+  static const int forced = [] {
+    const char* e = getenv("SINGA_FWD_BK");
+    return e ? atoi(e) : 0;
+  }();
+  if (forced == 32 || forced == 64) return forced;
+  return Kg >= 4096 ? 64 : 32;
+}
+
 bool use_large_fwd(long M, long Nn, long Kg) {
   if (forced_tile() == 128) return false;
   if (forced_tile() == 256) return ((M + L_BM - 1) / L_BM) * ((Nn + BN - 1) / BN) > 0;
@@ -1379,12 +1401,16 @@ hipError_t conv_fwd_dispatch(const ConvShape& s, const void* x, const void* w, c
     a.tiles_n = (a.Nn + BN - 1) / BN;
     a.tiles = ((a.M + L_BM - 1) / L_BM) * a.tiles_n;
     a.partial = nullptr;
-    a.kt_per_split = nkt;
+    const bool deep = fwd_large_bk(a.Kg) == 64;
+    a.kt_per_split = (a.Kg + (deep ? 64 : 32) - 1) / (deep ? 64 : 32);  // one split: every K-tile of this depth
     TraceScope ts(bwd ? fwd_large_name<true>() : fwd_large_name<false>(), st, flops, WORK_FLOP);
-    if (bwd)
-      hipLaunchKernelGGL(conv_fwd_large_kernel<true>, dim3(a.tiles), dim3(NT), 0, st, a);
-    else
-      hipLaunchKernelGGL(conv_fwd_large_kernel<false>, dim3(a.tiles), dim3(NT), 0, st, a);
+    if (bwd) {
+      if (deep) hipLaunchKernelGGL((conv_fwd_large_kernel<true, 64>), dim3(a.tiles), dim3(NT), 0, st, a);
+      else hipLaunchKernelGGL((conv_fwd_large_kernel<true, 32>), dim3(a.tiles), dim3(NT), 0, st, a);
+    } else {
+      if (deep) hipLaunchKernelGGL((conv_fwd_large_kernel<false, 64>), dim3(a.tiles), dim3(NT), 0, st, a);
+      else hipLaunchKernelGGL((conv_fwd_large_kernel<false, 32>), dim3(a.tiles), dim3(NT), 0, st, a);
+    }
     return hipGetLastError();
   }
   if (bwd)
