@@ -1322,9 +1322,8 @@ int fwd_large_bk(long Kg) {
 bool use_large_fwd(long M, long Nn, long Kg) {
   if (forced_tile() == 128) return false;
   if (forced_tile() == 256) return ((M + L_BM - 1) / L_BM) * ((Nn + BN - 1) / BN) > 0;
-  // a short reduction leaves the one-block-per-CU kernel's prologue and
-  // epilogue exposed; the two-blocks-per-CU kernel overlaps them
-  if ((Kg + 63) / 64 < 16) return false;
+  // a very short reduction leaves the prologue and epilogue exposed
+  if ((Kg + 63) / 64 < 4) return false;
   const long big = ((M + L_BM - 1) / L_BM) * ((Nn + BN - 1) / BN);
   const long small = ((M + BM - 1) / BM) * ((Nn + BN - 1) / BN);
   if (big < 256) return false;

@@ -349,7 +349,7 @@ def test_abi_errors_launch_nothing():
     assert e.value.status == -5
 
 
-# Shapes big enough (>= 256 tiles, >= 16 K-tiles) that the bf16 forward /
+# Shapes big enough (>= 256 tiles, a long reduction) that the bf16 forward /
 # backward-data passes take the 256 x 128 direct-to-LDS kernel (checked
 # through the kernel trace), with ragged M, N and K tails and stride 2;
 # compared element by element.
