@@ -171,7 +171,7 @@ def main():
     per_launch = dom["work"] / dom["launches"]
     if dom["unit"] == "flop":
         achieved = per_launch / (avg_ms / 1e3) / 1e12
-        peak = PEAK["bf16_tflops"] if "bf16" in dom_name else PEAK["f32_tflops"]
+        peak = mfma_peak  # the kernels compute in the workload's dtype
         roof = {"bound": "mfma", "unit": "TFLOP/s"}
     else:
         achieved = per_launch / (avg_ms / 1e3) / 1e9

@@ -146,25 +146,27 @@ __device__ __forceinline__ int xcd_remap(int b, int G) {
 // ------------------------------------------------------------ epilogue
 //
 // y[row][col] = act(acc + bias[col]), optionally zeroed where mask <= 0, for
-// one wave's (32 FM) x 64 quadrant of the output tile.  The accumulators hold
+// one wave's (32 FM) x (32 FN) quadrant of the output tile.  The accumulators hold
 // one column per lane (rows 8 (v / 4) + 4 (lane / 32) + v % 4 of each 32 x 32
 // block); they go through the wave's own LDS region as T so that the global
 // stores (and the mask loads) are 16-byte vectors of consecutive columns.
-// Needs (32 FM) * (64 * sizeof(T) + 16) bytes of LDS at `lds`; the caller
+// Needs (32 FM) * (32 FN * sizeof(T) + 16) bytes of LDS at `lds`; the caller
 // has finished with the operand tiles there (barrier).  `vec`: y, mask and Nn
 // allow 16-byte vectors; otherwise the staged values are stored one by one.
-template <typename T, int FM>
-__device__ __forceinline__ void store_quadrant(const f32x16 (&acc)[FM][2], char* lds, int lane, int row0, int col0,
+template <typename T, int FM, int FN>
+__device__ __forceinline__ void store_quadrant(const f32x16 (&acc)[FM][FN], char* lds, int lane, int row0, int col0,
                                                int M, int Nn, const float* bias, int relu, const void* mask,
                                                T* __restrict__ y, bool vec) {
   constexpr int ES = (int)sizeof(T);
-  constexpr int PIT = 64 * ES + 16;
+  constexpr int COLS = FN * 32;
+  constexpr int PIT = COLS * ES + 16;
   constexpr int VEC = 16 / ES;
-  constexpr int CPR = 64 / VEC;      // 16-byte chunks per row
-  constexpr int RPS = 64 / CPR;      // rows per pass of the wave
+  constexpr int CPR = COLS / VEC;    // 16-byte chunks per row
+  constexpr int RPS = 64 / CPR;      // rows per pass of the wave (lanes past RPS * CPR idle)
+  constexpr int PASSES = (FM * 32 + RPS - 1) / RPS;
   const int li = lane & 31, lh = lane >> 5;
 #pragma unroll
-  for (int bn = 0; bn < 2; ++bn) {
+  for (int bn = 0; bn < FN; ++bn) {
     const int c = bn * 32 + li;
     const float bv = (bias && col0 + c < Nn) ? bias[col0 + c] : 0.f;
 #pragma unroll
@@ -182,11 +184,13 @@ __device__ __forceinline__ void store_quadrant(const f32x16 (&acc)[FM][2], char*
   const int cc = lane % CPR, rr = lane / CPR;
   const int col = col0 + cc * VEC;
   const T* __restrict__ mk = (const T*)mask;
+  if (rr >= RPS) return;
   if (vec) {
 #pragma unroll
-    for (int pass = 0; pass < FM * 32 / RPS; ++pass) {
+    for (int pass = 0; pass < PASSES; ++pass) {
       const int r = pass * RPS + rr;
       const int row = row0 + r;
+      if (r >= FM * 32) break;
       union { uint4 u; T e[VEC]; } val, mv;
       val.u = *(const uint4*)(lds + r * PIT + cc * 16);
       if (row < M && col < Nn) {
@@ -202,9 +206,10 @@ __device__ __forceinline__ void store_quadrant(const f32x16 (&acc)[FM][2], char*
     }
   } else {
 #pragma unroll
-    for (int pass = 0; pass < FM * 32 / RPS; ++pass) {
+    for (int pass = 0; pass < PASSES; ++pass) {
       const int r = pass * RPS + rr;
       const int row = row0 + r;
+      if (r >= FM * 32) break;
       union { uint4 u; T e[VEC]; } val;
       val.u = *(const uint4*)(lds + r * PIT + cc * 16);
       if (row < M) {
@@ -430,7 +435,7 @@ __global__ __launch_bounds__(NT) void conv_fwd_kernel(FwdArgs a) {
   }
   __syncthreads();  // every wave is done with the operand tiles
   const bool vec = a.Nn % VEC == 0 && (((uintptr_t)a.y | (uintptr_t)a.mask) % 16) == 0;
-  store_quadrant<T, 2>(acc, smem + wave * 64 * (64 * (int)sizeof(T) + 16), lane, m0 + wm * 64, n0 + wn * 64, a.M,
+  store_quadrant<T, 2, 2>(acc, smem + wave * 64 * (64 * (int)sizeof(T) + 16), lane, m0 + wm * 64, n0 + wn * 64, a.M,
                        a.Nn, a.bias, a.relu, a.mask, (T*)a.y, vec);
 }
 
@@ -492,9 +497,14 @@ template <int N> __device__ __forceinline__ void wait_vmcnt() {
 
 __device__ __forceinline__ void block_barrier() { asm volatile("s_barrier" ::: "memory"); }
 
-template <bool BWD, int LBK>
+// WMW = 2: waves 2 (rows) x 2 (columns), each 128 x 64 of a 256 x 128 tile.
+// WMW = 4: waves stacked along the rows, each 64 x 96 of a 256 x 96 tile, for
+// layers with at most 96 output channels (the B tile still loads 128 rows,
+// the last 32 out of range: no memory traffic).
+template <bool BWD, int LBK, int WMW>
 __global__ __launch_bounds__(NT, LBK == 32 ? 2 : 1) void conv_fwd_large_kernel(FwdArgs a) {
   typedef LT<LBK> G;
+  constexpr int FM = WMW == 2 ? 4 : 2, FN = WMW == 2 ? 2 : 3;
   constexpr int LOADS = G::AI + G::BI;  // 16-byte loads per thread per K-tile
   __shared__ __attribute__((aligned(16))) char smem[G::SMEM];
 
@@ -584,36 +594,36 @@ __global__ __launch_bounds__(NT, LBK == 32 ? 2 : 1) void conv_fwd_large_kernel(F
     }
   };
 
-  f32x16 acc[4][2];
+  f32x16 acc[FM][FN];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < FM; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int j = 0; j < FN; ++j)
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = WMW == 2 ? wave >> 1 : wave, wn = WMW == 2 ? wave & 1 : 0;
   const int li = lane & 31, lh = lane >> 5;
   // chunk 2 kc + lh of row r sits in slot (2 kc + lh) ^ ((r / RPW) % SL); r % 16 = li % 16
   const int tsw = (lh ^ ((li / G::RPW) % G::SL)) << 4;
-  const int aoff = (wm * 128 + li) * G::RB, boff = G::ATILE + (wn * 64 + li) * G::RB;
+  const int aoff = (wm * FM * 32 + li) * G::RB, boff = G::ATILE + (wn * FN * 32 + li) * G::RB;
   struct Frags {
-    bf16x8 a[4], b[2];
+    bf16x8 a[FM], b[FN];
   };
   auto frags = [&](const char* S, int kc) {
     Frags f;
     const int co = (32 * kc) ^ tsw;
 #pragma unroll
-    for (int b = 0; b < 4; ++b) f.a[b] = *(const bf16x8*)(S + aoff + b * 32 * G::RB + co);
+    for (int b = 0; b < FM; ++b) f.a[b] = *(const bf16x8*)(S + aoff + b * 32 * G::RB + co);
 #pragma unroll
-    for (int b = 0; b < 2; ++b) f.b[b] = *(const bf16x8*)(S + boff + b * 32 * G::RB + co);
+    for (int b = 0; b < FN; ++b) f.b[b] = *(const bf16x8*)(S + boff + b * 32 * G::RB + co);
     return f;
   };
   auto mma = [&](const Frags& f) {
 #pragma unroll
-    for (int bm = 0; bm < 4; ++bm)
+    for (int bm = 0; bm < FM; ++bm)
 #pragma unroll
-      for (int bn = 0; bn < 2; ++bn)
+      for (int bn = 0; bn < FN; ++bn)
         acc[bm][bn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[bm], f.b[bn], acc[bm][bn], 0, 0, 0);
   };
 
@@ -651,14 +661,14 @@ __global__ __launch_bounds__(NT, LBK == 32 ? 2 : 1) void conv_fwd_large_kernel(F
   if (a.partial) {
     float* __restrict__ out = a.partial + (size_t)split * a.M * a.Nn;
 #pragma unroll
-    for (int bn = 0; bn < 2; ++bn) {
-      const int col = n0 + wn * 64 + bn * 32 + li;
+    for (int bn = 0; bn < FN; ++bn) {
+      const int col = n0 + wn * FN * 32 + bn * 32 + li;
       if (col >= a.Nn) continue;
 #pragma unroll
-      for (int bm = 0; bm < 4; ++bm)
+      for (int bm = 0; bm < FM; ++bm)
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
-          const int row = m0 + wm * 128 + bm * 32 + (v >> 2) * 8 + lh * 4 + (v & 3);
+          const int row = m0 + wm * FM * 32 + bm * 32 + (v >> 2) * 8 + lh * 4 + (v & 3);
           if (row < a.M) out[(size_t)row * a.Nn + col] = acc[bm][bn][v];
         }
     }
@@ -666,8 +676,8 @@ __global__ __launch_bounds__(NT, LBK == 32 ? 2 : 1) void conv_fwd_large_kernel(F
   }
   __syncthreads();  // every wave is done with the operand tiles
   const bool vec = a.Nn % 8 == 0 && (((uintptr_t)a.y | (uintptr_t)a.mask) % 16) == 0;
-  store_quadrant<bf16_t, 4>(acc, smem + wave * 128 * (64 * 2 + 16), lane, m0 + wm * 128, n0 + wn * 64, a.M, a.Nn,
-                            a.bias, a.relu, a.mask, (bf16_t*)a.y, vec);
+  store_quadrant<bf16_t, FM, FN>(acc, smem + wave * FM * 32 * (FN * 32 * 2 + 16), lane, m0 + wm * FM * 32,
+                                 n0 + wn * FN * 32, a.M, a.Nn, a.bias, a.relu, a.mask, (bf16_t*)a.y, vec);
 }
 
 // ----------------------------------------------------------- filter gradient
@@ -1289,8 +1299,14 @@ void launch_fwd_instance(const FwdArgs& a, dim3 grid, double flops, hipStream_t 
   hipLaunchKernelGGL((conv_fwd_kernel<T, AM, BMD, BWD>), grid, dim3(NT), 0, st, a);
 }
 
-template <bool BWD> const char* fwd_large_name() {
-  return BWD ? "conv_fwd_large_kernel<1>" : "conv_fwd_large_kernel<0>";
+// "conv_fwd_large_kernel<bwd,taps per K-tile,waves along the rows>"
+const char* fwd_large_name(bool bwd, bool deep, bool narrow) {
+  static const char* names[2][2][2] = {
+      {{"conv_fwd_large_kernel<0,32,2>", "conv_fwd_large_kernel<0,32,4>"},
+       {"conv_fwd_large_kernel<0,64,2>", "conv_fwd_large_kernel<0,64,4>"}},
+      {{"conv_fwd_large_kernel<1,32,2>", "conv_fwd_large_kernel<1,32,4>"},
+       {"conv_fwd_large_kernel<1,64,2>", "conv_fwd_large_kernel<1,64,4>"}}};
+  return names[bwd][deep][narrow];
 }
 
 // Workgroups of the 256 x 128 kernel per full round of the chip (one per CU)
@@ -1401,15 +1417,18 @@ hipError_t conv_fwd_dispatch(const ConvShape& s, const void* x, const void* w, c
     a.tiles = ((a.M + L_BM - 1) / L_BM) * a.tiles_n;
     a.partial = nullptr;
     const bool deep = fwd_large_bk(a.Kg) == 64;
+    const bool narrow = a.Nn <= 96;  // one 96-column tile
     a.kt_per_split = (a.Kg + (deep ? 64 : 32) - 1) / (deep ? 64 : 32);  // one split: every K-tile of this depth
-    TraceScope ts(bwd ? fwd_large_name<true>() : fwd_large_name<false>(), st, flops, WORK_FLOP);
+    TraceScope ts(fwd_large_name(bwd, deep, narrow), st, flops, WORK_FLOP);
+#define LAUNCH_LARGE(B, K, W) hipLaunchKernelGGL((conv_fwd_large_kernel<B, K, W>), dim3(a.tiles), dim3(NT), 0, st, a)
     if (bwd) {
-      if (deep) hipLaunchKernelGGL((conv_fwd_large_kernel<true, 64>), dim3(a.tiles), dim3(NT), 0, st, a);
-      else hipLaunchKernelGGL((conv_fwd_large_kernel<true, 32>), dim3(a.tiles), dim3(NT), 0, st, a);
+      if (narrow) { if (deep) LAUNCH_LARGE(true, 64, 4); else LAUNCH_LARGE(true, 32, 4); }
+      else { if (deep) LAUNCH_LARGE(true, 64, 2); else LAUNCH_LARGE(true, 32, 2); }
     } else {
-      if (deep) hipLaunchKernelGGL((conv_fwd_large_kernel<false, 64>), dim3(a.tiles), dim3(NT), 0, st, a);
-      else hipLaunchKernelGGL((conv_fwd_large_kernel<false, 32>), dim3(a.tiles), dim3(NT), 0, st, a);
+      if (narrow) { if (deep) LAUNCH_LARGE(false, 64, 4); else LAUNCH_LARGE(false, 32, 4); }
+      else { if (deep) LAUNCH_LARGE(false, 64, 2); else LAUNCH_LARGE(false, 32, 2); }
     }
+#undef LAUNCH_LARGE
     return hipGetLastError();
   }
   if (bwd)

@@ -260,8 +260,8 @@ def test_conv_bwd_data_relu_folded(case, layout, dt):
     assert rel_l2(got, ref) <= TOL[dt], case
 
 
-def test_conv_bwd_data_relu_folded_large_tile():
-    case = (15, 200, 47, 47, 128, 3, 3, 1, 1)
+@pytest.mark.parametrize("case", [(15, 200, 47, 47, 128, 3, 3, 1, 1), (30, 96, 47, 47, 40, 3, 3, 1, 1)])
+def test_conv_bwd_data_relu_folded_large_tile(case):
     N, C, H, W, K, R, S, pad, stride = case
     x, w, b, dy = _conv_inputs(case, "bf16", 91)
     xr = np.maximum(x, 0.0)
@@ -357,6 +357,11 @@ LARGE_CASES = [
     ("fwd", (10, 128, 47, 47, 300, 3, 3, 1, 1)),
     ("bwd_data", (15, 200, 47, 47, 128, 3, 3, 1, 1)),
     ("fwd", (40, 128, 59, 59, 136, 3, 3, 1, 2)),
+    # at most 96 output columns: the 256 x 96 wave layout
+    ("fwd", (30, 64, 47, 47, 96, 3, 3, 1, 1)),
+    ("fwd", (30, 32, 47, 47, 90, 3, 3, 1, 1)),   # ragged columns, element-wise epilogue
+    ("fwd", (30, 32, 47, 47, 40, 3, 3, 1, 1)),
+    ("bwd_data", (30, 96, 47, 47, 40, 3, 3, 1, 1)),
 ]
 
 
@@ -373,7 +378,10 @@ def test_conv_large_tile_path(op, case):
     torch.cuda.synchronize()
     names = [r[0] for r in singa.trace_records()]
     singa.trace_enable(False)
-    assert any(n.startswith("conv_fwd_large_kernel") for n in names), names
+    large = [n for n in names if n.startswith("conv_fwd_large_kernel")]
+    assert large, names
+    narrow = (K if op == "fwd" else C) <= 96  # GEMM columns: filters, or input channels for the data gradient
+    assert all(n.endswith(",4>") == narrow for n in large), large
     if op == "fwd":
         ref = oracle.relu_fwd(oracle.conv_fwd(x, w, b, pad=pad, stride=stride))
     else:
