@@ -296,6 +296,33 @@ __global__ __launch_bounds__(256) void pool_bwd_k3s2_kernel(PoolGeom g, FastDiv 
     const int wb = t1 - t2 * WB;
     const int n = (int)fdiv((uint32_t)t2, dHB);
     const int hb = t2 - n * HB;
+    // the four windows' vectors, all loaded before any is used; a window
+    // outside the output gets arg-max cells 0xff, which match no input
+    union U { uint4 u; T e[VEC]; };
+    U v[2][2], ym[2][2];
+    uint8_t am[2][2][VEC];
+#pragma unroll
+    for (int pi = 0; pi < 2; ++pi)
+#pragma unroll
+      for (int qi = 0; qi < 2; ++qi) {
+        const int p = hb - 1 + pi, q = wb - 1 + qi;
+        const bool ok = p >= 0 && p < g.P && q >= 0 && q < g.Q;
+        const int o = ok ? ((n * g.P + p) * g.Q + q) * g.C + cv * VEC : 0;
+        v[pi][qi].u = ok ? *(const uint4*)(dy + o) : make_uint4(0u, 0u, 0u, 0u);
+        if constexpr (MASK) ym[pi][qi].u = ok ? *(const uint4*)(ymask + o) : make_uint4(0u, 0u, 0u, 0u);
+        if constexpr (VEC == 8) {
+          const uint2 a = ok ? *(const uint2*)(argmax + o) : make_uint2(~0u, ~0u);
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            am[pi][qi][j] = (uint8_t)(a.x >> (8 * j));
+            am[pi][qi][4 + j] = (uint8_t)(a.y >> (8 * j));
+          }
+        } else {
+          const uint32_t a = ok ? *(const uint32_t*)(argmax + o) : ~0u;
+#pragma unroll
+          for (int j = 0; j < 4; ++j) am[pi][qi][j] = (uint8_t)(a >> (8 * j));
+        }
+      }
     float acc[2][2][VEC];
 #pragma unroll
     for (int a = 0; a < 2; ++a)
@@ -305,29 +332,8 @@ __global__ __launch_bounds__(256) void pool_bwd_k3s2_kernel(PoolGeom g, FastDiv 
         for (int j = 0; j < VEC; ++j) acc[a][b][j] = 0.f;
 #pragma unroll
     for (int pi = 0; pi < 2; ++pi) {
-      const int p = hb - 1 + pi;
-      if (p < 0 || p >= g.P) continue;
 #pragma unroll
       for (int qi = 0; qi < 2; ++qi) {
-        const int q = wb - 1 + qi;
-        if (q < 0 || q >= g.Q) continue;
-        const int o = ((n * g.P + p) * g.Q + q) * g.C + cv * VEC;
-        union { uint4 u; T e[VEC]; } v, ym;
-        v.u = *(const uint4*)(dy + o);
-        if constexpr (MASK) ym.u = *(const uint4*)(ymask + o);
-        uint8_t am[VEC];
-        if constexpr (VEC == 8) {
-          const uint2 a = *(const uint2*)(argmax + o);
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            am[j] = (uint8_t)(a.x >> (8 * j));
-            am[4 + j] = (uint8_t)(a.y >> (8 * j));
-          }
-        } else {
-          const uint32_t a = *(const uint32_t*)(argmax + o);
-#pragma unroll
-          for (int j = 0; j < 4; ++j) am[j] = (uint8_t)(a >> (8 * j));
-        }
         // input (2 hb + dh, 2 wb + dw) sits at cell (2 hb + dh - 2 p) * 3 + (2 wb + dw - 2 q) of this window;
         // window p = hb - 1 covers only dh = 0 (cell row 2), p = hb covers dh = 0, 1 (rows 0, 1)
 #pragma unroll
@@ -339,9 +345,9 @@ __global__ __launch_bounds__(256) void pool_bwd_k3s2_kernel(PoolGeom g, FastDiv 
             const int cell = (2 * (1 - pi) + dh) * 3 + (2 * (1 - qi) + dw);
 #pragma unroll
             for (int j = 0; j < VEC; ++j) {
-              bool take = am[j] == cell;
-              if constexpr (MASK) take = take && ld_f<T>(&ym.e[j]) > 0.f;
-              if (take) acc[dh][dw][j] += ld_f<T>(&v.e[j]);
+              bool take = am[pi][qi][j] == cell;
+              if constexpr (MASK) take = take && ld_f<T>(&ym[pi][qi].e[j]) > 0.f;
+              if (take) acc[dh][dw][j] += ld_f<T>(&v[pi][qi].e[j]);
             }
           }
         }

@@ -179,6 +179,9 @@ POOL_CASES = [
     (2, 7, 9, 10, "max", 3, 2, 1),     # padded ceil mode
     (2, 7, 9, 10, "avg", 3, 2, 1),
     (1, 3, 7, 7, "avg", 2, 2, 0),
+    (2, 16, 9, 10, "max", 3, 2, 1),    # padded, vector channels
+    (2, 16, 9, 10, "avg", 3, 2, 1),
+    (2, 8, 6, 6, "max", 3, 1, 1),      # overlapping stride-1 windows
 ]
 
 
