@@ -63,7 +63,12 @@ extern "C" {
 typedef enum { SINGA_F32 = 0, SINGA_BF16 = 1 } singa_dtype;
 typedef enum { SINGA_NCHW = 0, SINGA_NHWC = 1 } singa_layout;
 typedef enum { SINGA_POOL_MAX = 0, SINGA_POOL_AVG = 1 } singa_pool_mode;
-typedef enum { SINGA_OP_FWD = 0, SINGA_OP_BWD_DATA = 1, SINGA_OP_BWD_FILTER = 2 } singa_conv_op;
+typedef enum {
+  SINGA_OP_FWD = 0,
+  SINGA_OP_BWD_DATA = 1,
+  SINGA_OP_BWD_FILTER = 2,
+  SINGA_OP_BWD_FILTER_SGD = 3
+} singa_conv_op;
 
 /* Activation extents (batch, channels, height, width), whatever the layout. */
 typedef struct { int n, c, h, w; } singa_shape4;
@@ -152,6 +157,39 @@ int singa_conv_bwd_filter(singa_dtype dtype, singa_layout layout,
                           const singa_filter4* w, const singa_conv_desc* d,
                           const void* dy_ptr, float* dw, float* db, int accumulate,
                           void* ws, size_t ws_bytes, singa_stream stream);
+
+/* Convolution ComputeGradient for the Params followed at once by the
+ * Updater's step on them (Alg. 1 calls Update on a layer's Params right after
+ * its ComputeGradient; the Updater of Sec. 4.1.4, as in
+ * singa_sgd_momentum_update):
+ *   g = dW (and db) exactly as singa_conv_bwd_filter computes them;
+ *   v = momentum * v + lr * (g + weight_decay * w);  w = w - v;
+ *   w_bf16 = bf16(w) (round to nearest even) when w_bf16 != NULL
+ * for the filter (w_master, w_mom: fp32, w_bf16: bf16 bits, shape *w in the
+ * filter layout; updated in place) and, when b_master != NULL, for the bias
+ * (b_master, b_mom, b_bf16: w->k values).  Every element ends up exactly as
+ * singa_sgd_momentum_update leaves it given that gradient.
+ *   dw, db : NULL, or fp32 arrays (filter layout / w->k) that also receive
+ *            the gradient.
+ * The update arrays need 16-byte alignment.  The call reads the filter only
+ * through w_master, so a backward-data pass that needs the layer's current
+ * bf16 filter must be enqueued before it.
+ * singa_conv_workspace_bytes(SINGA_OP_BWD_FILTER_SGD, ...) is 0 exactly when
+ * the update is fused into the gradient kernel (bf16, NHWC, K and C multiples
+ * of 8, no rewrite of the input, and N*P*Q short enough for a single pass
+ * over the reduction, as for fully connected layers): each gradient element
+ * is applied where it is complete, without a round trip through memory, and
+ * x_ptr and dy_ptr must be 16-byte aligned (SINGA_ERR_ALIGN otherwise).  In
+ * every other case the gradient is formed in dw/db or in the workspace and
+ * the update follows. */
+int singa_conv_bwd_filter_sgd(singa_dtype dtype, singa_layout layout,
+                              const singa_shape4* x, const void* x_ptr,
+                              const singa_filter4* w, const singa_conv_desc* d,
+                              const void* dy_ptr, float* dw, float* db,
+                              float* w_master, float* w_mom, uint16_t* w_bf16,
+                              float* b_master, float* b_mom, uint16_t* b_bf16,
+                              float lr, float momentum, float weight_decay,
+                              void* ws, size_t ws_bytes, singa_stream stream);
 
 /* ------------------------------------------------------------------ pooling */
 

@@ -240,6 +240,37 @@ size_t carve_bwd_filter(const ConvShape& s, int dt, int layout, bool bias, void*
   return c.used;
 }
 
+// Filter gradient with the update: nothing when the update is fused into the
+// gradient kernel; otherwise fp32 staging for the gradient (used when the
+// caller passes no dw / db) and the filter gradient's own workspace.
+struct BwdFilterSgdWs {
+  bool fused;
+  float* g;
+  float* gb;
+  void* inner;
+  size_t inner_bytes;
+};
+
+bool bwd_filter_sgd_fused(const ConvShape& s, int dt, int layout, bool bias) {
+  ConvShape g;
+  return layout == SINGA_NHWC && input_rewrite(s, dt, &g) == RW_NONE && wgrad_update_fusable(s, dt, bias);
+}
+
+size_t carve_bwd_filter_sgd(const ConvShape& s, int dt, int layout, bool bias, void* ws, BwdFilterSgdWs* o) {
+  Carve c(ws);
+  o->fused = bwd_filter_sgd_fused(s, dt, layout, bias);
+  o->g = o->gb = nullptr;
+  o->inner = nullptr;
+  o->inner_bytes = 0;
+  if (o->fused) return 0;
+  o->g = (float*)c.take((size_t)s.K * s.R * s.S * s.C * sizeof(float));
+  if (bias) o->gb = (float*)c.take((size_t)s.K * sizeof(float));
+  BwdFilterWs f;
+  o->inner_bytes = carve_bwd_filter(s, dt, layout, bias, nullptr, &f);
+  o->inner = o->inner_bytes ? c.take(o->inner_bytes) : nullptr;
+  return c.used;
+}
+
 // Filter KCRS (NCHW callers) -> KRSC.
 hipError_t kcrs_to_krsc(int dt, const ConvShape& s, const void* in, void* out, hipStream_t st) {
   const int RS = s.R * s.S;
@@ -309,6 +340,11 @@ int singa_conv_workspace_bytes(int op, singa_dtype dtype, singa_layout layout, c
     case SINGA_OP_FWD: { FwdWs o; *bytes = carve_fwd(s, dtype, layout, nullptr, &o); break; }
     case SINGA_OP_BWD_DATA: { BwdDataWs o; *bytes = carve_bwd_data(s, dtype, layout, nullptr, &o); break; }
     case SINGA_OP_BWD_FILTER: { BwdFilterWs o; *bytes = carve_bwd_filter(s, dtype, layout, true, nullptr, &o); break; }
+    case SINGA_OP_BWD_FILTER_SGD: {
+      BwdFilterSgdWs o;
+      *bytes = carve_bwd_filter_sgd(s, dtype, layout, true, nullptr, &o);
+      break;
+    }
     default: return SINGA_ERR_UNSUPPORTED;
   }
   return SINGA_OK;
@@ -448,6 +484,42 @@ int singa_conv_bwd_filter(singa_dtype dtype, singa_layout layout, const singa_sh
     e = launch_unpad_channels_f32(o.dwp, krsc, (long)s.K * s.R * s.S, g.C, s.C, acc, st);
   if (e == hipSuccess && rw == RW_S2D) e = launch_s2d_to_filter_f32(s, g, o.dwp, krsc, acc, st);
   if (e == hipSuccess && layout == SINGA_NCHW) e = launch_krsc_to_kcrs_f32(o.dw, dw, s.K, s.C, s.R, s.S, accumulate, st);
+  return hip_status(e);
+}
+
+int singa_conv_bwd_filter_sgd(singa_dtype dtype, singa_layout layout, const singa_shape4* x, const void* x_ptr,
+                              const singa_filter4* w, const singa_conv_desc* d, const void* dy_ptr, float* dw,
+                              float* db, float* w_master, float* w_mom, uint16_t* w_bf16, float* b_master,
+                              float* b_mom, uint16_t* b_bf16, float lr, float momentum, float weight_decay,
+                              void* ws, size_t ws_bytes, singa_stream stream) {
+  if (!dtype_ok(dtype) || !layout_ok(layout)) return SINGA_ERR_UNSUPPORTED;
+  ConvShape s;
+  int rc = conv_geometry(x, w, d, &s);
+  if (rc != SINGA_OK) return rc;
+  if (!x_ptr || !dy_ptr || !w_master || !w_mom || (b_master == nullptr) != (b_mom == nullptr)) return SINGA_ERR_NULL;
+  if (b_bf16 && !b_master) return SINGA_ERR_NULL;
+  const size_t es = dt_size(dtype);
+  if (!aligned_to(x_ptr, es) || !aligned_to(dy_ptr, es) || !aligned_to(dw, 4) || !aligned_to(db, 4) ||
+      !aligned_to(w_master, 16) || !aligned_to(w_mom, 16) || !aligned_to(w_bf16, 16) || !aligned_to(b_master, 16) ||
+      !aligned_to(b_mom, 16) || !aligned_to(b_bf16, 16) || !aligned_to(ws, 16))
+    return SINGA_ERR_ALIGN;
+  const bool bias = b_master != nullptr;
+  BwdFilterSgdWs o;
+  const size_t need = carve_bwd_filter_sgd(s, dtype, layout, bias, nullptr, &o);
+  if (need > 0 && (!ws || ws_bytes < need)) return SINGA_ERR_WORKSPACE;
+  carve_bwd_filter_sgd(s, dtype, layout, bias, ws, &o);
+  hipStream_t st = (hipStream_t)stream;
+  if (o.fused) {
+    if (!aligned_to(x_ptr, 16) || !aligned_to(dy_ptr, 16)) return SINGA_ERR_ALIGN;
+    const SgdTargets u{w_master, w_mom, w_bf16, b_master, b_mom, b_bf16, lr, momentum, weight_decay};
+    return hip_status(launch_conv_wgrad_sgd(dtype, s, x_ptr, dy_ptr, dw, db, u, st));
+  }
+  float* g = dw ? dw : o.g;
+  float* gb = bias ? (db ? db : o.gb) : nullptr;
+  rc = singa_conv_bwd_filter(dtype, layout, x, x_ptr, w, d, dy_ptr, g, gb, 0, o.inner, o.inner_bytes, stream);
+  if (rc != SINGA_OK) return rc;
+  hipError_t e = launch_sgd((size_t)s.K * s.R * s.S * s.C, w_master, g, w_mom, w_bf16, lr, momentum, weight_decay, st);
+  if (e == hipSuccess && bias) e = launch_sgd((size_t)s.K, b_master, gb, b_mom, b_bf16, lr, momentum, weight_decay, st);
   return hip_status(e);
 }
 

@@ -24,6 +24,16 @@ __device__ __forceinline__ float bf16_to_f32(bf16_t b) {
   return __uint_as_float(((uint32_t)b) << 16);
 }
 
+// One step of SGD with momentum and weight decay on one parameter (the
+// Updater of Sec. 4.1.4): v <- momentum v + lr (g + wd w), w <- w - v.  The
+// multiply-adds are explicit so that every kernel applying the step (the
+// flat update, the filter-gradient kernel with the update fused) rounds
+// identically.
+__device__ __forceinline__ void sgd_step(float& w, float& v, float g, float lr, float mom, float wd) {
+  v = fmaf(mom, v, lr * fmaf(wd, w, g));
+  w = w - v;
+}
+
 // Division by a divisor fixed at launch time (Granlund & Montgomery, "Division
 // by invariant integers using multiplication", 1994): for 0 <= n < 2^31,
 // n / d = (umulhi(n, mul) + n) >> shift with shift = ceil(log2 d) and

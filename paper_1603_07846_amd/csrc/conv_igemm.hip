@@ -724,6 +724,8 @@ struct WgradArgs {
   FastDiv dN, dPQ, dQ, dC, dS;
   int tiles, tiles_n, kt_per_split, nkt;
   int direct, acc_dw, acc_db;
+  int update;    // direct only: each element is applied to `u` (out / db: NULL, or where g is also stored)
+  SgdTargets u;
 };
 
 __device__ __forceinline__ v4i16 lds_tr16(const char* p) {
@@ -1006,7 +1008,7 @@ constexpr int WL_AT = WL_BK * WL_ARB, WL_BT = WL_BK * WL_BRB;
 constexpr int WL_STAGE = WL_AT + WL_BT;
 constexpr int WL_SMEM = 3 * WL_STAGE;  // 72 KB: two workgroups per CU
 
-template <bool NFAST>
+template <bool NFAST, bool UPD>
 __global__ __launch_bounds__(NT, 2) void conv_wgrad_large_kernel(WgradArgs a) {
   constexpr uint32_t ES = 2;
   constexpr int RPW = WL_BK / 4;    // K-tile rows loaded by each wave (of A and of B)
@@ -1196,6 +1198,46 @@ __global__ __launch_bounds__(NT, 2) void conv_wgrad_large_kernel(WgradArgs a) {
         for (int v = 0; v < 16; ++v) {
           const int row = m0 + wm * 64 + bm * 32 + (v >> 2) * 8 + lh * 4 + (v & 3);
           if (row < a.M) out[(size_t)row * a.ldp + col] = acc[bm][bn][v];
+        }
+    }
+    return;
+  }
+  if constexpr (UPD) {
+    // Update fused: each lane owns one column (filter tap, or the bias) of
+    // 32 rows per block; the rows' w and v are loaded before any is used.
+#pragma unroll
+    for (int bn = 0; bn < 4; ++bn) {
+      const int col = n0 + wn * 128 + bn * 32 + li;
+      if (col >= a.Ng) continue;
+      const bool is_db = col == a.Nn;
+      float* __restrict__ W = is_db ? a.u.b : a.u.w + col;
+      float* __restrict__ V = is_db ? a.u.vb : a.u.v + col;
+      uint16_t* __restrict__ WB = is_db ? a.u.bb : (a.u.wb ? a.u.wb + col : nullptr);
+      float* __restrict__ G = is_db ? a.db : (a.out ? a.out + col : nullptr);
+      const size_t stride = is_db ? 1 : (size_t)a.Nn;
+      float wv[2][16], vv[2][16];
+#pragma unroll
+      for (int bm = 0; bm < 2; ++bm)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int row = m0 + wm * 64 + bm * 32 + (v >> 2) * 8 + lh * 4 + (v & 3);
+          const size_t o = (size_t)(row < a.M ? row : 0) * stride;
+          wv[bm][v] = W[o];
+          vv[bm][v] = V[o];
+        }
+#pragma unroll
+      for (int bm = 0; bm < 2; ++bm)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int row = m0 + wm * 64 + bm * 32 + (v >> 2) * 8 + lh * 4 + (v & 3);
+          if (row >= a.M) continue;
+          const size_t o = (size_t)row * stride;
+          const float g = acc[bm][bn][v];
+          sgd_step(wv[bm][v], vv[bm][v], g, a.u.lr, a.u.mom, a.u.wd);
+          W[o] = wv[bm][v];
+          V[o] = vv[bm][v];
+          if (WB) WB[o] = f32_to_bf16(wv[bm][v]);
+          if (G) G[o] = g;
         }
     }
     return;
@@ -1575,7 +1617,7 @@ int wgrad_splits_for(const ConvShape& s, int dt, bool bias, bool large) {
 
 template <typename T>
 hipError_t conv_wgrad_dispatch(const ConvShape& s, const void* x, const void* dy, float* partial, float* dw,
-                               float* db, int acc_dw, int acc_db, hipStream_t st) {
+                               float* db, int acc_dw, int acc_db, const SgdTargets* upd, hipStream_t st) {
   constexpr int VEC = 16 / (int)sizeof(T);
   constexpr int DT = sizeof(T) == 2 ? BF16 : F32;
   WgradArgs a;
@@ -1584,8 +1626,6 @@ hipError_t conv_wgrad_dispatch(const ConvShape& s, const void* x, const void* dy
   a.dy_bytes = (uint32_t)((size_t)s.N * s.P * s.Q * s.K * sizeof(T));
   a.M = s.K;
   a.Nn = s.R * s.S * s.C;
-  a.Ng = a.Nn + (db ? 1 : 0);
-  a.ldp = (a.Ng + 63) / 64 * 64;
   a.T = s.N * s.P * s.Q;
   a.N = s.N; a.H = s.H; a.W = s.W; a.C = s.C; a.S = s.S; a.P = s.P; a.Q = s.Q;
   a.sh = s.sh; a.sw = s.sw; a.ph = s.ph; a.pw = s.pw;
@@ -1598,25 +1638,37 @@ hipError_t conv_wgrad_dispatch(const ConvShape& s, const void* x, const void* dy
   const int vb = load_mode<T>(s.C, x);
   const bool large = wgrad_large_shape(s, DT) && va && vb == VEC16;
   const int bm = large ? WL_BM : BM, bn = large ? WL_BN : BN, bk = large ? WL_BK : WG<T>::BK;
+  a.nkt = (a.T + bk - 1) / bk;
+  const bool bias = upd ? upd->b != nullptr : db != nullptr;
+  a.Ng = a.Nn + (bias ? 1 : 0);
+  a.ldp = (a.Ng + 63) / 64 * 64;
   a.tiles_n = (a.Ng + bn - 1) / bn;
   a.tiles = ((a.M + bm - 1) / bm) * a.tiles_n;
-  a.nkt = (a.T + bk - 1) / bk;
-  const int splits = wgrad_splits_for(s, DT, db != nullptr, large);
+  const int splits = wgrad_splits_for(s, DT, bias, large);
+  if (upd && !(large && splits == 1 && wgrad_update_fusable(s, DT, bias))) return hipErrorNotSupported;
   a.kt_per_split = (a.nkt + splits - 1) / splits;
   a.direct = splits == 1;
-  a.acc_dw = acc_dw;
-  a.acc_db = acc_db;
+  a.acc_dw = upd ? 0 : acc_dw;
+  a.acc_db = upd ? 0 : acc_db;
   a.out = a.direct ? dw : partial;
   a.db = db;
+  a.update = upd != nullptr;
+  if (upd) a.u = *upd;
   dim3 grid(a.tiles * splits);
   const double flops = 2.0 * a.M * (double)a.Nn * (double)a.T;
   const bool nf = use_image_fastest(s, bk);
   if (large) {
-    TraceScope ts(nf ? "conv_wgrad_large_kernel<1>" : "conv_wgrad_large_kernel<0>", st, flops, WORK_FLOP);
-    if (nf)
-      hipLaunchKernelGGL(conv_wgrad_large_kernel<true>, grid, dim3(NT), 0, st, a);
-    else
-      hipLaunchKernelGGL(conv_wgrad_large_kernel<false>, grid, dim3(NT), 0, st, a);
+    // "conv_wgrad_large_kernel<image fastest,update fused>"
+    static const char* names[2][2] = {{"conv_wgrad_large_kernel<0,0>", "conv_wgrad_large_kernel<0,1>"},
+                                      {"conv_wgrad_large_kernel<1,0>", "conv_wgrad_large_kernel<1,1>"}};
+    TraceScope ts(names[nf][a.update], st, flops, WORK_FLOP);
+    if (a.update) {
+      if (nf) hipLaunchKernelGGL((conv_wgrad_large_kernel<true, true>), grid, dim3(NT), 0, st, a);
+      else hipLaunchKernelGGL((conv_wgrad_large_kernel<false, true>), grid, dim3(NT), 0, st, a);
+    } else {
+      if (nf) hipLaunchKernelGGL((conv_wgrad_large_kernel<true, false>), grid, dim3(NT), 0, st, a);
+      else hipLaunchKernelGGL((conv_wgrad_large_kernel<false, false>), grid, dim3(NT), 0, st, a);
+    }
   } else if (nf) {
     launch_wgrad_variant<T, true>(va, vb, a, grid, flops, st);
   } else {
@@ -1657,8 +1709,19 @@ size_t wgrad_partial_bytes(const ConvShape& s, int dt, bool bias) {
 
 hipError_t launch_conv_wgrad(int dt, const ConvShape& s, const void* x, const void* dy, float* partial, float* dw,
                              float* db, int acc_dw, int acc_db, hipStream_t st) {
-  if (dt == BF16) return conv_wgrad_dispatch<bf16_t>(s, x, dy, partial, dw, db, acc_dw, acc_db, st);
-  return conv_wgrad_dispatch<float>(s, x, dy, partial, dw, db, acc_dw, acc_db, st);
+  if (dt == BF16) return conv_wgrad_dispatch<bf16_t>(s, x, dy, partial, dw, db, acc_dw, acc_db, nullptr, st);
+  return conv_wgrad_dispatch<float>(s, x, dy, partial, dw, db, acc_dw, acc_db, nullptr, st);
+}
+
+bool wgrad_update_fusable(const ConvShape& s, int dt, bool bias) {
+  return wgrad_large_shape(s, dt) && wgrad_splits_for(s, dt, bias, true) == 1;
+}
+
+hipError_t launch_conv_wgrad_sgd(int dt, const ConvShape& s, const void* x, const void* dy, float* dw, float* db,
+                                 const SgdTargets& u, hipStream_t st) {
+  if (dt != BF16 || !wgrad_update_fusable(s, dt, u.b != nullptr) || (uintptr_t)x % 16 || (uintptr_t)dy % 16)
+    return hipErrorNotSupported;
+  return conv_wgrad_dispatch<bf16_t>(s, x, dy, nullptr, dw, u.b ? db : nullptr, 0, 0, &u, st);
 }
 
 }  // namespace singa

@@ -475,14 +475,10 @@ __global__ __launch_bounds__(256) void softmax_ce_mean_kernel(int B, float* __re
 // best of the variants tried, ~5.5 TB/s; streaming loads / stores were
 // slower).  n % 8 tail elements are handled one by one by the first threads.
 __device__ __forceinline__ void sgd4(float4& wv, float4 gv, float4& vv, float lr, float mom, float wd) {
-  vv.x = mom * vv.x + lr * (gv.x + wd * wv.x);
-  vv.y = mom * vv.y + lr * (gv.y + wd * wv.y);
-  vv.z = mom * vv.z + lr * (gv.z + wd * wv.z);
-  vv.w = mom * vv.w + lr * (gv.w + wd * wv.w);
-  wv.x -= vv.x;
-  wv.y -= vv.y;
-  wv.z -= vv.z;
-  wv.w -= vv.w;
+  sgd_step(wv.x, vv.x, gv.x, lr, mom, wd);
+  sgd_step(wv.y, vv.y, gv.y, lr, mom, wd);
+  sgd_step(wv.z, vv.z, gv.z, lr, mom, wd);
+  sgd_step(wv.w, vv.w, gv.w, lr, mom, wd);
 }
 
 __global__ __launch_bounds__(256) void sgd_kernel(size_t n, float* __restrict__ w, const float* __restrict__ g,
@@ -517,8 +513,8 @@ __global__ __launch_bounds__(256) void sgd_kernel(size_t n, float* __restrict__ 
   }
   const size_t t = n8 * 8 + (size_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (t < n) {
-    const float vt = mom * v[t] + lr * (g[t] + wd * w[t]);
-    const float wt = w[t] - vt;
+    float wt = w[t], vt = v[t];
+    sgd_step(wt, vt, g[t], lr, mom, wd);
     v[t] = vt;
     w[t] = wt;
     if (wb) wb[t] = f32_to_bf16(wt);

@@ -60,6 +60,32 @@ size_t wgrad_partial_bytes(const ConvShape& s, int dt, bool bias);
 hipError_t launch_conv_wgrad(int dt, const ConvShape& s, const void* x, const void* dy, float* partial, float* dw,
                              float* db, int acc_dw, int acc_db, hipStream_t st);
 
+// Parameters the filter-gradient kernel updates in place once a gradient
+// element is complete (SGD with momentum, one step per element): the fp32
+// master filter w (K, R, S, C), its momentum v and its bf16 compute copy wb
+// (NULL: none); the same for the bias (b NULL: no bias).
+struct SgdTargets {
+  float* w;
+  float* v;
+  uint16_t* wb;
+  float* b;
+  float* vb;
+  uint16_t* bb;
+  float lr, mom, wd;
+};
+
+// True when the filter gradient of s runs as one pass of the 128 x 256 kernel
+// writing each element once (bf16, K % 8 == 0, C % 8 == 0, one split), the
+// case in which the update is fused into it.
+bool wgrad_update_fusable(const ConvShape& s, int dt, bool bias);
+
+// The filter gradient with the update fused: every complete element g of dw
+// (and db) is applied to the targets and, when dw (db) is not NULL, also
+// stored there.  x and dy must be 16-byte aligned and wgrad_update_fusable()
+// true; otherwise returns hipErrorNotSupported and launches nothing.
+hipError_t launch_conv_wgrad_sgd(int dt, const ConvShape& s, const void* x, const void* dy, float* dw, float* db,
+                                 const SgdTargets& u, hipStream_t st);
+
 // Batched 2-D transpose: for b in [0, batch): out(b)[c][r] = in(b)[r][c] with
 // in(b) = in + in_base(b), out(b) = out + out_base(b), where
 // in_base(b) = b * in_bstride and out_base(b) = (flip ? batch-1-b : b) * out_bstride.

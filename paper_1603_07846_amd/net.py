@@ -19,10 +19,16 @@ Data layout in HBM (chosen for the gfx950 kernels, not the paper's CPUs):
 Every buffer is allocated once, when the net is built; a step allocates
 nothing.
 
-Alg. 1 calls Update(layer.params()) inside the backward loop.  The fresh
-values only reach the layers at the next iteration's Collect, so on one GPU a
-single fused update over the flat buffer after the backward loop is the same
-computation.
+Alg. 1 calls Update(layer.params()) inside the backward loop, right after the
+layer's ComputeGradient.  Layers whose filter gradient is one pass of the
+large gradient kernel (the fully connected layers, which hold almost all of
+the parameters) do exactly that: the update is fused into the gradient
+kernel, so their gradient never goes through memory, and their backward-data
+runs first because it still needs the old bf16 weights.  The other layers'
+gradients go to the flat gradient buffer and one fused update over their
+(contiguous) part of the flat buffers follows the backward loop; the fresh
+values only reach any layer at the next iteration's forward, so this is the
+same computation, element for element.
 """
 from __future__ import annotations
 
@@ -72,6 +78,9 @@ class ConvLayer(Layer):
         self.relu = False  # set when a ReLU layer directly follows and is fused
         self.relu_src = None  # the ReLU layer feeding this one, whose backward bwd-data folds in
         dev, dt = net.device, net.dtype
+        # update fused into the filter-gradient kernel (no workspace needed exactly then)
+        self.fused_update = bool(net.fuse_update and net.wl.update and singa.conv_workspace_bytes(
+            singa.OP_BWD_FILTER_SGD, dt, self.in_shape, self.w_shape, self.pad, self.stride) == 0)
         self.y = torch.empty(self.out_shape, dtype=dt, device=dev)
         self.dx = torch.empty(self.in_shape, dtype=dt, device=dev)
         self.x = None
@@ -79,8 +88,9 @@ class ConvLayer(Layer):
             net.need_workspace(singa.conv_workspace_bytes(op, dt, self.in_shape, self.w_shape, self.pad,
                                                           self.stride))
 
-    def bind(self, w, b, w_compute, dw, db):
+    def bind(self, w, b, w_compute, dw, db, v, vb, b_compute):
         self.w, self.b, self.w_compute, self.dw, self.db = w, b, w_compute, dw, db
+        self.v, self.vb, self.b_compute = v, vb, b_compute
 
     def compute_feature(self, x):
         self.x = x
@@ -89,8 +99,22 @@ class ConvLayer(Layer):
         return self.y
 
     def compute_gradient(self, dy, need_dx=True):
+        if self.fused_update:
+            # backward-data first: it reads the bf16 weights the update rewrites
+            self._bwd_data(dy, need_dx)
+            net, wl_ = self.net, self.net.wl
+            keep = net.keep_grads
+            singa.conv_bwd_filter_sgd(
+                self.x, dy, self.w_shape, self.w, self.v, self.w_compute if net.wb_flat is not None else None,
+                b=self.b, vb=self.vb, b_bf16=self.b_compute, lr=wl_.lr, momentum=wl_.momentum,
+                weight_decay=wl_.weight_decay, pad=self.pad, stride=self.stride, dw=self.dw if keep else None,
+                db=self.db if keep else None, workspace=net.workspace)
+            return self.dx if need_dx else None
         singa.conv_bwd_filter(self.x, dy, self.w_shape, self.pad, self.stride, with_bias=self.has_bias, dw=self.dw,
                               db=self.db, workspace=self.net.workspace)
+        return self._bwd_data(dy, need_dx)
+
+    def _bwd_data(self, dy, need_dx):
         if not need_dx:
             return None
         singa.conv_bwd_data(dy, self.w_compute, self.in_shape, self.pad, self.stride, out=self.dx,
@@ -167,8 +191,14 @@ class SoftmaxCELayer(Layer):
 class Net:
     """A workload's layer stack on one GPU, with flat parameter buffers."""
 
-    def __init__(self, workload: wl.Workload, batch: Optional[int] = None, device="cuda"):
+    def __init__(self, workload: wl.Workload, batch: Optional[int] = None, device="cuda", fuse_update: bool = True,
+                 keep_grads: bool = False):
+        """fuse_update: apply the update inside the filter-gradient kernel
+        where it can be fused; keep_grads: those layers also store their
+        gradients in the flat gradient buffer (for inspection)."""
         self.wl = workload
+        self.fuse_update = fuse_update
+        self.keep_grads = keep_grads
         self.batch = workload.batch if batch is None else batch
         self.device = torch.device(device)
         self.dtype = torch.bfloat16 if workload.dtype == "bf16" else torch.float32
@@ -229,12 +259,26 @@ class Net:
         self.wb_flat = torch.zeros(total, dtype=torch.bfloat16, device=dev) if self.dtype == torch.bfloat16 else None
         self.offsets = offs
         for l, (ow, nw, ob, nb) in zip(self.param_layers(), offs):
+            l.flat_range = (ow, ob + _pad(nb))  # the layer's weights and bias, padding included
             w = self.w_flat[ow:ow + nw].view(l.w_shape)
             dw = self.g_flat[ow:ow + nw].view(l.w_shape)
+            v = self.v_flat[ow:ow + nw].view(l.w_shape)
             b = self.w_flat[ob:ob + nb] if nb else None
             db = self.g_flat[ob:ob + nb] if nb else None
+            vb = self.v_flat[ob:ob + nb] if nb else None
             wc = self.wb_flat[ow:ow + nw].view(l.w_shape) if self.wb_flat is not None else w
-            l.bind(w, b, wc, dw, db)
+            bc = self.wb_flat[ob:ob + nb] if (nb and self.wb_flat is not None) else None
+            l.bind(w, b, wc, dw, db, v, vb, bc)
+        # contiguous runs of the flat buffers that the update after the backward loop covers
+        self.update_ranges = []
+        for l in self.param_layers():
+            if l.fused_update:
+                continue
+            a, e = l.flat_range
+            if self.update_ranges and self.update_ranges[-1][1] == a:
+                self.update_ranges[-1] = (self.update_ranges[-1][0], e)
+            else:
+                self.update_ranges.append((a, e))
 
     # ------------------------------------------------------------ marshalling
     def load_params(self, params: List[wl.LayerParams]):
@@ -274,8 +318,12 @@ class Net:
         return g
 
     def update(self):
-        singa.sgd_momentum_update(self.w_flat, self.g_flat, self.v_flat, self.wb_flat, self.wl.lr, self.wl.momentum,
-                                  self.wl.weight_decay)
+        """The update of every layer whose update is not fused into its
+        filter-gradient kernel, over their parts of the flat buffers."""
+        for a, e in self.update_ranges:
+            wb = self.wb_flat[a:e] if self.wb_flat is not None else None
+            singa.sgd_momentum_update(self.w_flat[a:e], self.g_flat[a:e], self.v_flat[a:e], wb, self.wl.lr,
+                                      self.wl.momentum, self.wl.weight_decay)
 
     def train_one_batch(self, x, labels=None, dy_top=None, need_input_grad=False):
         self.forward(x, labels)

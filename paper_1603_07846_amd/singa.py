@@ -26,11 +26,12 @@ ERRORS = {-1: "SINGA_ERR_NULL", -2: "SINGA_ERR_SHAPE", -3: "SINGA_ERR_UNSUPPORTE
 F32, BF16 = 0, 1
 NCHW, NHWC = 0, 1
 POOL_MAX, POOL_AVG = 0, 1
-OP_FWD, OP_BWD_DATA, OP_BWD_FILTER = 0, 1, 2
+OP_FWD, OP_BWD_DATA, OP_BWD_FILTER, OP_BWD_FILTER_SGD = 0, 1, 2, 3
 
 # every exported symbol of the C ABI (checked by the CPU tests against the header)
 EXPORTS = ["singa_strerror", "singa_conv_out_shape", "singa_pool_out_shape", "singa_conv_workspace_bytes",
-           "singa_conv_fwd", "singa_conv_bwd_data", "singa_conv_bwd_filter", "singa_pool_fwd", "singa_pool_bwd",
+           "singa_conv_fwd", "singa_conv_bwd_data", "singa_conv_bwd_filter", "singa_conv_bwd_filter_sgd",
+           "singa_pool_fwd", "singa_pool_bwd",
            "singa_relu_fwd", "singa_relu_bwd", "singa_softmax_ce", "singa_sgd_momentum_update",
            "singa_trace_enable", "singa_trace_count", "singa_trace_get"]
 
@@ -81,6 +82,9 @@ def _lib():
         lib.singa_conv_fwd.argtypes = [i32, i32, S4, vp, F4, vp, vp, CD, vp, i32, vp, sz, vp]
         lib.singa_conv_bwd_data.argtypes = [i32, i32, S4, F4, vp, CD, vp, vp, vp, vp, sz, vp]
         lib.singa_conv_bwd_filter.argtypes = [i32, i32, S4, vp, F4, CD, vp, vp, vp, i32, vp, sz, vp]
+        f32 = ctypes.c_float
+        lib.singa_conv_bwd_filter_sgd.argtypes = [i32, i32, S4, vp, F4, CD, vp, vp, vp, vp, vp, vp, vp, vp, vp,
+                                                  f32, f32, f32, vp, sz, vp]
         lib.singa_pool_fwd.argtypes = [i32, i32, S4, vp, PD, vp, vp, vp]
         lib.singa_pool_bwd.argtypes = [i32, i32, S4, PD, vp, vp, vp, vp, vp]
         lib.singa_relu_fwd.argtypes = [i32, sz, vp, vp, vp]
@@ -248,6 +252,23 @@ def conv_bwd_filter(x, dy, w_shape, pad=0, stride=1, layout="NHWC", with_bias=Tr
         ctypes.byref(_cdesc(pad, stride)), _ptr(dy), _ptr(dw), _ptr(db if with_bias else None),
         int(bool(accumulate)), _ptr(ws), 0 if ws is None else ws.numel(), _stream()))
     return dw, (db if with_bias else None)
+
+
+def conv_bwd_filter_sgd(x, dy, w_shape, w, v, w_bf16=None, b=None, vb=None, b_bf16=None, lr=0.01, momentum=0.9,
+                        weight_decay=0.0, pad=0, stride=1, layout="NHWC", dw=None, db=None, workspace=None):
+    """Param gradients of a convolution with the momentum SGD step applied to
+    them at once: w, v (fp32, filter shape) and w_bf16 updated in place, the
+    bias likewise when b is given; dw / db, if given, also receive the
+    gradient.  Returns (w, v)."""
+    lay = _layout(layout)
+    nbytes = conv_workspace_bytes(OP_BWD_FILTER_SGD, _dt(x), tuple(x.shape), tuple(w_shape), pad, stride, lay)
+    ws = _workspace(nbytes, x.device, workspace)
+    _check("singa_conv_bwd_filter_sgd", _lib().singa_conv_bwd_filter_sgd(
+        _dt(x), lay, ctypes.byref(_act_shape4(x.shape, lay)), _ptr(x), ctypes.byref(_filt4(w_shape, lay)),
+        ctypes.byref(_cdesc(pad, stride)), _ptr(dy), _ptr(dw), _ptr(db), _ptr(w), _ptr(v), _ptr(w_bf16), _ptr(b),
+        _ptr(vb), _ptr(b_bf16), float(lr), float(momentum), float(weight_decay), _ptr(ws),
+        0 if ws is None else ws.numel(), _stream()))
+    return w, v
 
 
 def _pdesc(mode, k, stride, pad, ceil_mode) -> PoolDesc:

@@ -24,7 +24,7 @@ def _declared():
 
 def test_every_declared_symbol_is_exported():
     names = _declared()
-    assert len(names) == 16
+    assert len(names) == 17
     lib = ctypes.CDLL(singa.lib()._name)
     for n in names:
         assert hasattr(lib, n), n
@@ -93,3 +93,48 @@ def test_workspace_sizes():
     with pytest.raises(singa.SingaError) as e:
         singa.conv_workspace_bytes(7, singa.F32, x, w, 2, 1)
     assert e.value.status == -3
+
+
+def test_bwd_filter_sgd_workspace_says_when_the_update_is_fused():
+    """0 bytes exactly for the fused case: bf16, NHWC, K and C multiples of 8,
+    no input rewrite, one pass over the reduction (fully connected layers at
+    batch 256); otherwise staging for the gradient plus the gradient's own."""
+    op = singa.OP_BWD_FILTER_SGD
+    fc6, w6 = (256, 6, 6, 256), (4096, 6, 6, 256)
+    assert singa.conv_workspace_bytes(op, singa.BF16, fc6, w6, 0, 1) == 0
+    assert singa.conv_workspace_bytes(op, singa.BF16, (256, 1, 1, 4096), (1000, 1, 1, 4096), 0, 1) == 0
+    g6 = 4096 * 6 * 6 * 256 * 4 + 4096 * 4
+    assert singa.conv_workspace_bytes(op, singa.F32, fc6, w6, 0, 1) >= g6          # fp32: no fused kernel
+    assert singa.conv_workspace_bytes(op, singa.BF16, (256, 256, 6, 6), (4096, 256, 6, 6), 0, 1,
+                                      layout="NCHW") >= g6                                # NCHW
+    # a convolution with a long reduction (split over the batch) is not fused
+    conv2 = singa.conv_workspace_bytes(op, singa.BF16, (256, 27, 27, 96), (256, 5, 5, 96), 2, 1)
+    assert conv2 >= 256 * 25 * 96 * 4 + singa.conv_workspace_bytes(singa.OP_BWD_FILTER, singa.BF16,
+                                                                    (256, 27, 27, 96), (256, 5, 5, 96), 2, 1)
+    # K or C not a multiple of 8
+    assert singa.conv_workspace_bytes(op, singa.BF16, (8, 1, 1, 256), (1001, 1, 1, 256), 0, 1) > 0
+    assert singa.conv_workspace_bytes(op, singa.BF16, (8, 1, 1, 250), (1000, 1, 1, 250), 0, 1) > 0
+
+
+def test_bwd_filter_sgd_argument_errors():
+    """Validation before anything is enqueued (fake, never dereferenced device addresses)."""
+    lib = singa.lib()
+    x = singa._act_shape4((4, 1, 1, 64), singa.NHWC)
+    w = singa._filt4((16, 1, 1, 64), singa.NHWC)
+    d = singa._cdesc(0, 1)
+    A = ctypes.c_void_p(1 << 20)  # 16-byte aligned stand-in pointers
+    B = ctypes.c_void_p((1 << 20) + 4)
+    N = None
+
+    def call(*ptrs, dt=singa.BF16):
+        xp, dyp, wm, vm, wb, bm, vb, bb = ptrs
+        return lib.singa_conv_bwd_filter_sgd(dt, singa.NHWC, ctypes.byref(x), xp, ctypes.byref(w), ctypes.byref(d),
+                                             dyp, N, N, wm, vm, wb, bm, vb, bb, 0.01, 0.9, 0.0005, N, 0, N)
+    assert call(A, A, N, A, N, N, N, N) == -1       # no master weights
+    assert call(A, A, A, N, N, N, N, N) == -1       # no momentum
+    assert call(A, A, A, A, N, A, N, N) == -1       # bias without its momentum
+    assert call(A, A, A, A, N, N, N, A) == -1       # bias shadow without the bias
+    assert call(A, A, B, A, N, N, N, N) == -5       # update arrays need 16 bytes
+    assert call(A, A, A, A, B, N, N, N) == -5
+    assert call(B, A, A, A, N, N, N, N) == -5       # fused case: x needs 16 bytes
+    assert call(A, A, A, A, N, N, N, N, dt=singa.F32) == -4  # unfused: staging workspace required

@@ -391,3 +391,87 @@ def test_conv_large_tile_path(op, case):
         ref = oracle.conv_bwd_data(dy, w, x.shape, pad=pad, stride=stride)
     err = rel_l2(dev_to_nchw(out), ref)
     assert err <= TOL["bf16"], (case, err)
+
+
+# (N, C, H, W, K, R, S, pad, stride, dtype, layout, bias): the first five take
+# the fused kernel (one pass over the reduction), the rest the gradient-then-
+# update path (long reduction split over the batch, fp32, NCHW, K % 8 != 0)
+SGD_CASES = [
+    (64, 32, 6, 6, 40, 6, 6, 0, 1, "bf16", "NHWC", True),      # fully connected, ragged taps (1152 + bias)
+    (16, 256, 1, 1, 1000, 1, 1, 0, 1, "bf16", "NHWC", True),   # 1000 filters: ragged rows
+    (16, 256, 1, 1, 1000, 1, 1, 0, 1, "bf16", "NHWC", False),
+    (4, 16, 8, 8, 24, 3, 3, 1, 1, "bf16", "NHWC", True),       # convolution with a one-pass reduction
+    (8, 64, 3, 3, 96, 3, 3, 0, 1, "bf16", "NHWC", True),
+    (16, 16, 16, 16, 32, 3, 3, 1, 1, "bf16", "NHWC", True),    # split reduction
+    (64, 32, 6, 6, 40, 6, 6, 0, 1, "f32", "NHWC", True),
+    (64, 32, 6, 6, 40, 6, 6, 0, 1, "bf16", "NCHW", True),
+    (16, 64, 1, 1, 30, 1, 1, 0, 1, "bf16", "NHWC", True),
+]
+
+
+def _sgd_state(K, C, R, S, layout, seed):
+    w = wl.random_array((K, C, R, S), seed, "normal", 0.1, "f32")
+    v = wl.random_array((K, C, R, S), seed + 1, "normal", 0.01, "f32")
+    b = wl.random_array((K,), seed + 2, "normal", 0.1, "f32")
+    vb = wl.random_array((K,), seed + 3, "normal", 0.01, "f32")
+    return (kcrs_to_dev(w, "f32", layout), kcrs_to_dev(v, "f32", layout), torch.from_numpy(b).cuda(),
+            torch.from_numpy(vb).cuda())
+
+
+@pytest.mark.parametrize("case", SGD_CASES, ids=["x".join(map(str, c)) for c in SGD_CASES])
+def test_conv_bwd_filter_sgd_matches_gradient_then_update(case):
+    """The fused call leaves w, v, the bf16 copies and the gradients bit for
+    bit as singa_conv_bwd_filter followed by singa_sgd_momentum_update."""
+    N, C, H, W, K, R, S, pad, stride, dt, layout, bias = case
+    x, _, _, dy = _conv_inputs((N, C, H, W, K, R, S, pad, stride), dt, 120)
+    xd, dyd = nchw_to_dev(x, dt, layout), nchw_to_dev(dy, dt, layout)
+    wshape = fphys((K, C, R, S), layout)
+    lr, mom, wd = 0.01, 0.9, 5e-4
+    fused_expected = singa.conv_workspace_bytes(singa.OP_BWD_FILTER_SGD, singa.BF16 if dt == "bf16" else singa.F32,
+                                                phys((N, C, H, W), layout), wshape, pad, stride, layout) == 0
+    assert fused_expected == (case in SGD_CASES[:5])
+    # reference: gradient, then the flat update
+    w0, v0, b0, vb0 = _sgd_state(K, C, R, S, layout, 130)
+    dw, db = singa.conv_bwd_filter(xd, dyd, wshape, pad, stride, layout=layout, with_bias=bias)
+    wr, vr, br, vbr = w0.clone(), v0.clone(), b0.clone(), vb0.clone()
+    wbr = torch.zeros(wr.shape, dtype=torch.bfloat16, device="cuda")
+    bbr = torch.zeros(br.shape, dtype=torch.bfloat16, device="cuda")
+    singa.sgd_momentum_update(wr, dw, vr, wbr, lr, mom, wd)
+    if bias:
+        singa.sgd_momentum_update(br, db, vbr, bbr, lr, mom, wd)
+    # the gradient also stored: 16-byte aligned (vector epilogue), or 4 bytes
+    # off (element-wise epilogue); or not stored
+    for mode in ("keep", "keep_unaligned", "none"):
+        keep = mode != "none"
+        wf, vf, bf, vbf = w0.clone(), v0.clone(), b0.clone(), vb0.clone()
+        wbf = torch.zeros(wf.shape, dtype=torch.bfloat16, device="cuda")
+        bbf = torch.zeros(bf.shape, dtype=torch.bfloat16, device="cuda")
+        gw = None
+        if mode == "keep":
+            gw = torch.full(dw.shape, float("nan"), device="cuda")
+        elif mode == "keep_unaligned":
+            gw = torch.full((dw.numel() + 1,), float("nan"), device="cuda")[1:].view(dw.shape)
+        gb = torch.full((K,), float("nan"), device="cuda") if keep and bias else None
+        singa.trace_enable(True)
+        singa.conv_bwd_filter_sgd(xd, dyd, wshape, wf, vf, wbf, b=bf if bias else None, vb=vbf if bias else None,
+                                  b_bf16=bbf if bias else None, lr=lr, momentum=mom, weight_decay=wd, pad=pad,
+                                  stride=stride, layout=layout, dw=gw, db=gb)
+        torch.cuda.synchronize()
+        names = [r[0] for r in singa.trace_records()]
+        singa.trace_enable(False)
+        assert any(n.endswith(",1>") and n.startswith("conv_wgrad_large") for n in names) == fused_expected, names
+        assert torch.equal(wf, wr) and torch.equal(vf, vr) and torch.equal(wbf, wbr), (case, mode)
+        if bias:
+            assert torch.equal(bf, br) and torch.equal(vbf, vbr) and torch.equal(bbf, bbr), (case, mode)
+        else:
+            assert torch.equal(bf, b0) and torch.equal(vbf, vb0)  # untouched
+        if keep:
+            assert torch.equal(gw, dw), case
+            if bias:
+                assert torch.equal(gb, db), case
+    # and the update itself against the oracle's, from the oracle's gradient
+    ref_dw, ref_db = oracle.conv_bwd_filter(x, dy, (K, C, R, S), pad=pad, stride=stride)
+    w_np, v_np = filt_to_kcrs(w0, layout), filt_to_kcrs(v0, layout)
+    ref_w, ref_v = oracle.sgd_momentum(w_np, ref_dw, v_np, lr, mom, wd)
+    assert rel_l2(filt_to_kcrs(wr, layout), ref_w) <= TOL["f32"]
+    assert rel_l2(filt_to_kcrs(vr, layout), ref_v) <= TOL["f32"]

@@ -74,7 +74,9 @@ def _oracle_params(inp, dtype):
 
 
 def _run_gpu(w, inp, batch, need_input_grad):
-    net = gnet.Net(w, batch=batch)
+    # keep_grads: the layers with the update fused into their gradient kernel
+    # also store the gradient, which the comparison reads
+    net = gnet.Net(w, batch=batch, keep_grads=True)
     net.load_params(inp.params)
     x = net.to_device_input(inp.x)
     labels = torch.from_numpy(inp.labels).cuda() if inp.labels is not None else None
