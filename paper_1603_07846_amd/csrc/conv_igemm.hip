@@ -1608,7 +1608,9 @@ int wgrad_splits_for(const ConvShape& s, int dt, bool bias, bool large) {
   const long M = s.K, Ng = (long)s.R * s.S * s.C + (bias ? 1 : 0), T = (long)s.N * s.P * s.Q;
   if (large) {
     const long tiles = ((M + WL_BM - 1) / WL_BM) * ((Ng + WL_BN - 1) / WL_BN);
-    return wgrad_split_count(tiles, (T + WL_BK - 1) / WL_BK, 1024);  // two workgroups per CU: two rounds
+    // about three workgroups per CU (one and a half rounds at two per CU):
+    // measured best of 512 - 1536 targets, fewer partial tiles than 1024
+    return wgrad_split_count(tiles, (T + WL_BK - 1) / WL_BK, 768);
   }
   const long tiles = ((M + BM - 1) / BM) * ((Ng + BN - 1) / BN);
   const long bk = dt == BF16 ? WG<bf16_t>::BK : WG<float>::BK;
