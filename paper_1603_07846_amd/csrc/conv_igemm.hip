@@ -245,6 +245,11 @@ struct FwdArgs {
   float* partial;  // split-K: fp32 partial tiles [split][M][Nn] instead of y
   int kt_per_split;
   const void* mask;  // optional [M][Nn] tensor: an output is zeroed where mask <= 0
+  // 256-row kernel: K-tile kt covers channels [cs BK, cs BK + BK) of tap
+  // rs = kt mod RS, cs = kt div RS (taps fastest), instead of taps [kt BK,
+  // kt BK + BK) in (r, s, c) order; needs C % BK == 0.
+  int tap_major, RS;
+  FastDiv dRS;
 };
 
 // Operand load modes.  VEC16: 16-byte vectors of VEC taps (C % VEC == 0 for
@@ -559,6 +564,13 @@ __global__ __launch_bounds__(NT, LBK == 32 ? 2 : 1) void conv_fwd_large_kernel(F
   };
   auto taps = [&](int k0) {
     Taps t;
+    if (a.tap_major && k0 < a.Kg) {
+      // consecutive K-tiles read the same channels one tap apart: the input
+      // rows they need overlap, so they meet in the caches
+      const int kt = k0 / LBK;
+      const int cs = (int)fdiv((uint32_t)kt, a.dRS);
+      k0 = (kt - cs * a.RS) * a.C + cs * LBK;
+    }
 #pragma unroll
     for (int p = 0; p < NPAR; ++p) {
       const int kk = k0 + 8 * cpar[p];
@@ -1475,6 +1487,9 @@ hipError_t conv_fwd_dispatch(const ConvShape& s, const void* x, const void* w, c
   constexpr int VEC = KT<T>::VEC;
   FwdArgs a;
   a.x = x; a.w = w; a.bias = bias; a.y = y; a.mask = mask;
+  a.tap_major = 0;
+  a.RS = s.R * s.S;
+  a.dRS = make_fastdiv((uint32_t)a.RS);
   a.x_bytes = (uint32_t)((size_t)s.N * s.H * s.W * s.C * sizeof(T));
   a.w_bytes = (uint32_t)((size_t)s.K * s.R * s.S * s.C * sizeof(T));
   a.M = s.N * s.P * s.Q;
@@ -1505,6 +1520,7 @@ hipError_t conv_fwd_dispatch(const ConvShape& s, const void* x, const void* w, c
     const bool deep = fwd_large_bk(a.Kg) == 64;
     const bool narrow = a.Nn <= 96;  // one 96-column tile
     a.kt_per_split = (a.Kg + (deep ? 64 : 32) - 1) / (deep ? 64 : 32);  // one split: every K-tile of this depth
+    a.tap_major = a.RS > 1 && s.C % (deep ? 64 : 32) == 0;
     TraceScope ts(fwd_large_name(bwd, deep, narrow), st, flops, WORK_FLOP);
 #define LAUNCH_LARGE(B, K, W) hipLaunchKernelGGL((conv_fwd_large_kernel<B, K, W>), dim3(a.tiles), dim3(NT), 0, st, a)
     if (bwd) {
