@@ -87,6 +87,8 @@ class ConvLayer(Layer):
         for op in (singa.OP_FWD, singa.OP_BWD_DATA, singa.OP_BWD_FILTER):
             net.need_workspace(singa.conv_workspace_bytes(op, dt, self.in_shape, self.w_shape, self.pad,
                                                           self.stride))
+        net.ws_wgrad_bytes = max(net.ws_wgrad_bytes, singa.conv_workspace_bytes(
+            singa.OP_BWD_FILTER, dt, self.in_shape, self.w_shape, self.pad, self.stride))
 
     def bind(self, w, b, w_compute, dw, db, v, vb, b_compute):
         self.w, self.b, self.w_compute, self.dw, self.db = w, b, w_compute, dw, db
@@ -110,8 +112,17 @@ class ConvLayer(Layer):
                 weight_decay=wl_.weight_decay, pad=self.pad, stride=self.stride, dw=self.dw if keep else None,
                 db=self.db if keep else None, workspace=net.workspace)
             return self.dx if need_dx else None
-        singa.conv_bwd_filter(self.x, dy, self.w_shape, self.pad, self.stride, with_bias=self.has_bias, dw=self.dw,
-                              db=self.db, workspace=self.net.workspace)
+        side = self.net.wgrad_stream
+        if side is None:
+            singa.conv_bwd_filter(self.x, dy, self.w_shape, self.pad, self.stride, with_bias=self.has_bias,
+                                  dw=self.dw, db=self.db, workspace=self.net.workspace)
+        else:
+            # the filter gradient on the second stream, beside this layer's
+            # backward-data and the layers below (both only read dy and x)
+            side.wait_stream(torch.cuda.current_stream(self.net.device))
+            with torch.cuda.stream(side):
+                singa.conv_bwd_filter(self.x, dy, self.w_shape, self.pad, self.stride, with_bias=self.has_bias,
+                                      dw=self.dw, db=self.db, workspace=self.net.workspace_wgrad)
         return self._bwd_data(dy, need_dx)
 
     def _bwd_data(self, dy, need_dx):
@@ -192,13 +203,16 @@ class Net:
     """A workload's layer stack on one GPU, with flat parameter buffers."""
 
     def __init__(self, workload: wl.Workload, batch: Optional[int] = None, device="cuda", fuse_update: bool = True,
-                 keep_grads: bool = False):
+                 keep_grads: bool = False, concurrent_wgrad: bool = True):
         """fuse_update: apply the update inside the filter-gradient kernel
         where it can be fused; keep_grads: those layers also store their
-        gradients in the flat gradient buffer (for inspection)."""
+        gradients in the flat gradient buffer (for inspection);
+        concurrent_wgrad: the other layers' filter gradients run on a second
+        stream, concurrently with the backward-data passes."""
         self.wl = workload
         self.fuse_update = fuse_update
         self.keep_grads = keep_grads
+        self.ws_wgrad_bytes = 0
         self.batch = workload.batch if batch is None else batch
         self.device = torch.device(device)
         self.dtype = torch.bfloat16 if workload.dtype == "bf16" else torch.float32
@@ -234,6 +248,12 @@ class Net:
             prev = layer
         self.out_shape = shape
         self.workspace = torch.empty(max(self.ws_bytes, 256), dtype=torch.uint8, device=self.device)
+        # default priority, like every stream the library runs on
+        self.wgrad_stream = None
+        if concurrent_wgrad and self.device.type == "cuda" and any(
+                not l.fused_update for l in self.layers if isinstance(l, ConvLayer)):
+            self.wgrad_stream = torch.cuda.Stream(device=self.device)
+            self.workspace_wgrad = torch.empty(max(self.ws_wgrad_bytes, 256), dtype=torch.uint8, device=self.device)
         self._build_params()
 
     def need_workspace(self, nbytes: int):
@@ -315,6 +335,8 @@ class Net:
         g = dy_top
         for i in range(len(self.layers) - 1, -1, -1):
             g = self.layers[i].compute_gradient(g, need_dx=(i > 0 or need_input_grad))
+        if self.wgrad_stream is not None:
+            torch.cuda.current_stream(self.device).wait_stream(self.wgrad_stream)
         return g
 
     def update(self):

@@ -1,9 +1,10 @@
 """A training step replayed from a HIP graph against the same step run eagerly.
 
 Two nets start from the same parameters.  One runs train_one_batch eagerly
-with every update after the backward loop, the other replays a graph
-captured from its own train_one_batch, with the update fused into the filter
-gradient kernel where the net does that.  Between
+on one stream with every update after the backward loop, the other replays a
+graph captured from its own train_one_batch, with the update fused into the
+filter-gradient kernel where the net does that and the other filter
+gradients on a second stream beside the backward-data passes.  Between
 replays the program does eager work of its own (the eager net's step, a copy
 into the captured input, synchronizations), and after every replay the
 graph's loss, updated master weights, momentum and bf16 shadow must equal the
@@ -26,7 +27,7 @@ def test_graph_replay_matches_eager(index, batch):
     w = wl.WORKLOADS[index]
     inp = wl.make_inputs(w, batch=batch, seed_offset=31)
     inp2 = wl.make_inputs(w, batch=batch, seed_offset=32)
-    eager = gnet.Net(w, batch=batch, device="cuda:0", fuse_update=False)
+    eager = gnet.Net(w, batch=batch, device="cuda:0", fuse_update=False, concurrent_wgrad=False)
     graphed = gnet.Net(w, batch=batch, device="cuda:0")
     if w.dtype == "bf16":
         assert any(l.fused_update for l in graphed.param_layers())
