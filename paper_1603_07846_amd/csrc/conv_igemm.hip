@@ -1517,8 +1517,10 @@ hipError_t conv_fwd_dispatch(const ConvShape& s, const void* x, const void* w, c
     a.tiles_n = (a.Nn + BN - 1) / BN;
     a.tiles = ((a.M + L_BM - 1) / L_BM) * a.tiles_n;
     a.partial = nullptr;
-    const bool deep = fwd_large_bk(a.Kg) == 64;
     const bool narrow = a.Nn <= 96;  // one 96-column tile
+    // 64-tap K-tiles only for the 256 x 128 layout (the 256 x 96 one measured
+    // faster at 32 taps, two workgroups per CU, on a 6400-tap reduction)
+    const bool deep = fwd_large_bk(narrow ? 0 : a.Kg) == 64;
     a.kt_per_split = (a.Kg + (deep ? 64 : 32) - 1) / (deep ? 64 : 32);  // one split: every K-tile of this depth
     a.tap_major = a.RS > 1 && s.C % (deep ? 64 : 32) == 0;
     TraceScope ts(fwd_large_name(bwd, deep, narrow), st, flops, WORK_FLOP);

@@ -360,6 +360,8 @@ LARGE_CASES = [
     ("fwd", (10, 128, 47, 47, 300, 3, 3, 1, 1)),
     ("bwd_data", (15, 200, 47, 47, 128, 3, 3, 1, 1)),
     ("fwd", (40, 128, 59, 59, 136, 3, 3, 1, 2)),
+    ("fwd", (15, 512, 47, 47, 136, 3, 3, 1, 1)),       # 4608 taps: 64-tap K-tiles
+    ("bwd_data", (15, 136, 47, 47, 512, 3, 3, 1, 1)),
     # at most 96 output columns: the 256 x 96 wave layout
     ("fwd", (30, 64, 47, 47, 96, 3, 3, 1, 1)),
     ("fwd", (30, 32, 47, 47, 90, 3, 3, 1, 1)),   # ragged columns, element-wise epilogue
@@ -385,6 +387,8 @@ def test_conv_large_tile_path(op, case):
     assert large, names
     narrow = (K if op == "fwd" else C) <= 96  # GEMM columns: filters, or input channels for the data gradient
     assert all(n.endswith(",4>") == narrow for n in large), large
+    deep = not narrow and R * S * (C if op == "fwd" else K) >= 4096  # reduction length
+    assert all((",64," in n) == deep for n in large), large
     if op == "fwd":
         ref = oracle.relu_fwd(oracle.conv_fwd(x, w, b, pad=pad, stride=stride))
     else:
