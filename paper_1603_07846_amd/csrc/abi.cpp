@@ -421,15 +421,21 @@ int singa_conv_bwd_data(singa_dtype dtype, singa_layout layout, const singa_shap
                             nullptr, st);
       if (e == hipSuccess) e = launch_depth_to_space(dtype, s, g, o.dxs, nhwc_mask, dx, st);
     } else if (bwd_data_gemm(s)) {
-      if (bwd_data_fc(s)) {
-        const int J = RS * s.C;  // wt[(r,s,c)][k] = w[k][(r,s,c)]
-        e = launch_transpose(dtype, wk, o.wt, 1, s.K, J, 0, J, 0, s.K, 0, st);
-      } else {  // wt[c][r'][s'][k] = w[k][R-1-r'][S-1-s'][c]
-        e = launch_transpose(dtype, wk, o.wt, RS, s.K, s.C, s.C, (long)RS * s.C, s.K, (long)RS * s.K, 1, st);
+      // dense geometry: the GEMM reads w itself as the transposed filter when it can
+      e = bwd_data_fc(s) ? launch_conv_fwd_wt(dtype, bwd_data_inner(s), dy, wk, dx, 1, conv_flops(s), o.partial,
+                                              nhwc_mask, st)
+                         : hipErrorNotSupported;
+      if (e == hipErrorNotSupported) {
+        if (bwd_data_fc(s)) {
+          const int J = RS * s.C;  // wt[(r,s,c)][k] = w[k][(r,s,c)]
+          e = launch_transpose(dtype, wk, o.wt, 1, s.K, J, 0, J, 0, s.K, 0, st);
+        } else {  // wt[c][r'][s'][k] = w[k][R-1-r'][S-1-s'][c]
+          e = launch_transpose(dtype, wk, o.wt, RS, s.K, s.C, s.C, (long)RS * s.C, s.K, (long)RS * s.K, 1, st);
+        }
+        if (e == hipSuccess)
+          e = launch_conv_fwd(dtype, bwd_data_inner(s), dy, o.wt, nullptr, dx, 0, 1, conv_flops(s), o.partial,
+                              nhwc_mask, st);
       }
-      if (e == hipSuccess)
-        e = launch_conv_fwd(dtype, bwd_data_inner(s), dy, o.wt, nullptr, dx, 0, 1, conv_flops(s), o.partial,
-                            nhwc_mask, st);
     } else {
       e = launch_conv_bwd_data_direct(dtype, s, dy, wk, dx, nhwc_mask, st);
     }

@@ -40,6 +40,9 @@ constexpr int ROWB = 128;               // bytes of one operand row per K-tile
 constexpr int PITCH = ROWB + 16;        // padded LDS row pitch
 constexpr int TILE = BM * PITCH;        // bytes of one operand tile
 constexpr int SMEM = 2 * 2 * TILE;      // 2 stages x (A, B)
+constexpr int BT_PITCH = 320;            // transposed-filter mode: 256-byte tap-major B row (128 columns) + 64
+constexpr int BT_TILE = 64 * BT_PITCH;   // its B tile of one K-tile (64 bf16 taps)
+constexpr int BT_SMEM = 2 * (TILE + BT_TILE);
 
 template <typename T> struct KT {
   static constexpr int VEC = 16 / (int)sizeof(T);  // elements per 16 bytes
@@ -108,6 +111,46 @@ __device__ __forceinline__ void mma_tile(const char* As, const char* Bs, f32x16 
         acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1[j], b1[j], acc[1][1], 0, 0, 0);
       }
     }
+  }
+}
+
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+
+// ds_read_b64_tr_b16: within each 16-lane group, lane i receives element
+// i % 4 of the 8-byte chunks addressed by lanes 4k + i / 4 (k = 0..3).
+__device__ __forceinline__ v4i16 lds_tr16(const char* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) v4i16*)(__attribute__((address_space(3))) char*)p);
+}
+
+// The same K-tile product with the B operand in tap-major rows (BT_PITCH
+// bytes, 128 columns each; the transposed-filter mode): A fragments as in
+// mma_tile, B fragments (8 consecutive taps of one column) from pairs of
+// transposing reads.  bf16 only.
+__device__ __forceinline__ void mma_tile_bt(const char* As, const char* Bs, f32x16 (&acc)[2][2], int wm, int wn,
+                                            int lane) {
+  const int li = lane & 31, lh = lane >> 5;
+  const char* ab = As + (wm * 64 + li) * PITCH + lh * 16;
+  // lane l: column (l & 15) of a 16-column group, taps 8 (l >> 5) + 0..7 of the 16-tap step
+  const int g = lane >> 4, sl = lane & 15;
+  const int row = 8 * (g >> 1) + (sl >> 2);
+  const int colb = 2 * (16 * (g & 1) + 4 * (sl & 3));
+  const char* bb = Bs + row * BT_PITCH + 2 * (wn * 64) + colb;
+#pragma unroll
+  for (int kc = 0; kc < ROWB / 32; ++kc) {
+    const bf16x8 a0 = *(const bf16x8*)(ab + kc * 32);
+    const bf16x8 a1 = *(const bf16x8*)(ab + 32 * PITCH + kc * 32);
+    bf16x8 bfr[2];
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+      const v4i16 lo = lds_tr16(bb + kc * 16 * BT_PITCH + b * 64);
+      const v4i16 hi = lds_tr16(bb + (kc * 16 + 4) * BT_PITCH + b * 64);
+      bfr[b] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+    }
+    acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, bfr[0], acc[0][0], 0, 0, 0);
+    acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, bfr[1], acc[0][1], 0, 0, 0);
+    acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, bfr[0], acc[1][0], 0, 0, 0);
+    acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, bfr[1], acc[1][1], 0, 0, 0);
   }
 }
 
@@ -257,7 +300,13 @@ struct FwdArgs {
 // halves of 4 taps each, for channel counts that are a multiple of 4 but not
 // of 8 (the first layer's colour channels padded to 4).  ELEM: one element at
 // a time.
-constexpr int ELEM = 0, VEC8 = 1, VEC16 = 2;
+// BT16 (bf16 filter only): the filter is given transposed, w[tap][col] with
+// the Nn columns contiguous (Nn % 8 == 0); 16-byte vectors of 8 columns go
+// into LDS as tap-major rows and the MFMA fragments come from transposing
+// reads.  Serves the dense backward-data, whose B operand is the weight
+// matrix as stored, without a transposed copy.
+constexpr int ELEM = 0, VEC8 = 1, VEC16 = 2, BT16 = 3;
+
 
 // AM / BMD: load mode of the input taps / filter rows.  BWD only names the
 // instance that serves backward-data, so profiles tell them apart.
@@ -266,7 +315,10 @@ __global__ __launch_bounds__(NT) void conv_fwd_kernel(FwdArgs a) {
   constexpr int VEC = KT<T>::VEC;
   constexpr int BK = KT<T>::BK;
   constexpr uint32_t ES = sizeof(T);
-  __shared__ __attribute__((aligned(16))) char smem[SMEM];
+  constexpr bool BT = BMD == BT16;
+  static_assert(!BT || sizeof(T) == 2, "transposed filter: bf16 only");
+  constexpr int BTILE = BT ? BT_TILE : TILE;  // bytes of the B tile
+  __shared__ __attribute__((aligned(16))) char smem[BT ? BT_SMEM : SMEM];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int L = xcd_remap(blockIdx.x, gridDim.x);
@@ -360,7 +412,12 @@ __global__ __launch_bounds__(NT) void conv_fwd_kernel(FwdArgs a) {
     }
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      if constexpr (BMD == VEC16) {
+      if constexpr (BT) {
+        // chunk tid + 256 i of the 64 x 128 tile: tap k0 + q / 16, columns n0 + 8 (q % 16) ..
+        const int q = tid + 256 * i, kt = k0 + (q >> 4), col = n0 + 8 * (q & 15);
+        const bool ok = kt < a.Kg && col < a.Nn;
+        rb[i].u = ld16(wr, ok ? (uint32_t)(kt * a.Nn + col) * ES : OOB);
+      } else if constexpr (BMD == VEC16) {
         const bool ok = brow[i] >= 0 && kk < a.Kg;
         rb[i].u = ld16(wr, ok ? (uint32_t)(brow[i] + kk) * ES : OOB);
       } else if constexpr (BMD == VEC8) {
@@ -378,14 +435,20 @@ __global__ __launch_bounds__(NT) void conv_fwd_kernel(FwdArgs a) {
     }
   };
   auto store_tile = [&](int stage, const V16 (&ra)[4], const V16 (&rb)[4]) {
-    char* As = smem + stage * 2 * TILE;
+    char* As = smem + stage * (TILE + BTILE);
     char* Bs = As + TILE;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       *(uint4*)(As + (rl + 32 * i) * PITCH + cv * 16) = ra[i].u;
-      *(uint4*)(Bs + (rl + 32 * i) * PITCH + cv * 16) = rb[i].u;
+      if constexpr (BT) {
+        const int q = tid + 256 * i;
+        *(uint4*)(Bs + (q >> 4) * BT_PITCH + (q & 15) * 16) = rb[i].u;
+      } else {
+        *(uint4*)(Bs + (rl + 32 * i) * PITCH + cv * 16) = rb[i].u;
+      }
     }
   };
+
 
   f32x16 acc[2][2];
 #pragma unroll
@@ -398,6 +461,10 @@ __global__ __launch_bounds__(NT) void conv_fwd_kernel(FwdArgs a) {
   // Two LDS stages and two register sets: the global loads of tile k+2 are in
   // flight while tile k is multiplied and tile k+1 goes from registers to LDS.
   const int wm = wave >> 1, wn = wave & 1;
+  auto mma = [&](const char* S) {
+    if constexpr (BT) mma_tile_bt(S, S + TILE, acc, wm, wn, lane);
+    else mma_tile<T>(S, S + TILE, acc, wm, wn, lane);
+  };
   const int nkt_all = (a.Kg + BK - 1) / BK;
   const int kbase = split * a.kt_per_split * BK;                   // first tap of this split
   const int nkt = min(a.kt_per_split, nkt_all - split * a.kt_per_split);  // K-tiles of this split (>= 1)
@@ -409,15 +476,15 @@ __global__ __launch_bounds__(NT) void conv_fwd_kernel(FwdArgs a) {
   int kt = 0;
   for (; kt + 1 < nkt; kt += 2) {  // tiles kt (stage 0) and kt + 1 (stage 1)
     if (kt + 2 < nkt) load_tile(kbase + (kt + 2) * BK, a0, b0);
-    mma_tile<T>(smem, smem + TILE, acc, wm, wn, lane);
+    mma(smem);
     store_tile(1, a1, b1);
     __syncthreads();
     if (kt + 3 < nkt) load_tile(kbase + (kt + 3) * BK, a1, b1);
-    mma_tile<T>(smem + 2 * TILE, smem + 3 * TILE, acc, wm, wn, lane);
+    mma(smem + TILE + BTILE);
     if (kt + 2 < nkt) store_tile(0, a0, b0);
     __syncthreads();
   }
-  if (kt < nkt) mma_tile<T>(smem, smem + TILE, acc, wm, wn, lane);  // odd count: last tile is in stage 0
+  if (kt < nkt) mma(smem);  // odd count: last tile is in stage 0
 
   // Epilogue: lane holds column li of each 32x32 block, rows 8*(v/4) + 4*lh + v%4.
   const int li = lane & 31, lh = lane >> 5;
@@ -708,7 +775,6 @@ __global__ __launch_bounds__(NT, LBK == 32 ? 2 : 1) void conv_fwd_large_kernel(F
 // addresses; for fp32 (v_mfma_f32_32x32x2_f32) a lane needs a single value and
 // reads it directly.
 
-typedef short v4i16 __attribute__((ext_vector_type(4)));
 
 template <typename T> struct WG;
 template <> struct WG<bf16_t> {
@@ -740,10 +806,6 @@ struct WgradArgs {
   SgdTargets u;
 };
 
-__device__ __forceinline__ v4i16 lds_tr16(const char* p) {
-  return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-      (__attribute__((address_space(3))) v4i16*)(__attribute__((address_space(3))) char*)p);
-}
 
 // One K-tile of t-major operand rows: acc[bm][bn] += A(rows) * B(cols)^T.
 template <typename T>
@@ -1460,7 +1522,8 @@ int fwd_splits_for(long M, long Nn, long Kg, long bk) {
 
 template <typename T, int AM, bool BWD>
 void launch_fwd_bmode(int bm, const FwdArgs& a, dim3 grid, double flops, hipStream_t st) {
-  if (bm == VEC16) launch_fwd_instance<T, AM, VEC16, BWD>(a, grid, flops, st);
+  if (sizeof(T) == 2 && bm == BT16) launch_fwd_instance<T, AM, sizeof(T) == 2 ? BT16 : ELEM, BWD>(a, grid, flops, st);
+  else if (bm == VEC16) launch_fwd_instance<T, AM, VEC16, BWD>(a, grid, flops, st);
   else if (sizeof(T) == 2 && bm == VEC8) launch_fwd_instance<T, AM, sizeof(T) == 2 ? VEC8 : ELEM, BWD>(a, grid, flops, st);
   else launch_fwd_instance<T, AM, ELEM, BWD>(a, grid, flops, st);
 }
@@ -1483,7 +1546,8 @@ template <typename T> int load_mode(long len, const void* p) {
 
 template <typename T>
 hipError_t conv_fwd_dispatch(const ConvShape& s, const void* x, const void* w, const float* bias, void* y,
-                             int relu, int bwd, double flops, float* partial, const void* mask, hipStream_t st) {
+                             int relu, int bwd, double flops, float* partial, const void* mask, hipStream_t st,
+                             bool wt = false) {
   constexpr int VEC = KT<T>::VEC;
   FwdArgs a;
   a.x = x; a.w = w; a.bias = bias; a.y = y; a.mask = mask;
@@ -1512,8 +1576,8 @@ hipError_t conv_fwd_dispatch(const ConvShape& s, const void* x, const void* w, c
   a.kt_per_split = (nkt + splits - 1) / splits;
   dim3 grid(a.tiles * splits);
   const int am = load_mode<T>(s.C, x);
-  const int bm = load_mode<T>(a.Kg, w);
-  if (sizeof(T) == 2 && am == VEC16 && bm == VEC16 && splits == 1 && use_large_fwd(a.M, a.Nn, a.Kg)) {
+  const int bm = wt ? BT16 : load_mode<T>(a.Kg, w);
+  if (!wt && sizeof(T) == 2 && am == VEC16 && bm == VEC16 && splits == 1 && use_large_fwd(a.M, a.Nn, a.Kg)) {
     a.tiles_n = (a.Nn + BN - 1) / BN;
     a.tiles = ((a.M + L_BM - 1) / L_BM) * a.tiles_n;
     a.partial = nullptr;
@@ -1710,6 +1774,14 @@ hipError_t launch_conv_fwd(int dt, const ConvShape& s, const void* x, const void
                            int relu, int bwd, double flops, float* partial, const void* mask, hipStream_t st) {
   if (dt == BF16) return conv_fwd_dispatch<bf16_t>(s, x, w, bias, y, relu, bwd, flops, partial, mask, st);
   return conv_fwd_dispatch<float>(s, x, w, bias, y, relu, bwd, flops, partial, mask, st);
+}
+
+hipError_t launch_conv_fwd_wt(int dt, const ConvShape& s, const void* x, const void* wt, void* y, int bwd,
+                              double flops, float* partial, const void* mask, hipStream_t st) {
+  if (dt != BF16 || s.R != 1 || s.S != 1 || s.K % 8 != 0 || (uintptr_t)wt % 16 != 0 ||
+      (size_t)s.C * s.K * 2 > 0x7fffffffu)
+    return hipErrorNotSupported;
+  return conv_fwd_dispatch<bf16_t>(s, x, wt, nullptr, y, 0, bwd, flops, partial, mask, st, true);
 }
 
 size_t fwd_partial_bytes(const ConvShape& s, int dt) {

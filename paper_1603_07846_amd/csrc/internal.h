@@ -50,6 +50,14 @@ hipError_t launch_conv_fwd(int dt, const ConvShape& s, const void* x, const void
                            hipStream_t st);
 size_t fwd_partial_bytes(const ConvShape& s, int dt);
 
+// The same GEMM for a 1x1 geometry (R = S = 1) with the filter given
+// transposed, wt[c][k] (the K filter columns contiguous), as the dense
+// backward-data needs it: the weight matrix as stored, no transposed copy.
+// bf16 only, K % 8 == 0, 16-byte aligned wt; otherwise returns
+// hipErrorNotSupported and launches nothing.  No bias, no ReLU.
+hipError_t launch_conv_fwd_wt(int dt, const ConvShape& s, const void* x, const void* wt, void* y, int bwd,
+                              double flops, float* partial, const void* mask, hipStream_t st);
+
 // Split-K implicit-GEMM filter gradient, dw (K, R, S, C) and, with db, the
 // bias gradient from one more GEMM column against ones.  With one split the
 // kernel writes (or, with acc_dw / acc_db, adds into) dw and db directly;

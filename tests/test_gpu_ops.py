@@ -45,6 +45,7 @@ CONV_CASES = [
     (3, 5, 9, 9, 16, 3, 3, 1, 1),        # C=5: zero-padded channels in the forward pass
     (2, 12, 10, 10, 24, 3, 3, 1, 1),     # C=12: bf16 8-byte tap halves that wrap to the next tap
     (3, 4, 19, 19, 16, 5, 5, 2, 2),      # C=4, filter rows of 100 taps: 8-byte halves for both operands
+    (3, 5, 3, 3, 16, 3, 3, 0, 1),        # FC with 45 inputs: backward-data through a transposed copy
 ]
 
 
@@ -94,6 +95,31 @@ def test_conv_bwd_data(case, layout, dt):
     torch.cuda.synchronize()
     err = rel_l2(dev_to_nchw(dx, layout), ref)
     assert err <= TOL[dt], (case, err)
+
+
+# dense (fully connected) backward-data in bf16: the GEMM reads the weight
+# matrix as stored when the input width is a multiple of 8, else a transposed copy
+FC_BWD_CASES = [((16, 256, 6, 6, 96, 6, 6, 0, 1), True), ((8, 64, 4, 4, 520, 4, 4, 0, 1), True),
+                ((256, 1024, 1, 1, 4096, 1, 1, 0, 1), True), ((6, 7, 2, 2, 40, 2, 2, 0, 1), False)]
+
+
+@pytest.mark.parametrize("case,direct", FC_BWD_CASES, ids=[_ids([c])[0] for c, _ in FC_BWD_CASES])
+def test_fc_bwd_data_reads_weights_as_stored(case, direct):
+    N, C, H, W, K, R, S, pad, stride = case
+    x, w, b, dy = _conv_inputs(case, "bf16", 25)
+    xr = np.maximum(x, 0.0)
+    singa.trace_enable(True)
+    dx = singa.conv_bwd_data(nchw_to_dev(dy, "bf16"), kcrs_to_dev(w, "bf16"), phys(x.shape), pad, stride,
+                             relu_y=nchw_to_dev(xr, "bf16"))
+    torch.cuda.synchronize()
+    names = [r[0] for r in singa.trace_records()]
+    singa.trace_enable(False)
+    assert any(n.startswith("conv_fwd_kernel<bf16,2,3,1>") for n in names) == direct, names
+    assert (not any(n.startswith("transpose") for n in names)) == direct, names
+    ref = oracle.relu_bwd(xr, oracle.conv_bwd_data(dy, w, x.shape, pad=pad, stride=stride))
+    got = dev_to_nchw(dx)
+    np.testing.assert_array_equal(got[xr <= 0], 0.0)
+    assert rel_l2(got, ref) <= TOL["bf16"], case
 
 
 @pytest.mark.parametrize("dt", ["f32", "bf16"])
