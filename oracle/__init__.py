@@ -73,6 +73,7 @@ def _load():
         lib.oracle_round_bf16.argtypes = [_i64, _dp]
         lib.oracle_sgd_momentum.argtypes = [_i64, _dp, _dp, _dp,
                                             ctypes.c_double, ctypes.c_double, ctypes.c_double]
+        lib.oracle_adagrad.argtypes = [_i64, _dp, _dp, _dp, ctypes.c_double, ctypes.c_double, ctypes.c_double]
         _lib = lib
         return lib
 
@@ -251,6 +252,16 @@ def round_bf16(x) -> np.ndarray:
     y = _f64(x).copy()
     _load().oracle_round_bf16(y.size, _ptr(y))
     return y
+
+
+def adagrad(w, g, h, lr, delta, wd=0.0):
+    """One AdaGrad Updater step (Sec. 4.1.4; Duchi et al. 2011, diagonal form);
+    returns new (w, h) and leaves inputs alone."""
+    w = _f64(w).copy()
+    h = _f64(h).copy()
+    g = _f64(g)
+    _load().oracle_adagrad(w.size, _ptr(w), _ptr(g), _ptr(h), float(lr), float(delta), float(wd))
+    return w, h
 
 
 def sgd_momentum(w, g, v, lr, momentum, wd=0.0):

@@ -453,3 +453,16 @@ void oracle_sgd_momentum(int64_t n, double* w, const double* g, double* v,
         w[i] = w[i] - v[i];
     }
 }
+
+/* AdaGrad (Duchi, Hazan and Singer, JMLR 2011), the diagonal form: the
+ * squared gradients accumulate per parameter, and the step divides the
+ * learning rate by delta plus the square root of that sum. */
+void oracle_adagrad(int64_t n, double* w, const double* g, double* h,
+                    double lr, double delta, double wd)
+{
+    for (int64_t i = 0; i < n; ++i) {
+        double gi = g[i] + wd * w[i];
+        h[i] = h[i] + gi * gi;
+        w[i] = w[i] - lr * gi / (delta + sqrt(h[i]));
+    }
+}

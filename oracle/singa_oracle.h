@@ -142,6 +142,13 @@ void oracle_round_bf16(int64_t n, double* x);
 void oracle_sgd_momentum(int64_t n, double* w, const double* g, double* v,
                          double lr, double momentum, double wd);
 
+/* Updater (Sec. 4.1.4): one AdaGrad step (the protocol the section names;
+ * Duchi, Hazan and Singer 2011, diagonal form), in place on w and the sum of
+ * squared gradients h:
+ *   g' = g + wd * w;  h = h + g'^2;  w = w - lr * g' / (delta + sqrt(h)). */
+void oracle_adagrad(int64_t n, double* w, const double* g, double* h,
+                    double lr, double delta, double wd);
+
 #ifdef __cplusplus
 }
 #endif

@@ -438,6 +438,45 @@ def test_sgd_momentum_closed_forms():
         np.testing.assert_allclose(w, w0 - lr * g * coef, rtol=1e-13, atol=1e-15)
 
 
+def test_adagrad_closed_forms():
+    """AdaGrad (Duchi et al. 2011, diagonal form): closed forms of the first
+    step and of a constant gradient; the sign step at delta = 0."""
+    rng = _rng(73)
+    w0 = rng.standard_normal(100)
+    g = rng.standard_normal(100)
+    lr, delta, wd = 0.01, 1e-6, 5e-4
+    w1, h1 = oracle.adagrad(w0, g, np.zeros(100), lr, delta, wd)
+    g1 = g + wd * w0
+    np.testing.assert_allclose(h1, g1 * g1, rtol=1e-15)
+    np.testing.assert_allclose(w1, w0 - lr * g1 / (delta + np.abs(g1)), rtol=1e-14, atol=1e-16)
+    w1, _ = oracle.adagrad(w0, g, np.zeros(100), lr, 0.0, 0.0)
+    np.testing.assert_allclose(w1, w0 - lr * np.sign(g), rtol=1e-15, atol=1e-16)
+    # constant gradient, no decay: h_t = t g^2, w_t = w0 - lr g sum_{i=1..t} 1 / (delta + sqrt(i) |g|)
+    w, h = w0, np.zeros(100)
+    for t in range(1, 8):
+        w, h = oracle.adagrad(w, g, h, lr, delta, 0.0)
+        np.testing.assert_allclose(h, t * g * g, rtol=1e-14)
+        coef = sum(1.0 / (delta + np.sqrt(i) * np.abs(g)) for i in range(1, t + 1))
+        np.testing.assert_allclose(w, w0 - lr * g * coef, rtol=1e-13, atol=1e-15)
+
+
+def test_adagrad_against_torch_optim():
+    # torch's Adagrad with no learning-rate decay and a zero initial sum:
+    # sum += g'^2, w -= lr g' / (sqrt(sum) + eps), g' = g + wd w
+    rng = _rng(74)
+    w0 = rng.standard_normal(64)
+    tw = torch.tensor(w0.copy(), requires_grad=True)
+    opt = torch.optim.Adagrad([tw], lr=0.01, lr_decay=0.0, weight_decay=5e-4, initial_accumulator_value=0.0,
+                              eps=1e-6)
+    w, h = w0, np.zeros(64)
+    for step in range(5):
+        g = rng.standard_normal(64)
+        tw.grad = torch.tensor(g)
+        opt.step()
+        w, h = oracle.adagrad(w, g, h, 0.01, 1e-6, 5e-4)
+        np.testing.assert_allclose(w, tw.detach().numpy(), rtol=1e-13, atol=1e-15)
+
+
 def test_sgd_momentum_against_torch_optim():
     # torch keeps v' = mu v' + g', w -= lr v'; with a constant lr that is the
     # same trajectory as v = mu v + lr g', w -= v
