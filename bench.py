@@ -10,14 +10,19 @@ softmax cross-entropy over random labels, and one fused SGD-momentum update
 (lr 0.01, momentum 0.9, weight decay 5e-4) of all 62,378,344 parameters.
 Inputs are seeded synthetic tensors resident in HBM before timing starts.
 
+The step runs the filter gradients of the convolution layers on a second
+stream, beside the backward-data passes (--single-stream: one stream).
+
 Timing follows the paper's protocol by default (Sec. 6.2.2: run 100
 iterations, average iterations 30-80): 30 warm-up steps, then 50 timed steps
-between two device synchronizations.  The timed steps are replays of a HIP
-graph holding one whole step (--eager launches them one by one instead; the
-eager rate is reported beside it).  Then the same number of steps runs
-eagerly with the library's kernel trace on, which brackets every launch with
-HIP events on the launch's own stream; the per-kernel figures (and the
-roofline of the dominant kernel) come from those.
+between two device synchronizations, twice: replays of a HIP graph holding
+one whole step, and the same steps launched eagerly (--eager: eager only).
+`value` is the faster of the two (`launch` says which; both are reported).
+Then the same number of steps runs eagerly on one stream with the library's
+kernel trace on, which brackets every launch with HIP events: each kernel
+runs alone on the GPU, and the per-kernel figures (and the roofline of the
+dominant kernel) come from those.  A rocprofv3 summary whose average
+durations match these comes from a --single-stream run.
 
 Prints one JSON line.
 """
@@ -43,7 +48,9 @@ def parse():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=30)
     ap.add_argument("--workload", type=int, default=5, help="workload index (5 = AlexNet-shaped training step)")
-    ap.add_argument("--eager", action="store_true", help="time eager launches instead of graph replays")
+    ap.add_argument("--eager", action="store_true", help="time eager launches only (no graph replays)")
+    ap.add_argument("--single-stream", action="store_true",
+                    help="run every pass on one stream (no concurrent filter gradients), as the per-kernel pass does")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-images", type=int, default=8, help="images in the oracle's timed sample")
     return ap.parse_args()
@@ -110,7 +117,7 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     inp = wl.make_inputs(w)
-    net = gnet.Net(w, device=dev)
+    net = gnet.Net(w, device=dev, concurrent_wgrad=not args.single_stream)
     net.load_params(inp.params)
     x = net.to_device_input(inp.x)
     labels = torch.from_numpy(inp.labels).to(dev) if inp.labels is not None else None
@@ -132,24 +139,29 @@ def main():
     def eager_step():
         net.train_one_batch(x, labels=labels, dy_top=dy)
 
-    # timed region: K steps replayed from a HIP graph of one step (or eager)
-    if args.eager:
-        ms_per_step = timed(eager_step)
-        eager_ms = ms_per_step
-    else:
+    # timed region: K steps replayed from a HIP graph of one step, and K steps
+    # launched eagerly (the step's two streams overlap more when launched
+    # eagerly); `value` is the faster of the two
+    graph_ms = None
+    if not args.eager:
         graph = net.capture(x, labels=labels, dy_top=dy)
         for _ in range(3):
             graph.replay()
-        ms_per_step = timed(graph.replay)
-        eager_ms = timed(eager_step)
+        graph_ms = timed(graph.replay)
+    eager_ms = timed(eager_step)
+    launch = "eager" if graph_ms is None or eager_ms < graph_ms else "hip_graph"
+    ms_per_step = eager_ms if launch == "eager" else graph_ms
     loss = float(net.layers[-1].loss[0].item()) if w.classes else None
     images_per_s = net.batch / (ms_per_step / 1e3)
 
-    # per-kernel pass: the same K steps launched eagerly, every launch
-    # bracketed by HIP events on its own stream
+    # per-kernel pass: the same K steps launched eagerly on one stream (each
+    # kernel alone on the GPU), every launch bracketed by HIP events
+    side = net.wgrad_stream
+    net.wgrad_stream = None
     singa.trace_enable(True)
     traced_ms = timed(eager_step)
     singa.trace_enable(False)
+    net.wgrad_stream = side
     recs = singa.trace_records()
 
     # per-kernel aggregates over the timed steps
@@ -187,7 +199,31 @@ def main():
     if upd:
         gbs = upd["work"] / (upd["ms"] / 1e3) / 1e9
         update = {"ms_per_step": round(upd["ms"] / args.steps, 4), "GB_per_s": round(gbs, 1),
-                  "frac_hbm_peak": round(gbs / PEAK["hbm_gbs"], 4), "bytes_per_param": 22 if is_bf16 else 20}
+                  "frac_hbm_peak": round(gbs / PEAK["hbm_gbs"], 4), "bytes_per_param": 22 if is_bf16 else 20,
+                  "params_per_step": int(upd["work"] / args.steps / (22 if is_bf16 else 20)),
+                  "note": "layers whose update is not fused into their filter-gradient kernel"}
+    # both Updater protocols over the whole flat parameter buffer, alone
+    # (a copy of the net's buffers, so the step's state is left as it was)
+    updaters = {}
+    wf, gf, vf = net.w_flat.clone(), net.g_flat.clone(), torch.zeros_like(net.v_flat)
+    wbf = net.wb_flat.clone() if net.wb_flat is not None else None
+    nbytes = net.n_params_padded * (22 if wbf is not None else 20)
+    for name, fn in (("sgd_momentum", lambda: singa.sgd_momentum_update(wf, gf, vf, wbf, w.lr, w.momentum,
+                                                                        w.weight_decay)),
+                     ("adagrad", lambda: singa.adagrad_update(wf, gf, vf, wbf, w.lr, 1e-6, w.weight_decay))):
+        for _ in range(3):
+            fn()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(20):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / 20
+        updaters[name] = {"ms": round(ms, 4), "GB_per_s": round(nbytes / (ms / 1e3) / 1e9, 1),
+                          "frac_hbm_peak": round(nbytes / (ms / 1e3) / 1e9 / PEAK["hbm_gbs"], 4),
+                          "params": net.n_params_padded}
+    del wf, gf, vf, wbf
 
     kernels = sorted(({"kernel": n, "launches_per_step": a["launches"] / args.steps,
                        "ms_per_step": round(a["ms"] / args.steps, 4),
@@ -217,12 +253,14 @@ def main():
         "conv_gflop_per_step": round(conv_flops / args.steps / 1e9, 2),
         "conv_ms_per_step": round(conv_ms / args.steps, 4),
         "kernel_ms_per_step": round(kernel_ms / args.steps, 4),
-        "launch": "eager" if args.eager else "hip_graph",
+        "launch": launch,
+        "graph_ms_per_step": None if graph_ms is None else round(graph_ms, 4),
         "eager_ms_per_step": round(eager_ms, 4),
         "traced_eager_ms_per_step": round(traced_ms, 4),
         "loss": loss,
         "roofline": roof,
         "update": update,
+        "updaters_full_buffer": updaters,
         "kernels": kernels[:16],
     }
     if not args.no_cpu_baseline:

@@ -250,6 +250,17 @@ int singa_softmax_ce(singa_dtype dtype, int batch, int classes, const void* logi
 int singa_sgd_momentum_update(size_t n, float* w, const float* g, float* v, uint16_t* w_bf16,
                               float lr, float momentum, float weight_decay, singa_stream stream);
 
+/* Updater (Sec. 4.1.4), the AdaGrad protocol the section names (Duchi, Hazan
+ * and Singer, JMLR 2011, diagonal form): one fused step over n fp32 values,
+ *   g' = g + weight_decay * w;  h = h + g'^2;  w = w - lr * g' / (delta + sqrt(h))
+ * and, if w_bf16 != NULL, w_bf16 = bf16(w) (round to nearest even).
+ *   w, h : updated in place (h, the running sum of squared gradients, starts
+ *          at 0);  g : read.  All four pointers 16-byte aligned.
+ *   delta > 0 (SINGA_ERR_UNSUPPORTED otherwise: the first step divides by
+ *   delta + |g'|), lr >= 0. */
+int singa_adagrad_update(size_t n, float* w, const float* g, float* h, uint16_t* w_bf16,
+                         float lr, float delta, float weight_decay, singa_stream stream);
+
 /* ------------------------------------------------------ per-kernel timing */
 
 /* Kernel timing trace, a profiling aid for the per-iteration timing protocol

@@ -18,7 +18,7 @@ from typing import Dict, List, Optional
 
 import numpy as np
 
-from . import (AVG, MAX, conv_bwd_data, conv_bwd_filter, conv_fwd, fc_bwd, fc_fwd,
+from . import (AVG, MAX, adagrad, conv_bwd_data, conv_bwd_filter, conv_fwd, fc_bwd, fc_fwd,
                pool_bwd, pool_fwd, relu_bwd, relu_fwd, sgd_momentum, softmax_ce)
 
 
@@ -120,13 +120,15 @@ def backward(layers, params: List, acts: Dict, dy_top=None, need_input_grad: boo
 
 def train_one_batch(layers, x, params: List, master: Optional[List] = None, labels=None, dy_top=None,
                     lr: float = 0.0, momentum: float = 0.0, wd: float = 0.0, velocity: Optional[List] = None,
-                    need_input_grad: bool = False, store=None) -> Dict:
+                    need_input_grad: bool = False, store=None, adagrad_delta: Optional[float] = None) -> Dict:
     """Alg. 1 followed by the Updater.  ``params`` are the values the layers
     compute with; ``master`` (default: ``params``) are the values the Updater
     steps (for bf16 compute these are the fp32 master weights).  Returns the
     forward dict, the backward dict and the updated (w, b) and momentum.
     ``store`` rounds stored activations and activation gradients (see
-    ``forward``); parameter gradients and the update stay in fp64."""
+    ``forward``); parameter gradients and the update stay in fp64.  With
+    ``adagrad_delta`` the Updater is AdaGrad (``momentum`` unused) and
+    ``velocity`` holds its sums of squared gradients."""
     acts = forward(layers, x, params, labels=labels, store=store)
     grads = backward(layers, params, acts, dy_top=dy_top, need_input_grad=need_input_grad, store=store)
     master = params if master is None else master
@@ -136,10 +138,14 @@ def train_one_batch(layers, x, params: List, master: Optional[List] = None, labe
         w, b = master[i]
         vw, vb = (None, None) if velocity is None else velocity[i]
         vw = np.zeros(np.shape(w)) if vw is None else vw
-        w2, vw2 = sgd_momentum(w, grads["dw"][name], vw, lr, momentum, wd)
+        def step(p, g, state):
+            if adagrad_delta is not None:
+                return adagrad(p, g, state, lr, adagrad_delta, wd)
+            return sgd_momentum(p, g, state, lr, momentum, wd)
+        w2, vw2 = step(w, grads["dw"][name], vw)
         if b is not None:
             vb = np.zeros(np.shape(b)) if vb is None else vb
-            b2, vb2 = sgd_momentum(b, grads["db"][name], vb, lr, momentum, wd)
+            b2, vb2 = step(b, grads["db"][name], vb)
         else:
             b2 = vb2 = None
         new_params.append((w2, b2))

@@ -587,6 +587,16 @@ int singa_softmax_ce(singa_dtype dtype, int batch, int classes, const void* logi
   return hip_status(launch_softmax_ce(dtype, batch, classes, logits, labels, loss, dlogits, (hipStream_t)stream));
 }
 
+int singa_adagrad_update(size_t n, float* w, const float* g, float* h, uint16_t* w_bf16, float lr, float delta,
+                         float weight_decay, singa_stream stream) {
+  if (n == 0) return SINGA_OK;
+  if (!w || !g || !h) return SINGA_ERR_NULL;
+  if (!aligned_to(w, 16) || !aligned_to(g, 16) || !aligned_to(h, 16) || !aligned_to(w_bf16, 16))
+    return SINGA_ERR_ALIGN;
+  if (!(delta > 0.f) || !(lr >= 0.f)) return SINGA_ERR_UNSUPPORTED;
+  return hip_status(launch_adagrad(n, w, g, h, w_bf16, lr, delta, weight_decay, (hipStream_t)stream));
+}
+
 int singa_sgd_momentum_update(size_t n, float* w, const float* g, float* v, uint16_t* w_bf16, float lr,
                               float momentum, float weight_decay, singa_stream stream) {
   if (n == 0) return SINGA_OK;

@@ -34,6 +34,15 @@ __device__ __forceinline__ void sgd_step(float& w, float& v, float g, float lr, 
   w = w - v;
 }
 
+// One AdaGrad step on one parameter (the Updater protocol Sec. 4.1.4 names;
+// Duchi, Hazan and Singer 2011, diagonal form): h <- h + g'^2 with
+// g' = g + wd w, then w <- w - lr g' / (delta + sqrt(h)).
+__device__ __forceinline__ void adagrad_step(float& w, float& h, float g, float lr, float delta, float wd) {
+  const float gd = fmaf(wd, w, g);
+  h = fmaf(gd, gd, h);
+  w = w - lr * gd / (delta + sqrtf(h));
+}
+
 // Division by a divisor fixed at launch time (Granlund & Montgomery, "Division
 // by invariant integers using multiplication", 1994): for 0 <= n < 2^31,
 // n / d = (umulhi(n, mul) + n) >> shift with shift = ceil(log2 d) and

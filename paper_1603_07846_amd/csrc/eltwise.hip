@@ -521,7 +521,58 @@ __global__ __launch_bounds__(256) void sgd_kernel(size_t n, float* __restrict__ 
   }
 }
 
+// AdaGrad over a flat parameter buffer, laid out like sgd_kernel: 8
+// consecutive parameters per thread, every load issued before the arithmetic.
+__global__ __launch_bounds__(256) void adagrad_kernel(size_t n, float* __restrict__ w, const float* __restrict__ g,
+                                                      float* __restrict__ h, uint16_t* __restrict__ wb, float lr,
+                                                      float delta, float wd) {
+  const size_t n8 = n / 8;
+  const size_t stride = (size_t)gridDim.x * blockDim.x;
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n8; i += stride) {
+    float4 w4[2], g4[2], h4[2];
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      w4[u] = ((const float4*)w)[2 * i + u];
+      g4[u] = ((const float4*)g)[2 * i + u];
+      h4[u] = ((const float4*)h)[2 * i + u];
+    }
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      adagrad_step(w4[u].x, h4[u].x, g4[u].x, lr, delta, wd);
+      adagrad_step(w4[u].y, h4[u].y, g4[u].y, lr, delta, wd);
+      adagrad_step(w4[u].z, h4[u].z, g4[u].z, lr, delta, wd);
+      adagrad_step(w4[u].w, h4[u].w, g4[u].w, lr, delta, wd);
+      ((float4*)h)[2 * i + u] = h4[u];
+      ((float4*)w)[2 * i + u] = w4[u];
+    }
+    if (wb) {
+      uint4 b;
+      b.x = (uint32_t)f32_to_bf16(w4[0].x) | ((uint32_t)f32_to_bf16(w4[0].y) << 16);
+      b.y = (uint32_t)f32_to_bf16(w4[0].z) | ((uint32_t)f32_to_bf16(w4[0].w) << 16);
+      b.z = (uint32_t)f32_to_bf16(w4[1].x) | ((uint32_t)f32_to_bf16(w4[1].y) << 16);
+      b.w = (uint32_t)f32_to_bf16(w4[1].z) | ((uint32_t)f32_to_bf16(w4[1].w) << 16);
+      ((uint4*)wb)[i] = b;
+    }
+  }
+  const size_t t = n8 * 8 + (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t < n) {
+    float wt = w[t], ht = h[t];
+    adagrad_step(wt, ht, g[t], lr, delta, wd);
+    h[t] = ht;
+    w[t] = wt;
+    if (wb) wb[t] = f32_to_bf16(wt);
+  }
+}
+
 }  // namespace
+
+hipError_t launch_adagrad(size_t n, float* w, const float* g, float* h, uint16_t* wb, float lr, float delta,
+                          float wd, hipStream_t st) {
+  const unsigned grid = grid_for(n / 8 + 1, 256, 1u << 20);
+  TraceScope ts("adagrad_kernel", st, (double)n * (20.0 + (wb ? 2.0 : 0.0)), WORK_BYTE);
+  hipLaunchKernelGGL(adagrad_kernel, dim3(grid), dim3(256), 0, st, n, w, g, h, wb, lr, delta, wd);
+  return hipGetLastError();
+}
 
 hipError_t launch_pool_fwd(int dt, int mode, int N, int C, int H, int W, int P, int Q, int kh, int kw, int sh, int sw,
                            int ph, int pw, const void* x, void* y, uint8_t* argmax, int nchw, hipStream_t st) {

@@ -144,6 +144,8 @@ hipError_t launch_relu_fwd(int dt, size_t n, const void* x, void* y, hipStream_t
 hipError_t launch_relu_bwd(int dt, size_t n, const void* y, const void* dy, void* dx, hipStream_t st);
 hipError_t launch_softmax_ce(int dt, int B, int classes, const void* z, const int32_t* labels, float* loss,
                              void* dz, hipStream_t st);
+hipError_t launch_adagrad(size_t n, float* w, const float* g, float* h, uint16_t* wb, float lr, float delta,
+                          float wd, hipStream_t st);
 hipError_t launch_sgd(size_t n, float* w, const float* g, float* v, uint16_t* wb, float lr, float mom, float wd,
                       hipStream_t st);
 

@@ -79,7 +79,7 @@ class ConvLayer(Layer):
         self.relu_src = None  # the ReLU layer feeding this one, whose backward bwd-data folds in
         dev, dt = net.device, net.dtype
         # update fused into the filter-gradient kernel (no workspace needed exactly then)
-        self.fused_update = bool(net.fuse_update and net.wl.update and singa.conv_workspace_bytes(
+        self.fused_update = bool(net.fuse_update and net.wl.update and net.updater == "sgd" and singa.conv_workspace_bytes(
             singa.OP_BWD_FILTER_SGD, dt, self.in_shape, self.w_shape, self.pad, self.stride) == 0)
         self.y = torch.empty(self.out_shape, dtype=dt, device=dev)
         self.dx = torch.empty(self.in_shape, dtype=dt, device=dev)
@@ -203,12 +203,20 @@ class Net:
     """A workload's layer stack on one GPU, with flat parameter buffers."""
 
     def __init__(self, workload: wl.Workload, batch: Optional[int] = None, device="cuda", fuse_update: bool = True,
-                 keep_grads: bool = False, concurrent_wgrad: bool = True):
+                 keep_grads: bool = False, concurrent_wgrad: bool = True, updater: str = "sgd",
+                 adagrad_delta: float = 1e-6):
         """fuse_update: apply the update inside the filter-gradient kernel
         where it can be fused; keep_grads: those layers also store their
         gradients in the flat gradient buffer (for inspection);
         concurrent_wgrad: the other layers' filter gradients run on a second
-        stream, concurrently with the backward-data passes."""
+        stream, concurrently with the backward-data passes; updater: "sgd"
+        (momentum, the workloads' Updater) or "adagrad" (Sec. 4.1.4's named
+        protocol, with the workload's learning rate and weight decay; the
+        momentum buffer holds its sums of squared gradients)."""
+        if updater not in ("sgd", "adagrad"):
+            raise ValueError(updater)
+        self.updater = updater
+        self.adagrad_delta = adagrad_delta
         self.wl = workload
         self.fuse_update = fuse_update
         self.keep_grads = keep_grads
@@ -344,8 +352,12 @@ class Net:
         filter-gradient kernel, over their parts of the flat buffers."""
         for a, e in self.update_ranges:
             wb = self.wb_flat[a:e] if self.wb_flat is not None else None
-            singa.sgd_momentum_update(self.w_flat[a:e], self.g_flat[a:e], self.v_flat[a:e], wb, self.wl.lr,
-                                      self.wl.momentum, self.wl.weight_decay)
+            if self.updater == "adagrad":
+                singa.adagrad_update(self.w_flat[a:e], self.g_flat[a:e], self.v_flat[a:e], wb, self.wl.lr,
+                                     self.adagrad_delta, self.wl.weight_decay)
+            else:
+                singa.sgd_momentum_update(self.w_flat[a:e], self.g_flat[a:e], self.v_flat[a:e], wb, self.wl.lr,
+                                          self.wl.momentum, self.wl.weight_decay)
 
     def train_one_batch(self, x, labels=None, dy_top=None, need_input_grad=False):
         self.forward(x, labels)

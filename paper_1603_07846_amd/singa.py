@@ -33,6 +33,7 @@ EXPORTS = ["singa_strerror", "singa_conv_out_shape", "singa_pool_out_shape", "si
            "singa_conv_fwd", "singa_conv_bwd_data", "singa_conv_bwd_filter", "singa_conv_bwd_filter_sgd",
            "singa_pool_fwd", "singa_pool_bwd",
            "singa_relu_fwd", "singa_relu_bwd", "singa_softmax_ce", "singa_sgd_momentum_update",
+           "singa_adagrad_update",
            "singa_trace_enable", "singa_trace_count", "singa_trace_get"]
 
 
@@ -90,6 +91,8 @@ def _lib():
         lib.singa_relu_fwd.argtypes = [i32, sz, vp, vp, vp]
         lib.singa_relu_bwd.argtypes = [i32, sz, vp, vp, vp, vp]
         lib.singa_softmax_ce.argtypes = [i32, i32, i32, vp, vp, vp, vp, vp]
+        lib.singa_adagrad_update.argtypes = [sz, vp, vp, vp, vp, ctypes.c_float, ctypes.c_float, ctypes.c_float,
+                                             vp]
         lib.singa_sgd_momentum_update.argtypes = [sz, vp, vp, vp, vp, ctypes.c_float, ctypes.c_float,
                                                   ctypes.c_float, vp]
         lib.singa_trace_enable.argtypes = [i32]
@@ -335,6 +338,14 @@ def sgd_momentum_update(w, g, v, w_bf16=None, lr=0.01, momentum=0.9, weight_deca
         w.numel(), _ptr(w), _ptr(g), _ptr(v), _ptr(w_bf16), float(lr), float(momentum), float(weight_decay),
         _stream()))
     return w, v
+
+
+def adagrad_update(w, g, h, w_bf16=None, lr=0.01, delta=1e-6, weight_decay=0.0):
+    """AdaGrad Updater step in place on fp32 w and h (and the bf16 shadow if given)."""
+    _check("singa_adagrad_update", _lib().singa_adagrad_update(
+        w.numel(), _ptr(w), _ptr(g), _ptr(h), _ptr(w_bf16), float(lr), float(delta), float(weight_decay),
+        _stream()))
+    return w, h
 
 
 def trace_enable(on: bool = True):

@@ -139,6 +139,21 @@ def test_softmax_ce_full_size():
     assert rel_l2(dz.float().cpu().numpy(), ref_dz) <= TOL["bf16"]
 
 
+def test_adagrad_full_size():
+    n = 62378344
+    w = wl.random_array((n,), 822, "normal", 0.01)
+    g = wl.random_array((n,), 823, "normal", 1e-3)
+    h = wl.random_array((n,), 824, "uniform01", 1e-6)  # a running sum of squares: non-negative
+    wd, gd, hd = (torch.from_numpy(np.ascontiguousarray(a, np.float32)).cuda() for a in (w, g, h))
+    wb = torch.empty(n, dtype=torch.bfloat16, device="cuda")
+    singa.adagrad_update(wd, gd, hd, wb, 0.01, 1e-6, 5e-4)
+    torch.cuda.synchronize()
+    w1, h1 = oracle.adagrad(w, g, h, 0.01, 1e-6, 5e-4)
+    assert rel_l2(wd.cpu().numpy(), w1) <= TOL["f32"]
+    assert rel_l2(hd.cpu().numpy(), h1) <= TOL["f32"]
+    np.testing.assert_array_equal(wb.cpu().view(torch.int16).numpy().view(np.uint16), wl.bf16_bits(wd.cpu().numpy()))
+
+
 def test_sgd_full_size():
     n = 62378344
     w = wl.random_array((n,), 820, "normal", 0.01)

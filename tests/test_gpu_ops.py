@@ -362,6 +362,35 @@ def test_sgd_momentum(n, shadow):
                                       wl.bf16_bits(wd.cpu().numpy()))
 
 
+@pytest.mark.parametrize("n", [1, 5, 7, 8, 2400, 89578, 1 << 20])
+@pytest.mark.parametrize("shadow", [False, True])
+def test_adagrad(n, shadow):
+    w = wl.random_array((n,), 93, "normal", 0.01)
+    g = wl.random_array((n,), 94, "normal", 1.0)
+    h = np.zeros(n)
+    wd, hd, gd = torch.from_numpy(w).cuda(), torch.zeros(n, device="cuda"), torch.from_numpy(g).cuda()
+    wb = torch.empty(n, dtype=torch.bfloat16, device="cuda") if shadow else None
+    for step in range(3):
+        singa.adagrad_update(wd, gd, hd, wb, lr=0.01, delta=1e-6, weight_decay=5e-4)
+        w, h = oracle.adagrad(w, g, h, 0.01, 1e-6, 5e-4)
+    torch.cuda.synchronize()
+    assert rel_l2(wd.cpu().numpy(), w) <= TOL["f32"]
+    assert rel_l2(hd.cpu().numpy(), h) <= TOL["f32"]
+    if shadow:
+        np.testing.assert_array_equal(wb.cpu().view(torch.int16).numpy().view(np.uint16),
+                                      wl.bf16_bits(wd.cpu().numpy()))
+
+
+def test_adagrad_errors():
+    w = torch.zeros(64, device="cuda")
+    with pytest.raises(singa.SingaError) as e:
+        singa.adagrad_update(w, w, w, delta=0.0)
+    assert e.value.status == -3
+    with pytest.raises(singa.SingaError) as e:
+        singa.adagrad_update(w[1:], w[1:], w[1:])
+    assert e.value.status == -5
+
+
 def test_abi_errors_launch_nothing():
     x = torch.zeros((2, 8, 8, 4), device="cuda")
     w = torch.zeros((4, 3, 3, 4), device="cuda")

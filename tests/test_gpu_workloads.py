@@ -73,10 +73,10 @@ def _oracle_params(inp, dtype):
     return [(p.w, p.b) for p in inp.params]
 
 
-def _run_gpu(w, inp, batch, need_input_grad):
+def _run_gpu(w, inp, batch, need_input_grad, updater="sgd"):
     # keep_grads: the layers with the update fused into their gradient kernel
     # also store the gradient, which the comparison reads
-    net = gnet.Net(w, batch=batch, keep_grads=True)
+    net = gnet.Net(w, batch=batch, keep_grads=True, updater=updater)
     net.load_params(inp.params)
     x = net.to_device_input(inp.x)
     labels = torch.from_numpy(inp.labels).cuda() if inp.labels is not None else None
@@ -86,12 +86,12 @@ def _run_gpu(w, inp, batch, need_input_grad):
     return net, gx
 
 
-def _train_ref(w, inp, need_input_grad):
+def _train_ref(w, inp, need_input_grad, adagrad_delta=None):
     store = oracle.round_bf16 if w.dtype == "bf16" else None
     return onet.train_one_batch(w.layers, inp.x, _oracle_params(inp, w.dtype),
                                 master=[(p.w, p.b) for p in inp.params], labels=inp.labels, dy_top=inp.dy,
                                 lr=w.lr, momentum=w.momentum, wd=w.weight_decay, need_input_grad=need_input_grad,
-                                store=store)
+                                store=store, adagrad_delta=adagrad_delta)
 
 
 def _output_of(acts, layers, i):
@@ -217,6 +217,28 @@ def test_workload2_full():
     ref = _train_ref(w, inp, False)
     _check_free_running(net, ref, w, False)
     assert abs(ref["acts"]["loss"] - np.log(10)) < 1e-2
+
+
+@pytest.mark.parametrize("index,batch", [(2, None)])
+def test_adagrad_training_step(index, batch):
+    """The step with the AdaGrad Updater (Sec. 4.1.4's named protocol):
+    updated weights and the sums of squared gradients against the oracle.
+    The fp32 CIFAR-shaped step at full size, whose decisions match the
+    oracle's: AdaGrad's first step moves every weight by about lr * sign(g)
+    whatever |g| is, so a gradient element near zero whose sign a valid
+    bf16 near-tie decision flipped would move its weight by 2 lr; the bf16
+    Updater kernel is covered at the operator level (62.4M parameters)."""
+    w = wl.WORKLOADS[index]
+    inp = wl.make_inputs(w, batch=batch)
+    net, _ = _run_gpu(w, inp, batch, False, updater="adagrad")
+    assert not any(l.fused_update for l in net.param_layers())
+    ref = _train_ref(w, inp, False, adagrad_delta=net.adagrad_delta)
+    errs, flips = _check_free_running(net, ref, w, False)
+    if flips == 0:
+        for l, (hw, hb) in zip(net.param_layers(), ref["velocity"]):
+            a, _ = l.flat_range
+            h = net.v_flat[a:a + l.w.numel()].view(l.w_shape).cpu().numpy().transpose(0, 3, 1, 2)
+            assert rel_l2(h, hw.reshape(h.shape)) <= TOL[w.dtype], l.name
 
 
 @pytest.mark.parametrize("index", [3, 4, 5])
