@@ -68,6 +68,9 @@ def _load():
         lib.oracle_pool_bwd.argtypes = pool + [_dp, _u8p, _dp]
         lib.oracle_relu_fwd.argtypes = [_i64, _dp, _dp]
         lib.oracle_relu_bwd.argtypes = [_i64, _dp, _dp, _dp]
+        _d = ctypes.c_double
+        lib.oracle_lrn_fwd.argtypes = [_i64, _i64, _i64, _i64, _dp, _i64, _d, _d, _d, _dp]
+        lib.oracle_lrn_bwd.argtypes = [_i64, _i64, _i64, _i64, _dp, _dp, _i64, _d, _d, _d, _dp]
         lib.oracle_softmax_ce.argtypes = [_i64, _i64, _dp, _i32p, _dp]
         lib.oracle_softmax_ce.restype = ctypes.c_double
         lib.oracle_round_bf16.argtypes = [_i64, _dp]
@@ -228,6 +231,26 @@ def relu_fwd(x) -> np.ndarray:
     y = np.empty_like(x)
     _load().oracle_relu_fwd(x.size, _ptr(x), _ptr(y))
     return y
+
+
+def lrn_fwd(x, size=5, alpha=1e-4, beta=0.75, k=1.0) -> np.ndarray:
+    """Local response normalization across channels (NCHW), Caffe's form:
+    y = x * (k + alpha/size * sum of x^2 over the channel window)^-beta."""
+    x = _f64(x)
+    y = np.empty_like(x)
+    N, C, H, W = x.shape
+    _load().oracle_lrn_fwd(N, C, H, W, _ptr(x), int(size), float(alpha), float(beta), float(k), _ptr(y))
+    return y
+
+
+def lrn_bwd(x, dy, size=5, alpha=1e-4, beta=0.75, k=1.0) -> np.ndarray:
+    """Gradient of sum(dy * lrn_fwd(x)) with respect to x."""
+    x, dy = _f64(x), _f64(dy)
+    dx = np.empty_like(x)
+    N, C, H, W = x.shape
+    _load().oracle_lrn_bwd(N, C, H, W, _ptr(x), _ptr(dy), int(size), float(alpha), float(beta), float(k),
+                           _ptr(dx))
+    return dx
 
 
 def relu_bwd(y, dy) -> np.ndarray:

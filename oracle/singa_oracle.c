@@ -394,6 +394,65 @@ void oracle_relu_bwd(int64_t n, const double* y, const double* dy, double* dx)
         dx[i] = y[i] > 0.0 ? dy[i] : 0.0;
 }
 
+/* ------------------------------------------------- local response norm */
+
+/* Channels c' of the window around c: |c' - c| <= size / 2, inside [0, C). */
+static double lrn_scale(const double* x, int64_t C, int64_t HW, int64_t c, int64_t size,
+                        double alpha, double k)
+{
+    int64_t lo = c - size / 2, hi = c + (size - 1) / 2;
+    double s = 0.0;
+    if (lo < 0) lo = 0;
+    if (hi > C - 1) hi = C - 1;
+    for (int64_t j = lo; j <= hi; ++j) {
+        double v = x[j * HW];
+        s += v * v;
+    }
+    return k + alpha / (double)size * s;
+}
+
+void oracle_lrn_fwd(int64_t N, int64_t C, int64_t H, int64_t W, const double* x,
+                    int64_t size, double alpha, double beta, double k, double* y)
+{
+    const int64_t HW = H * W;
+    #pragma omp parallel for collapse(2) schedule(static)
+    for (int64_t n = 0; n < N; ++n)
+        for (int64_t c = 0; c < C; ++c)
+            for (int64_t p = 0; p < HW; ++p) {
+                const double* xp = x + n * C * HW + p;
+                double sc = lrn_scale(xp, C, HW, c, size, alpha, k);
+                y[(n * C + c) * HW + p] = xp[c * HW] * pow(sc, -beta);
+            }
+}
+
+/* dx[c] = dy[c] s[c]^-beta - (2 alpha beta / size) x[c]
+ *         * sum over the channels j whose window holds c of dy[j] x[j] s[j]^(-beta-1),
+ * the derivative of y[j] = x[j] s[j]^-beta, s[j] = k + alpha/size sum_{i in window(j)} x[i]^2. */
+void oracle_lrn_bwd(int64_t N, int64_t C, int64_t H, int64_t W, const double* x, const double* dy,
+                    int64_t size, double alpha, double beta, double k, double* dx)
+{
+    const int64_t HW = H * W;
+    #pragma omp parallel for collapse(2) schedule(static)
+    for (int64_t n = 0; n < N; ++n)
+        for (int64_t c = 0; c < C; ++c)
+            for (int64_t p = 0; p < HW; ++p) {
+                const double* xp = x + n * C * HW + p;
+                const double* dyp = dy + n * C * HW + p;
+                double sc = lrn_scale(xp, C, HW, c, size, alpha, k);
+                double acc = 0.0;
+                /* j's window holds c when j - size/2 <= c <= j + (size-1)/2 */
+                int64_t lo = c - (size - 1) / 2, hi = c + size / 2;
+                if (lo < 0) lo = 0;
+                if (hi > C - 1) hi = C - 1;
+                for (int64_t j = lo; j <= hi; ++j) {
+                    double sj = lrn_scale(xp, C, HW, j, size, alpha, k);
+                    acc += dyp[j * HW] * xp[j * HW] * pow(sj, -beta - 1.0);
+                }
+                dx[(n * C + c) * HW + p] = dyp[c * HW] * pow(sc, -beta)
+                                           - 2.0 * alpha * beta / (double)size * xp[c * HW] * acc;
+            }
+}
+
 /* ------------------------------------------------------ softmax + x-entropy */
 
 double oracle_softmax_ce(int64_t B, int64_t classes, const double* z,

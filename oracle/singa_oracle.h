@@ -121,6 +121,17 @@ void oracle_pool_bwd(int mode, int64_t N, int64_t C, int64_t H, int64_t W,
 void oracle_relu_fwd(int64_t n, const double* x, double* y);
 void oracle_relu_bwd(int64_t n, const double* y, const double* dy, double* dx);
 
+/* Local response normalization across channels (the layer of Sec. 5.4.1
+ * that the paper's GPU AlexNet leaves out), with Caffe's conventions as for
+ * convolution and pooling (Sec. 6.2.1), NCHW:
+ *   s[n,c,h,w] = k + alpha/size * sum_{c' in [c - size/2, c + (size-1)/2] cap [0, C)} x[n,c',h,w]^2
+ *   y[n,c,h,w] = x[n,c,h,w] * s[n,c,h,w]^-beta
+ * lrn_bwd: dx = the gradient of sum(dy * y) with respect to x. */
+void oracle_lrn_fwd(int64_t N, int64_t C, int64_t H, int64_t W, const double* x,
+                    int64_t size, double alpha, double beta, double k, double* y);
+void oracle_lrn_bwd(int64_t N, int64_t C, int64_t H, int64_t W, const double* x, const double* dy,
+                    int64_t size, double alpha, double beta, double k, double* dx);
+
 /* Softmax cross-entropy loss layer (Sec. 2.1, Table 2 and Sec. 4.2.3 name
  * the cross-entropy loss and the softmax loss layer), mean over the batch:
  *   loss = (1/B) sum_n ( log sum_j exp(z[n,j]) - z[n, label[n]] )

@@ -491,3 +491,51 @@ def test_sgd_momentum_against_torch_optim():
         opt.step()
         w, v = oracle.sgd_momentum(w, g, v, 0.01, 0.9, 5e-4)
         np.testing.assert_allclose(w, tw.detach().numpy(), rtol=1e-13, atol=1e-15)
+
+
+# ------------------------------------------------------------------ LRN
+# Local response normalization across channels (Caffe's form, the reading of
+# the layer Sec. 5.4.1 names): pinned by torch's local_response_norm and its
+# autograd in float64, closed forms, and finite differences.
+
+@pytest.mark.parametrize("shape,size", [((2, 7, 3, 4), 5), ((1, 3, 2, 2), 5), ((2, 8, 2, 3), 4), ((1, 6, 1, 1), 3),
+                                        ((1, 1, 3, 3), 1)])
+def test_lrn_against_torch(shape, size):
+    rng = _rng(80)
+    x = rng.standard_normal(shape) * 3.0
+    dy = rng.standard_normal(shape)
+    alpha, beta, k = 0.3, 0.75, 1.5
+    tx = torch.tensor(x, requires_grad=True)
+    ty = torch.nn.functional.local_response_norm(tx, size, alpha=alpha, beta=beta, k=k)
+    ty.backward(torch.tensor(dy))
+    np.testing.assert_allclose(oracle.lrn_fwd(x, size, alpha, beta, k), ty.detach().numpy(), rtol=1e-12, atol=1e-14)
+    np.testing.assert_allclose(oracle.lrn_bwd(x, dy, size, alpha, beta, k), tx.grad.numpy(), rtol=1e-11, atol=1e-13)
+
+
+def test_lrn_closed_forms():
+    rng = _rng(81)
+    x = rng.standard_normal((2, 5, 3, 3))
+    dy = rng.standard_normal(x.shape)
+    # alpha = 0: a constant scale k^-beta
+    np.testing.assert_allclose(oracle.lrn_fwd(x, 5, 0.0, 0.75, 2.0), x * 2.0 ** -0.75, rtol=1e-15)
+    np.testing.assert_allclose(oracle.lrn_bwd(x, dy, 5, 0.0, 0.75, 2.0), dy * 2.0 ** -0.75, rtol=1e-15)
+    # one channel in the window: y = x (k + alpha x^2)^-beta, dy/dx = s^-beta - 2 alpha beta x^2 s^(-beta-1)
+    s = 1.0 + 0.5 * x * x
+    np.testing.assert_allclose(oracle.lrn_fwd(x, 1, 0.5, 0.75, 1.0), x * s ** -0.75, rtol=1e-14)
+    np.testing.assert_allclose(oracle.lrn_bwd(x, dy, 1, 0.5, 0.75, 1.0),
+                               dy * (s ** -0.75 - 2 * 0.5 * 0.75 * x * x * s ** -1.75), rtol=1e-13)
+
+
+def test_lrn_finite_differences():
+    rng = _rng(82)
+    x = rng.standard_normal((1, 6, 2, 2)) * 2.0
+    dy = rng.standard_normal(x.shape)
+    args = (5, 0.4, 0.75, 1.0)
+    dx = oracle.lrn_bwd(x, dy, *args)
+    eps = 1e-6
+    for idx in [(0, 0, 0, 0), (0, 2, 1, 0), (0, 5, 1, 1), (0, 3, 0, 1)]:
+        xp, xm = x.copy(), x.copy()
+        xp[idx] += eps
+        xm[idx] -= eps
+        fd = (np.sum(dy * oracle.lrn_fwd(xp, *args)) - np.sum(dy * oracle.lrn_fwd(xm, *args))) / (2 * eps)
+        assert abs(fd - dx[idx]) <= 1e-7 * max(1.0, abs(fd)), (idx, fd, dx[idx])
