@@ -224,6 +224,33 @@ def main():
                           "frac_hbm_peak": round(nbytes / (ms / 1e3) / 1e9 / PEAK["hbm_gbs"], 4),
                           "params": net.n_params_padded}
     del wf, gf, vf, wbf
+    # local response normalization (not part of this step: the paper's GPU
+    # AlexNet leaves it out) at the two AlexNet positions, batch 256, alone
+    lrn = {}
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(1603078465)
+    dt_t = torch.bfloat16 if is_bf16 else torch.float32
+    es = 2 if is_bf16 else 4
+    for name, (C, H) in (("after_conv1", (96, 55)), ("after_conv2", (256, 27))):
+        xl = torch.randn((net.batch, H, H, C), device=dev, generator=gen).relu_().to(dt_t)
+        dyl = torch.randn((net.batch, H, H, C), device=dev, generator=gen).to(dt_t)
+        yl, dxl = torch.empty_like(xl), torch.empty_like(xl)
+        res = {}
+        for kind, fn, nb in (("fwd", lambda: singa.lrn_fwd(xl, 5, 1e-4, 0.75, 1.0, out=yl), 2 * es),
+                             ("bwd", lambda: singa.lrn_bwd(xl, dyl, 5, 1e-4, 0.75, 1.0, out=dxl), 3 * es)):
+            for _ in range(3):
+                fn()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(20):
+                fn()
+            e1.record()
+            torch.cuda.synchronize()
+            ms = e0.elapsed_time(e1) / 20
+            gbs = xl.numel() * nb / (ms / 1e3) / 1e9
+            res[kind] = {"ms": round(ms, 4), "GB_per_s": round(gbs, 1), "frac_hbm_peak": round(gbs / PEAK["hbm_gbs"], 4)}
+        lrn[name] = dict(res, shape=[net.batch, C, H, H])
+        del xl, dyl, yl, dxl
 
     kernels = sorted(({"kernel": n, "launches_per_step": a["launches"] / args.steps,
                        "ms_per_step": round(a["ms"] / args.steps, 4),
@@ -261,6 +288,7 @@ def main():
         "roofline": roof,
         "update": update,
         "updaters_full_buffer": updaters,
+        "lrn_alone": lrn,
         "kernels": kernels[:16],
     }
     if not args.no_cpu_baseline:

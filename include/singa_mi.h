@@ -78,6 +78,9 @@ typedef struct { int k, c, r, s; } singa_filter4;
 typedef struct { int pad_h, pad_w, stride_h, stride_w; } singa_conv_desc;
 /* Pooling window; ceil_mode != 0 rounds the output extent up (Caffe's rule). */
 typedef struct { int mode, kh, kw, stride_h, stride_w, pad_h, pad_w, ceil_mode; } singa_pool_desc;
+/* Local response normalization across channels: window of `size` channels,
+ * s = k + alpha/size * (sum of squares over the window), y = x * s^-beta. */
+typedef struct { int size; float alpha, beta, k; } singa_lrn_desc;
 
 typedef void* singa_stream; /* a hipStream_t */
 
@@ -225,6 +228,25 @@ int singa_relu_fwd(singa_dtype dtype, size_t n, const void* x, void* y, singa_st
 /* dx = y > 0 ? dy : 0 over n elements (in place allowed: dx == dy). */
 int singa_relu_bwd(singa_dtype dtype, size_t n, const void* y, const void* dy, void* dx,
                    singa_stream stream);
+
+/* ---------------------------------------------- local response normalization */
+
+/* Local response normalization across channels, the layer Sec. 5.4.1 names
+ * beside pooling (the paper's GPU AlexNet leaves it out), in Caffe's form as
+ * SINGA's convolution and pooling are (Sec. 6.2.1):
+ *   s[n,c,h,w] = k + alpha/size * sum_{c'} x[n,c',h,w]^2 over the channels
+ *                c' in [c - size/2, c + (size-1)/2] that exist (in [0, C))
+ *   y = x * s^-beta
+ * singa_lrn_bwd: dx = the gradient of sum(dy * y) with respect to x,
+ *   dx[c] = dy[c] s[c]^-beta - (2 alpha beta / size) x[c]
+ *           * sum over the channels j whose window holds c of dy[j] x[j] s[j]^(-beta-1)
+ * (s recomputed from x).  fp32 arithmetic for both dtypes.
+ *   x_ptr, dy_ptr : dtype, shape *x in `layout` (read);  y_ptr / dx_ptr (written)
+ *   d: size >= 1, alpha >= 0, k > 0 (SINGA_ERR_UNSUPPORTED otherwise). */
+int singa_lrn_fwd(singa_dtype dtype, singa_layout layout, const singa_shape4* x, const void* x_ptr,
+                  const singa_lrn_desc* d, void* y_ptr, singa_stream stream);
+int singa_lrn_bwd(singa_dtype dtype, singa_layout layout, const singa_shape4* x, const void* x_ptr,
+                  const void* dy_ptr, const singa_lrn_desc* d, void* dx_ptr, singa_stream stream);
 
 /* ------------------------------------------------------------ softmax loss */
 

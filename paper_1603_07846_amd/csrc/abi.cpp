@@ -587,6 +587,37 @@ int singa_softmax_ce(singa_dtype dtype, int batch, int classes, const void* logi
   return hip_status(launch_softmax_ce(dtype, batch, classes, logits, labels, loss, dlogits, (hipStream_t)stream));
 }
 
+static int lrn_check(singa_dtype dtype, singa_layout layout, const singa_shape4* x, const singa_lrn_desc* d) {
+  if (!x || !d) return SINGA_ERR_NULL;
+  if (!dtype_ok(dtype) || !layout_ok(layout)) return SINGA_ERR_UNSUPPORTED;
+  if (x->n <= 0 || x->c <= 0 || x->h <= 0 || x->w <= 0) return SINGA_ERR_SHAPE;
+  if (!fits_i32((long long)x->n * x->c * x->h * x->w)) return SINGA_ERR_UNSUPPORTED;
+  if (d->size < 1 || !(d->alpha >= 0.f) || !(d->k > 0.f) || !(d->beta == d->beta)) return SINGA_ERR_UNSUPPORTED;
+  return SINGA_OK;
+}
+
+int singa_lrn_fwd(singa_dtype dtype, singa_layout layout, const singa_shape4* x, const void* x_ptr,
+                  const singa_lrn_desc* d, void* y_ptr, singa_stream stream) {
+  int rc = lrn_check(dtype, layout, x, d);
+  if (rc != SINGA_OK) return rc;
+  if (!x_ptr || !y_ptr) return SINGA_ERR_NULL;
+  const size_t es = dt_size(dtype);
+  if (!aligned_to(x_ptr, es) || !aligned_to(y_ptr, es)) return SINGA_ERR_ALIGN;
+  return hip_status(launch_lrn(dtype, 0, x->n, x->c, x->h * x->w, d->size, d->alpha, d->beta, d->k, x_ptr, nullptr,
+                               y_ptr, layout == SINGA_NCHW, (hipStream_t)stream));
+}
+
+int singa_lrn_bwd(singa_dtype dtype, singa_layout layout, const singa_shape4* x, const void* x_ptr,
+                  const void* dy_ptr, const singa_lrn_desc* d, void* dx_ptr, singa_stream stream) {
+  int rc = lrn_check(dtype, layout, x, d);
+  if (rc != SINGA_OK) return rc;
+  if (!x_ptr || !dy_ptr || !dx_ptr) return SINGA_ERR_NULL;
+  const size_t es = dt_size(dtype);
+  if (!aligned_to(x_ptr, es) || !aligned_to(dy_ptr, es) || !aligned_to(dx_ptr, es)) return SINGA_ERR_ALIGN;
+  return hip_status(launch_lrn(dtype, 1, x->n, x->c, x->h * x->w, d->size, d->alpha, d->beta, d->k, x_ptr, dy_ptr,
+                               dx_ptr, layout == SINGA_NCHW, (hipStream_t)stream));
+}
+
 int singa_adagrad_update(size_t n, float* w, const float* g, float* h, uint16_t* w_bf16, float lr, float delta,
                          float weight_decay, singa_stream stream) {
   if (n == 0) return SINGA_OK;

@@ -564,7 +564,156 @@ __global__ __launch_bounds__(256) void adagrad_kernel(size_t n, float* __restric
   }
 }
 
+// ------------------------------------------------- local response norm
+//
+// Across channels, Caffe's form: s = k + alpha/size * (sum of x^2 over the
+// channels [c - size/2, c + (size-1)/2] that exist), y = x s^-beta;
+// backward dx[c] = dy[c] s[c]^-beta - (2 alpha beta / size) x[c] *
+// sum over the channels j whose window holds c of dy[j] x[j] s[j]^(-beta-1),
+// with s recomputed from x.  All in fp32.
+struct LrnGeom {
+  int N, C, HW, size;
+  float alpha, beta, k;
+};
+
+__device__ __forceinline__ float pow_neg(float s, float e) { return exp2f(-e * log2f(s)); }  // s^-e, s > 0
+
+// One element per thread, any layout: channel stride cs (1 for NHWC, HW for NCHW).
+template <typename T, bool NCHW, bool BWD>
+__global__ __launch_bounds__(256) void lrn_kernel(LrnGeom g, const T* __restrict__ x, const T* __restrict__ dy,
+                                                  T* __restrict__ out, long total) {
+  const long cs = NCHW ? g.HW : 1;
+  for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += (long)gridDim.x * blockDim.x) {
+    int c;
+    long base;  // element (n, channel 0, p)
+    if (NCHW) {
+      const long n = i / ((long)g.C * g.HW), r = i - n * g.C * g.HW;
+      c = (int)(r / g.HW);
+      base = n * g.C * g.HW + (r - (long)c * g.HW);
+    } else {
+      c = (int)(i % g.C);
+      base = i - c;
+    }
+    auto scale = [&](int j) {
+      const int lo = max(j - g.size / 2, 0), hi = min(j + (g.size - 1) / 2, g.C - 1);
+      float acc = 0.f;
+      for (int t = lo; t <= hi; ++t) {
+        const float v = ld_f<T>(x + base + t * cs);
+        acc = fmaf(v, v, acc);
+      }
+      return fmaf(g.alpha / (float)g.size, acc, g.k);
+    };
+    const float xc = ld_f<T>(x + base + c * cs);
+    if (!BWD) {
+      st_f<T>(out + i, xc * pow_neg(scale(c), g.beta));
+    } else {
+      const int lo = max(c - (g.size - 1) / 2, 0), hi = min(c + g.size / 2, g.C - 1);
+      float acc = 0.f;
+      for (int j = lo; j <= hi; ++j)
+        acc += ld_f<T>(dy + base + j * cs) * ld_f<T>(x + base + j * cs) * pow_neg(scale(j), g.beta + 1.f);
+      const float r = ld_f<T>(dy + i) * pow_neg(scale(c), g.beta) - 2.f * g.alpha * g.beta / (float)g.size * xc * acc;
+      st_f<T>(out + i, r);
+    }
+  }
+}
+
+// NHWC, VEC channels (16 bytes) per thread: the chunk and its two neighbours
+// are loaded (zeros past the ends of the channel axis, which add nothing to
+// a sum of squares), so every window the chunk needs is in registers.  The
+// window SIZE is a compile-time constant (3 or 5), so all register indices
+// are static.
+template <typename T, int VEC, bool BWD, int SIZE>
+__global__ __launch_bounds__(256) void lrn_vec_kernel(LrnGeom g, const T* __restrict__ x, const T* __restrict__ dy,
+                                                      T* __restrict__ out, long chunks) {
+  const int CV = g.C / VEC;
+  union U { uint4 u; T e[VEC]; };
+  for (long t = (long)blockIdx.x * blockDim.x + threadIdx.x; t < chunks; t += (long)gridDim.x * blockDim.x) {
+    const int cv = (int)(t % CV);
+    const long pix = t / CV;
+    const T* xp = x + pix * g.C;
+    float xv[3 * VEC], dv[3 * VEC];
+#pragma unroll
+    for (int h = 0; h < 3; ++h) {
+      const int q = cv - 1 + h;
+      U a, d;
+      a.u = (q >= 0 && q < CV) ? *(const uint4*)(xp + q * VEC) : make_uint4(0u, 0u, 0u, 0u);
+      if (BWD) d.u = (q >= 0 && q < CV) ? *(const uint4*)(dy + pix * g.C + q * VEC) : make_uint4(0u, 0u, 0u, 0u);
+#pragma unroll
+      for (int j = 0; j < VEC; ++j) {
+        xv[h * VEC + j] = ld_f<T>(&a.e[j]);
+        dv[h * VEC + j] = BWD ? ld_f<T>(&d.e[j]) : 0.f;
+      }
+    }
+    const float an = g.alpha / (float)SIZE;
+    auto scale = [&](int r) {  // r: index into xv
+      float acc = 0.f;
+#pragma unroll
+      for (int d = -(SIZE / 2); d <= (SIZE - 1) / 2; ++d) acc = fmaf(xv[r + d], xv[r + d], acc);
+      return fmaf(an, acc, g.k);
+    };
+    U o;
+    if (!BWD) {
+#pragma unroll
+      for (int j = 0; j < VEC; ++j) st_f<T>(&o.e[j], xv[VEC + j] * pow_neg(scale(VEC + j), g.beta));
+    } else {
+      // q[r] = dy[r] x[r] s[r]^(-beta-1) for the channels some window of the chunk needs
+      constexpr int lo = VEC - (SIZE - 1) / 2, hi = 2 * VEC - 1 + SIZE / 2;
+      float q[3 * VEC];
+#pragma unroll
+      for (int r = 0; r < 3 * VEC; ++r)
+        q[r] = (r >= lo && r <= hi) ? dv[r] * xv[r] * pow_neg(scale(r), g.beta + 1.f) : 0.f;
+      const float c2 = 2.f * g.alpha * g.beta / (float)SIZE;
+#pragma unroll
+      for (int j = 0; j < VEC; ++j) {
+        const int r = VEC + j;
+        float acc = 0.f;
+#pragma unroll
+        for (int d = -((SIZE - 1) / 2); d <= SIZE / 2; ++d) acc += q[r + d];
+        st_f<T>(&o.e[j], dv[r] * pow_neg(scale(r), g.beta) - c2 * xv[r] * acc);
+      }
+    }
+    *(uint4*)(out + pix * g.C + cv * VEC) = o.u;
+  }
+}
+
 }  // namespace
+
+hipError_t launch_lrn(int dt, int bwd, int N, int C, int HW, int size, float alpha, float beta, float k,
+                      const void* x, const void* dy, void* out, int nchw, hipStream_t st) {
+  LrnGeom g{N, C, HW, size, alpha, beta, k};
+  const long total = (long)N * C * HW;
+  const int vec = dt == BF16 ? 8 : 4;
+  const bool v = !nchw && C % vec == 0 && (uintptr_t)x % 16 == 0 && (uintptr_t)out % 16 == 0 &&
+                 (uintptr_t)dy % 16 == 0 && (size == 3 || size == 5);
+  TraceScope ts(bwd ? "lrn_bwd_kernel" : "lrn_fwd_kernel", st, (double)total * dt_size(dt) * (bwd ? 3 : 2),
+                WORK_BYTE);
+  if (v) {
+    const long chunks = total / vec;
+    const unsigned grid = grid_for((size_t)chunks);
+#define LRN_VEC(T, VV, B, Z)                                                                                   \
+  hipLaunchKernelGGL((lrn_vec_kernel<T, VV, B, Z>), dim3(grid), dim3(256), 0, st, g, (const T*)x, (const T*)dy, \
+                     (T*)out, chunks)
+#define LRN_VEC_SIZE(T, VV, B) \
+  if (size == 5) LRN_VEC(T, VV, B, 5); else LRN_VEC(T, VV, B, 3);
+    if (dt == BF16) { if (bwd) { LRN_VEC_SIZE(bf16_t, 8, true) } else { LRN_VEC_SIZE(bf16_t, 8, false) } }
+    else { if (bwd) { LRN_VEC_SIZE(float, 4, true) } else { LRN_VEC_SIZE(float, 4, false) } }
+#undef LRN_VEC_SIZE
+#undef LRN_VEC
+    return hipGetLastError();
+  }
+  const unsigned grid = grid_for((size_t)total);
+#define LRN_EL(T, L, B) \
+  hipLaunchKernelGGL((lrn_kernel<T, L, B>), dim3(grid), dim3(256), 0, st, g, (const T*)x, (const T*)dy, (T*)out, total)
+  if (dt == BF16) {
+    if (nchw) { if (bwd) LRN_EL(bf16_t, true, true); else LRN_EL(bf16_t, true, false); }
+    else { if (bwd) LRN_EL(bf16_t, false, true); else LRN_EL(bf16_t, false, false); }
+  } else {
+    if (nchw) { if (bwd) LRN_EL(float, true, true); else LRN_EL(float, true, false); }
+    else { if (bwd) LRN_EL(float, false, true); else LRN_EL(float, false, false); }
+  }
+#undef LRN_EL
+  return hipGetLastError();
+}
 
 hipError_t launch_adagrad(size_t n, float* w, const float* g, float* h, uint16_t* wb, float lr, float delta,
                           float wd, hipStream_t st) {

@@ -142,6 +142,11 @@ hipError_t launch_pool_bwd(int dt, int mode, int N, int C, int H, int W, int P, 
                            void* dx, int nchw, hipStream_t st);
 hipError_t launch_relu_fwd(int dt, size_t n, const void* x, void* y, hipStream_t st);
 hipError_t launch_relu_bwd(int dt, size_t n, const void* y, const void* dy, void* dx, hipStream_t st);
+
+// Local response normalization across channels (bwd = 0: y = lrn(x) into
+// out; bwd = 1: dx into out from x and dy), N x C x HW elements, NHWC or NCHW.
+hipError_t launch_lrn(int dt, int bwd, int N, int C, int HW, int size, float alpha, float beta, float k,
+                      const void* x, const void* dy, void* out, int nchw, hipStream_t st);
 hipError_t launch_softmax_ce(int dt, int B, int classes, const void* z, const int32_t* labels, float* loss,
                              void* dz, hipStream_t st);
 hipError_t launch_adagrad(size_t n, float* w, const float* g, float* h, uint16_t* wb, float lr, float delta,

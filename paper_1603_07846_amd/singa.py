@@ -33,8 +33,12 @@ EXPORTS = ["singa_strerror", "singa_conv_out_shape", "singa_pool_out_shape", "si
            "singa_conv_fwd", "singa_conv_bwd_data", "singa_conv_bwd_filter", "singa_conv_bwd_filter_sgd",
            "singa_pool_fwd", "singa_pool_bwd",
            "singa_relu_fwd", "singa_relu_bwd", "singa_softmax_ce", "singa_sgd_momentum_update",
-           "singa_adagrad_update",
+           "singa_adagrad_update", "singa_lrn_fwd", "singa_lrn_bwd",
            "singa_trace_enable", "singa_trace_count", "singa_trace_get"]
+
+
+class LrnDesc(ctypes.Structure):
+    _fields_ = [("size", ctypes.c_int), ("alpha", ctypes.c_float), ("beta", ctypes.c_float), ("k", ctypes.c_float)]
 
 
 class Shape4(ctypes.Structure):
@@ -91,6 +95,9 @@ def _lib():
         lib.singa_relu_fwd.argtypes = [i32, sz, vp, vp, vp]
         lib.singa_relu_bwd.argtypes = [i32, sz, vp, vp, vp, vp]
         lib.singa_softmax_ce.argtypes = [i32, i32, i32, vp, vp, vp, vp, vp]
+        LD = ctypes.POINTER(LrnDesc)
+        lib.singa_lrn_fwd.argtypes = [i32, i32, S4, vp, LD, vp, vp]
+        lib.singa_lrn_bwd.argtypes = [i32, i32, S4, vp, vp, LD, vp, vp]
         lib.singa_adagrad_update.argtypes = [sz, vp, vp, vp, vp, ctypes.c_float, ctypes.c_float, ctypes.c_float,
                                              vp]
         lib.singa_sgd_momentum_update.argtypes = [sz, vp, vp, vp, vp, ctypes.c_float, ctypes.c_float,
@@ -338,6 +345,26 @@ def sgd_momentum_update(w, g, v, w_bf16=None, lr=0.01, momentum=0.9, weight_deca
         w.numel(), _ptr(w), _ptr(g), _ptr(v), _ptr(w_bf16), float(lr), float(momentum), float(weight_decay),
         _stream()))
     return w, v
+
+
+def lrn_fwd(x, size=5, alpha=1e-4, beta=0.75, k=1.0, layout="NHWC", out=None):
+    """Local response normalization across channels (Caffe's form)."""
+    lay = _layout(layout)
+    y = torch.empty_like(x) if out is None else out
+    _check("singa_lrn_fwd", _lib().singa_lrn_fwd(
+        _dt(x), lay, ctypes.byref(_act_shape4(x.shape, lay)), _ptr(x),
+        ctypes.byref(LrnDesc(int(size), float(alpha), float(beta), float(k))), _ptr(y), _stream()))
+    return y
+
+
+def lrn_bwd(x, dy, size=5, alpha=1e-4, beta=0.75, k=1.0, layout="NHWC", out=None):
+    """Gradient of sum(dy * lrn_fwd(x)) with respect to x."""
+    lay = _layout(layout)
+    dx = torch.empty_like(x) if out is None else out
+    _check("singa_lrn_bwd", _lib().singa_lrn_bwd(
+        _dt(x), lay, ctypes.byref(_act_shape4(x.shape, lay)), _ptr(x), _ptr(dy),
+        ctypes.byref(LrnDesc(int(size), float(alpha), float(beta), float(k))), _ptr(dx), _stream()))
+    return dx
 
 
 def adagrad_update(w, g, h, w_bf16=None, lr=0.01, delta=1e-6, weight_decay=0.0):

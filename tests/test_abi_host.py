@@ -24,7 +24,7 @@ def _declared():
 
 def test_every_declared_symbol_is_exported():
     names = _declared()
-    assert len(names) == 18
+    assert len(names) == 20
     lib = ctypes.CDLL(singa.lib()._name)
     for n in names:
         assert hasattr(lib, n), n

@@ -534,3 +534,45 @@ def test_conv_bwd_filter_sgd_matches_gradient_then_update(case):
     ref_w, ref_v = oracle.sgd_momentum(w_np, ref_dw, v_np, lr, mom, wd)
     assert rel_l2(filt_to_kcrs(wr, layout), ref_w) <= TOL["f32"]
     assert rel_l2(filt_to_kcrs(vr, layout), ref_v) <= TOL["f32"]
+
+
+# local response normalization: (N, C, H, W, size); sizes 3 and 5 with C a
+# multiple of the vector width take the vector kernel (NHWC), the rest the
+# element-wise one
+LRN_CASES = [(2, 96, 13, 13, 5), (3, 64, 7, 9, 3), (2, 16, 5, 5, 5), (2, 8, 4, 4, 5), (1, 3, 6, 6, 5),
+             (2, 12, 5, 4, 4), (2, 20, 3, 3, 7), (1, 5, 2, 2, 9)]
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("layout", ["NHWC", "NCHW"])
+@pytest.mark.parametrize("case", LRN_CASES, ids=_ids(LRN_CASES))
+def test_lrn(case, layout, dt):
+    N, C, H, W, size = case
+    x = wl.random_array((N, C, H, W), 110, "normal", 4.0, dt)
+    dy = wl.random_array((N, C, H, W), 111, "normal", 1.0, dt)
+    args = (size, 2e-2, 0.75, 1.0)  # alpha large enough that the window matters
+    y = singa.lrn_fwd(nchw_to_dev(x, dt, layout), *args, layout=layout)
+    dx = singa.lrn_bwd(nchw_to_dev(x, dt, layout), nchw_to_dev(dy, dt, layout), *args, layout=layout)
+    torch.cuda.synchronize()
+    assert rel_l2(dev_to_nchw(y, layout), oracle.lrn_fwd(x, *args)) <= TOL[dt], case
+    assert rel_l2(dev_to_nchw(dx, layout), oracle.lrn_bwd(x, dy, *args)) <= TOL[dt], case
+
+
+def test_lrn_alexnet_shapes():
+    # the two layers of AlexNet (after conv1 and conv2), Krizhevsky's constants in Caffe's form
+    for C, H in ((96, 55), (256, 27)):
+        x = np.maximum(wl.random_array((4, C, H, H), 112, "normal", 1.0, "bf16"), 0.0)
+        dy = wl.random_array((4, C, H, H), 113, "normal", 1.0, "bf16")
+        y = singa.lrn_fwd(nchw_to_dev(x, "bf16"), 5, 1e-4, 0.75, 1.0)
+        dx = singa.lrn_bwd(nchw_to_dev(x, "bf16"), nchw_to_dev(dy, "bf16"), 5, 1e-4, 0.75, 1.0)
+        torch.cuda.synchronize()
+        assert rel_l2(dev_to_nchw(y), oracle.lrn_fwd(x, 5, 1e-4, 0.75, 1.0)) <= TOL["bf16"]
+        assert rel_l2(dev_to_nchw(dx), oracle.lrn_bwd(x, dy, 5, 1e-4, 0.75, 1.0)) <= TOL["bf16"]
+
+
+def test_lrn_errors():
+    x = torch.zeros((2, 4, 4, 8), device="cuda")
+    for bad in ((0, 1e-4, 0.75, 1.0), (5, -1.0, 0.75, 1.0), (5, 1e-4, 0.75, 0.0)):
+        with pytest.raises(singa.SingaError) as e:
+            singa.lrn_fwd(x, *bad)
+        assert e.value.status == -3
