@@ -271,7 +271,8 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16" if is_bf16 else "f32",
         "data": "synthetic",
-        "config": {"workload": "alexnet_shaped_train_step" if args.workload == 5 else "workload%d" % args.workload,
+        "config": {"workload": {5: "alexnet_shaped_train_step", 6: "alexnet_lrn_train_step"}.get(
+                       args.workload, "workload%d" % args.workload),
                    "description": w.name, "global_batch": net.batch, "image": list(w.in_shape),
                    "classes": w.classes, "params": net.n_params, "layout": "NHWC",
                    "parallelism": "none (1 GPU)"},

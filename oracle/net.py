@@ -18,7 +18,7 @@ from typing import Dict, List, Optional
 
 import numpy as np
 
-from . import (AVG, MAX, adagrad, conv_bwd_data, conv_bwd_filter, conv_fwd, fc_bwd, fc_fwd,
+from . import (AVG, MAX, adagrad, conv_bwd_data, conv_bwd_filter, conv_fwd, fc_bwd, fc_fwd, lrn_bwd, lrn_fwd,
                pool_bwd, pool_fwd, relu_bwd, relu_fwd, sgd_momentum, softmax_ce)
 
 
@@ -50,6 +50,8 @@ def forward(layers, x, params: List, labels=None, store=None) -> Dict:
             acts["argmax"][l.name] = am
         elif k == "Relu":
             h = relu_fwd(h)
+        elif k == "Lrn":
+            h = lrn_fwd(h, l.size, l.alpha, l.beta, l.k)
         elif k == "FC":
             w, b = params[pi]
             pi += 1
@@ -92,6 +94,8 @@ def backward(layers, params: List, acts: Dict, dy_top=None, need_input_grad: boo
             g = acts["dlogits"]
         elif k == "Relu":
             g = relu_bwd(acts["out"][l.name], g)
+        elif k == "Lrn":
+            g = lrn_bwd(xin, g, l.size, l.alpha, l.beta, l.k)
         elif k == "Pool":
             mode = MAX if l.mode == "max" else AVG
             g = pool_bwd(g, acts["argmax"].get(l.name), xin.shape, mode, k=l.kernel,

@@ -181,6 +181,28 @@ class ReluLayer(Layer):
         return singa.relu_bwd(self.y, dy, out=dy)
 
 
+class LrnLayer(Layer):
+    """Local response normalization across channels (the layer Sec. 5.4.1
+    names beside pooling)."""
+
+    def __init__(self, net, spec, in_shape):
+        self.name = spec.name
+        self.args = (spec.size, spec.alpha, spec.beta, spec.k)
+        self.in_shape = self.out_shape = tuple(in_shape)
+        self.y = torch.empty(self.out_shape, dtype=net.dtype, device=net.device)
+        self.dx = torch.empty(self.in_shape, dtype=net.dtype, device=net.device)
+        self.x = None
+
+    def compute_feature(self, x):
+        self.x = x
+        return singa.lrn_fwd(x, *self.args, out=self.y)
+
+    def compute_gradient(self, dy, need_dx=True):
+        if not need_dx:
+            return None
+        return singa.lrn_bwd(self.x, dy, *self.args, out=self.dx)
+
+
 class SoftmaxCELayer(Layer):
     def __init__(self, net, spec, in_shape):
         self.name = spec.name
@@ -241,6 +263,8 @@ class Net:
                 if fuse is not None:
                     fuse.relu = True
                 layer = ReluLayer(self, spec, shape, fuse)
+            elif isinstance(spec, wl.Lrn):
+                layer = LrnLayer(self, spec, shape)
             elif isinstance(spec, wl.SoftmaxCE):
                 layer = SoftmaxCELayer(self, spec, shape)
             else:

@@ -57,6 +57,17 @@ class Relu:
 
 
 @dataclass(frozen=True)
+class Lrn:
+    """Local response normalization across channels (Caffe's form):
+    y = x * (k + alpha/size * sum of x^2 over `size` channels)^-beta."""
+    name: str
+    size: int = 5
+    alpha: float = 1e-4
+    beta: float = 0.75
+    k: float = 1.0
+
+
+@dataclass(frozen=True)
 class FC:
     name: str
     out_features: int
@@ -155,7 +166,18 @@ CFG5 = Workload(
     classes=1000, lr=0.01, momentum=0.9, weight_decay=5e-4, update=True,
     description="full step: conv stack + FC 9216-4096-4096-1000 + softmax-CE + fused SGD on all params")
 
-WORKLOADS = {1: CFG1, 2: CFG2, 3: CFG3, 4: CFG4, 5: CFG5}
+# The paper's full AlexNet: workload 5 with the local response normalization
+# layers its GPU runs left out (Sec. 5.4.1 names them beside pooling), after
+# the first two ReLUs, with AlexNet's constants in Caffe's form.
+_ALEX_LRN_STACK = (_ALEX_STACK[:2] + (Lrn("norm1"),) + _ALEX_STACK[2:5] + (Lrn("norm2"),) + _ALEX_STACK[5:])
+
+CFG6 = Workload(
+    6, "AlexNet-shaped training step with LRN, batch 256, bf16 compute, fp32 master weights", "bf16", 256,
+    (3, 227, 227), "normal", _ALEX_LRN_STACK + CFG5.layers[len(_ALEX_STACK):],
+    classes=1000, lr=0.01, momentum=0.9, weight_decay=5e-4, update=True,
+    description="workload 5 with LRN (size 5, alpha 1e-4, beta 0.75, k 1) after relu1 and relu2")
+
+WORKLOADS = {1: CFG1, 2: CFG2, 3: CFG3, 4: CFG4, 5: CFG5, 6: CFG6}
 
 
 def bf16_bits(a: np.ndarray) -> np.ndarray:

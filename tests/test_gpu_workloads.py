@@ -241,7 +241,7 @@ def test_adagrad_training_step(index, batch):
             assert rel_l2(h, hw.reshape(h.shape)) <= TOL[w.dtype], l.name
 
 
-@pytest.mark.parametrize("index", [3, 4, 5])
+@pytest.mark.parametrize("index", [3, 4, 5, 6])
 def test_alexnet_workloads_batch2(index):
     w = wl.WORKLOADS[index]
     inp = wl.make_inputs(w, batch=2)
@@ -266,7 +266,7 @@ def _dev(a, dt):
     return torch.from_numpy(np.ascontiguousarray(a)).cuda().to(torch.bfloat16 if dt == "bf16" else torch.float32)
 
 
-@pytest.mark.parametrize("index,batch", [(2, None), (3, 2), (4, 2), (5, 2)])
+@pytest.mark.parametrize("index,batch", [(2, None), (3, 2), (4, 2), (5, 2), (6, 2)])
 def test_backward_teacher_forced(index, batch):
     """Each layer's GPU ComputeGradient, fed the oracle's stored input
     activation and upstream gradient of the real step, against the oracle's
@@ -300,6 +300,11 @@ def test_backward_teacher_forced(index, batch):
                                           grads["grad_in"][spec.name].astype(np.float32).astype(np.float64))
             continue
         below_relu = li > 0 and isinstance(layers[li - 1], wl.Relu)
+        if isinstance(spec, wl.Lrn):
+            got = singa.lrn_bwd(_dev(xin, dt), _dev(up, dt), spec.size, spec.alpha, spec.beta, spec.k)
+            torch.cuda.synchronize()
+            errs["dx:" + spec.name] = rel_l2(_nhwc_to_nchw(got), grads["grad_in"][spec.name])
+            continue
         if isinstance(spec, wl.Pool):
             shape = (xin.shape[0], xin.shape[2], xin.shape[3], xin.shape[1])
             yp, am = singa.pool_fwd(_dev(xin, dt), spec.mode, spec.kernel, spec.stride, spec.pad, spec.ceil_mode)

@@ -110,7 +110,31 @@ def test_net_against_torch_autograd():
         np.testing.assert_allclose(res["params"][li][1], tp[li][1].detach().numpy(), rtol=1e-13, atol=1e-15)
 
 
-@pytest.mark.parametrize("index", [1, 2, 3, 4, 5])
+def test_net_with_lrn_against_torch_autograd():
+    # conv - ReLU - LRN - max pool - FC - softmax-CE (the first block of AlexNet, shrunk)
+    layers = (wl.Conv("c1", 6, 3, 1, 1, out_shape=(6, 6, 6)), wl.Relu("r1"), wl.Lrn("n1", 5, 0.3, 0.75, 1.0),
+              wl.Pool("p1", "max", 3, 2, 0, True, (6, 3, 3)), wl.FC("fc", 4, out_shape=(4, 1, 1)), wl.SoftmaxCE())
+    rng = np.random.default_rng(11)
+    x = rng.standard_normal((2, 3, 6, 6))
+    params = [(rng.standard_normal((6, 3, 3, 3)) * 0.5, rng.standard_normal(6) * 0.1),
+              (rng.standard_normal((4, 54)) * 0.3, rng.standard_normal(4) * 0.1)]
+    labels = np.array([3, 0], np.int32)
+    res = onet.train_one_batch(layers, x, params, labels=labels, need_input_grad=True)
+    tp = [(torch.tensor(w, requires_grad=True), torch.tensor(b, requires_grad=True)) for w, b in params]
+    tx = torch.tensor(x, requires_grad=True)
+    h = F.relu(F.conv2d(tx, tp[0][0], tp[0][1], padding=1))
+    h = F.local_response_norm(h, 5, alpha=0.3, beta=0.75, k=1.0)
+    h = F.max_pool2d(h, 3, 2, ceil_mode=True)
+    z = F.linear(h.reshape(2, -1), tp[1][0], tp[1][1])
+    loss = F.cross_entropy(z, torch.tensor(labels, dtype=torch.long))
+    loss.backward()
+    assert abs(res["acts"]["loss"] - loss.item()) < 1e-12
+    for li, name in enumerate(["c1", "fc"]):
+        np.testing.assert_allclose(res["grads"]["dw"][name], tp[li][0].grad.numpy(), rtol=1e-10, atol=1e-13)
+    np.testing.assert_allclose(res["grads"]["grad_in"]["c1"], tx.grad.numpy(), rtol=1e-10, atol=1e-13)
+
+
+@pytest.mark.parametrize("index", [1, 2, 3, 4, 5, 6])
 def test_workload_listed_shapes_match_oracle_arithmetic(index):
     w = wl.WORKLOADS[index]
     c, h, ww = w.in_shape
