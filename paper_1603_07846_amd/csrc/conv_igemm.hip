@@ -189,14 +189,15 @@ __device__ __forceinline__ int xcd_remap(int b, int G) {
 // ------------------------------------------------------------ epilogue
 //
 // y[row][col] = act(acc + bias[col]), optionally zeroed where mask <= 0, for
-// one wave's (32 FM) x (32 FN) quadrant of the output tile.  The accumulators hold
+// row blocks B0 .. B0 + NB - 1 of one wave's (32 FM) x (32 FN) quadrant of
+// the output tile (row0: the first row of block B0).  The accumulators hold
 // one column per lane (rows 8 (v / 4) + 4 (lane / 32) + v % 4 of each 32 x 32
 // block); they go through the wave's own LDS region as T so that the global
 // stores (and the mask loads) are 16-byte vectors of consecutive columns.
-// Needs (32 FM) * (32 FN * sizeof(T) + 16) bytes of LDS at `lds`; the caller
+// Needs (32 NB) * (32 FN * sizeof(T) + 16) bytes of LDS at `lds`; the caller
 // has finished with the operand tiles there (barrier).  `vec`: y, mask and Nn
 // allow 16-byte vectors; otherwise the staged values are stored one by one.
-template <typename T, int FM, int FN>
+template <typename T, int FM, int FN, int B0 = 0, int NB = FM>
 __device__ __forceinline__ void store_quadrant(const f32x16 (&acc)[FM][FN], char* lds, int lane, int row0, int col0,
                                                int M, int Nn, const float* bias, int relu, const void* mask,
                                                T* __restrict__ y, bool vec) {
@@ -206,19 +207,19 @@ __device__ __forceinline__ void store_quadrant(const f32x16 (&acc)[FM][FN], char
   constexpr int VEC = 16 / ES;
   constexpr int CPR = COLS / VEC;    // 16-byte chunks per row
   constexpr int RPS = 64 / CPR;      // rows per pass of the wave (lanes past RPS * CPR idle)
-  constexpr int PASSES = (FM * 32 + RPS - 1) / RPS;
+  constexpr int PASSES = (NB * 32 + RPS - 1) / RPS;
   const int li = lane & 31, lh = lane >> 5;
 #pragma unroll
   for (int bn = 0; bn < FN; ++bn) {
     const int c = bn * 32 + li;
     const float bv = (bias && col0 + c < Nn) ? bias[col0 + c] : 0.f;
 #pragma unroll
-    for (int bm = 0; bm < FM; ++bm)
+    for (int bm = B0; bm < B0 + NB; ++bm)
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
         float val = acc[bm][bn][v] + bv;
         if (relu) val = fmaxf(val, 0.f);
-        const int r = bm * 32 + (v >> 2) * 8 + lh * 4 + (v & 3);
+        const int r = (bm - B0) * 32 + (v >> 2) * 8 + lh * 4 + (v & 3);
         store_out<T>((T*)(lds + r * PIT + c * ES), val);
       }
   }
@@ -233,7 +234,7 @@ __device__ __forceinline__ void store_quadrant(const f32x16 (&acc)[FM][FN], char
     for (int pass = 0; pass < PASSES; ++pass) {
       const int r = pass * RPS + rr;
       const int row = row0 + r;
-      if (r >= FM * 32) break;
+      if (r >= NB * 32) break;
       union { uint4 u; T e[VEC]; } val, mv;
       val.u = *(const uint4*)(lds + r * PIT + cc * 16);
       if (row < M && col < Nn) {
@@ -252,7 +253,7 @@ __device__ __forceinline__ void store_quadrant(const f32x16 (&acc)[FM][FN], char
     for (int pass = 0; pass < PASSES; ++pass) {
       const int r = pass * RPS + rr;
       const int row = row0 + r;
-      if (r >= FM * 32) break;
+      if (r >= NB * 32) break;
       union { uint4 u; T e[VEC]; } val;
       val.u = *(const uint4*)(lds + r * PIT + cc * 16);
       if (row < M) {
@@ -573,18 +574,29 @@ __device__ __forceinline__ void block_barrier() { asm volatile("s_barrier" ::: "
 // WMW = 4: waves stacked along the rows, each 64 x 96 of a 256 x 96 tile, for
 // layers with at most 96 output channels (the B tile still loads 128 rows,
 // the last 32 out of range: no memory traffic).
+// WMW = 8: 8 waves, 2 (rows) x 4 (columns), each 128 x 64 of a 256 x 256
+// tile (512 threads, one workgroup per CU): half the operand bytes per flop
+// of the 256 x 128 tile on the B side, for 256-column layers with enough
+// row tiles.
 template <bool BWD, int LBK, int WMW>
-__global__ __launch_bounds__(NT, LBK == 32 ? 2 : 1) void conv_fwd_large_kernel(FwdArgs a) {
+__global__ __launch_bounds__(WMW == 8 ? 2 * NT : NT, (LBK == 32 && WMW != 8) ? 2 : 1) void conv_fwd_large_kernel(
+    FwdArgs a) {
   typedef LT<LBK> G;
-  constexpr int FM = WMW == 2 ? 4 : 2, FN = WMW == 2 ? 2 : 3;
-  constexpr int LOADS = G::AI + G::BI;  // 16-byte loads per thread per K-tile
-  __shared__ __attribute__((aligned(16))) char smem[G::SMEM];
+  constexpr int NW = WMW == 8 ? 8 : 4;       // waves
+  constexpr int BNT = WMW == 8 ? 256 : BN;   // tile columns
+  constexpr int FM = WMW == 4 ? 2 : 4, FN = WMW == 4 ? 3 : 2;
+  constexpr int ABAND = L_BM / NW, BBAND = BNT / NW;  // operand rows each wave loads
+  constexpr int AI = ABAND / G::RPI, BI = BBAND / G::RPI;  // its load instructions per K-tile
+  constexpr int ATILE = L_BM * G::RB, STAGE = ATILE + BNT * G::RB;
+  constexpr int LOADS = AI + BI;  // 16-byte loads per thread per K-tile
+  static_assert(AI * G::RPI == ABAND && BI * G::RPI == BBAND, "load bands");
+  __shared__ __attribute__((aligned(16))) char smem[L_STAGES * STAGE];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int L = xcd_remap(blockIdx.x, gridDim.x);
   const int split = L / a.tiles, tile = L - split * a.tiles;
   const int tm = tile / a.tiles_n, tn = tile - tm * a.tiles_n;
-  const int m0 = tm * L_BM, n0 = tn * BN;
+  const int m0 = tm * L_BM, n0 = tn * BNT;
   const __amdgpu_buffer_rsrc_t xr = make_rsrc(a.x, a.x_bytes);
   const __amdgpu_buffer_rsrc_t wr = make_rsrc(a.w, a.w_bytes);
 
@@ -597,10 +609,10 @@ __global__ __launch_bounds__(NT, LBK == 32 ? 2 : 1) void conv_fwd_large_kernel(F
 #pragma unroll
   for (int p = 0; p < 2; ++p) cpar[p] = (lane % G::SL) ^ ((4 * p * (G::SL == 8) + (lane >> 4)) % G::SL);
   constexpr int NPAR = G::SL == 8 ? 2 : 1;
-  int apix[G::AI], ah0[G::AI], aw0[G::AI];
+  int apix[AI], ah0[AI], aw0[AI];
 #pragma unroll
-  for (int i = 0; i < G::AI; ++i) {
-    const int m = m0 + 64 * wave + G::RPI * i + lrow;
+  for (int i = 0; i < AI; ++i) {
+    const int m = m0 + ABAND * wave + G::RPI * i + lrow;
     if (m < a.M) {
       const int n = (int)fdiv((uint32_t)m, a.dPQ);
       const int pq = m - n * a.P * a.Q;
@@ -615,10 +627,10 @@ __global__ __launch_bounds__(NT, LBK == 32 ? 2 : 1) void conv_fwd_large_kernel(F
       apix[i] = 0;
     }
   }
-  int brow[G::BI];
+  int brow[BI];
 #pragma unroll
-  for (int i = 0; i < G::BI; ++i) {
-    const int n = n0 + 32 * wave + G::RPI * i + lrow;
+  for (int i = 0; i < BI; ++i) {
+    const int n = n0 + BBAND * wave + G::RPI * i + lrow;
     brow[i] = n < a.Nn ? n * a.Kg : -1;
   }
 
@@ -655,21 +667,21 @@ __global__ __launch_bounds__(NT, LBK == 32 ? 2 : 1) void conv_fwd_large_kernel(F
     const int p = NPAR == 2 ? (i & 1) : 0;
     const int h = ah0[i] + t.r[p], w = aw0[i] + t.s[p];
     const bool ok = t.kin[p] & ((unsigned)h < (unsigned)a.H) & ((unsigned)w < (unsigned)a.W);
-    ld_lds16(xr, ok ? (uint32_t)(apix[i] + t.tap[p]) * 2u : OOB, As + (64 * wave + G::RPI * i) * G::RB);
+    ld_lds16(xr, ok ? (uint32_t)(apix[i] + t.tap[p]) * 2u : OOB, As + (ABAND * wave + G::RPI * i) * G::RB);
   };
   auto issue_b = [&](const Taps& t, char* Bs, int i) {
     const int p = NPAR == 2 ? (i & 1) : 0;
     const bool ok = (brow[i] >= 0) & t.kin[p];
-    ld_lds16(wr, ok ? (uint32_t)(brow[i] + t.kk[p]) * 2u : OOB, Bs + (32 * wave + G::RPI * i) * G::RB);
+    ld_lds16(wr, ok ? (uint32_t)(brow[i] + t.kk[p]) * 2u : OOB, Bs + (BBAND * wave + G::RPI * i) * G::RB);
   };
   // the j-th of KS slices of the K-tile's loads (spread over its k-steps)
   auto issue_slice = [&](const Taps& t, char* St, int j) {
-    constexpr int TOT = G::AI + G::BI;
+    constexpr int TOT = AI + BI;
 #pragma unroll
     for (int q = 0; q < TOT; ++q) {
       if (q * G::KS / TOT != j) continue;
-      if (q < G::AI) issue_a(t, St, q);
-      else issue_b(t, St + G::ATILE, q - G::AI);
+      if (q < AI) issue_a(t, St, q);
+      else issue_b(t, St + ATILE, q - AI);
     }
   };
 
@@ -681,11 +693,12 @@ __global__ __launch_bounds__(NT, LBK == 32 ? 2 : 1) void conv_fwd_large_kernel(F
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
-  const int wm = WMW == 2 ? wave >> 1 : wave, wn = WMW == 2 ? wave & 1 : 0;
+  const int wm = WMW == 2 ? wave >> 1 : WMW == 8 ? wave >> 2 : wave;
+  const int wn = WMW == 2 ? wave & 1 : WMW == 8 ? wave & 3 : 0;
   const int li = lane & 31, lh = lane >> 5;
   // chunk 2 kc + lh of row r sits in slot (2 kc + lh) ^ ((r / RPW) % SL); r % 16 = li % 16
   const int tsw = (lh ^ ((li / G::RPW) % G::SL)) << 4;
-  const int aoff = (wm * FM * 32 + li) * G::RB, boff = G::ATILE + (wn * FN * 32 + li) * G::RB;
+  const int aoff = (wm * FM * 32 + li) * G::RB, boff = ATILE + (wn * FN * 32 + li) * G::RB;
   struct Frags {
     bf16x8 a[FM], b[FN];
   };
@@ -713,16 +726,16 @@ __global__ __launch_bounds__(NT, LBK == 32 ? 2 : 1) void conv_fwd_large_kernel(F
 #pragma unroll
   for (int j = 0; j < G::KS; ++j) issue_slice(taps(kbase), smem, j);
 #pragma unroll
-  for (int j = 0; j < G::KS; ++j) issue_slice(taps(nkt > 1 ? kbase + LBK : a.Kg), smem + G::STAGE, j);
+  for (int j = 0; j < G::KS; ++j) issue_slice(taps(nkt > 1 ? kbase + LBK : a.Kg), smem + STAGE, j);
   int stage = 0;
   for (int kt = 0; kt < nkt; ++kt) {
     wait_vmcnt<LOADS>();  // this thread's loads of tile kt have landed (tile kt+1's may be in flight)
     block_barrier();      // ... and everyone's; everyone is also done with tile kt-1
     const int nstage = stage == 0 ? 2 : stage - 1;
-    char* Ns = smem + nstage * G::STAGE;
+    char* Ns = smem + nstage * STAGE;
     const int knext = kbase + (kt + 2) * LBK;
     const Taps t = taps(knext < kend ? knext : a.Kg);
-    const char* S = smem + stage * G::STAGE;
+    const char* S = smem + stage * STAGE;
     // fragments one k-step ahead; the loads of tile kt+2 spread over the k-steps
     Frags f = frags(S, 0);
 #pragma unroll
@@ -755,8 +768,17 @@ __global__ __launch_bounds__(NT, LBK == 32 ? 2 : 1) void conv_fwd_large_kernel(F
   }
   __syncthreads();  // every wave is done with the operand tiles
   const bool vec = a.Nn % 8 == 0 && (((uintptr_t)a.y | (uintptr_t)a.mask) % 16) == 0;
-  store_quadrant<bf16_t, FM, FN>(acc, smem + wave * FM * 32 * (FN * 32 * 2 + 16), lane, m0 + wm * FM * 32,
-                                 n0 + wn * FN * 32, a.M, a.Nn, a.bias, a.relu, a.mask, (bf16_t*)a.y, vec);
+  if constexpr (WMW == 8) {
+    // the quadrant in two halves of 64 rows: 8 waves x 9 KB of staging
+    char* q = smem + wave * 64 * (FN * 32 * 2 + 16);
+    store_quadrant<bf16_t, FM, FN, 0, 2>(acc, q, lane, m0 + wm * FM * 32, n0 + wn * FN * 32, a.M, a.Nn, a.bias,
+                                         a.relu, a.mask, (bf16_t*)a.y, vec);
+    store_quadrant<bf16_t, FM, FN, 2, 2>(acc, q, lane, m0 + wm * FM * 32 + 64, n0 + wn * FN * 32, a.M, a.Nn,
+                                         a.bias, a.relu, a.mask, (bf16_t*)a.y, vec);
+  } else {
+    store_quadrant<bf16_t, FM, FN>(acc, smem + wave * FM * 32 * (FN * 32 * 2 + 16), lane, m0 + wm * FM * 32,
+                                   n0 + wn * FN * 32, a.M, a.Nn, a.bias, a.relu, a.mask, (bf16_t*)a.y, vec);
+  }
 }
 
 // ----------------------------------------------------------- filter gradient
@@ -1338,35 +1360,54 @@ __global__ __launch_bounds__(NT, 2) void conv_wgrad_large_kernel(WgradArgs a) {
 }
 
 // Filter-gradient split-K reduction over partial[split][M][Ng] (rows of ldp
-// floats, ldp % 64 == 0): element (row, col) goes to dw[row][col] for col < Nn
+// floats, ldp % 4 == 0): element (row, col) goes to dw[row][col] for col < Nn
 // and to db[row] for col == Nn (the bias column), each added to or
-// overwriting its target.  A block owns 256 consecutive elements of one row
-// (ldp % 256 == 0 is not required: a block never straddles rows because it
-// covers 4 groups of 64 from the same 64-aligned start); its 4 waves each sum
-// every 4th split with 16-byte loads, then wave 0 adds the 4 partial sums in a
-// fixed order, so the result does not depend on timing.
+// overwriting its target.  A block of 256 threads is G groups of 256 / G
+// lanes; a lane owns 4 consecutive elements of one row, group g sums splits
+// g, g + G, g + 2G, ... in that order (four 16-byte loads in flight), then
+// group 0 adds the G partial sums in group order, so the result does not
+// depend on timing.  Many splits (the first layer's long reduction over few
+// filter elements) take G = 16, so the grid still fills the chip.
+template <int G>
 __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restrict__ partial, int splits, int M,
                                                             int ldp, int Ng, int Nn, float* __restrict__ dw,
                                                             float* __restrict__ db, int acc_dw, int acc_db) {
-  __shared__ float4 part[4][64];
+  constexpr int LG = 256 / G;
+  __shared__ float4 part[G][LG];
   const size_t n = (size_t)M * ldp;
-  const int g = threadIdx.x >> 6, l = threadIdx.x & 63;
-  const size_t i = ((size_t)blockIdx.x * 64 + l) * 4;  // 4 consecutive elements of one row (ldp % 4 == 0)
+  const int g = threadIdx.x / LG, l = threadIdx.x % LG;
+  const size_t i = ((size_t)blockIdx.x * LG + l) * 4;  // 4 consecutive elements of one row (ldp % 4 == 0)
   const int row = (int)(i / (size_t)ldp);
   const int col = (int)(i - (size_t)row * ldp);
   float4 t = make_float4(0.f, 0.f, 0.f, 0.f);
   if (i < n && col < Ng) {
-    for (int k = g; k < splits; k += 4) {
-      const float4 v = *(const float4*)(partial + (size_t)k * n + i);
-      t.x += v.x; t.y += v.y; t.z += v.z; t.w += v.w;
+    const float4* __restrict__ p = (const float4*)(partial + i);
+    const size_t n4 = n / 4;
+    int k = g;
+    for (; k + 3 * G < splits; k += 4 * G) {
+      float4 q[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) q[u] = p[(size_t)(k + u * G) * n4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        t.x += q[u].x; t.y += q[u].y; t.z += q[u].z; t.w += q[u].w;
+      }
+    }
+    for (; k < splits; k += G) {
+      const float4 q = p[(size_t)k * n4];
+      t.x += q.x; t.y += q.y; t.z += q.z; t.w += q.w;
     }
   }
   part[g][l] = t;
   __syncthreads();
   if (g == 0 && i < n) {
-    const float4 a = part[0][l], b = part[1][l], c = part[2][l], d = part[3][l];
-    const float s4[4] = {(a.x + b.x) + (c.x + d.x), (a.y + b.y) + (c.y + d.y), (a.z + b.z) + (c.z + d.z),
-                         (a.w + b.w) + (c.w + d.w)};
+    float4 s = part[0][l];
+#pragma unroll
+    for (int h = 1; h < G; ++h) {
+      const float4 q = part[h][l];
+      s.x += q.x; s.y += q.y; s.z += q.z; s.w += q.w;
+    }
+    const float s4[4] = {s.x, s.y, s.z, s.w};
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       const int ce = col + e;
@@ -1459,13 +1500,14 @@ void launch_fwd_instance(const FwdArgs& a, dim3 grid, double flops, hipStream_t 
   hipLaunchKernelGGL((conv_fwd_kernel<T, AM, BMD, BWD>), grid, dim3(NT), 0, st, a);
 }
 
-// "conv_fwd_large_kernel<bwd,taps per K-tile,waves along the rows>"
-const char* fwd_large_name(bool bwd, bool deep, bool narrow) {
+// "conv_fwd_large_kernel<bwd,taps per K-tile,wave layout>"
+const char* fwd_large_name(bool bwd, bool deep, bool narrow, bool wide) {
   static const char* names[2][2][2] = {
       {{"conv_fwd_large_kernel<0,32,2>", "conv_fwd_large_kernel<0,32,4>"},
        {"conv_fwd_large_kernel<0,64,2>", "conv_fwd_large_kernel<0,64,4>"}},
       {{"conv_fwd_large_kernel<1,32,2>", "conv_fwd_large_kernel<1,32,4>"},
        {"conv_fwd_large_kernel<1,64,2>", "conv_fwd_large_kernel<1,64,4>"}}};
+  if (wide) return bwd ? "conv_fwd_large_kernel<1,32,8>" : "conv_fwd_large_kernel<0,32,8>";
   return names[bwd][deep][narrow];
 }
 
@@ -1506,6 +1548,25 @@ bool use_large_fwd(long M, long Nn, long Kg) {
   const double eff_big = (double)big / (double)(((big + 255) / 256) * 256);
   const double eff_small = (double)small / (double)(((small + 511) / 512) * 512);
   return eff_big >= 0.85 * eff_small;
+}
+
+// The 256 x 256 layout (one workgroup of 8 waves per CU) instead of 256 x 128
+// (two of 4 waves): when its columns are at least 3/4 used, pad no more than
+// the 128-column tiles do, and its rounds of 256 workgroups are about as full
+// as the other's rounds of 512.  SINGA_FWD_WIDE=0|1 forces the choice.
+bool use_wide_fwd(long M, long Nn) {
+  static const int forced = [] {
+    const char* e = getenv("SINGA_FWD_WIDE");
+    return e ? atoi(e) : -1;
+  }();
+  if (Nn <= 96) return false;
+  if (forced == 0 || forced == 1) return forced == 1;
+  const long cw = (Nn + 255) / 256 * 256, cn = (Nn + BN - 1) / BN * BN;
+  if (cw > cn || 4 * Nn < 3 * cw) return false;
+  const long rows = (M + L_BM - 1) / L_BM, tw = rows * (cw / 256), tn = rows * (cn / BN);
+  const double eff_w = (double)tw / (double)(((tw + 255) / 256) * 256);
+  const double eff_n = (double)tn / (double)(((tn + 511) / 512) * 512);
+  return eff_w >= 0.95 * eff_n;
 }
 
 int fwd_splits_for(long M, long Nn, long Kg, long bk) {
@@ -1578,18 +1639,23 @@ hipError_t conv_fwd_dispatch(const ConvShape& s, const void* x, const void* w, c
   const int am = load_mode<T>(s.C, x);
   const int bm = wt ? BT16 : load_mode<T>(a.Kg, w);
   if (!wt && sizeof(T) == 2 && am == VEC16 && bm == VEC16 && splits == 1 && use_large_fwd(a.M, a.Nn, a.Kg)) {
-    a.tiles_n = (a.Nn + BN - 1) / BN;
+    const bool narrow = a.Nn <= 96;  // one 96-column tile
+    const bool wide = use_wide_fwd(a.M, a.Nn);
+    a.tiles_n = (a.Nn + (wide ? 255 : BN - 1)) / (wide ? 256 : BN);
     a.tiles = ((a.M + L_BM - 1) / L_BM) * a.tiles_n;
     a.partial = nullptr;
-    const bool narrow = a.Nn <= 96;  // one 96-column tile
     // 64-tap K-tiles only for the 256 x 128 layout (the 256 x 96 one measured
-    // faster at 32 taps, two workgroups per CU, on a 6400-tap reduction)
-    const bool deep = fwd_large_bk(narrow ? 0 : a.Kg) == 64;
+    // faster at 32 taps, two workgroups per CU, on a 6400-tap reduction; the
+    // 256 x 256 one has LDS for three 32-tap stages only)
+    const bool deep = fwd_large_bk(narrow || wide ? 0 : a.Kg) == 64;
     a.kt_per_split = (a.Kg + (deep ? 64 : 32) - 1) / (deep ? 64 : 32);  // one split: every K-tile of this depth
     a.tap_major = a.RS > 1 && s.C % (deep ? 64 : 32) == 0;
-    TraceScope ts(fwd_large_name(bwd, deep, narrow), st, flops, WORK_FLOP);
-#define LAUNCH_LARGE(B, K, W) hipLaunchKernelGGL((conv_fwd_large_kernel<B, K, W>), dim3(a.tiles), dim3(NT), 0, st, a)
-    if (bwd) {
+    TraceScope ts(fwd_large_name(bwd, deep, narrow, wide), st, flops, WORK_FLOP);
+#define LAUNCH_LARGE(B, K, W) \
+  hipLaunchKernelGGL((conv_fwd_large_kernel<B, K, W>), dim3(a.tiles), dim3(W == 8 ? 2 * NT : NT), 0, st, a)
+    if (wide) {
+      if (bwd) LAUNCH_LARGE(true, 32, 8); else LAUNCH_LARGE(false, 32, 8);
+    } else if (bwd) {
       if (narrow) { if (deep) LAUNCH_LARGE(true, 64, 4); else LAUNCH_LARGE(true, 32, 4); }
       else { if (deep) LAUNCH_LARGE(true, 64, 2); else LAUNCH_LARGE(true, 32, 2); }
     } else {
@@ -1763,8 +1829,12 @@ hipError_t conv_wgrad_dispatch(const ConvShape& s, const void* x, const void* dy
   // fixed-order sum of the partial tiles into dw (and db)
   const size_t n = (size_t)a.M * a.ldp;
   TraceScope ts("splitk_reduce_kernel", st, (double)a.M * a.Ng * 4.0 * (splits + 1 + (acc_dw ? 1 : 0)), WORK_BYTE);
-  hipLaunchKernelGGL(splitk_reduce_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, partial, splits, a.M,
-                     a.ldp, a.Ng, a.Nn, dw, db, acc_dw, acc_db);
+  if (splits >= 64)
+    hipLaunchKernelGGL(splitk_reduce_kernel<16>, dim3((unsigned)((n + 63) / 64)), dim3(256), 0, st, partial, splits,
+                       a.M, a.ldp, a.Ng, a.Nn, dw, db, acc_dw, acc_db);
+  else
+    hipLaunchKernelGGL(splitk_reduce_kernel<4>, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, partial, splits,
+                       a.M, a.ldp, a.Ng, a.Nn, dw, db, acc_dw, acc_db);
   return hipGetLastError();
 }
 

@@ -46,6 +46,8 @@ CONV_CASES = [
     (2, 12, 10, 10, 24, 3, 3, 1, 1),     # C=12: bf16 8-byte tap halves that wrap to the next tap
     (3, 4, 19, 19, 16, 5, 5, 2, 2),      # C=4, filter rows of 100 taps: 8-byte halves for both operands
     (3, 5, 3, 3, 16, 3, 3, 0, 1),        # FC with 45 inputs: backward-data through a transposed copy
+    (2, 3, 33, 33, 8, 7, 7, 3, 4),       # space-to-depth rewrite with padding
+    (1, 3, 6, 1400, 4, 3, 3, 1, 2),      # stride 2 on 3 channels: space-to-depth (f32), padded channels (bf16)
 ]
 
 
@@ -422,6 +424,10 @@ LARGE_CASES = [
     ("fwd", (30, 32, 47, 47, 90, 3, 3, 1, 1)),   # ragged columns, element-wise epilogue
     ("fwd", (30, 32, 47, 47, 40, 3, 3, 1, 1)),
     ("bwd_data", (30, 96, 47, 47, 40, 3, 3, 1, 1)),
+    # 256 columns and enough row tiles: the 256 x 256 layout of 8 waves
+    ("fwd", (30, 64, 47, 47, 256, 3, 3, 1, 1)),
+    ("bwd_data", (30, 256, 47, 47, 64, 3, 3, 1, 1)),
+    ("fwd", (25, 64, 47, 47, 250, 3, 3, 1, 1)),  # ragged columns, element-wise epilogue
 ]
 
 
@@ -440,9 +446,12 @@ def test_conv_large_tile_path(op, case):
     singa.trace_enable(False)
     large = [n for n in names if n.startswith("conv_fwd_large_kernel")]
     assert large, names
-    narrow = (K if op == "fwd" else C) <= 96  # GEMM columns: filters, or input channels for the data gradient
+    cols = K if op == "fwd" else C  # GEMM columns: filters, or input channels for the data gradient
+    narrow = cols <= 96
     assert all(n.endswith(",4>") == narrow for n in large), large
-    deep = not narrow and R * S * (C if op == "fwd" else K) >= 4096  # reduction length
+    wide = 192 < cols <= 256  # 256-column tiles at least 3/4 used (every case here has enough row tiles)
+    assert all(n.endswith(",8>") == wide for n in large), large
+    deep = not narrow and not wide and R * S * (C if op == "fwd" else K) >= 4096  # reduction length
     assert all((",64," in n) == deep for n in large), large
     if op == "fwd":
         ref = oracle.relu_fwd(oracle.conv_fwd(x, w, b, pad=pad, stride=stride))
