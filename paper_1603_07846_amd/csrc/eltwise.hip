@@ -418,25 +418,35 @@ __device__ __forceinline__ float wave_sum(float v) {
 }
 
 // One wave per row.  The row's maximum and the sum of exp(z - max) are
-// built in one pass with the running-max rescaling of the sum; a second pass
-// writes the gradient.  The row's loss goes to loss[1 + row].
+// built in one pass with the running-max rescaling of the sum, in chunks of
+// 16 values per lane whose loads are all issued before any is used; a second
+// pass, chunked the same way, writes the gradient.  The row's loss goes to
+// loss[1 + row].
 template <typename T>
 __global__ __launch_bounds__(256) void softmax_ce_rows_kernel(int B, int classes, const T* __restrict__ z,
                                                               const int32_t* __restrict__ labels,
                                                               float* __restrict__ loss, T* __restrict__ dz) {
+  constexpr int U = 16;
   const int lane = threadIdx.x & 63;
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= B) return;
   const T* zr = z + (size_t)row * classes;
   float m = -INFINITY, s = 0.f;
-  for (int j = lane; j < classes; j += 64) {
-    const float v = ld_f<T>(zr + j);
-    if (v > m) {
-      s = s * expf(m - v) + 1.f;
-      m = v;
-    } else {
-      s += expf(v - m);
+  for (int base = 0; base < classes; base += 64 * U) {
+    float v[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int j = base + 64 * u + lane;
+      v[u] = j < classes ? ld_f<T>(zr + j) : -INFINITY;
     }
+    float mc = m;
+#pragma unroll
+    for (int u = 0; u < U; ++u) mc = fmaxf(mc, v[u]);
+    if (mc == -INFINITY) continue;  // nothing in this chunk for this lane
+    s *= expf(m - mc);              // m = -inf: s is 0 and stays 0
+#pragma unroll
+    for (int u = 0; u < U; ++u) s += expf(v[u] - mc);
+    m = mc;
   }
   // combine the lanes' (max, sum) pairs
   const float mw = wave_max(m);
@@ -446,9 +456,18 @@ __global__ __launch_bounds__(256) void softmax_ce_rows_kernel(int B, int classes
   const int lab = labels[row];
   const float invB = 1.f / (float)B;
   T* dr = dz + (size_t)row * classes;
-  for (int j = lane; j < classes; j += 64) {
-    const float prob = expf(ld_f<T>(zr + j) - lse);
-    st_f<T>(dr + j, (prob - (j == lab ? 1.f : 0.f)) * invB);
+  for (int base = 0; base < classes; base += 64 * U) {
+    float v[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int j = base + 64 * u + lane;
+      v[u] = j < classes ? ld_f<T>(zr + j) : 0.f;
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int j = base + 64 * u + lane;
+      if (j < classes) st_f<T>(dr + j, (expf(v[u] - lse) - (j == lab ? 1.f : 0.f)) * invB);
+    }
   }
   if (lane == 0) loss[1 + row] = (lab >= 0 && lab < classes) ? lse - ld_f<T>(zr + lab) : 0.f;
 }

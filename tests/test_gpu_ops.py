@@ -187,6 +187,44 @@ def test_conv_bwd_filter_without_bias(layout, dt):
     assert rel_l2(filt_to_kcrs(dw, layout), ref_dw) <= TOL["f32"]
 
 
+# the 128 x 256 filter-gradient tile: several row tiles, direct and split
+# reductions, image-fastest order with accumulation, no bias
+LARGE_WGRAD_CASES = [
+    ((8, 32, 15, 15, 512, 3, 3, 1, 1), True, False),    # two row tiles, ragged taps + bias, split reduction
+    ((4, 64, 9, 9, 256, 3, 3, 1, 1), True, False),      # short reduction: one split, written directly
+    ((32, 16, 12, 12, 256, 3, 3, 1, 1), True, True),    # image-fastest order, accumulated in two halves
+    ((8, 32, 15, 15, 256, 3, 3, 1, 1), False, False),   # without bias
+    ((6, 24, 13, 13, 304, 3, 3, 1, 1), True, False),    # 304 filters: ragged row tile
+]
+
+
+@pytest.mark.parametrize("case,bias,halves", LARGE_WGRAD_CASES,
+                         ids=["x".join(map(str, c)) + ("-bias" if b else "") + ("-acc" if h else "")
+                              for c, b, h in LARGE_WGRAD_CASES])
+def test_conv_bwd_filter_large_tile(case, bias, halves):
+    N, C, H, W, K, R, S, pad, stride = case
+    x, w, b, dy = _conv_inputs(case, "bf16", 43)
+    ref_dw, ref_db = oracle.conv_bwd_filter(x, dy, w.shape, pad=pad, stride=stride)
+    xd, dyd = nchw_to_dev(x, "bf16"), nchw_to_dev(dy, "bf16")
+    singa.trace_enable(True)
+    if halves:
+        h = N // 2
+        dw, db = singa.conv_bwd_filter(xd[:h], dyd[:h], fphys(w.shape), pad, stride, with_bias=bias)
+        singa.conv_bwd_filter(xd[h:], dyd[h:], fphys(w.shape), pad, stride, dw=dw, db=db, accumulate=True,
+                              with_bias=bias)
+    else:
+        dw, db = singa.conv_bwd_filter(xd, dyd, fphys(w.shape), pad, stride, with_bias=bias)
+    torch.cuda.synchronize()
+    names = [r[0] for r in singa.trace_records()]
+    singa.trace_enable(False)
+    assert any(n.startswith("conv_wgrad_large_kernel") for n in names), names
+    assert rel_l2(filt_to_kcrs(dw), ref_dw) <= TOL["f32"]
+    if bias:
+        assert rel_l2(db.cpu().numpy(), ref_db) <= TOL["f32"]
+    else:
+        assert db is None
+
+
 def test_conv_bwd_filter_deterministic():
     case = (4, 32, 15, 15, 48, 3, 3, 1, 1)
     x, w, b, dy = _conv_inputs(case, "f32", 50)
