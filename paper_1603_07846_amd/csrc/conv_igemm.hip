@@ -1098,6 +1098,11 @@ __global__ __launch_bounds__(NT) void conv_wgrad_kernel(WgradArgs a) {
 // transpose read touch fall in 8 distinct 32-byte bank groups.  Three LDS stages; loads of K-tile k+2 are issued while k
 // is multiplied; one barrier per K-tile.  The bias column (tap index Nn) is
 // loaded as an out-of-range zero and set to 1 in the B fragments.
+// With NFAST, K-tile kt holds images 32 g .. 32 g + 31 at output pixel pq,
+// kt = g P Q + pq: consecutive K-tiles step to the neighbouring pixel of the
+// same images, whose 3x3 / 5x5 input windows overlap, so the tap rows of a
+// split meet again in the L2 (2-3 % faster than running the image groups of
+// one pixel back to back).
 constexpr int WL_BM = 128, WL_BN = 256, WL_BK = 32;  // BK: reduction rows per K-tile
 constexpr int WL_ARB = WL_BM * 2, WL_BRB = WL_BN * 2;  // row bytes
 constexpr int WL_AT = WL_BK * WL_ARB, WL_BT = WL_BK * WL_BRB;
@@ -1146,8 +1151,10 @@ __global__ __launch_bounds__(NT, 2) void conv_wgrad_large_kernel(WgradArgs a) {
   // row d of the K-tile starting at t0 -> (n, output pixel) and validity
   auto row_pix = [&](int t0, int d, int& n, int& pq, bool& tin) {
     if constexpr (NFAST) {
-      pq = (int)fdiv((uint32_t)t0, a.dN);
-      n = t0 - pq * a.N + d;
+      const int kt = t0 / WL_BK;
+      const int g = (int)fdiv((uint32_t)kt, a.dPQ);
+      pq = kt - g * PQ;
+      n = g * WL_BK + d;
       tin = true;
     } else {
       const int t = t0 + d;
