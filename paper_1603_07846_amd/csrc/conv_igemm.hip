@@ -1725,10 +1725,14 @@ void launch_wgrad_variant(bool va, int bm, const WgradArgs& a, dim3 grid, double
   else launch_wgrad_bmode<T, false, NF>(bm, a, grid, flops, st);
 }
 
-// Reduction order of the filter gradient: image fastest (needs N % BK == 0)
-// unless an image has many output pixels, where image-major keeps the input
-// reads of a workgroup local.  SINGA_WGRAD_ORDER=image|pixel forces one.
-bool use_image_fastest(const ConvShape& s, int bk) {
+// Reduction order of the filter gradient: K-tiles of BK images at one output
+// pixel (needs N % BK == 0) or image-major.  The large kernel, which steps
+// such K-tiles along neighbouring pixels, takes the former whenever it can
+// (measured faster on every AlexNet layer, the first one included); the
+// 128 x 128 kernel only when an image has few output pixels (otherwise
+// image-major keeps a workgroup's input reads local).
+// SINGA_WGRAD_ORDER=image|pixel forces one.
+bool use_image_fastest(const ConvShape& s, int bk, bool large) {
   static const int forced = [] {
     const char* e = getenv("SINGA_WGRAD_ORDER");
     if (!e) return 0;
@@ -1736,7 +1740,7 @@ bool use_image_fastest(const ConvShape& s, int bk) {
   }();
   if (s.N % bk != 0) return false;
   if (forced) return forced == 1;
-  return s.P * s.Q < 1024;
+  return large || s.P * s.Q < 1024;
 }
 
 // Split-K count of the filter gradient on `tiles` output tiles and `nkt`
@@ -1813,7 +1817,7 @@ hipError_t conv_wgrad_dispatch(const ConvShape& s, const void* x, const void* dy
   if (upd) a.u = *upd;
   dim3 grid(a.tiles * splits);
   const double flops = 2.0 * a.M * (double)a.Nn * (double)a.T;
-  const bool nf = use_image_fastest(s, bk);
+  const bool nf = use_image_fastest(s, bk, large);
   if (large) {
     // "conv_wgrad_large_kernel<image fastest,update fused>"
     static const char* names[2][2] = {{"conv_wgrad_large_kernel<0,0>", "conv_wgrad_large_kernel<0,1>"},
