@@ -462,6 +462,7 @@ LARGE_CASES = [
     ("fwd", (30, 32, 47, 47, 90, 3, 3, 1, 1)),   # ragged columns, element-wise epilogue
     ("fwd", (30, 32, 47, 47, 40, 3, 3, 1, 1)),
     ("bwd_data", (30, 96, 47, 47, 40, 3, 3, 1, 1)),
+    ("fwd", (32, 24, 64, 64, 96, 3, 3, 1, 1)),   # 512 row tiles of 256 x 96: one full round
     # 256 columns and enough row tiles: the 256 x 256 layout of 8 waves
     ("fwd", (30, 64, 47, 47, 256, 3, 3, 1, 1)),
     ("bwd_data", (30, 256, 47, 47, 64, 3, 3, 1, 1)),
