@@ -254,8 +254,8 @@ __global__ __launch_bounds__(256) void space_to_depth_kernel(const T* __restrict
 }
 
 template <typename T>
-__global__ __launch_bounds__(256) void filter_to_s2d_kernel(const T* __restrict__ w, T* __restrict__ ws, int K,
-                                                            int R, int S, int C, int Rs, int Ss, int sh, int sw,
+__global__ __launch_bounds__(256) void filter_to_s2d_kernel(const T* __restrict__ w, T* __restrict__ ws, int R,
+                                                            int S, int C, int Rs, int Ss, int sh, int sw,
                                                             int total) {
   for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < total; i += gridDim.x * blockDim.x) {
     const int Cs = sh * sw * C;
@@ -273,8 +273,8 @@ __global__ __launch_bounds__(256) void filter_to_s2d_kernel(const T* __restrict_
 
 // dw[k][r][s][c] (+)= dws[k][r / sh][s / sw][((r % sh)*sw + s % sw)*C + c] (fp32 filter gradients).
 __global__ __launch_bounds__(256) void s2d_to_filter_f32_kernel(const float* __restrict__ dws, float* __restrict__ dw,
-                                                                int K, int R, int S, int C, int Rs, int Ss, int sh,
-                                                                int sw, int accumulate, int total) {
+                                                                int R, int S, int C, int Rs, int Ss, int sh, int sw,
+                                                                int accumulate, int total) {
   for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < total; i += gridDim.x * blockDim.x) {
     const int c = i % C;
     int t = i / C;
@@ -440,10 +440,10 @@ hipError_t launch_filter_to_s2d(int dt, const ConvShape& s, const ConvShape& g, 
   TraceScope ts("filter_to_s2d_kernel", st, (double)total * 2 * dt_size(dt), WORK_BYTE);
   if (dt == BF16)
     hipLaunchKernelGGL(filter_to_s2d_kernel<bf16_t>, dim3(grid_for(total)), dim3(256), 0, st, (const bf16_t*)w,
-                       (bf16_t*)ws, s.K, s.R, s.S, s.C, g.R, g.S, s.sh, s.sw, total);
+                       (bf16_t*)ws, s.R, s.S, s.C, g.R, g.S, s.sh, s.sw, total);
   else
     hipLaunchKernelGGL(filter_to_s2d_kernel<float>, dim3(grid_for(total)), dim3(256), 0, st, (const float*)w,
-                       (float*)ws, s.K, s.R, s.S, s.C, g.R, g.S, s.sh, s.sw, total);
+                       (float*)ws, s.R, s.S, s.C, g.R, g.S, s.sh, s.sw, total);
   return hipGetLastError();
 }
 
@@ -451,8 +451,8 @@ hipError_t launch_s2d_to_filter_f32(const ConvShape& s, const ConvShape& g, cons
                                     int accumulate, hipStream_t st) {
   const int total = s.K * s.R * s.S * s.C;
   TraceScope ts("s2d_to_filter_f32_kernel", st, (double)total * (accumulate ? 12.0 : 8.0), WORK_BYTE);
-  hipLaunchKernelGGL(s2d_to_filter_f32_kernel, dim3(grid_for(total)), dim3(256), 0, st, dws, dw, s.K, s.R, s.S, s.C,
-                     g.R, g.S, s.sh, s.sw, accumulate, total);
+  hipLaunchKernelGGL(s2d_to_filter_f32_kernel, dim3(grid_for(total)), dim3(256), 0, st, dws, dw, s.R, s.S, s.C, g.R,
+                     g.S, s.sh, s.sw, accumulate, total);
   return hipGetLastError();
 }
 

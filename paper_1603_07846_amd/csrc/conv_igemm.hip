@@ -1616,7 +1616,6 @@ template <typename T>
 hipError_t conv_fwd_dispatch(const ConvShape& s, const void* x, const void* w, const float* bias, void* y,
                              int relu, int bwd, double flops, float* partial, const void* mask, hipStream_t st,
                              bool wt = false) {
-  constexpr int VEC = KT<T>::VEC;
   FwdArgs a;
   a.x = x; a.w = w; a.bias = bias; a.y = y; a.mask = mask;
   a.tap_major = 0;

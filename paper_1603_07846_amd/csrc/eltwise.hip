@@ -481,7 +481,7 @@ __global__ __launch_bounds__(256) void softmax_ce_mean_kernel(int B, float* __re
   red[threadIdx.x] = s;
   __syncthreads();
   for (int w = 128; w > 0; w >>= 1) {
-    if (threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
+    if ((int)threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
     __syncthreads();
   }
   if (threadIdx.x == 0) loss[0] = red[0] / (float)B;

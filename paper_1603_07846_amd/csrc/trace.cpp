@@ -58,7 +58,8 @@ TraceScope::TraceScope(const char* name, hipStream_t st, double work, int unit) 
 TraceScope::~TraceScope() {
   if (idx_ < 0) return;
   std::lock_guard<std::mutex> lk(g_mu);
-  if ((size_t)idx_ < g_records.size()) hipEventRecord(g_records[idx_].stop, st_);
+  // a failed record leaves this launch untimed; the trace is diagnostic only
+  if ((size_t)idx_ < g_records.size()) (void)hipEventRecord(g_records[idx_].stop, st_);
 }
 
 }  // namespace singa
