@@ -1652,8 +1652,9 @@ hipError_t conv_fwd_dispatch(const ConvShape& s, const void* x, const void* w, c
     a.partial = nullptr;
     // 64-tap K-tiles only for the 256 x 128 layout (the 256 x 96 one measured
     // faster at 32 taps, two workgroups per CU, on a 6400-tap reduction; the
-    // 256 x 256 one has LDS for three 32-tap stages only)
-    const bool deep = fwd_large_bk(narrow || wide ? 0 : a.Kg) == 64;
+    // 256 x 256 one has LDS for three 32-tap stages only and is never deep,
+    // whatever SINGA_FWD_BK says)
+    const bool deep = !wide && fwd_large_bk(narrow ? 0 : a.Kg) == 64;
     a.kt_per_split = (a.Kg + (deep ? 64 : 32) - 1) / (deep ? 64 : 32);  // one split: every K-tile of this depth
     a.tap_major = a.RS > 1 && s.C % (deep ? 64 : 32) == 0;
     TraceScope ts(fwd_large_name(bwd, deep, narrow, wide), st, flops, WORK_FLOP);
