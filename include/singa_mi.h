@@ -61,7 +61,12 @@ extern "C" {
 #define SINGA_ERR_HIP (-6)         /* the HIP runtime rejected a launch */
 
 typedef enum { SINGA_F32 = 0, SINGA_BF16 = 1 } singa_dtype;
-typedef enum { SINGA_NCHW = 0, SINGA_NHWC = 1 } singa_layout;
+/* SINGA_NHWC_S2D: the input of a strided convolution already in its
+ * space-to-depth form (see singa_space_to_depth); accepted as the input
+ * layout of singa_conv_fwd, singa_conv_bwd_filter and their workspace
+ * queries only, for the convolutions singa_space_to_depth_bytes reports a
+ * size for (filters, gradients and outputs then as for SINGA_NHWC). */
+typedef enum { SINGA_NCHW = 0, SINGA_NHWC = 1, SINGA_NHWC_S2D = 2 } singa_layout;
 typedef enum { SINGA_POOL_MAX = 0, SINGA_POOL_AVG = 1 } singa_pool_mode;
 typedef enum {
   SINGA_OP_FWD = 0,
@@ -112,7 +117,8 @@ int singa_conv_workspace_bytes(int op, singa_dtype dtype, singa_layout layout,
  * cross-correlation as in Caffe's im2col that SINGA adopts (Sec. 6.2.1):
  *   y[n,k,p,q] = bias[k] + sum_{c,r,s} W[k,c,r,s] * x[n,c,p*sh-ph+r, q*sw-pw+s]
  * with zero padding, then y = max(y, 0) if fuse_relu.
- *   x_ptr : dtype, shape *x in `layout`            (read)
+ *   x_ptr : dtype, shape *x in `layout`            (read; with SINGA_NHWC_S2D
+ *           the output of singa_space_to_depth for this convolution)
  *   w_ptr : dtype, shape *w (KRSC for NHWC, KCRS for NCHW)   (read)
  *   bias  : fp32[w->k] or NULL                      (read)
  *   y_ptr : dtype, shape singa_conv_out_shape()     (written)
@@ -124,6 +130,25 @@ int singa_conv_fwd(singa_dtype dtype, singa_layout layout,
                    const singa_filter4* w, const void* w_ptr, const float* bias,
                    const singa_conv_desc* d, void* y_ptr, int fuse_relu,
                    void* ws, size_t ws_bytes, singa_stream stream);
+
+/* Space-to-depth form of a strided convolution's NHWC input, for callers
+ * that pass the same input to both singa_conv_fwd and singa_conv_bwd_filter
+ * (the first layer of a network): each of those calls otherwise builds this
+ * form itself in its workspace.  With stride (sh, sw), padding (ph, pw),
+ * R' = ceil(R/sh), S' = ceil(S/sw), P x Q the output extents:
+ *   xs[n][h'][w'][(dh*sw + dw)*C + c] = x[n][sh*h' + dh - ph][sw*w' + dw - pw][c]
+ *   (0 outside x), h' < P + R' - 1, w' < Q + S' - 1, dh < sh, dw < sw,
+ * and the convolution equals the stride-1 unpadded convolution of xs with
+ * the filter rearranged the same way (the library rearranges it).
+ *   x_ptr  : dtype, shape *x, NHWC                  (read)
+ *   xs_ptr : dtype, singa_space_to_depth_bytes() bytes, 16-byte aligned (written)
+ * Errors: NULL, SHAPE, ALIGN, UNSUPPORTED (this convolution is not run on
+ * the space-to-depth form: singa_space_to_depth_bytes reports 0), HIP. */
+int singa_space_to_depth_bytes(singa_dtype dtype, const singa_shape4* x, const singa_filter4* w,
+                               const singa_conv_desc* d, size_t* bytes);
+int singa_space_to_depth(singa_dtype dtype, const singa_shape4* x, const void* x_ptr,
+                         const singa_filter4* w, const singa_conv_desc* d, void* xs_ptr,
+                         singa_stream stream);
 
 /* Convolution ComputeGradient, gradient of the source layer (Sec. 4.1.2):
  *   dx[n,c,h,w] = sum over (k,r,s,p,q) with p*sh-ph+r = h, q*sw-pw+s = w
@@ -147,7 +172,7 @@ int singa_conv_bwd_data(singa_dtype dtype, singa_layout layout,
 /* Convolution ComputeGradient, Param gradients (Sec. 4.1.2):
  *   dW[k,c,r,s] = sum_{n,p,q} dy[n,k,p,q] * x[n,c,p*sh-ph+r, q*sw-pw+s]
  *   db[k]       = sum_{n,p,q} dy[n,k,p,q]
- *   x_ptr  : dtype, shape *x                        (read)
+ *   x_ptr  : dtype, shape *x (SINGA_NHWC_S2D: its space-to-depth form)  (read)
  *   dy_ptr : dtype, shape singa_conv_out_shape()    (read)
  *   dw     : fp32, shape *w in the filter layout    (written, or added to)
  *   db     : fp32[w->k] or NULL                     (written, or added to)

@@ -152,6 +152,13 @@ bool bwd_data_s2d(const ConvShape& s, ConvShape* g) {
   return s2d_fits(*g);
 }
 
+// A convolution whose input may be given in the space-to-depth layout: the
+// ones input_rewrite runs on that form.
+bool s2d_input_ok(const ConvShape& s, int dt) {
+  ConvShape g;
+  return input_rewrite(s, dt, &g) == RW_S2D;
+}
+
 // One function computes both the size and the layout of every workspace, so
 // the two can never disagree.
 struct FwdWs { void *x, *w, *y, *xp, *wp; float* partial; };
@@ -169,7 +176,8 @@ size_t carve_fwd(const ConvShape& s, int dt, int layout, void* ws, FwdWs* o) {
   }
   ConvShape g;
   if (input_rewrite(s, dt, &g) != RW_NONE) {
-    o->xp = c.take((size_t)g.N * g.H * g.W * g.C * dt_size(dt));
+    // an input given in the space-to-depth layout is the rewritten input
+    if (layout != SINGA_NHWC_S2D) o->xp = c.take((size_t)g.N * g.H * g.W * g.C * dt_size(dt));
     o->wp = c.take((size_t)g.K * g.R * g.S * g.C * dt_size(dt));
   }
   const size_t pb = fwd_partial_bytes(g, dt);
@@ -178,9 +186,9 @@ size_t carve_fwd(const ConvShape& s, int dt, int layout, void* ws, FwdWs* o) {
 }
 
 // NHWC forward on (x, w): through the rewritten input and filter when
-// input_rewrite says so.
+// input_rewrite says so (x_s2d: x is already the space-to-depth input).
 hipError_t conv_fwd_nhwc(int dt, const ConvShape& s, const void* x, const void* w, const float* bias, void* y,
-                         int relu, const FwdWs& o, hipStream_t st) {
+                         int relu, const FwdWs& o, hipStream_t st, bool x_s2d = false) {
   ConvShape g;
   const Rewrite rw = input_rewrite(s, dt, &g);
   if (rw == RW_NONE) return launch_conv_fwd(dt, s, x, w, bias, y, relu, 0, conv_flops(s), o.partial, nullptr, st);
@@ -189,11 +197,11 @@ hipError_t conv_fwd_nhwc(int dt, const ConvShape& s, const void* x, const void* 
     e = launch_pad_channels(dt, x, o.xp, (long)s.N * s.H * s.W, s.C, g.C, st);
     if (e == hipSuccess) e = launch_pad_channels(dt, w, o.wp, (long)s.K * s.R * s.S, s.C, g.C, st);
   } else {
-    e = launch_space_to_depth(dt, s, g, x, o.xp, st);
+    e = x_s2d ? hipSuccess : launch_space_to_depth(dt, s, g, x, o.xp, st);
     if (e == hipSuccess) e = launch_filter_to_s2d(dt, s, g, w, o.wp, st);
   }
   if (e == hipSuccess)
-    e = launch_conv_fwd(dt, g, o.xp, o.wp, bias, y, relu, 0, conv_flops(s), o.partial, nullptr, st);
+    e = launch_conv_fwd(dt, g, x_s2d ? x : o.xp, o.wp, bias, y, relu, 0, conv_flops(s), o.partial, nullptr, st);
   return e;
 }
 
@@ -232,7 +240,7 @@ size_t carve_bwd_filter(const ConvShape& s, int dt, int layout, bool bias, void*
   }
   ConvShape g;
   if (input_rewrite(s, dt, &g) != RW_NONE) {
-    o->xp = c.take((size_t)g.N * g.H * g.W * g.C * dt_size(dt));
+    if (layout != SINGA_NHWC_S2D) o->xp = c.take((size_t)g.N * g.H * g.W * g.C * dt_size(dt));
     o->dwp = (float*)c.take((size_t)g.K * g.R * g.S * g.C * sizeof(float));
   }
   const size_t pb = wgrad_partial_bytes(g, dt, bias);
@@ -332,10 +340,12 @@ int singa_pool_out_shape(const singa_shape4* x, const singa_pool_desc* d, singa_
 int singa_conv_workspace_bytes(int op, singa_dtype dtype, singa_layout layout, const singa_shape4* x,
                                const singa_filter4* w, const singa_conv_desc* d, size_t* bytes) {
   if (!bytes) return SINGA_ERR_NULL;
-  if (!dtype_ok(dtype) || !layout_ok(layout)) return SINGA_ERR_UNSUPPORTED;
+  if (!dtype_ok(dtype) || !(layout_ok(layout) || layout == SINGA_NHWC_S2D)) return SINGA_ERR_UNSUPPORTED;
   ConvShape s;
   int rc = conv_geometry(x, w, d, &s);
   if (rc != SINGA_OK) return rc;
+  if (layout == SINGA_NHWC_S2D && !(s2d_input_ok(s, dtype) && (op == SINGA_OP_FWD || op == SINGA_OP_BWD_FILTER)))
+    return SINGA_ERR_UNSUPPORTED;
   switch (op) {
     case SINGA_OP_FWD: { FwdWs o; *bytes = carve_fwd(s, dtype, layout, nullptr, &o); break; }
     case SINGA_OP_BWD_DATA: { BwdDataWs o; *bytes = carve_bwd_data(s, dtype, layout, nullptr, &o); break; }
@@ -350,13 +360,39 @@ int singa_conv_workspace_bytes(int op, singa_dtype dtype, singa_layout layout, c
   return SINGA_OK;
 }
 
-int singa_conv_fwd(singa_dtype dtype, singa_layout layout, const singa_shape4* x, const void* x_ptr,
-                   const singa_filter4* w, const void* w_ptr, const float* bias, const singa_conv_desc* d,
-                   void* y_ptr, int fuse_relu, void* ws, size_t ws_bytes, singa_stream stream) {
-  if (!dtype_ok(dtype) || !layout_ok(layout)) return SINGA_ERR_UNSUPPORTED;
+int singa_space_to_depth_bytes(singa_dtype dtype, const singa_shape4* x, const singa_filter4* w,
+                               const singa_conv_desc* d, size_t* bytes) {
+  if (!bytes) return SINGA_ERR_NULL;
+  if (!dtype_ok(dtype)) return SINGA_ERR_UNSUPPORTED;
   ConvShape s;
   int rc = conv_geometry(x, w, d, &s);
   if (rc != SINGA_OK) return rc;
+  ConvShape g;
+  *bytes = input_rewrite(s, dtype, &g) == RW_S2D ? (size_t)g.N * g.H * g.W * g.C * dt_size(dtype) : 0;
+  return SINGA_OK;
+}
+
+int singa_space_to_depth(singa_dtype dtype, const singa_shape4* x, const void* x_ptr, const singa_filter4* w,
+                         const singa_conv_desc* d, void* xs_ptr, singa_stream stream) {
+  if (!dtype_ok(dtype)) return SINGA_ERR_UNSUPPORTED;
+  ConvShape s;
+  int rc = conv_geometry(x, w, d, &s);
+  if (rc != SINGA_OK) return rc;
+  ConvShape g;
+  if (input_rewrite(s, dtype, &g) != RW_S2D) return SINGA_ERR_UNSUPPORTED;
+  if (!x_ptr || !xs_ptr) return SINGA_ERR_NULL;
+  if (!aligned_to(x_ptr, dt_size(dtype)) || !aligned_to(xs_ptr, 16)) return SINGA_ERR_ALIGN;
+  return hip_status(launch_space_to_depth(dtype, s, g, x_ptr, xs_ptr, (hipStream_t)stream));
+}
+
+int singa_conv_fwd(singa_dtype dtype, singa_layout layout, const singa_shape4* x, const void* x_ptr,
+                   const singa_filter4* w, const void* w_ptr, const float* bias, const singa_conv_desc* d,
+                   void* y_ptr, int fuse_relu, void* ws, size_t ws_bytes, singa_stream stream) {
+  if (!dtype_ok(dtype) || !(layout_ok(layout) || layout == SINGA_NHWC_S2D)) return SINGA_ERR_UNSUPPORTED;
+  ConvShape s;
+  int rc = conv_geometry(x, w, d, &s);
+  if (rc != SINGA_OK) return rc;
+  if (layout == SINGA_NHWC_S2D && !s2d_input_ok(s, dtype)) return SINGA_ERR_UNSUPPORTED;
   if (!x_ptr || !w_ptr || !y_ptr) return SINGA_ERR_NULL;
   const size_t es = dt_size(dtype);
   if (!aligned_to(x_ptr, es) || !aligned_to(w_ptr, es) || !aligned_to(y_ptr, es) || !aligned_to(bias, 4) ||
@@ -367,7 +403,8 @@ int singa_conv_fwd(singa_dtype dtype, singa_layout layout, const singa_shape4* x
   if (need > 0 && (!ws || ws_bytes < need)) return SINGA_ERR_WORKSPACE;
   carve_fwd(s, dtype, layout, ws, &o);
   hipStream_t st = (hipStream_t)stream;
-  if (layout == SINGA_NHWC) return hip_status(conv_fwd_nhwc(dtype, s, x_ptr, w_ptr, bias, y_ptr, fuse_relu, o, st));
+  if (layout != SINGA_NCHW)
+    return hip_status(conv_fwd_nhwc(dtype, s, x_ptr, w_ptr, bias, y_ptr, fuse_relu, o, st, layout == SINGA_NHWC_S2D));
   hipError_t e = launch_nchw_to_nhwc(dtype, x_ptr, o.x, s.N, s.C, s.H, s.W, st);
   if (e == hipSuccess) e = kcrs_to_krsc(dtype, s, w_ptr, o.w, st);
   if (e == hipSuccess) e = conv_fwd_nhwc(dtype, s, o.x, o.w, bias, o.y, fuse_relu, o, st);
@@ -450,10 +487,11 @@ int singa_conv_bwd_data(singa_dtype dtype, singa_layout layout, const singa_shap
 int singa_conv_bwd_filter(singa_dtype dtype, singa_layout layout, const singa_shape4* x, const void* x_ptr,
                           const singa_filter4* w, const singa_conv_desc* d, const void* dy_ptr, float* dw,
                           float* db, int accumulate, void* ws, size_t ws_bytes, singa_stream stream) {
-  if (!dtype_ok(dtype) || !layout_ok(layout)) return SINGA_ERR_UNSUPPORTED;
+  if (!dtype_ok(dtype) || !(layout_ok(layout) || layout == SINGA_NHWC_S2D)) return SINGA_ERR_UNSUPPORTED;
   ConvShape s;
   int rc = conv_geometry(x, w, d, &s);
   if (rc != SINGA_OK) return rc;
+  if (layout == SINGA_NHWC_S2D && !s2d_input_ok(s, dtype)) return SINGA_ERR_UNSUPPORTED;
   if (!x_ptr || !dy_ptr || !dw) return SINGA_ERR_NULL;
   const size_t es = dt_size(dtype);
   if (!aligned_to(x_ptr, es) || !aligned_to(dy_ptr, es) || !aligned_to(dw, 4) || !aligned_to(db, 4) ||
@@ -478,10 +516,10 @@ int singa_conv_bwd_filter(singa_dtype dtype, singa_layout layout, const singa_sh
   ConvShape g;
   const Rewrite rw = input_rewrite(s, dtype, &g);
   if (rw == RW_PAD && e == hipSuccess) e = launch_pad_channels(dtype, xx, o.xp, (long)s.N * s.H * s.W, s.C, g.C, st);
-  if (rw == RW_S2D && e == hipSuccess) e = launch_space_to_depth(dtype, s, g, xx, o.xp, st);
-  if (rw != RW_NONE) xx = o.xp;
-  float* krsc = layout == SINGA_NHWC ? dw : o.dw;  // KRSC result
-  const int acc = layout == SINGA_NHWC ? accumulate : 0;
+  if (rw == RW_S2D && e == hipSuccess && layout != SINGA_NHWC_S2D) e = launch_space_to_depth(dtype, s, g, xx, o.xp, st);
+  if (rw != RW_NONE && layout != SINGA_NHWC_S2D) xx = o.xp;
+  float* krsc = layout != SINGA_NCHW ? dw : o.dw;  // KRSC result
+  const int acc = layout != SINGA_NCHW ? accumulate : 0;
   float* target = rw != RW_NONE ? o.dwp : krsc;  // the GEMM's (K, g.R, g.S, g.C) result
   const int tacc = rw != RW_NONE ? 0 : acc;
   // db is written in place by the GEMM's bias column, with the caller's accumulate

@@ -84,20 +84,32 @@ class ConvLayer(Layer):
         self.y = torch.empty(self.out_shape, dtype=dt, device=dev)
         self.dx = torch.empty(self.in_shape, dtype=dt, device=dev)
         self.x = None
+        # a strided layer that the library runs on the space-to-depth form of
+        # its input (the first layer): that form is built once per step and
+        # read by both the forward pass and the filter gradient
+        self.xs = None
+        if not fc and singa.space_to_depth_bytes(dt, self.in_shape, self.w_shape, self.pad, self.stride) > 0:
+            self.xs = torch.empty(singa.space_to_depth_shape(self.in_shape, self.w_shape, self.pad, self.stride),
+                                  dtype=dt, device=dev)
+        self.x_layout = "NHWC_S2D" if self.xs is not None else "NHWC"
         for op in (singa.OP_FWD, singa.OP_BWD_DATA, singa.OP_BWD_FILTER):
             net.need_workspace(singa.conv_workspace_bytes(op, dt, self.in_shape, self.w_shape, self.pad,
-                                                          self.stride))
+                                                          self.stride,
+                                                          self.x_layout if op != singa.OP_BWD_DATA else "NHWC"))
         net.ws_wgrad_bytes = max(net.ws_wgrad_bytes, singa.conv_workspace_bytes(
-            singa.OP_BWD_FILTER, dt, self.in_shape, self.w_shape, self.pad, self.stride))
+            singa.OP_BWD_FILTER, dt, self.in_shape, self.w_shape, self.pad, self.stride, self.x_layout))
 
     def bind(self, w, b, w_compute, dw, db, v, vb, b_compute):
         self.w, self.b, self.w_compute, self.dw, self.db = w, b, w_compute, dw, db
         self.v, self.vb, self.b_compute = v, vb, b_compute
 
     def compute_feature(self, x):
+        if self.xs is not None:
+            singa.space_to_depth(x, self.w_shape, self.pad, self.stride, out=self.xs)
+            x = self.xs
         self.x = x
         singa.conv_fwd(x, self.w_compute, self.b, self.pad, self.stride, relu=self.relu, out=self.y,
-                       workspace=self.net.workspace)
+                       workspace=self.net.workspace, layout=self.x_layout, x_shape=self.in_shape)
         return self.y
 
     def compute_gradient(self, dy, need_dx=True):
@@ -115,14 +127,16 @@ class ConvLayer(Layer):
         side = self.net.wgrad_stream
         if side is None:
             singa.conv_bwd_filter(self.x, dy, self.w_shape, self.pad, self.stride, with_bias=self.has_bias,
-                                  dw=self.dw, db=self.db, workspace=self.net.workspace)
+                                  dw=self.dw, db=self.db, workspace=self.net.workspace, layout=self.x_layout,
+                                  x_shape=self.in_shape)
         else:
             # the filter gradient on the second stream, beside this layer's
             # backward-data and the layers below (both only read dy and x)
             side.wait_stream(torch.cuda.current_stream(self.net.device))
             with torch.cuda.stream(side):
                 singa.conv_bwd_filter(self.x, dy, self.w_shape, self.pad, self.stride, with_bias=self.has_bias,
-                                      dw=self.dw, db=self.db, workspace=self.net.workspace_wgrad)
+                                      dw=self.dw, db=self.db, workspace=self.net.workspace_wgrad,
+                                      layout=self.x_layout, x_shape=self.in_shape)
         return self._bwd_data(dy, need_dx)
 
     def _bwd_data(self, dy, need_dx):

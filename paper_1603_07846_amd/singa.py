@@ -24,7 +24,7 @@ OK = 0
 ERRORS = {-1: "SINGA_ERR_NULL", -2: "SINGA_ERR_SHAPE", -3: "SINGA_ERR_UNSUPPORTED", -4: "SINGA_ERR_WORKSPACE",
           -5: "SINGA_ERR_ALIGN", -6: "SINGA_ERR_HIP"}
 F32, BF16 = 0, 1
-NCHW, NHWC = 0, 1
+NCHW, NHWC, NHWC_S2D = 0, 1, 2
 POOL_MAX, POOL_AVG = 0, 1
 OP_FWD, OP_BWD_DATA, OP_BWD_FILTER, OP_BWD_FILTER_SGD = 0, 1, 2, 3
 
@@ -33,7 +33,8 @@ EXPORTS = ["singa_strerror", "singa_conv_out_shape", "singa_pool_out_shape", "si
            "singa_conv_fwd", "singa_conv_bwd_data", "singa_conv_bwd_filter", "singa_conv_bwd_filter_sgd",
            "singa_pool_fwd", "singa_pool_bwd",
            "singa_relu_fwd", "singa_relu_bwd", "singa_softmax_ce", "singa_sgd_momentum_update",
-           "singa_adagrad_update", "singa_lrn_fwd", "singa_lrn_bwd",
+           "singa_adagrad_update", "singa_lrn_fwd", "singa_lrn_bwd", "singa_space_to_depth_bytes",
+           "singa_space_to_depth",
            "singa_trace_enable", "singa_trace_count", "singa_trace_get"]
 
 
@@ -148,12 +149,15 @@ def _layout(layout) -> int:
         return NHWC
     if layout in (NCHW, "NCHW"):
         return NCHW
+    if layout in (NHWC_S2D, "NHWC_S2D"):
+        return NHWC_S2D
     raise ValueError(layout)
 
 
 def _act_shape4(shape, layout) -> Shape4:
-    """Shape4 from a physical activation shape."""
-    if layout == NHWC:
+    """Shape4 from a physical activation shape (NHWC_S2D: the NHWC shape of
+    the input before its space-to-depth rewrite)."""
+    if layout in (NHWC, NHWC_S2D):
         n, h, w, c = shape
     else:
         n, c, h, w = shape
@@ -161,7 +165,7 @@ def _act_shape4(shape, layout) -> Shape4:
 
 
 def _filt4(shape, layout) -> Filter4:
-    if layout == NHWC:
+    if layout in (NHWC, NHWC_S2D):
         k, r, s, c = shape
     else:
         k, c, r, s = shape
@@ -169,7 +173,7 @@ def _filt4(shape, layout) -> Filter4:
 
 
 def _phys(s: Shape4, layout):
-    return (s.n, s.h, s.w, s.c) if layout == NHWC else (s.n, s.c, s.h, s.w)
+    return (s.n, s.h, s.w, s.c) if layout in (NHWC, NHWC_S2D) else (s.n, s.c, s.h, s.w)
 
 
 def _cdesc(pad, stride) -> ConvDesc:
@@ -215,15 +219,48 @@ def _workspace(nbytes, device, ws):
     return torch.empty(nbytes, dtype=torch.uint8, device=device)
 
 
-def conv_fwd(x, w, bias=None, pad=0, stride=1, relu=False, layout="NHWC", out=None, workspace=None):
-    """Convolution ComputeFeature: y = [relu](conv(x, w) + bias)."""
+def space_to_depth_shape(x_shape, w_shape, pad=0, stride=1):
+    """NHWC shape of the space-to-depth form of a convolution's NHWC input:
+    (N, P + ceil(R/sh) - 1, Q + ceil(S/sw) - 1, sh sw C)."""
+    n, _, _, c = x_shape
+    _, r, s_, _ = w_shape
+    sh, sw = _pair(stride)
+    p, q = conv_out_shape(x_shape, w_shape, pad, stride)[1:3]
+    return (n, p + (r + sh - 1) // sh - 1, q + (s_ + sw - 1) // sw - 1, c * sh * sw)
+
+
+def space_to_depth_bytes(dtype, x_shape, w_shape, pad=0, stride=1) -> int:
+    dt = dtype if isinstance(dtype, int) else (BF16 if dtype == torch.bfloat16 else F32)
+    out = ctypes.c_size_t(0)
+    _check("singa_space_to_depth_bytes", _lib().singa_space_to_depth_bytes(
+        dt, ctypes.byref(_act_shape4(x_shape, NHWC)), ctypes.byref(_filt4(w_shape, NHWC)),
+        ctypes.byref(_cdesc(pad, stride)), ctypes.byref(out)))
+    return int(out.value)
+
+
+def space_to_depth(x, w_shape, pad=0, stride=1, out=None):
+    """The space-to-depth form of the NHWC input x of a strided convolution
+    (layout "NHWC_S2D" of conv_fwd / conv_bwd_filter, with x_shape=x.shape)."""
+    shape = space_to_depth_shape(tuple(x.shape), tuple(w_shape), pad, stride)
+    xs = torch.empty(shape, dtype=x.dtype, device=x.device) if out is None else out
+    _check("singa_space_to_depth", _lib().singa_space_to_depth(
+        _dt(x), ctypes.byref(_act_shape4(x.shape, NHWC)), _ptr(x), ctypes.byref(_filt4(w_shape, NHWC)),
+        ctypes.byref(_cdesc(pad, stride)), _ptr(xs), _stream()))
+    return xs
+
+
+def conv_fwd(x, w, bias=None, pad=0, stride=1, relu=False, layout="NHWC", out=None, workspace=None, x_shape=None):
+    """Convolution ComputeFeature: y = [relu](conv(x, w) + bias).  With layout
+    "NHWC_S2D", x is space_to_depth()'s output and x_shape the NHWC shape of
+    the input it was made from."""
     lay = _layout(layout)
-    yshape = conv_out_shape(tuple(x.shape), tuple(w.shape), pad, stride, lay)
+    xs = tuple(x.shape) if lay != NHWC_S2D else tuple(x_shape)
+    yshape = conv_out_shape(xs, tuple(w.shape), pad, stride, NHWC if lay == NHWC_S2D else lay)
     y = torch.empty(yshape, dtype=x.dtype, device=x.device) if out is None else out
-    nbytes = conv_workspace_bytes(OP_FWD, _dt(x), tuple(x.shape), tuple(w.shape), pad, stride, lay)
+    nbytes = conv_workspace_bytes(OP_FWD, _dt(x), xs, tuple(w.shape), pad, stride, lay)
     ws = _workspace(nbytes, x.device, workspace)
     _check("singa_conv_fwd", _lib().singa_conv_fwd(
-        _dt(x), lay, ctypes.byref(_act_shape4(x.shape, lay)), _ptr(x), ctypes.byref(_filt4(w.shape, lay)), _ptr(w),
+        _dt(x), lay, ctypes.byref(_act_shape4(xs, lay)), _ptr(x), ctypes.byref(_filt4(w.shape, lay)), _ptr(w),
         _ptr(bias), ctypes.byref(_cdesc(pad, stride)), _ptr(y), int(bool(relu)), _ptr(ws),
         0 if ws is None else ws.numel(), _stream()))
     return y
@@ -247,18 +284,21 @@ def conv_bwd_data(dy, w, x_shape, pad=0, stride=1, layout="NHWC", out=None, work
 
 
 def conv_bwd_filter(x, dy, w_shape, pad=0, stride=1, layout="NHWC", with_bias=True, dw=None, db=None,
-                    accumulate=False, workspace=None):
-    """Convolution ComputeGradient, Param gradients (fp32 dw and db)."""
+                    accumulate=False, workspace=None, x_shape=None):
+    """Convolution ComputeGradient, Param gradients (fp32 dw and db).  With
+    layout "NHWC_S2D", x is space_to_depth()'s output and x_shape the NHWC
+    shape of the input it was made from."""
     lay = _layout(layout)
+    xs = tuple(x.shape) if lay != NHWC_S2D else tuple(x_shape)
     if dw is None:
         dw = torch.empty(tuple(w_shape), dtype=torch.float32, device=x.device)
     if with_bias and db is None:
         k = w_shape[0]
         db = torch.empty((k,), dtype=torch.float32, device=x.device)
-    nbytes = conv_workspace_bytes(OP_BWD_FILTER, _dt(x), tuple(x.shape), tuple(w_shape), pad, stride, lay)
+    nbytes = conv_workspace_bytes(OP_BWD_FILTER, _dt(x), xs, tuple(w_shape), pad, stride, lay)
     ws = _workspace(nbytes, x.device, workspace)
     _check("singa_conv_bwd_filter", _lib().singa_conv_bwd_filter(
-        _dt(x), lay, ctypes.byref(_act_shape4(x.shape, lay)), _ptr(x), ctypes.byref(_filt4(w_shape, lay)),
+        _dt(x), lay, ctypes.byref(_act_shape4(xs, lay)), _ptr(x), ctypes.byref(_filt4(w_shape, lay)),
         ctypes.byref(_cdesc(pad, stride)), _ptr(dy), _ptr(dw), _ptr(db if with_bias else None),
         int(bool(accumulate)), _ptr(ws), 0 if ws is None else ws.numel(), _stream()))
     return dw, (db if with_bias else None)

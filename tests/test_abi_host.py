@@ -24,7 +24,7 @@ def _declared():
 
 def test_every_declared_symbol_is_exported():
     names = _declared()
-    assert len(names) == 20
+    assert len(names) == 22
     lib = ctypes.CDLL(singa.lib()._name)
     for n in names:
         assert hasattr(lib, n), n
@@ -138,3 +138,45 @@ def test_bwd_filter_sgd_argument_errors():
     assert call(A, A, A, A, B, N, N, N) == -5
     assert call(B, A, A, A, N, N, N, N) == -5       # fused case: x needs 16 bytes
     assert call(A, A, A, A, N, N, N, N, dt=singa.F32) == -4  # unfused: staging workspace required
+
+
+def test_space_to_depth_layout_sizes_and_errors():
+    """The space-to-depth input form exists exactly for the convolutions the
+    library rewrites that way (strided, channels too few for vector loads,
+    rewritten channels enough); its size is N (P + ceil(R/s) - 1)
+    (Q + ceil(S/s) - 1) s^2 C elements; workspaces shrink by the rewritten
+    input the call no longer builds; other entry points reject the layout."""
+    conv1x, conv1w = (256, 227, 227, 3), (96, 11, 11, 3)
+    nbytes = singa.space_to_depth_bytes(singa.BF16, conv1x, conv1w, 0, 4)
+    assert nbytes == 256 * 57 * 57 * 48 * 2
+    assert singa.space_to_depth_shape(conv1x, conv1w, 0, 4) == (256, 57, 57, 48)
+    assert singa.space_to_depth_bytes(singa.BF16, (2, 33, 33, 3), (8, 7, 7, 3), 3, 4) == 2 * 10 * 10 * 48 * 2
+    # no rewrite: stride 1, or vector-friendly channels
+    assert singa.space_to_depth_bytes(singa.BF16, (256, 27, 27, 96), (256, 5, 5, 96), 2, 1) == 0
+    assert singa.space_to_depth_bytes(singa.BF16, (2, 35, 35, 16), (8, 11, 11, 16), 0, 4) == 0
+    for op in (singa.OP_FWD, singa.OP_BWD_FILTER):
+        nhwc = singa.conv_workspace_bytes(op, singa.BF16, conv1x, conv1w, 0, 4)
+        s2d = singa.conv_workspace_bytes(op, singa.BF16, conv1x, conv1w, 0, 4, layout="NHWC_S2D")
+        assert nhwc - s2d == nbytes
+    for op in (singa.OP_BWD_DATA, singa.OP_BWD_FILTER_SGD):
+        with pytest.raises(singa.SingaError) as e:
+            singa.conv_workspace_bytes(op, singa.BF16, conv1x, conv1w, 0, 4, layout="NHWC_S2D")
+        assert e.value.status == -3
+    with pytest.raises(singa.SingaError) as e:  # a convolution that is not rewritten
+        singa.conv_workspace_bytes(singa.OP_FWD, singa.BF16, (256, 27, 27, 96), (256, 5, 5, 96), 2, 1,
+                                   layout="NHWC_S2D")
+    assert e.value.status == -3
+    lib = singa.lib()
+    x, w, d = singa._act_shape4(conv1x, singa.NHWC), singa._filt4(conv1w, singa.NHWC), singa._cdesc(0, 4)
+    A, B = ctypes.c_void_p(1 << 20), ctypes.c_void_p((1 << 20) + 4)
+    assert lib.singa_space_to_depth(singa.BF16, ctypes.byref(x), A, ctypes.byref(w), ctypes.byref(d), None,
+                                    None) == -1
+    assert lib.singa_space_to_depth(singa.BF16, ctypes.byref(x), A, ctypes.byref(w), ctypes.byref(d), B,
+                                    None) == -5
+    d1 = singa._cdesc(2, 1)
+    x2, w2 = singa._act_shape4((256, 27, 27, 96), singa.NHWC), singa._filt4((256, 5, 5, 96), singa.NHWC)
+    assert lib.singa_space_to_depth(singa.BF16, ctypes.byref(x2), A, ctypes.byref(w2), ctypes.byref(d1), A,
+                                    None) == -3
+    # pooling and LRN do not take the layout
+    pd = singa._pdesc("max", 3, 2, 0, True)
+    assert lib.singa_pool_fwd(singa.BF16, singa.NHWC_S2D, ctypes.byref(x), A, ctypes.byref(pd), A, A, None) == -3

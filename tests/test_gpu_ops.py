@@ -235,6 +235,53 @@ def test_conv_bwd_filter_deterministic():
     assert torch.equal(a[0], c[0]) and torch.equal(a[1], c[1])
 
 
+def _s2d_reference(x_nhwc, R, S, pad, stride):
+    """The space-to-depth input written out from its definition (NHWC)."""
+    n, H, W, C = x_nhwc.shape
+    P, Q = (H + 2 * pad - R) // stride + 1, (W + 2 * pad - S) // stride + 1
+    Rs, Ss = -(-R // stride), -(-S // stride)
+    out = np.zeros((n, P + Rs - 1, Q + Ss - 1, stride * stride * C), x_nhwc.dtype)
+    for hq in range(P + Rs - 1):
+        for wq in range(Q + Ss - 1):
+            for dh in range(stride):
+                for dw in range(stride):
+                    h, w = stride * hq + dh - pad, stride * wq + dw - pad
+                    if 0 <= h < H and 0 <= w < W:
+                        c0 = (dh * stride + dw) * C
+                        out[:, hq, wq, c0:c0 + C] = x_nhwc[:, h, w, :]
+    return out
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("case", [(2, 3, 35, 35, 8, 11, 11, 0, 4), (2, 3, 33, 33, 8, 7, 7, 3, 4)],
+                         ids=["conv1-shrunk", "padded"])
+def test_space_to_depth_input_layout(case, dt):
+    """The caller-side space-to-depth input: its layout follows the
+    definition, and the forward pass and filter gradient computed from it are
+    bitwise those of the NHWC calls (which build the same form themselves)."""
+    N, C, H, W, K, R, S, pad, stride = case
+    x, w, b, dy = _conv_inputs(case, dt, 71)
+    xd, wd = nchw_to_dev(x, dt), kcrs_to_dev(w, dt)
+    xs = singa.space_to_depth(xd, tuple(wd.shape), pad, stride)
+    torch.cuda.synchronize()
+    ref = _s2d_reference(xd.float().cpu().numpy(), R, S, pad, stride)
+    assert np.array_equal(xs.float().cpu().numpy(), ref)
+    bias = torch.from_numpy(b).cuda()
+    y0 = singa.conv_fwd(xd, wd, bias, pad, stride, relu=True)
+    y1 = singa.conv_fwd(xs, wd, bias, pad, stride, relu=True, layout="NHWC_S2D", x_shape=tuple(xd.shape))
+    dyd = nchw_to_dev(dy, dt)
+    dw0, db0 = singa.conv_bwd_filter(xd, dyd, tuple(wd.shape), pad, stride)
+    dw1, db1 = singa.conv_bwd_filter(xs, dyd, tuple(wd.shape), pad, stride, layout="NHWC_S2D",
+                                     x_shape=tuple(xd.shape))
+    torch.cuda.synchronize()
+    assert torch.equal(y0, y1) and torch.equal(dw0, dw1) and torch.equal(db0, db1)
+    ref_y = oracle.relu_fwd(oracle.conv_fwd(x, w, b, pad=pad, stride=stride))
+    assert rel_l2(dev_to_nchw(y1), ref_y) <= TOL[dt]
+    ref_dw, ref_db = oracle.conv_bwd_filter(x, dy, w.shape, pad=pad, stride=stride)
+    assert rel_l2(filt_to_kcrs(dw1), ref_dw) <= TOL["f32"]
+    assert rel_l2(db1.cpu().numpy(), ref_db) <= TOL["f32"]
+
+
 # N, C, H, W, mode, k, stride, pad
 POOL_CASES = [
     (2, 32, 32, 32, "max", 3, 2, 0),   # CIFAR pool1 (ceil-mode edge windows)
