@@ -264,7 +264,7 @@ def test_space_to_depth_input_layout(case, dt):
     xd, wd = nchw_to_dev(x, dt), kcrs_to_dev(w, dt)
     xs = singa.space_to_depth(xd, tuple(wd.shape), pad, stride)
     torch.cuda.synchronize()
-    ref = _s2d_reference(xd.float().cpu().numpy(), R, S, pad, stride)
+    ref = _s2d_reference(np.ascontiguousarray(np.asarray(x, np.float32).transpose(0, 2, 3, 1)), R, S, pad, stride)
     assert np.array_equal(xs.float().cpu().numpy(), ref)
     bias = torch.from_numpy(b).cuda()
     y0 = singa.conv_fwd(xd, wd, bias, pad, stride, relu=True)
