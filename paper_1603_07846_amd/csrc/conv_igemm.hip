@@ -522,7 +522,8 @@ __global__ __launch_bounds__(NT) void conv_fwd_kernel(FwdArgs a) {
 // instruction writes 64 consecutive 16-byte slots) with no register staging.
 // Three LDS stages: the loads of K-tile k+2 are in flight while tile k is
 // multiplied; one barrier per K-tile.  LBK taps per K-tile: 64 (144 KB of
-// LDS, one workgroup per CU) or 32 (72 KB, two workgroups per CU).
+// LDS, one workgroup per CU) or 32 (72 KB, two workgroups per CU; the
+// 256 x 96 layout keeps two stages, 48 KB, three workgroups per CU).
 //
 // LDS rows (LBK * 2 bytes) are unpadded and XOR-swizzled: slot s of row r
 // holds the 16-byte tap chunk s ^ ((r / RPW) % SL), with SL slots per row and
@@ -579,8 +580,8 @@ __device__ __forceinline__ void block_barrier() { asm volatile("s_barrier" ::: "
 // of the 256 x 128 tile on the B side, for 256-column layers with enough
 // row tiles.
 template <bool BWD, int LBK, int WMW>
-__global__ __launch_bounds__(WMW == 8 ? 2 * NT : NT, (LBK == 32 && WMW != 8) ? 2 : 1) void conv_fwd_large_kernel(
-    FwdArgs a) {
+__global__ __launch_bounds__(WMW == 8 ? 2 * NT : NT, (LBK == 32 && WMW == 4) ? 3 : (LBK == 32 && WMW != 8) ? 2 : 1)
+void conv_fwd_large_kernel(FwdArgs a) {
   typedef LT<LBK> G;
   constexpr int NW = WMW == 8 ? 8 : 4;       // waves
   constexpr int BNT = WMW == 8 ? 256 : BN;   // tile columns
@@ -590,7 +591,11 @@ __global__ __launch_bounds__(WMW == 8 ? 2 * NT : NT, (LBK == 32 && WMW != 8) ? 2
   constexpr int ATILE = L_BM * G::RB, STAGE = ATILE + BNT * G::RB;
   constexpr int LOADS = AI + BI;  // 16-byte loads per thread per K-tile
   static_assert(AI * G::RPI == ABAND && BI * G::RPI == BBAND, "load bands");
-  __shared__ __attribute__((aligned(16))) char smem[L_STAGES * STAGE];
+  // LDS stages: K-tiles kt+1 .. kt+NS-1 are in flight while kt is multiplied.
+  // The 256 x 96 layout keeps two (48 KB, three workgroups per CU): measured
+  // 5 % faster on conv2's backward-data than three stages at two per CU.
+  constexpr int NS = (WMW == 4 && LBK == 32) ? 2 : L_STAGES;
+  __shared__ __attribute__((aligned(16))) char smem[NS * STAGE];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int L = xcd_remap(blockIdx.x, gridDim.x);
@@ -724,16 +729,16 @@ __global__ __launch_bounds__(WMW == 8 ? 2 * NT : NT, (LBK == 32 && WMW != 8) ? 2
   const int nkt = min(a.kt_per_split, nkt_all - split * a.kt_per_split);
   const int kend = kbase + nkt * LBK;  // K-tiles from here on are issued as all-OOB (zeros, no traffic)
 #pragma unroll
-  for (int j = 0; j < G::KS; ++j) issue_slice(taps(kbase), smem, j);
+  for (int s = 0; s < NS - 1; ++s)
 #pragma unroll
-  for (int j = 0; j < G::KS; ++j) issue_slice(taps(nkt > 1 ? kbase + LBK : a.Kg), smem + STAGE, j);
+    for (int j = 0; j < G::KS; ++j) issue_slice(taps(nkt > s ? kbase + s * LBK : a.Kg), smem + s * STAGE, j);
   int stage = 0;
   for (int kt = 0; kt < nkt; ++kt) {
-    wait_vmcnt<LOADS>();  // this thread's loads of tile kt have landed (tile kt+1's may be in flight)
-    block_barrier();      // ... and everyone's; everyone is also done with tile kt-1
-    const int nstage = stage == 0 ? 2 : stage - 1;
+    wait_vmcnt<(NS - 2) * LOADS>();  // this thread's loads of tile kt have landed (later tiles' may be in flight)
+    block_barrier();                 // ... and everyone's; everyone is also done with tile kt-1
+    const int nstage = stage == 0 ? NS - 1 : stage - 1;
     char* Ns = smem + nstage * STAGE;
-    const int knext = kbase + (kt + 2) * LBK;
+    const int knext = kbase + (kt + NS - 1) * LBK;
     const Taps t = taps(knext < kend ? knext : a.Kg);
     const char* S = smem + stage * STAGE;
     // fragments one k-step ahead; the loads of tile kt+2 spread over the k-steps
@@ -746,7 +751,7 @@ __global__ __launch_bounds__(WMW == 8 ? 2 * NT : NT, (LBK == 32 && WMW != 8) ? 2
       issue_slice(t, Ns, kc);
       if (kc + 1 < G::KS) f = g;
     }
-    stage = stage == 2 ? 0 : stage + 1;
+    stage = stage == NS - 1 ? 0 : stage + 1;
   }
   wait_vmcnt<0>();  // the trailing all-OOB loads still write LDS
 
@@ -774,6 +779,13 @@ __global__ __launch_bounds__(WMW == 8 ? 2 * NT : NT, (LBK == 32 && WMW != 8) ? 2
     store_quadrant<bf16_t, FM, FN, 0, 2>(acc, q, lane, m0 + wm * FM * 32, n0 + wn * FN * 32, a.M, a.Nn, a.bias,
                                          a.relu, a.mask, (bf16_t*)a.y, vec);
     store_quadrant<bf16_t, FM, FN, 2, 2>(acc, q, lane, m0 + wm * FM * 32 + 64, n0 + wn * FN * 32, a.M, a.Nn,
+                                         a.bias, a.relu, a.mask, (bf16_t*)a.y, vec);
+  } else if constexpr (NS == 2) {
+    // two LDS stages hold less than the quadrant: two passes of 32 rows
+    char* q = smem + wave * 32 * (FN * 32 * 2 + 16);
+    store_quadrant<bf16_t, FM, FN, 0, 1>(acc, q, lane, m0 + wm * FM * 32, n0 + wn * FN * 32, a.M, a.Nn, a.bias,
+                                         a.relu, a.mask, (bf16_t*)a.y, vec);
+    store_quadrant<bf16_t, FM, FN, 1, 1>(acc, q, lane, m0 + wm * FM * 32 + 32, n0 + wn * FN * 32, a.M, a.Nn,
                                          a.bias, a.relu, a.mask, (bf16_t*)a.y, vec);
   } else {
     store_quadrant<bf16_t, FM, FN>(acc, smem + wave * FM * 32 * (FN * 32 * 2 + 16), lane, m0 + wm * FM * 32,
