@@ -22,7 +22,9 @@ Then the same number of steps runs eagerly on one stream with the library's
 kernel trace on, which brackets every launch with HIP events: each kernel
 runs alone on the GPU, and the per-kernel figures (and the roofline of the
 dominant kernel) come from those.  A rocprofv3 summary whose average
-durations match these comes from a --single-stream run.
+durations match these comes from a --single-stream run.  Last, the step runs
+for one more second while a side thread reads the graphics clock (amdsmi),
+and the MFMA roofline is also priced at the clock measured (`sclk`).
 
 Prints one JSON line.
 """
@@ -71,6 +73,97 @@ def measured_traffic(kernel):
     if t.get("kernel") != kernel or not os.path.exists(src) or sha256_of(src) != t.get("source_sha256"):
         return None
     return round(t["bytes_per_launch"])
+
+
+class GfxClock:
+    """Reads the GPU's current graphics clock (SCLK, MHz) through the amdsmi
+    library while the step runs, so the MFMA peak (quoted at 2400 MHz) can also
+    be priced at the clock the kernels actually ran at.  The reading lags the
+    load by a hundred milliseconds or more (it can still show the idle clock
+    through a whole 50-step timed region that ran at full speed), so the clock
+    is taken over a separate run of the same steps after the timed regions,
+    from its second half.  Any failure (no amdsmi, no permission, several GPUs
+    with no match) leaves the figures null; it never stops the benchmark."""
+
+    NOMINAL_MHZ = 2400.0
+
+    def __init__(self, period_s=0.005):
+        self.period = period_s
+        self.h = None
+        self.err = None
+        self.vals = []
+        self.window = None
+        try:
+            import amdsmi
+            self.smi = amdsmi
+            amdsmi.amdsmi_init(amdsmi.AmdSmiInitFlags.INIT_AMD_GPUS)
+            hs = amdsmi.amdsmi_get_processor_handles()
+            if len(hs) == 1:
+                self.h = hs[0]
+            else:
+                import torch
+                p = torch.cuda.get_device_properties(0)
+                want = (getattr(p, "pci_domain_id", 0), getattr(p, "pci_bus_id", -1), getattr(p, "pci_device_id", -1))
+                for h in hs:
+                    dom, rest = amdsmi.amdsmi_get_gpu_device_bdf(h).split(":", 1)
+                    bus, devfn = rest.split(":")
+                    if (int(dom, 16), int(bus, 16), int(devfn.split(".")[0], 16)) == want:
+                        self.h = h
+                if self.h is None:
+                    self.err = "%d GPUs visible to amdsmi and none matches device 0" % len(hs)
+            if self.h is not None:
+                self.read()
+        except Exception as e:  # noqa: BLE001 - any failure only disables the figure
+            self.h, self.err = None, "%s: %s" % (type(e).__name__, (str(e).strip().splitlines() or [""])[-1].strip())
+
+    def read(self):
+        return float(self.smi.amdsmi_get_clock_info(self.h, self.smi.AmdSmiClkType.GFX)["clk"])
+
+    def steady(self, step, seconds=1.0, settle=0.5):
+        """Runs step() back to back for `seconds` while a side thread reads the
+        clock every period; keeps the readings taken after `settle` seconds."""
+        import threading
+        import torch
+        if self.h is None:
+            return
+        got, stop = [], threading.Event()
+        t0 = time.perf_counter()
+
+        def loop():
+            while not stop.is_set():
+                try:
+                    got.append((time.perf_counter() - t0, self.read()))
+                except Exception:  # noqa: BLE001
+                    return
+                stop.wait(self.period)
+
+        t = threading.Thread(target=loop, daemon=True)
+        t.start()
+        try:
+            n = 0
+            while time.perf_counter() - t0 < seconds:
+                step()
+                n += 1
+                if n % 8 == 0:  # bound the queue so the window is time on the GPU
+                    torch.cuda.synchronize()
+            torch.cuda.synchronize()
+        finally:
+            stop.set()
+            t.join()
+        self.vals = [v for ts, v in got if ts >= settle]
+        self.window = (seconds, settle, n)
+
+    def mhz(self):
+        return sum(self.vals) / len(self.vals) if self.vals else None
+
+    def summary(self):
+        if not self.vals:
+            return {"error": self.err or "no readings"}
+        return {"mhz_mean": round(self.mhz(), 1), "mhz_min": min(self.vals), "mhz_max": max(self.vals),
+                "samples": len(self.vals), "nominal_mhz": self.NOMINAL_MHZ,
+                "source": "amdsmi current GFX clock every %g ms over the last %g s of a %g s run of %d eager "
+                          "steps after the timed regions" % (self.period * 1e3, self.window[0] - self.window[1],
+                                                             self.window[0], self.window[2])}
 
 
 def cpu_baseline(w, n_images):
@@ -163,6 +256,9 @@ def main():
     singa.trace_enable(False)
     net.wgrad_stream = side
     recs = singa.trace_records()
+    # the graphics clock under the same load (outside every timed region)
+    clock = GfxClock()
+    clock.steady(eager_step)
 
     # per-kernel aggregates over the timed steps
     agg = {}
@@ -193,6 +289,12 @@ def main():
                  "frac": round(achieved / peak, 4), "traffic": measured_traffic(dom_name),
                  "avg_launch_ms": round(avg_ms, 4), "work_per_launch": per_launch,
                  "launches_per_step": dom["launches"] / args.steps})
+    # the MFMA peak scales with the graphics clock: the same fraction priced
+    # at the clock measured under the same steps
+    mhz = clock.mhz()
+    if roof["bound"] == "mfma" and mhz:
+        roof["peak_at_measured_sclk"] = round(peak * mhz / GfxClock.NOMINAL_MHZ, 1)
+        roof["frac_at_measured_sclk"] = round(achieved / roof["peak_at_measured_sclk"], 4)
 
     upd = agg.get("sgd_kernel")
     update = None
@@ -278,6 +380,9 @@ def main():
                    "parallelism": "none (1 GPU)"},
         "conv_fwd_bwd_tflops": round(conv_tflops, 2),
         "conv_frac_mfma_peak": round(conv_tflops / mfma_peak, 4),
+        "conv_frac_mfma_peak_at_measured_sclk": (round(conv_tflops / (mfma_peak * mhz / GfxClock.NOMINAL_MHZ), 4)
+                                                 if mhz else None),
+        "sclk": clock.summary(),
         "conv_gflop_per_step": round(conv_flops / args.steps / 1e9, 2),
         "conv_ms_per_step": round(conv_ms / args.steps, 4),
         "kernel_ms_per_step": round(kernel_ms / args.steps, 4),
