@@ -29,9 +29,15 @@ gradients go to the flat gradient buffer and one fused update over their
 (contiguous) part of the flat buffers follows the backward loop; the fresh
 values only reach any layer at the next iteration's forward, so this is the
 same computation, element for element.
+
+With ``concurrent_wgrad`` (the default on a GPU) the filter gradients, and
+the fused gradient + update of the fully connected layers, run on a second
+stream as soon as their inputs exist, beside the backward-data passes of the
+layers below; the backward loop ends by joining the two streams.
 """
 from __future__ import annotations
 
+import contextlib
 from typing import Dict, List, Optional
 
 import numpy as np
@@ -118,11 +124,18 @@ class ConvLayer(Layer):
             self._bwd_data(dy, need_dx)
             net, wl_ = self.net, self.net.wl
             keep = net.keep_grads
-            singa.conv_bwd_filter_sgd(
-                self.x, dy, self.w_shape, self.w, self.v, self.w_compute if net.wb_flat is not None else None,
-                b=self.b, vb=self.vb, b_bf16=self.b_compute, lr=wl_.lr, momentum=wl_.momentum,
-                weight_decay=wl_.weight_decay, pad=self.pad, stride=self.stride, dw=self.dw if keep else None,
-                db=self.db if keep else None, workspace=net.workspace)
+            side = net.wgrad_stream
+            # with a second stream, gradient + update run there, beside the
+            # backward passes of the layers below (which read neither this
+            # layer's weights nor write its x or dy)
+            if side is not None:
+                side.wait_stream(torch.cuda.current_stream(net.device))
+            with torch.cuda.stream(side) if side is not None else contextlib.nullcontext():
+                singa.conv_bwd_filter_sgd(
+                    self.x, dy, self.w_shape, self.w, self.v, self.w_compute if net.wb_flat is not None else None,
+                    b=self.b, vb=self.vb, b_bf16=self.b_compute, lr=wl_.lr, momentum=wl_.momentum,
+                    weight_decay=wl_.weight_decay, pad=self.pad, stride=self.stride, dw=self.dw if keep else None,
+                    db=self.db if keep else None, workspace=net.workspace if side is None else net.workspace_wgrad)
             return self.dx if need_dx else None
         side = self.net.wgrad_stream
         if side is None:
@@ -244,8 +257,9 @@ class Net:
         """fuse_update: apply the update inside the filter-gradient kernel
         where it can be fused; keep_grads: those layers also store their
         gradients in the flat gradient buffer (for inspection);
-        concurrent_wgrad: the other layers' filter gradients run on a second
-        stream, concurrently with the backward-data passes; updater: "sgd"
+        concurrent_wgrad: the filter gradients (with the fused update where
+        there is one) run on a second stream, concurrently with the
+        backward-data passes; updater: "sgd"
         (momentum, the workloads' Updater) or "adagrad" (Sec. 4.1.4's named
         protocol, with the workload's learning rate and weight decay; the
         momentum buffer holds its sums of squared gradients)."""
@@ -296,8 +310,7 @@ class Net:
         self.workspace = torch.empty(max(self.ws_bytes, 256), dtype=torch.uint8, device=self.device)
         # default priority, like every stream the library runs on
         self.wgrad_stream = None
-        if concurrent_wgrad and self.device.type == "cuda" and any(
-                not l.fused_update for l in self.layers if isinstance(l, ConvLayer)):
+        if concurrent_wgrad and self.device.type == "cuda" and any(isinstance(l, ConvLayer) for l in self.layers):
             self.wgrad_stream = torch.cuda.Stream(device=self.device)
             self.workspace_wgrad = torch.empty(max(self.ws_wgrad_bytes, 256), dtype=torch.uint8, device=self.device)
         self._build_params()

@@ -54,3 +54,29 @@ def test_graph_replay_matches_eager(index, batch):
         if eager.wb_flat is not None:
             assert torch.equal(graphed.wb_flat, eager.wb_flat), step
         assert np.isfinite(float(eager.layers[-1].loss[0]))
+
+
+@pytest.mark.parametrize("index,batch", [(5, 8), (5, 32), (6, 8)])
+def test_two_stream_eager_matches_one_stream(index, batch):
+    """The default step launched eagerly (filter gradients, and the fully
+    connected layers' fused gradient + update, on the second stream) against
+    one stream with every update after the backward loop: bit for bit, over
+    three steps, with no synchronization inside a step."""
+    from paper_1603_07846_amd import net as gnet
+    w = wl.WORKLOADS[index]
+    inp = wl.make_inputs(w, batch=batch, seed_offset=33)
+    one = gnet.Net(w, batch=batch, device="cuda:0", fuse_update=False, concurrent_wgrad=False)
+    two = gnet.Net(w, batch=batch, device="cuda:0")
+    assert two.wgrad_stream is not None and any(l.fused_update for l in two.param_layers())
+    for n in (one, two):
+        n.load_params(inp.params)
+    x = one.to_device_input(inp.x)
+    lab = torch.from_numpy(inp.labels).cuda()
+    for step in range(3):
+        one.train_one_batch(x, labels=lab)
+        two.train_one_batch(x, labels=lab)
+    torch.cuda.synchronize()
+    assert torch.equal(two.layers[-1].loss, one.layers[-1].loss)
+    assert torch.equal(two.w_flat, one.w_flat)
+    assert torch.equal(two.v_flat, one.v_flat)
+    assert torch.equal(two.wb_flat, one.wb_flat)
