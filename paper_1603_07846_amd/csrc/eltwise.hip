@@ -147,7 +147,10 @@ __global__ __launch_bounds__(256) void pool_bwd_kernel(PoolGeom g, int mode, con
 // NHWC pooling over 16-byte channel vectors: one thread per (output pixel,
 // VEC consecutive channels).  Same window scan and first-maximum rule as the
 // scalar kernel, applied per channel; the VEC argmax bytes are stored together.
-template <typename T, int VEC>
+// KS > 0: a KS x KS window known at compile time, whose KS^2 loads are all
+// issued before the scan (cells outside the input load a clamped, in-bounds
+// pixel and are skipped by the scan, which keeps the generic order).
+template <typename T, int VEC, int KS>
 __global__ __launch_bounds__(256) void pool_fwd_nhwc_vec_kernel(PoolGeom g, FastDiv dCV, FastDiv dQ, FastDiv dP,
                                                                 int mode, const T* __restrict__ x,
                                                                 T* __restrict__ y, uint8_t* __restrict__ argmax,
@@ -169,27 +172,46 @@ __global__ __launch_bounds__(256) void pool_fwd_nhwc_vec_kernel(PoolGeom g, Fast
       cell[j] = 0;
     }
     bool found = false;
-    for (int r = 0; r < g.kh; ++r) {
-      const int h = h0 + r;
-      if ((unsigned)h >= (unsigned)g.H) continue;
-      for (int s = 0; s < g.kw; ++s) {
-        const int w = w0 + s;
-        if ((unsigned)w >= (unsigned)g.W) continue;
-        union { uint4 u; T e[VEC]; } v;
-        v.u = *(const uint4*)(x + ((n * g.H + h) * g.W + w) * g.C + cv * VEC);
+    auto scan = [&](const uint4& u, int r, int s) {
+      union { uint4 u; T e[VEC]; } v;
+      v.u = u;
 #pragma unroll
-        for (int j = 0; j < VEC; ++j) {
-          const float f = ld_f<T>(&v.e[j]);
-          if (mode == 0) {
-            if (!found || f > best[j]) {
-              best[j] = f;
-              cell[j] = (uint8_t)(r * g.kw + s);
-            }
-          } else {
-            best[j] += f;
+      for (int j = 0; j < VEC; ++j) {
+        const float f = ld_f<T>(&v.e[j]);
+        if (mode == 0) {
+          if (!found || f > best[j]) {
+            best[j] = f;
+            cell[j] = (uint8_t)(r * g.kw + s);
           }
+        } else {
+          best[j] += f;
         }
-        found = true;
+      }
+      found = true;
+    };
+    if constexpr (KS > 0) {
+      uint4 v[KS * KS];
+#pragma unroll
+      for (int r = 0; r < KS; ++r)
+#pragma unroll
+        for (int s = 0; s < KS; ++s) {
+          const int h = min(max(h0 + r, 0), g.H - 1), w = min(max(w0 + s, 0), g.W - 1);
+          v[r * KS + s] = *(const uint4*)(x + ((n * g.H + h) * g.W + w) * g.C + cv * VEC);
+        }
+#pragma unroll
+      for (int r = 0; r < KS; ++r)
+#pragma unroll
+        for (int s = 0; s < KS; ++s)
+          if ((unsigned)(h0 + r) < (unsigned)g.H && (unsigned)(w0 + s) < (unsigned)g.W) scan(v[r * KS + s], r, s);
+    } else {
+      for (int r = 0; r < g.kh; ++r) {
+        const int h = h0 + r;
+        if ((unsigned)h >= (unsigned)g.H) continue;
+        for (int s = 0; s < g.kw; ++s) {
+          const int w = w0 + s;
+          if ((unsigned)w >= (unsigned)g.W) continue;
+          scan(*(const uint4*)(x + ((n * g.H + h) * g.W + w) * g.C + cv * VEC), r, s);
+        }
       }
     }
     union { uint4 u; T e[VEC]; } o;
@@ -756,12 +778,16 @@ hipError_t launch_pool_fwd(int dt, int mode, int N, int C, int H, int W, int P, 
     const unsigned grid = grid_for((size_t)tv);
     const FastDiv dCV = make_fastdiv((uint32_t)(C / vec)), dQ = make_fastdiv((uint32_t)Q),
                   dP = make_fastdiv((uint32_t)P);
-    if (dt == BF16)
-      hipLaunchKernelGGL((pool_fwd_nhwc_vec_kernel<bf16_t, 8>), dim3(grid), dim3(256), 0, st, g, dCV, dQ, dP, mode,
-                         (const bf16_t*)x, (bf16_t*)y, argmax, tv);
-    else
-      hipLaunchKernelGGL((pool_fwd_nhwc_vec_kernel<float, 4>), dim3(grid), dim3(256), 0, st, g, dCV, dQ, dP, mode,
-                         (const float*)x, (float*)y, argmax, tv);
+    const bool k3 = kh == 3 && kw == 3;
+#define POOL_FWD_VEC(T, V, KS)                                                                                  \
+  hipLaunchKernelGGL((pool_fwd_nhwc_vec_kernel<T, V, KS>), dim3(grid), dim3(256), 0, st, g, dCV, dQ, dP, mode, \
+                     (const T*)x, (T*)y, argmax, tv)
+    if (dt == BF16) {
+      if (k3) POOL_FWD_VEC(bf16_t, 8, 3); else POOL_FWD_VEC(bf16_t, 8, 0);
+    } else {
+      if (k3) POOL_FWD_VEC(float, 4, 3); else POOL_FWD_VEC(float, 4, 0);
+    }
+#undef POOL_FWD_VEC
     return hipGetLastError();
   }
   const unsigned grid = grid_for((size_t)total);
