@@ -180,3 +180,27 @@ def test_space_to_depth_layout_sizes_and_errors():
     # pooling and LRN do not take the layout
     pd = singa._pdesc("max", 3, 2, 0, True)
     assert lib.singa_pool_fwd(singa.BF16, singa.NHWC_S2D, ctypes.byref(x), A, ctypes.byref(pd), A, A, None) == -3
+
+
+def test_empty_and_degenerate_sizes_answered_before_any_launch():
+    """n = 0 element-wise calls and updates succeed without touching a
+    pointer (here NULL) or the GPU; an empty batch or class count, and every
+    NULL pointer of a non-empty call, are rejected before any launch."""
+    lib = singa.lib()
+    null = ctypes.c_void_p(0)
+    for dt in (singa.F32, singa.BF16):
+        assert lib.singa_relu_fwd(dt, ctypes.c_size_t(0), null, null, null) == 0
+        assert lib.singa_relu_bwd(dt, ctypes.c_size_t(0), null, null, null, null) == 0
+        assert lib.singa_relu_fwd(dt, ctypes.c_size_t(8), null, null, null) == -1
+        for batch, classes in ((0, 10), (4, 0), (-1, 10)):
+            assert lib.singa_softmax_ce(dt, batch, classes, null, null, null, null, null) == -2
+        assert lib.singa_softmax_ce(dt, 4, 10, null, null, null, null, null) == -1
+    f = ctypes.c_float
+    assert lib.singa_sgd_momentum_update(ctypes.c_size_t(0), null, null, null, null, f(0.01), f(0.9), f(5e-4),
+                                         null) == 0
+    assert lib.singa_sgd_momentum_update(ctypes.c_size_t(8), null, null, null, null, f(0.01), f(0.9), f(5e-4),
+                                         null) == -1
+    assert lib.singa_adagrad_update(ctypes.c_size_t(0), null, null, null, null, f(0.01), f(1e-6), f(5e-4),
+                                    null) == 0
+    assert lib.singa_adagrad_update(ctypes.c_size_t(8), null, null, null, null, f(0.01), f(1e-6), f(5e-4),
+                                    null) == -1
