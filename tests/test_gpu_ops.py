@@ -282,6 +282,21 @@ def test_space_to_depth_input_layout(case, dt):
     assert rel_l2(db1.cpu().numpy(), ref_db) <= TOL["f32"]
 
 
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("batch", [1, 3])
+def test_space_to_depth_alexnet_conv1_layout(batch, dt):
+    """AlexNet's first layer (227 x 227 x 3, 11 x 11 stride 4): the rewritten
+    input at full image size, bit for bit against the definition; an odd
+    batch puts the end of x inside a 16-byte chunk."""
+    x = wl.random_array((batch, 3, 227, 227), 72, "normal", 1.0, dt)
+    xd = nchw_to_dev(x, dt)
+    xs = singa.space_to_depth(xd, (96, 11, 11, 3), 0, 4)
+    torch.cuda.synchronize()
+    ref = _s2d_reference(np.ascontiguousarray(np.asarray(x, np.float32).transpose(0, 2, 3, 1)), 11, 11, 0, 4)
+    assert xs.shape == (batch, 57, 57, 48)
+    assert np.array_equal(xs.float().cpu().numpy(), ref)
+
+
 # N, C, H, W, mode, k, stride, pad
 POOL_CASES = [
     (2, 32, 32, 32, "max", 3, 2, 0),   # CIFAR pool1 (ceil-mode edge windows)
