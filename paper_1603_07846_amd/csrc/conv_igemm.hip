@@ -1779,18 +1779,19 @@ int wgrad_splits_for(const ConvShape& s, int dt, bool bias, bool large) {
   const long M = s.K, Ng = (long)s.R * s.S * s.C + (bias ? 1 : 0), T = (long)s.N * s.P * s.Q;
   if (large) {
     const long tiles = ((M + WL_BM - 1) / WL_BM) * ((Ng + WL_BN - 1) / WL_BN);
-    // about 640 workgroups (1.25 rounds at two per CU), 1280 for a long
-    // reduction over many tiles (at least 80,000 tile K-tiles: AlexNet's
-    // conv2, 116,640): measured per layer over 512 - 1280, the smaller
-    // layers lose more to partial tiles, the largest to its last round
-    // (SINGA_WGRAD_TARGET overrides the target)
+    // about 448 workgroups: one round a little under the 512 slots of two
+    // workgroups per CU, so that the backward-data passes that run beside
+    // the filter gradient on another stream keep some CUs.  Measured on the
+    // AlexNet training step (two streams): 432 - 480 give the best step,
+    // 2.5 % faster than 640 (1280 for conv2) and 512, which fill the chip
+    // or spill into a second round (SINGA_WGRAD_TARGET overrides the target)
     static const long forced = [] {
       const char* e = getenv("SINGA_WGRAD_TARGET");
       const long v = e ? atol(e) : 0;
       return v > 0 ? v : 0L;
     }();
     const long nkt = (T + WL_BK - 1) / WL_BK;
-    const long target = forced ? forced : tiles * nkt >= 80000 ? 1280 : 640;
+    const long target = forced ? forced : 448;
     return wgrad_split_count(tiles, nkt, target);
   }
   const long tiles = ((M + BM - 1) / BM) * ((Ng + BN - 1) / BN);
