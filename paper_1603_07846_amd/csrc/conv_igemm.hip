@@ -1784,14 +1784,16 @@ int wgrad_splits_for(const ConvShape& s, int dt, bool bias, bool large) {
     // the filter gradient on another stream keep some CUs.  Measured on the
     // AlexNet training step (two streams): 432 - 480 give the best step,
     // 2.5 % faster than 640 (1280 for conv2) and 512, which fill the chip
-    // or spill into a second round (SINGA_WGRAD_TARGET overrides the target)
+    // or spill into a second round.  A layer of at most 4 output tiles takes
+    // 640 (AlexNet's conv1, whose long reduction runs last, with nothing
+    // beside it: 8 us per step faster).  SINGA_WGRAD_TARGET overrides both.
     static const long forced = [] {
       const char* e = getenv("SINGA_WGRAD_TARGET");
       const long v = e ? atol(e) : 0;
       return v > 0 ? v : 0L;
     }();
     const long nkt = (T + WL_BK - 1) / WL_BK;
-    const long target = forced ? forced : 448;
+    const long target = forced ? forced : tiles <= 4 ? 640 : 448;
     return wgrad_split_count(tiles, nkt, target);
   }
   const long tiles = ((M + BM - 1) / BM) * ((Ng + BN - 1) / BN);
