@@ -38,8 +38,12 @@
  *     up at the caller's next synchronization.
  *   - Validation happens before anything is enqueued: a non-zero return means
  *     no work was launched and no output was touched.
- *   - Functions are stateless and reentrant.  Concurrent calls on different
- *     streams must not share output or workspace buffers.
+ *   - Functions keep no state between calls and may be called from several
+ *     threads at once; the only process-wide state is the optional timing
+ *     trace (singa_trace_*), a switch the caller sets.  Concurrent calls on
+ *     different streams must not share output or workspace buffers.  The
+ *     dispatch rules (tile layouts, split counts) depend on the shapes only,
+ *     never on the environment.
  */
 #ifndef SINGA_MI_H
 #define SINGA_MI_H
@@ -247,10 +251,17 @@ int singa_pool_bwd(singa_dtype dtype, singa_layout layout,
 
 /* --------------------------------------------------------------------- ReLU */
 
-/* y = x > 0 ? x : 0 over n elements (in place allowed: y == x). */
+/* The rectified linear unit that follows every convolution of the
+ * CIFAR-shaped and AlexNet-shaped workloads (the cuda-convnet DCNN of
+ * Sec. 6.2.1 and the AlexNet variant of Sec. 6.3.1), as a layer of its own
+ * in the layer abstraction of Sec. 4.1.2 (Table 2 lists the neuron layers).
+ * ComputeFeature: y = x > 0 ? x : 0 over n elements (in place allowed:
+ * y == x).  x, y: dtype arrays of n elements, 16-byte aligned. */
 int singa_relu_fwd(singa_dtype dtype, size_t n, const void* x, void* y, singa_stream stream);
 
-/* dx = y > 0 ? dy : 0 over n elements (in place allowed: dx == dy). */
+/* ComputeGradient of the same layer: dx = y > 0 ? dy : 0 over n elements
+ * (the derivative at 0 is taken as 0; in place allowed: dx == dy).  y is the
+ * layer's output, dy the gradient at it; 16-byte aligned. */
 int singa_relu_bwd(singa_dtype dtype, size_t n, const void* y, const void* dy, void* dx,
                    singa_stream stream);
 

@@ -523,7 +523,8 @@ int singa_conv_bwd_filter(singa_dtype dtype, singa_layout layout, const singa_sh
   float* target = rw != RW_NONE ? o.dwp : krsc;  // the GEMM's (K, g.R, g.S, g.C) result
   const int tacc = rw != RW_NONE ? 0 : acc;
   // db is written in place by the GEMM's bias column, with the caller's accumulate
-  if (e == hipSuccess) e = launch_conv_wgrad(dtype, g, xx, dy, o.partial, target, db, tacc, accumulate, st);
+  if (e == hipSuccess)
+    e = launch_conv_wgrad(dtype, g, xx, dy, o.partial, target, db, tacc, accumulate, conv_flops(s), st);
   if (e == hipSuccess && rw == RW_PAD)
     e = launch_unpad_channels_f32(o.dwp, krsc, (long)s.K * s.R * s.S, g.C, s.C, acc, st);
   if (e == hipSuccess && rw == RW_S2D) e = launch_s2d_to_filter_f32(s, g, o.dwp, krsc, acc, st);

@@ -1498,19 +1498,32 @@ __global__ __launch_bounds__(256) void splitk_epilogue_vec_kernel(const float* _
   }
 }
 
-template <typename T> constexpr const char* tname();
-template <> constexpr const char* tname<float>() { return "f32"; }
-template <> constexpr const char* tname<bf16_t>() { return "bf16"; }
+// Layout and split overrides for A/B measurements (SINGA_CONV_TILE,
+// SINGA_FWD_BK, SINGA_FWD_WIDE, SINGA_WGRAD_ORDER, SINGA_WGRAD_TARGET): read
+// from the environment only in a library built with -DSINGA_TUNING.  The
+// default build ignores the environment; its dispatch rules are the tested
+// ones.
+#ifdef SINGA_TUNING
+inline const char* tuning_env(const char* name) { return getenv(name); }
+#else
+constexpr const char* tuning_env(const char*) { return nullptr; }
+#endif
 
-// "conv_fwd_kernel<dtype,modeA,modeB,bwd>" for each instance
-template <typename T, int AM, int BMD, bool BWD> const char* fwd_name() {
-  static char buf[48];
-  static bool init = false;
-  if (!init) {
-    snprintf(buf, sizeof buf, "conv_fwd_kernel<%s,%d,%d,%d>", tname<T>(), AM, BMD, (int)BWD);
-    init = true;
-  }
-  return buf;
+// "conv_fwd_kernel<dtype,modeA,modeB,bwd>" for each instance, as string
+// literals (the launch path writes no state)
+#define FWD_NAME(T, A, B, W) "conv_fwd_kernel<" T "," #A "," #B "," #W ">"
+#define FWD_NAME_W(T, A, B) {FWD_NAME(T, A, B, 0), FWD_NAME(T, A, B, 1)}
+#define FWD_NAME_B(T, A) {FWD_NAME_W(T, A, 0), FWD_NAME_W(T, A, 1), FWD_NAME_W(T, A, 2), FWD_NAME_W(T, A, 3)}
+#define FWD_NAME_A(T) {FWD_NAME_B(T, 0), FWD_NAME_B(T, 1), FWD_NAME_B(T, 2)}
+constexpr const char* kFwdNames[2][3][4][2] = {FWD_NAME_A("f32"), FWD_NAME_A("bf16")};
+#undef FWD_NAME_A
+#undef FWD_NAME_B
+#undef FWD_NAME_W
+#undef FWD_NAME
+static_assert(ELEM == 0 && VEC8 == 1 && VEC16 == 2 && BT16 == 3, "name table order");
+
+template <typename T, int AM, int BMD, bool BWD> constexpr const char* fwd_name() {
+  return kFwdNames[sizeof(T) == 2][AM][BMD][BWD];
 }
 
 template <typename T, int AM, int BMD, bool BWD>
@@ -1533,11 +1546,11 @@ const char* fwd_large_name(bool bwd, bool deep, bool narrow, bool wide) {
 // Workgroups of the 256 x 128 kernel per full round of the chip (one per CU)
 // against those of the 128 x 128 kernel (two per CU): the large tile is used
 // when it does not leave a much emptier last round.
-// SINGA_CONV_TILE=128 or =256 in the environment forces the tile choice
+// SINGA_CONV_TILE=128 or =256 forces the tile choice in a tuning build
 // (read once; anything else, or unset, keeps the automatic rule).
 int forced_tile() {
   static const int v = [] {
-    const char* e = getenv("SINGA_CONV_TILE");
+    const char* e = tuning_env("SINGA_CONV_TILE");
     return e ? atoi(e) : 0;
   }();
   return v;
@@ -1549,7 +1562,7 @@ int forced_tile() {
 // forces one.
 int fwd_large_bk(long Kg) {
   static const int forced = [] {
-    const char* e = getenv("SINGA_FWD_BK");
+    const char* e = tuning_env("SINGA_FWD_BK");
     return e ? atoi(e) : 0;
   }();
   if (forced == 32 || forced == 64) return forced;
@@ -1575,7 +1588,7 @@ bool use_large_fwd(long M, long Nn, long Kg) {
 // as the other's rounds of 512.  SINGA_FWD_WIDE=0|1 forces the choice.
 bool use_wide_fwd(long M, long Nn) {
   static const int forced = [] {
-    const char* e = getenv("SINGA_FWD_WIDE");
+    const char* e = tuning_env("SINGA_FWD_WIDE");
     return e ? atoi(e) : -1;
   }();
   if (Nn <= 96) return false;
@@ -1707,14 +1720,19 @@ hipError_t conv_fwd_dispatch(const ConvShape& s, const void* x, const void* w, c
   return hipGetLastError();
 }
 
-template <typename T, bool VA, int BMD, bool NF> const char* wgrad_name() {
-  static char buf[48];
-  static bool init = false;
-  if (!init) {
-    snprintf(buf, sizeof buf, "conv_wgrad_kernel<%s,%d,%d,%d>", tname<T>(), (int)VA, BMD, (int)NF);
-    init = true;
-  }
-  return buf;
+// "conv_wgrad_kernel<dtype,vector A,modeB,image fastest>", as literals
+#define WG_NAME(T, V, B, F) "conv_wgrad_kernel<" T "," #V "," #B "," #F ">"
+#define WG_NAME_F(T, V, B) {WG_NAME(T, V, B, 0), WG_NAME(T, V, B, 1)}
+#define WG_NAME_B(T, V) {WG_NAME_F(T, V, 0), WG_NAME_F(T, V, 1), WG_NAME_F(T, V, 2)}
+#define WG_NAME_V(T) {WG_NAME_B(T, 0), WG_NAME_B(T, 1)}
+constexpr const char* kWgradNames[2][2][3][2] = {WG_NAME_V("f32"), WG_NAME_V("bf16")};
+#undef WG_NAME_V
+#undef WG_NAME_B
+#undef WG_NAME_F
+#undef WG_NAME
+
+template <typename T, bool VA, int BMD, bool NF> constexpr const char* wgrad_name() {
+  return kWgradNames[sizeof(T) == 2][VA][BMD][NF];
 }
 
 template <typename T, bool VA, int BMD, bool NF>
@@ -1746,7 +1764,7 @@ void launch_wgrad_variant(bool va, int bm, const WgradArgs& a, dim3 grid, double
 // SINGA_WGRAD_ORDER=image|pixel forces one.
 bool use_image_fastest(const ConvShape& s, int bk, bool large) {
   static const int forced = [] {
-    const char* e = getenv("SINGA_WGRAD_ORDER");
+    const char* e = tuning_env("SINGA_WGRAD_ORDER");
     if (!e) return 0;
     return e[0] == 'p' ? 1 : e[0] == 'i' ? 2 : 0;  // pixel-major (image fastest) / image-major
   }();
@@ -1788,7 +1806,7 @@ int wgrad_splits_for(const ConvShape& s, int dt, bool bias, bool large) {
     // 640 (AlexNet's conv1, whose long reduction runs last, with nothing
     // beside it: 8 us per step faster).  SINGA_WGRAD_TARGET overrides both.
     static const long forced = [] {
-      const char* e = getenv("SINGA_WGRAD_TARGET");
+      const char* e = tuning_env("SINGA_WGRAD_TARGET");
       const long v = e ? atol(e) : 0;
       return v > 0 ? v : 0L;
     }();
@@ -1803,7 +1821,8 @@ int wgrad_splits_for(const ConvShape& s, int dt, bool bias, bool large) {
 
 template <typename T>
 hipError_t conv_wgrad_dispatch(const ConvShape& s, const void* x, const void* dy, float* partial, float* dw,
-                               float* db, int acc_dw, int acc_db, const SgdTargets* upd, hipStream_t st) {
+                               float* db, int acc_dw, int acc_db, const SgdTargets* upd, double flops,
+                               hipStream_t st) {
   constexpr int VEC = 16 / (int)sizeof(T);
   constexpr int DT = sizeof(T) == 2 ? BF16 : F32;
   WgradArgs a;
@@ -1841,7 +1860,6 @@ hipError_t conv_wgrad_dispatch(const ConvShape& s, const void* x, const void* dy
   a.update = upd != nullptr;
   if (upd) a.u = *upd;
   dim3 grid(a.tiles * splits);
-  const double flops = 2.0 * a.M * (double)a.Nn * (double)a.T;
   const bool nf = use_image_fastest(s, bk, large);
   if (large) {
     // "conv_wgrad_large_kernel<image fastest,update fused>"
@@ -1906,9 +1924,9 @@ size_t wgrad_partial_bytes(const ConvShape& s, int dt, bool bias) {
 }
 
 hipError_t launch_conv_wgrad(int dt, const ConvShape& s, const void* x, const void* dy, float* partial, float* dw,
-                             float* db, int acc_dw, int acc_db, hipStream_t st) {
-  if (dt == BF16) return conv_wgrad_dispatch<bf16_t>(s, x, dy, partial, dw, db, acc_dw, acc_db, nullptr, st);
-  return conv_wgrad_dispatch<float>(s, x, dy, partial, dw, db, acc_dw, acc_db, nullptr, st);
+                             float* db, int acc_dw, int acc_db, double flops, hipStream_t st) {
+  if (dt == BF16) return conv_wgrad_dispatch<bf16_t>(s, x, dy, partial, dw, db, acc_dw, acc_db, nullptr, flops, st);
+  return conv_wgrad_dispatch<float>(s, x, dy, partial, dw, db, acc_dw, acc_db, nullptr, flops, st);
 }
 
 bool wgrad_update_fusable(const ConvShape& s, int dt, bool bias) {
@@ -1919,7 +1937,9 @@ hipError_t launch_conv_wgrad_sgd(int dt, const ConvShape& s, const void* x, cons
                                  const SgdTargets& u, hipStream_t st) {
   if (dt != BF16 || !wgrad_update_fusable(s, dt, u.b != nullptr) || (uintptr_t)x % 16 || (uintptr_t)dy % 16)
     return hipErrorNotSupported;
-  return conv_wgrad_dispatch<bf16_t>(s, x, dy, nullptr, dw, u.b ? db : nullptr, 0, 0, &u, st);
+  // never a rewritten geometry: the GEMM's work is the layer's
+  const double flops = 2.0 * s.N * (double)s.P * s.Q * s.K * (double)s.R * s.S * s.C;
+  return conv_wgrad_dispatch<bf16_t>(s, x, dy, nullptr, dw, u.b ? db : nullptr, 0, 0, &u, flops, st);
 }
 
 }  // namespace singa

@@ -63,10 +63,11 @@ hipError_t launch_conv_fwd_wt(int dt, const ConvShape& s, const void* x, const v
 // kernel writes (or, with acc_dw / acc_db, adds into) dw and db directly;
 // otherwise it writes partial tiles into `partial` (wgrad_partial_bytes() of
 // workspace; NULL when that is 0) and a second kernel adds them in a fixed
-// order.
+// order.  `flops` is the algorithmic work of the layer pass this launch
+// carries out (s may be a rewritten geometry with zero taps).
 size_t wgrad_partial_bytes(const ConvShape& s, int dt, bool bias);
 hipError_t launch_conv_wgrad(int dt, const ConvShape& s, const void* x, const void* dy, float* partial, float* dw,
-                             float* db, int acc_dw, int acc_db, hipStream_t st);
+                             float* db, int acc_dw, int acc_db, double flops, hipStream_t st);
 
 // Parameters the filter-gradient kernel updates in place once a gradient
 // element is complete (SGD with momentum, one step per element): the fp32
