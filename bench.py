@@ -39,9 +39,45 @@ sys.path.insert(0, ROOT)
 
 PEAK = {"bf16_tflops": 2516.6, "f32_tflops": 157.3, "hbm_gbs": 8000.0}
 METRIC = "conv fwd+bwd TFLOP/s (% MFMA peak) and training images/sec, 1×MI355X"
-CONV_KERNELS = ("conv_fwd_kernel", "conv_fwd_large_kernel", "conv_wgrad_kernel", "bwd_data_direct_kernel")
-CONV_HELPERS = ("transpose_kernel", "splitk_reduce_kernel", "splitk_epilogue_kernel", "colsum_partial_kernel",
-                "colsum_final_kernel", "pad_channels_kernel", "unpad_channels_f32_kernel")
+# the GEMM kernels of the conv / FC passes (each tagged with its layer pass's
+# algorithmic flops) and the helper kernels those passes launch
+CONV_KERNELS = ("conv_fwd_kernel", "conv_fwd_large_kernel", "conv_wgrad_kernel", "conv_wgrad_large_kernel",
+                "bwd_data_direct_kernel")
+CONV_HELPERS = ("transpose_kernel", "transpose_vec_kernel", "splitk_reduce_kernel", "splitk_epilogue_kernel",
+                "splitk_epilogue_vec_kernel", "pad_channels_kernel", "unpad_channels_f32_kernel",
+                "space_to_depth_kernel", "filter_to_s2d_kernel", "s2d_to_filter_f32_kernel",
+                "depth_to_space_kernel")
+
+
+def is_conv_kernel(name):
+    """A conv / FC GEMM kernel (the name up to its template arguments)."""
+    return name.split("<")[0] in CONV_KERNELS
+
+
+def is_conv_helper(name):
+    return name.split("<")[0] in CONV_HELPERS
+
+
+def step_conv_flops(w, batch, need_input_grad=False):
+    """Algorithmic flops of the conv / FC passes of one step of workload w:
+    2 x the multiply-adds of the direct definition (padded taps included) for
+    the forward pass, the filter gradient and the input gradient of every
+    layer, except the first layer's input gradient, which training does not
+    need (counted only with need_input_grad)."""
+    from paper_1603_07846_amd import workloads as wl
+    total = 0.0
+    c, h, ww = w.in_shape
+    first = True
+    for l in w.layers:
+        if isinstance(l, (wl.Conv, wl.FC)):
+            k, p, q = l.out_shape
+            r, s = (l.kernel, l.kernel) if isinstance(l, wl.Conv) else (h, ww)
+            one = 2.0 * batch * p * q * k * c * r * s
+            total += one * (3 if (not first or need_input_grad) else 2)
+            first = False
+        if isinstance(l, (wl.Conv, wl.Pool, wl.FC)):
+            c, h, ww = l.out_shape
+    return total
 
 
 def parse():
@@ -55,6 +91,8 @@ def parse():
                     help="run every pass on one stream (no concurrent filter gradients), as the per-kernel pass does")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-images", type=int, default=8, help="images in the oracle's timed sample")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the other workloads' lines (single layer, CIFAR-shaped net, fp32 / bf16 conv stacks)")
     return ap.parse_args()
 
 
@@ -166,6 +204,70 @@ class GfxClock:
                                                              self.window[0], self.window[2])}
 
 
+CONFIG_NAMES = {1: "single_conv_layer_fwd_bwd_sgd_f32_b16", 2: "cifar_convnet_train_step_f32_b100",
+                3: "alexnet_conv_stack_fwd_bwd_f32_b128", 4: "alexnet_conv_stack_fwd_bwd_bf16_b256"}
+
+
+def measure_config(index, steps, warmup):
+    """One of the other workloads, timed on its own: `steps` eager steps
+    between two device synchronizations after `warmup` untimed ones (the
+    single-layer workload also computes its input gradient, as its three
+    passes define it), then the same steps with the kernel trace on.  The
+    step's algorithmic conv / FC flops over the step time and over the
+    summed conv-kernel time, against the peak of the workload's dtype."""
+    import torch
+    from paper_1603_07846_amd import net as gnet
+    from paper_1603_07846_amd import singa
+    from paper_1603_07846_amd import workloads as wl
+
+    w = wl.WORKLOADS[index]
+    dev = torch.device("cuda:0")
+    inp = wl.make_inputs(w)
+    net = gnet.Net(w, device=dev)
+    net.load_params(inp.params)
+    x = net.to_device_input(inp.x)
+    labels = torch.from_numpy(inp.labels).to(dev) if inp.labels is not None else None
+    dy = net.to_device_input(inp.dy) if inp.dy is not None else None
+    need_dx = index == 1
+
+    def step():
+        net.train_one_batch(x, labels=labels, dy_top=dy, need_input_grad=need_dx)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / steps
+    side = net.wgrad_stream
+    net.wgrad_stream = None
+    singa.trace_enable(True)
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    singa.trace_enable(False)
+    net.wgrad_stream = side
+    recs = singa.trace_records()
+    traced_flops = sum(r[2] for r in recs if is_conv_kernel(r[0])) / steps
+    conv_ms = sum(r[1] for r in recs if is_conv_kernel(r[0]) or is_conv_helper(r[0])) / steps
+    flops = step_conv_flops(w, net.batch, need_dx)
+    peak = PEAK["bf16_tflops"] if w.dtype == "bf16" else PEAK["f32_tflops"]
+    tf_step = flops / (ms / 1e3) / 1e12
+    tf_conv = flops / (conv_ms / 1e3) / 1e12
+    out = {"workload": CONFIG_NAMES[index], "description": w.name, "dtype": w.dtype, "batch": net.batch,
+           "ms_per_step": round(ms, 4), "images_per_s": round(net.batch / (ms / 1e3), 1),
+           "conv_gflop_per_step": round(flops / 1e9, 4), "traced_conv_gflop_per_step": round(traced_flops / 1e9, 4),
+           "tflops_over_step": round(tf_step, 3), "frac_peak_over_step": round(tf_step / peak, 4),
+           "conv_kernel_ms_per_step": round(conv_ms, 4), "tflops_over_conv_kernels": round(tf_conv, 3),
+           "frac_peak_over_conv_kernels": round(tf_conv / peak, 4), "peak_tflops": peak,
+           "steps": steps, "warmup": warmup}
+    del net, x, labels, dy
+    torch.cuda.empty_cache()
+    return out
+
+
 def cpu_baseline(w, n_images):
     """The oracle (fp64 C, OpenMP) on a bounded sample of the same step: the
     full forward/backward of `n_images` images of the workload plus the
@@ -236,6 +338,7 @@ def main():
     # launched eagerly (the step's two streams overlap more when launched
     # eagerly); `value` is the faster of the two
     graph_ms = None
+    graph = None
     if not args.eager:
         graph = net.capture(x, labels=labels, dy_top=dy)
         for _ in range(3):
@@ -267,8 +370,8 @@ def main():
         a["launches"] += 1
         a["ms"] += ms
         a["work"] += work
-    conv_flops = sum(a["work"] for n, a in agg.items() if n.startswith(CONV_KERNELS))
-    conv_ms = sum(a["ms"] for n, a in agg.items() if n.startswith(CONV_KERNELS + CONV_HELPERS))
+    conv_flops = sum(a["work"] for n, a in agg.items() if is_conv_kernel(n))
+    conv_ms = sum(a["ms"] for n, a in agg.items() if is_conv_kernel(n) or is_conv_helper(n))
     is_bf16 = w.dtype == "bf16"
     mfma_peak = PEAK["bf16_tflops"] if is_bf16 else PEAK["f32_tflops"]
     conv_tflops = conv_flops / (conv_ms / 1e3) / 1e12 if conv_ms > 0 else 0.0
@@ -397,6 +500,12 @@ def main():
         "lrn_alone": lrn,
         "kernels": kernels[:16],
     }
+    out["conv_gflop_per_step_algorithmic"] = round(step_conv_flops(w, net.batch) / 1e9, 2)
+    if not args.no_configs and args.workload in (5, 6):
+        graph = None
+        del net, x, labels, dy
+        torch.cuda.empty_cache()
+        out["configs"] = {str(i): measure_config(i, args.steps, args.warmup) for i in (1, 2, 3, 4)}
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, args.cpu_images)
     print(json.dumps(out), flush=True)

@@ -32,14 +32,24 @@ _i32p = ctypes.POINTER(ctypes.c_int32)
 _i64p = ctypes.POINTER(ctypes.c_int64)
 
 
-def build() -> str:
+# A checking build (sanitize=True: AddressSanitizer and UndefinedBehavior-
+# Sanitizer, every report fatal) loads only in a process that preloads the
+# ASan runtime; SINGA_ORACLE_LIB names the library to load instead of the
+# default build.
+SANITIZE_FLAGS = ["-O1", "-g", "-fsanitize=address,undefined", "-fno-sanitize-recover=undefined",
+                  "-fno-omit-frame-pointer"]
+
+
+def build(path: str = None, sanitize: bool = False) -> str:
     """Compile the oracle with gcc (always recompiles).  Returns the .so path."""
-    tmp = _LIB_PATH + ".tmp%d" % os.getpid()
-    cmd = ["gcc", "-O2", "-std=c99", "-fopenmp", "-fPIC", "-shared",
-           "-Wall", "-Wextra", "-o", tmp, _SRC, "-lm"]
+    path = _LIB_PATH if path is None else path
+    tmp = path + ".tmp%d" % os.getpid()
+    opt = SANITIZE_FLAGS if sanitize else ["-O2"]
+    cmd = (["gcc"] + opt + ["-std=c99", "-fopenmp", "-fPIC", "-shared", "-Wall", "-Wextra", "-o", tmp, _SRC,
+                            "-lm"])
     subprocess.run(cmd, check=True)
-    os.replace(tmp, _LIB_PATH)
-    return _LIB_PATH
+    os.replace(tmp, path)
+    return path
 
 
 def _load():
@@ -47,9 +57,10 @@ def _load():
     with _lock:
         if _lib is not None:
             return _lib
-        if not os.path.exists(_LIB_PATH):
+        path = os.environ.get("SINGA_ORACLE_LIB") or _LIB_PATH
+        if path == _LIB_PATH and not os.path.exists(_LIB_PATH):
             build()
-        lib = ctypes.CDLL(_LIB_PATH)
+        lib = ctypes.CDLL(path)
         geo = [_i64] * 11
         lib.oracle_conv_out.argtypes = [_i64] * 4
         lib.oracle_conv_out.restype = _i64

@@ -87,16 +87,16 @@ class ConvLayer(Layer):
         # update fused into the filter-gradient kernel (no workspace needed exactly then)
         self.fused_update = bool(net.fuse_update and net.wl.update and net.updater == "sgd" and singa.conv_workspace_bytes(
             singa.OP_BWD_FILTER_SGD, dt, self.in_shape, self.w_shape, self.pad, self.stride) == 0)
-        self.y = torch.empty(self.out_shape, dtype=dt, device=dev)
-        self.dx = torch.empty(self.in_shape, dtype=dt, device=dev)
+        self.y = singa.empty(self.out_shape, dt, dev)
+        self.dx = singa.empty(self.in_shape, dt, dev)
         self.x = None
         # a strided layer that the library runs on the space-to-depth form of
         # its input (the first layer): that form is built once per step and
         # read by both the forward pass and the filter gradient
         self.xs = None
         if not fc and singa.space_to_depth_bytes(dt, self.in_shape, self.w_shape, self.pad, self.stride) > 0:
-            self.xs = torch.empty(singa.space_to_depth_shape(self.in_shape, self.w_shape, self.pad, self.stride),
-                                  dtype=dt, device=dev)
+            self.xs = singa.empty(singa.space_to_depth_shape(self.in_shape, self.w_shape, self.pad, self.stride),
+                                  dt, dev)
         self.x_layout = "NHWC_S2D" if self.xs is not None else "NHWC"
         for op in (singa.OP_FWD, singa.OP_BWD_DATA, singa.OP_BWD_FILTER):
             net.need_workspace(singa.conv_workspace_bytes(op, dt, self.in_shape, self.w_shape, self.pad,
@@ -169,9 +169,9 @@ class PoolLayer(Layer):
         self.in_shape = tuple(in_shape)
         self.out_shape = singa.pool_out_shape(self.in_shape, self.mode, self.k, self.stride, self.pad, self.ceil)
         dev, dt = net.device, net.dtype
-        self.y = torch.empty(self.out_shape, dtype=dt, device=dev)
-        self.argmax = torch.empty(self.out_shape, dtype=torch.uint8, device=dev) if self.mode == "max" else None
-        self.dx = torch.empty(self.in_shape, dtype=dt, device=dev)
+        self.y = singa.empty(self.out_shape, dt, dev)
+        self.argmax = singa.empty(self.out_shape, torch.uint8, dev) if self.mode == "max" else None
+        self.dx = singa.empty(self.in_shape, dt, dev)
         self.relu_src = None  # the ReLU layer feeding this max pooling, whose backward folds in
 
     def compute_feature(self, x):
@@ -192,7 +192,7 @@ class ReluLayer(Layer):
         self.out_shape = tuple(in_shape)
         self.y = None
         if fused_into is None:
-            self.y = torch.empty(self.out_shape, dtype=net.dtype, device=net.device)
+            self.y = singa.empty(self.out_shape, net.dtype, net.device)
 
     def compute_feature(self, x):
         if self.fused is not None:
@@ -216,8 +216,8 @@ class LrnLayer(Layer):
         self.name = spec.name
         self.args = (spec.size, spec.alpha, spec.beta, spec.k)
         self.in_shape = self.out_shape = tuple(in_shape)
-        self.y = torch.empty(self.out_shape, dtype=net.dtype, device=net.device)
-        self.dx = torch.empty(self.in_shape, dtype=net.dtype, device=net.device)
+        self.y = singa.empty(self.out_shape, net.dtype, net.device)
+        self.dx = singa.empty(self.in_shape, net.dtype, net.device)
         self.x = None
 
     def compute_feature(self, x):
@@ -234,8 +234,8 @@ class SoftmaxCELayer(Layer):
     def __init__(self, net, spec, in_shape):
         self.name = spec.name
         self.in_shape = tuple(in_shape)
-        self.loss = torch.empty((in_shape[0] + 1,), dtype=torch.float32, device=net.device)  # mean, then rows
-        self.dz = torch.empty(self.in_shape, dtype=net.dtype, device=net.device)
+        self.loss = singa.empty((in_shape[0] + 1,), torch.float32, net.device)  # mean, then rows
+        self.dz = singa.empty(self.in_shape, net.dtype, net.device)
         self.labels = None
         self.out_shape = (1,)
 
@@ -307,12 +307,12 @@ class Net:
             shape = layer.out_shape
             prev = layer
         self.out_shape = shape
-        self.workspace = torch.empty(max(self.ws_bytes, 256), dtype=torch.uint8, device=self.device)
+        self.workspace = singa.empty((max(self.ws_bytes, 256),), torch.uint8, self.device)
         # default priority, like every stream the library runs on
         self.wgrad_stream = None
         if concurrent_wgrad and self.device.type == "cuda" and any(isinstance(l, ConvLayer) for l in self.layers):
             self.wgrad_stream = torch.cuda.Stream(device=self.device)
-            self.workspace_wgrad = torch.empty(max(self.ws_wgrad_bytes, 256), dtype=torch.uint8, device=self.device)
+            self.workspace_wgrad = singa.empty((max(self.ws_wgrad_bytes, 256),), torch.uint8, self.device)
         self._build_params()
 
     def need_workspace(self, nbytes: int):
@@ -332,10 +332,10 @@ class Net:
         self.n_params_padded = total
         self.n_params = sum(o[1] + o[3] for o in offs)
         dev = self.device
-        self.w_flat = torch.zeros(total, dtype=torch.float32, device=dev)
-        self.g_flat = torch.zeros(total, dtype=torch.float32, device=dev)
-        self.v_flat = torch.zeros(total, dtype=torch.float32, device=dev)
-        self.wb_flat = torch.zeros(total, dtype=torch.bfloat16, device=dev) if self.dtype == torch.bfloat16 else None
+        self.w_flat = singa.empty((total,), torch.float32, dev).zero_()
+        self.g_flat = singa.empty((total,), torch.float32, dev).zero_()
+        self.v_flat = singa.empty((total,), torch.float32, dev).zero_()
+        self.wb_flat = singa.empty((total,), torch.bfloat16, dev).zero_() if self.dtype == torch.bfloat16 else None
         self.offsets = offs
         for l, (ow, nw, ob, nb) in zip(self.param_layers(), offs):
             l.flat_range = (ow, ob + _pad(nb))  # the layer's weights and bias, padding included

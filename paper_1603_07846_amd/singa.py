@@ -119,6 +119,28 @@ def lib():
     return _lib()
 
 
+def _torch_empty(shape, dtype, device):
+    return torch.empty(shape, dtype=dtype, device=device)
+
+
+_ALLOC = _torch_empty
+
+
+def empty(shape, dtype, device):
+    """Device memory for an output or workspace tensor.  Every output and
+    workspace this module (and the step driver) allocates comes from here,
+    so a test can substitute an allocator that surrounds each tensor with
+    guard bands (set_allocator)."""
+    return _ALLOC(tuple(int(d) for d in shape), dtype, device)
+
+
+def set_allocator(fn=None):
+    """Replace the tensor allocator behind empty() (fn(shape, dtype, device)
+    -> a contiguous tensor of that shape); None restores torch.empty."""
+    global _ALLOC
+    _ALLOC = _torch_empty if fn is None else fn
+
+
 def _check(fn, status):
     if status != OK:
         raise SingaError(fn, status)
@@ -216,7 +238,7 @@ def _workspace(nbytes, device, ws):
         return None
     if ws is not None:
         return ws
-    return torch.empty(nbytes, dtype=torch.uint8, device=device)
+    return empty((nbytes,), torch.uint8, device)
 
 
 def space_to_depth_shape(x_shape, w_shape, pad=0, stride=1):
@@ -242,7 +264,7 @@ def space_to_depth(x, w_shape, pad=0, stride=1, out=None):
     """The space-to-depth form of the NHWC input x of a strided convolution
     (layout "NHWC_S2D" of conv_fwd / conv_bwd_filter, with x_shape=x.shape)."""
     shape = space_to_depth_shape(tuple(x.shape), tuple(w_shape), pad, stride)
-    xs = torch.empty(shape, dtype=x.dtype, device=x.device) if out is None else out
+    xs = empty(shape, x.dtype, x.device) if out is None else out
     _check("singa_space_to_depth", _lib().singa_space_to_depth(
         _dt(x), ctypes.byref(_act_shape4(x.shape, NHWC)), _ptr(x), ctypes.byref(_filt4(w_shape, NHWC)),
         ctypes.byref(_cdesc(pad, stride)), _ptr(xs), _stream()))
@@ -256,7 +278,7 @@ def conv_fwd(x, w, bias=None, pad=0, stride=1, relu=False, layout="NHWC", out=No
     lay = _layout(layout)
     xs = tuple(x.shape) if lay != NHWC_S2D else tuple(x_shape)
     yshape = conv_out_shape(xs, tuple(w.shape), pad, stride, NHWC if lay == NHWC_S2D else lay)
-    y = torch.empty(yshape, dtype=x.dtype, device=x.device) if out is None else out
+    y = empty(yshape, x.dtype, x.device) if out is None else out
     nbytes = conv_workspace_bytes(OP_FWD, _dt(x), xs, tuple(w.shape), pad, stride, lay)
     ws = _workspace(nbytes, x.device, workspace)
     _check("singa_conv_fwd", _lib().singa_conv_fwd(
@@ -273,7 +295,7 @@ def conv_bwd_data(dy, w, x_shape, pad=0, stride=1, layout="NHWC", out=None, work
     result is then the gradient at that ReLU's input (its ComputeGradient
     folded into this call)."""
     lay = _layout(layout)
-    dx = torch.empty(tuple(x_shape), dtype=dy.dtype, device=dy.device) if out is None else out
+    dx = empty(tuple(x_shape), dy.dtype, dy.device) if out is None else out
     nbytes = conv_workspace_bytes(OP_BWD_DATA, _dt(dy), tuple(x_shape), tuple(w.shape), pad, stride, lay)
     ws = _workspace(nbytes, dy.device, workspace)
     _check("singa_conv_bwd_data", _lib().singa_conv_bwd_data(
@@ -291,10 +313,10 @@ def conv_bwd_filter(x, dy, w_shape, pad=0, stride=1, layout="NHWC", with_bias=Tr
     lay = _layout(layout)
     xs = tuple(x.shape) if lay != NHWC_S2D else tuple(x_shape)
     if dw is None:
-        dw = torch.empty(tuple(w_shape), dtype=torch.float32, device=x.device)
+        dw = empty(tuple(w_shape), torch.float32, x.device)
     if with_bias and db is None:
         k = w_shape[0]
-        db = torch.empty((k,), dtype=torch.float32, device=x.device)
+        db = empty((k,), torch.float32, x.device)
     nbytes = conv_workspace_bytes(OP_BWD_FILTER, _dt(x), xs, tuple(w_shape), pad, stride, lay)
     ws = _workspace(nbytes, x.device, workspace)
     _check("singa_conv_bwd_filter", _lib().singa_conv_bwd_filter(
@@ -334,9 +356,9 @@ def pool_fwd(x, mode, k=3, stride=2, pad=0, ceil_mode=True, layout="NHWC", out=N
     lay = _layout(layout)
     d = _pdesc(mode, k, stride, pad, ceil_mode)
     yshape = pool_out_shape(tuple(x.shape), mode, k, stride, pad, ceil_mode, lay)
-    y = torch.empty(yshape, dtype=x.dtype, device=x.device) if out is None else out
+    y = empty(yshape, x.dtype, x.device) if out is None else out
     if d.mode == POOL_MAX and argmax is None:
-        argmax = torch.empty(yshape, dtype=torch.uint8, device=x.device)
+        argmax = empty(yshape, torch.uint8, x.device)
     _check("singa_pool_fwd", _lib().singa_pool_fwd(
         _dt(x), lay, ctypes.byref(_act_shape4(x.shape, lay)), _ptr(x), ctypes.byref(d), _ptr(y),
         _ptr(argmax if d.mode == POOL_MAX else None), _stream()))
@@ -349,7 +371,7 @@ def pool_bwd(dy, argmax, x_shape, mode, k=3, stride=2, pad=0, ceil_mode=True, la
     ReLU's input."""
     lay = _layout(layout)
     d = _pdesc(mode, k, stride, pad, ceil_mode)
-    dx = torch.empty(tuple(x_shape), dtype=dy.dtype, device=dy.device) if out is None else out
+    dx = empty(tuple(x_shape), dy.dtype, dy.device) if out is None else out
     _check("singa_pool_bwd", _lib().singa_pool_bwd(
         _dt(dy), lay, ctypes.byref(_act_shape4(x_shape, lay)), ctypes.byref(d), _ptr(dy),
         _ptr(argmax if d.mode == POOL_MAX else None), _ptr(relu_y), _ptr(dx), _stream()))
@@ -357,13 +379,13 @@ def pool_bwd(dy, argmax, x_shape, mode, k=3, stride=2, pad=0, ceil_mode=True, la
 
 
 def relu_fwd(x, out=None):
-    y = torch.empty_like(x) if out is None else out
+    y = empty(x.shape, x.dtype, x.device) if out is None else out
     _check("singa_relu_fwd", _lib().singa_relu_fwd(_dt(x), x.numel(), _ptr(x), _ptr(y), _stream()))
     return y
 
 
 def relu_bwd(y, dy, out=None):
-    dx = torch.empty_like(dy) if out is None else out
+    dx = empty(dy.shape, dy.dtype, dy.device) if out is None else out
     _check("singa_relu_bwd", _lib().singa_relu_bwd(_dt(y), y.numel(), _ptr(y), _ptr(dy), _ptr(dx), _stream()))
     return dx
 
@@ -372,8 +394,8 @@ def softmax_ce(z, labels, loss=None, dz=None):
     """Softmax cross-entropy over rows of z (batch, classes); returns (loss, dz) where
     loss is an fp32 tensor of batch + 1 values: the mean, then each row's loss."""
     B, classes = z.shape[0], z[0].numel()
-    loss = torch.empty((B + 1,), dtype=torch.float32, device=z.device) if loss is None else loss
-    dz = torch.empty_like(z) if dz is None else dz
+    loss = empty((B + 1,), torch.float32, z.device) if loss is None else loss
+    dz = empty(z.shape, z.dtype, z.device) if dz is None else dz
     _check("singa_softmax_ce", _lib().singa_softmax_ce(_dt(z), B, classes, _ptr(z), _ptr(labels), _ptr(loss),
                                                        _ptr(dz), _stream()))
     return loss, dz
@@ -390,7 +412,7 @@ def sgd_momentum_update(w, g, v, w_bf16=None, lr=0.01, momentum=0.9, weight_deca
 def lrn_fwd(x, size=5, alpha=1e-4, beta=0.75, k=1.0, layout="NHWC", out=None):
     """Local response normalization across channels (Caffe's form)."""
     lay = _layout(layout)
-    y = torch.empty_like(x) if out is None else out
+    y = empty(x.shape, x.dtype, x.device) if out is None else out
     _check("singa_lrn_fwd", _lib().singa_lrn_fwd(
         _dt(x), lay, ctypes.byref(_act_shape4(x.shape, lay)), _ptr(x),
         ctypes.byref(LrnDesc(int(size), float(alpha), float(beta), float(k))), _ptr(y), _stream()))
@@ -400,7 +422,7 @@ def lrn_fwd(x, size=5, alpha=1e-4, beta=0.75, k=1.0, layout="NHWC", out=None):
 def lrn_bwd(x, dy, size=5, alpha=1e-4, beta=0.75, k=1.0, layout="NHWC", out=None):
     """Gradient of sum(dy * lrn_fwd(x)) with respect to x."""
     lay = _layout(layout)
-    dx = torch.empty_like(x) if out is None else out
+    dx = empty(x.shape, x.dtype, x.device) if out is None else out
     _check("singa_lrn_bwd", _lib().singa_lrn_bwd(
         _dt(x), lay, ctypes.byref(_act_shape4(x.shape, lay)), _ptr(x), _ptr(dy),
         ctypes.byref(LrnDesc(int(size), float(alpha), float(beta), float(k))), _ptr(dx), _stream()))

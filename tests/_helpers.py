@@ -21,19 +21,39 @@ def torch_dtype(dt: str):
     return torch.bfloat16 if dt == "bf16" else torch.float32
 
 
+def to_gpu(t, dtype=None):
+    """A device copy of host tensor / array t (optionally converted to dtype),
+    allocated through the binding's allocator: inside a GPU test it carries
+    guard bands that are checked when the test ends."""
+    from paper_1603_07846_amd import singa
+    if not isinstance(t, torch.Tensor):
+        t = torch.from_numpy(np.ascontiguousarray(t))
+    t = t.contiguous()
+    dtype = t.dtype if dtype is None else dtype
+    out = singa.empty(tuple(t.shape), dtype, "cuda")
+    out.copy_(t.to(dtype))
+    return out
+
+
+def gpu_full(shape, value, dtype=torch.float32):
+    """A device tensor filled with value, through the binding's allocator."""
+    from paper_1603_07846_amd import singa
+    return singa.empty(tuple(shape), dtype, "cuda").fill_(value)
+
+
 def nchw_to_dev(a, dt="f32", layout="NHWC"):
     """numpy NCHW (values already representable in dt) -> device tensor in layout."""
     a = np.asarray(a, np.float32)
     if layout == "NHWC" and a.ndim == 4:
         a = a.transpose(0, 2, 3, 1)
-    return torch.from_numpy(np.ascontiguousarray(a)).to("cuda").to(torch_dtype(dt))
+    return to_gpu(a, torch_dtype(dt))
 
 
 def kcrs_to_dev(w, dt="f32", layout="NHWC"):
     w = np.asarray(w, np.float32)
     if layout == "NHWC":
         w = w.transpose(0, 2, 3, 1)
-    return torch.from_numpy(np.ascontiguousarray(w)).to("cuda").to(torch_dtype(dt))
+    return to_gpu(w, torch_dtype(dt))
 
 
 def dev_to_nchw(t, layout="NHWC"):

@@ -1,24 +1,38 @@
 """Parity at the workloads' full sizes, in the launch configuration the
 benchmark times (NHWC, batch 128 fp32 / 256 bf16).
 
-Every layer shape of the AlexNet-shaped workloads is run on seeded inputs of
-exactly that shape.  Convolutions are checked on 1,500 sampled outputs per
-pass, each evaluated one by one by the oracle's point evaluators (a filter
-gradient point sums over all N*P*Q output pixels); pooling, ReLU,
-softmax-CE and the Updater are checked element by element over the whole
-tensor.
+Every conv / FC layer shape of the AlexNet-shaped workloads is run on seeded
+inputs of exactly that shape.  Each pass is a GEMM over an output matrix
+(forward: output pixels x filters; input gradient: input pixels x channels,
+or images x (h, w, c) for a fully connected layer; filter gradient: filters x
+taps); every tile any of the kernels uses starts at a multiple of 128 rows
+and of 32 columns of that matrix and spans at least 128 x 96, so one sampled
+point in every 128 x 32 block, plus the four corners, puts at least one
+point in every output tile of whatever tiling ran (and every split-K
+partition adds into every point of its tile).  The strided first layer's
+input gradient is a GEMM over its space-to-depth form, whose rows are 4 x 4
+blocks of input pixels: there one such block per 128 rows is checked whole.
+Each point is evaluated one by one by the oracle's point evaluators and held
+to a per-point bound (the output rounding plus fp32 accumulation error over
+the sum of absolute products, which the same evaluators give on |x| and |w|),
+and the sampled set to rel-L2.  The bias gradient is checked against the
+oracle over the whole vector, and the full filter gradients of the bf16
+stack's conv3-5 and of fc6-8 element by element.  Pooling, ReLU, softmax-CE
+and the Updater are checked element by element over the whole tensor.
 """
 import numpy as np
 import pytest
 import torch
 
 import oracle
-from _helpers import TOL, rel_l2
+from _helpers import TOL, rel_l2, to_gpu
 from paper_1603_07846_amd import workloads as wl
 
 pytestmark = pytest.mark.gpu
 
-NPTS = 1500
+BM, BN = 128, 32  # block grid that every kernel's output tiles are unions of
+EPS32 = 2.0 ** -24
+OUT_ROUND = {"f32": 2.0 ** -23, "bf16": 2.0 ** -7}  # twice the largest relative rounding error of a stored output
 
 
 @pytest.fixture(scope="module", autouse=True)
@@ -45,53 +59,129 @@ def _conv_layers(w):
 
 CASES = [(3, l) for l in _conv_layers(wl.CFG3)] + [(4, l) for l in _conv_layers(wl.CFG4)] + \
         [(5, l) for l in _conv_layers(wl.CFG5) if l[0].startswith("fc")]
+# filter gradients checked over every element (the bf16 benchmark stack's
+# 3x3 layers and the fully connected layers)
+FULL_DW = {(4, "conv3"), (4, "conv4"), (4, "conv5"), (5, "fc6"), (5, "fc7"), (5, "fc8")}
 
 
-def _nchw_flat_to_nhwc_flat(idx, shape_nchw):
-    n, c, h, w = np.unravel_index(idx, shape_nchw)
-    N, C, H, W = shape_nchw
-    return ((n * H + h) * W + w) * C + c
+def block_points(rows, cols, rng, bm=BM, bn=BN):
+    """(row, col) of one random element in every bm x bn block of a rows x
+    cols matrix (ragged last blocks included) and of its four corners."""
+    r0 = np.arange(0, rows, bm)
+    c0 = np.arange(0, cols, bn)
+    hr = np.minimum(bm, rows - r0)
+    hc = np.minimum(bn, cols - c0)
+    R = (r0[:, None] + (rng.random((len(r0), len(c0))) * hr[:, None]).astype(np.int64)).ravel()
+    C = (c0[None, :] + (rng.random((len(r0), len(c0))) * hc[None, :]).astype(np.int64)).ravel()
+    R = np.concatenate([R, [0, 0, rows - 1, rows - 1]])
+    C = np.concatenate([C, [0, cols - 1, 0, cols - 1]])
+    return R.astype(np.int64), C.astype(np.int64)
 
 
 def _to_dev(a_nchw, dt):
-    t = torch.from_numpy(np.ascontiguousarray(a_nchw.transpose(0, 2, 3, 1)))
-    return t.cuda().to(torch.bfloat16 if dt == "bf16" else torch.float32)
+    return to_gpu(np.ascontiguousarray(a_nchw.transpose(0, 2, 3, 1)), torch.bfloat16 if dt == "bf16" else torch.float32)
 
 
 def _take(t, idx):
     return t.reshape(-1)[torch.from_numpy(idx).cuda()].float().cpu().numpy().astype(np.float64)
 
 
+def _check_points(name, got, ref, absum, n_acc, dt_out):
+    """rel-L2 over the sample and the per-point bound
+    |got - ref| <= OUT_ROUND |ref| + 8 sqrt(n_acc) 2^-24 sum|a b|."""
+    bound = OUT_ROUND[dt_out] * np.abs(ref) + 8.0 * np.sqrt(n_acc) * EPS32 * absum
+    worst = float(np.max(np.abs(got - ref) / np.maximum(bound, 1e-300)))
+    assert worst <= 1.0, (name, "per-point bound exceeded", worst)
+    return rel_l2(got, ref), worst
+
+
 @pytest.mark.parametrize("index,layer", CASES, ids=["w%d-%s" % (i, l[0]) for i, l in CASES])
 def test_conv_layer_full_size(index, layer):
     name, N, C, H, W, K, R, S, pad, stride = layer
     dt = wl.WORKLOADS[index].dtype
+    fc = R == H and S == W and pad == 0 and H > 1 and name.startswith("fc")
     seed = 500 + index * 10 + len(name) + K
     x = wl.random_array((N, C, H, W), seed, "normal", 1.0, dt)
     w = wl.random_array((K, C, R, S), seed + 1, "normal", 0.01, dt)
     b = wl.random_array((K,), seed + 2, "normal", 0.01, "f32")
     P, Q = oracle.conv_out(H, R, pad, stride), oracle.conv_out(W, S, pad, stride)
     dy = wl.random_array((N, K, P, Q), seed + 3, "normal", 1.0, dt)
-    xd, dyd = _to_dev(x, dt), _to_dev(dy, dt)
-    wd = torch.from_numpy(np.ascontiguousarray(w.transpose(0, 2, 3, 1))).cuda().to(xd.dtype)
-    y = singa.conv_fwd(xd, wd, torch.from_numpy(b).cuda(), pad, stride, relu=False)
+    tdt = torch.bfloat16 if dt == "bf16" else torch.float32
+    xd = to_gpu(np.ascontiguousarray(x.transpose(0, 2, 3, 1)), tdt)
+    dyd = to_gpu(np.ascontiguousarray(dy.transpose(0, 2, 3, 1)), tdt)
+    wd = to_gpu(np.ascontiguousarray(w.transpose(0, 2, 3, 1)), tdt)
+    y = singa.conv_fwd(xd, wd, to_gpu(b), pad, stride, relu=False)
     dx = singa.conv_bwd_data(dyd, wd, (N, H, W, C), pad, stride)
     dw, db = singa.conv_bwd_filter(xd, dyd, (K, R, S, C), pad, stride)
     torch.cuda.synchronize()
     rng = np.random.default_rng(seed)
-    iy = rng.choice(N * K * P * Q, NPTS, replace=False)
-    ix = rng.choice(N * C * H * W, NPTS, replace=False)
-    iw = rng.choice(K * C * R * S, min(NPTS, K * C * R * S), replace=False)
-    ref_y = oracle.conv_fwd_points(x, w, b, iy, pad=pad, stride=stride)
-    ref_dx = oracle.conv_bwd_data_points(dy, w, x.shape, ix, pad=pad, stride=stride)
-    ref_dw = oracle.conv_bwd_filter_points(x, dy, w.shape, iw, pad=pad, stride=stride)
-    got_y = _take(y, _nchw_flat_to_nhwc_flat(iy, (N, K, P, Q)))
-    got_dx = _take(dx, _nchw_flat_to_nhwc_flat(ix, (N, C, H, W)))
-    k, c, r, s = np.unravel_index(iw, (K, C, R, S))
-    got_dw = _take(dw, ((k * R + r) * S + s) * C + c)
-    errs = {"y": rel_l2(got_y, ref_y), "dx": rel_l2(got_dx, ref_dx), "dw": rel_l2(got_dw, ref_dw),
-            "db": rel_l2(db.cpu().numpy(), dy.astype(np.float64).sum(axis=(0, 2, 3)))}
+    ax, aw, ady, ab = np.abs(x), np.abs(w), np.abs(dy), np.abs(b)
+    errs, worst = {}, {}
+
+    # forward: rows (n, p, q), columns k
+    r, c = block_points(N * P * Q, K, rng)
+    n, p, q = r // (P * Q), (r // Q) % P, r % Q
+    iy = ((n * K + c) * P + p) * Q + q
+    ref = oracle.conv_fwd_points(x, w, b, iy, pad=pad, stride=stride)
+    absum = oracle.conv_fwd_points(ax, aw, ab, iy, pad=pad, stride=stride)
+    errs["y"], worst["y"] = _check_points(name + " y", _take(y, r * K + c), ref, absum, C * R * S, dt)
+
+    # input gradient
+    if fc:  # rows n, columns (h, w, c)
+        r, c = block_points(N, H * W * C, rng)
+        hh, ww_, cc = c // (W * C), (c // C) % W, c % C
+        nn = r
+    elif stride == 1:  # rows (n, h, w), columns c
+        r, cc = block_points(N * H * W, C, rng)
+        nn, hh, ww_ = r // (H * W), (r // W) % H, r % W
+    else:  # space-to-depth rows: whole stride x stride pixel blocks, every channel
+        Hs, Ws = P + (R + stride - 1) // stride - 1, Q + (S + stride - 1) // stride - 1
+        rows = N * Hs * Ws
+        r0 = np.arange(0, rows, BM)
+        rr = np.concatenate([r0 + (rng.random(len(r0)) * np.minimum(BM, rows - r0)).astype(np.int64),
+                             [0, rows - 1]])
+        nb, hb, wb = rr // (Hs * Ws), (rr // Ws) % Hs, rr % Ws
+        dh, dw_, cg = np.meshgrid(np.arange(stride), np.arange(stride), np.arange(C), indexing="ij")
+        nn = np.repeat(nb, dh.size)
+        hh = (hb[:, None] * stride + dh.ravel()[None, :]).ravel()
+        ww_ = (wb[:, None] * stride + dw_.ravel()[None, :]).ravel()
+        cc = np.tile(cg.ravel(), len(rr))
+        keep = (hh < H) & (ww_ < W)
+        nn, hh, ww_, cc = nn[keep], hh[keep], ww_[keep], cc[keep]
+    ix = ((nn * C + cc) * H + hh) * W + ww_
+    ref = oracle.conv_bwd_data_points(dy, w, x.shape, ix, pad=pad, stride=stride)
+    absum = oracle.conv_bwd_data_points(ady, aw, x.shape, ix, pad=pad, stride=stride)
+    got = _take(dx, ((nn * H + hh) * W + ww_) * C + cc)
+    errs["dx"], worst["dx"] = _check_points(name + " dx", got, ref, absum, K * R * S, dt)
+
+    # filter gradient: rows k, columns (r, s, c); every element where it is cheap enough
+    if (index, name) in FULL_DW:
+        ref_dw = oracle.conv_bwd_filter(x, dy, w.shape, pad=pad, stride=stride, with_bias=False)
+        abs_dw = oracle.conv_bwd_filter(ax, ady, w.shape, pad=pad, stride=stride, with_bias=False)
+        got = dw.cpu().numpy().astype(np.float64).transpose(0, 3, 1, 2)
+        errs["dw"], worst["dw"] = _check_points(name + " dw", got.ravel(), ref_dw.ravel(), abs_dw.ravel(),
+                                                N * P * Q, "f32")
+    else:
+        if stride == 1:
+            k, j = block_points(K, R * S * C, rng)
+        else:  # space-to-depth taps: every tap of eight filters and of the last one
+            ks = np.concatenate([rng.choice(K, min(K, 8), replace=False), [K - 1]])
+            k = np.repeat(ks, R * S * C)
+            j = np.tile(np.arange(R * S * C), len(ks))
+        rr_, ss, cc = j // (S * C), (j // C) % S, j % C
+        iw = ((k * C + cc) * R + rr_) * S + ss
+        ref = oracle.conv_bwd_filter_points(x, dy, w.shape, iw, pad=pad, stride=stride)
+        absum = oracle.conv_bwd_filter_points(ax, ady, w.shape, iw, pad=pad, stride=stride)
+        errs["dw"], worst["dw"] = _check_points(name + " dw", _take(dw, k * R * S * C + j), ref, absum,
+                                                N * P * Q, "f32")
+    # bias gradient, every element: the oracle's filter gradient of a one-channel
+    # all-ones input under a 1x1 filter is the sum of dy over (n, p, q), as is its db
+    _, ref_db = oracle.conv_bwd_filter(np.ones((N, 1, P, Q)), dy, (K, 1, 1, 1), with_bias=True)
+    abs_db = oracle.conv_bwd_filter(np.ones((N, 1, P, Q)), ady, (K, 1, 1, 1), with_bias=False).ravel()
+    errs["db"], worst["db"] = _check_points(name + " db", db.cpu().numpy().astype(np.float64), ref_db, abs_db,
+                                            N * P * Q, "f32")
     tol = TOL[dt]
+    print("%s w%d: rel-L2 %s, worst point / bound %s" % (name, index, errs, worst))
     # dw and db are fp32 sums of exact products of representable inputs
     assert errs["y"] <= tol and errs["dx"] <= tol and errs["dw"] <= TOL["f32"] and errs["db"] <= TOL["f32"], errs
 
@@ -144,8 +234,8 @@ def test_adagrad_full_size():
     w = wl.random_array((n,), 822, "normal", 0.01)
     g = wl.random_array((n,), 823, "normal", 1e-3)
     h = wl.random_array((n,), 824, "uniform01", 1e-6)  # a running sum of squares: non-negative
-    wd, gd, hd = (torch.from_numpy(np.ascontiguousarray(a, np.float32)).cuda() for a in (w, g, h))
-    wb = torch.empty(n, dtype=torch.bfloat16, device="cuda")
+    wd, gd, hd = (to_gpu(np.ascontiguousarray(a, np.float32)) for a in (w, g, h))
+    wb = singa.empty((n,), torch.bfloat16, "cuda")
     singa.adagrad_update(wd, gd, hd, wb, 0.01, 1e-6, 5e-4)
     torch.cuda.synchronize()
     w1, h1 = oracle.adagrad(w, g, h, 0.01, 1e-6, 5e-4)
@@ -159,8 +249,8 @@ def test_sgd_full_size():
     w = wl.random_array((n,), 820, "normal", 0.01)
     g = wl.random_array((n,), 821, "normal", 1e-3)
     v = np.zeros(n, np.float32)
-    wd, gd, vd = (torch.from_numpy(a).cuda() for a in (w, g, v))
-    wb = torch.empty(n, dtype=torch.bfloat16, device="cuda")
+    wd, gd, vd = (to_gpu(a) for a in (w, g, v))
+    wb = singa.empty((n,), torch.bfloat16, "cuda")
     singa.sgd_momentum_update(wd, gd, vd, wb, 0.01, 0.9, 5e-4)
     torch.cuda.synchronize()
     w1, v1 = oracle.sgd_momentum(w, g, v, 0.01, 0.9, 5e-4)

@@ -56,7 +56,7 @@ def test_graph_replay_matches_eager(index, batch):
         assert np.isfinite(float(eager.layers[-1].loss[0]))
 
 
-@pytest.mark.parametrize("index,batch", [(5, 8), (5, 32), (6, 8)])
+@pytest.mark.parametrize("index,batch", [(5, 8), (5, 32), (6, 8), (5, 256)])
 def test_two_stream_eager_matches_one_stream(index, batch):
     """The default step launched eagerly (filter gradients, and the fully
     connected layers' fused gradient + update, on the second stream) against

@@ -13,7 +13,7 @@ import pytest
 import torch
 
 import oracle
-from _helpers import TOL, dev_to_nchw, filt_to_kcrs, kcrs_to_dev, nchw_to_dev, phys, fphys, rel_l2
+from _helpers import TOL, dev_to_nchw, filt_to_kcrs, fphys, gpu_full, kcrs_to_dev, nchw_to_dev, phys, rel_l2, to_gpu
 from paper_1603_07846_amd import workloads as wl
 
 pytestmark = pytest.mark.gpu
@@ -450,8 +450,8 @@ def test_sgd_momentum(n, shadow):
     w = wl.random_array((n,), 90, "normal", 0.01)
     g = wl.random_array((n,), 91, "normal", 1.0)
     v = wl.random_array((n,), 92, "normal", 0.01)
-    wd, vd, gd = torch.from_numpy(w).cuda(), torch.from_numpy(v).cuda(), torch.from_numpy(g).cuda()
-    wb = torch.empty(n, dtype=torch.bfloat16, device="cuda") if shadow else None
+    wd, vd, gd = to_gpu(w), to_gpu(v), to_gpu(g)
+    wb = gpu_full((n,), 0.0, torch.bfloat16) if shadow else None
     for step in range(3):
         singa.sgd_momentum_update(wd, gd, vd, wb, lr=0.01, momentum=0.9, weight_decay=5e-4)
         w, v = oracle.sgd_momentum(w, g, v, 0.01, 0.9, 5e-4)
@@ -470,8 +470,8 @@ def test_adagrad(n, shadow):
     w = wl.random_array((n,), 93, "normal", 0.01)
     g = wl.random_array((n,), 94, "normal", 1.0)
     h = np.zeros(n)
-    wd, hd, gd = torch.from_numpy(w).cuda(), torch.zeros(n, device="cuda"), torch.from_numpy(g).cuda()
-    wb = torch.empty(n, dtype=torch.bfloat16, device="cuda") if shadow else None
+    wd, hd, gd = to_gpu(w), gpu_full((n,), 0.0), to_gpu(g)
+    wb = gpu_full((n,), 0.0, torch.bfloat16) if shadow else None
     for step in range(3):
         singa.adagrad_update(wd, gd, hd, wb, lr=0.01, delta=1e-6, weight_decay=5e-4)
         w, h = oracle.adagrad(w, g, h, 0.01, 1e-6, 5e-4)
@@ -583,8 +583,7 @@ def _sgd_state(K, C, R, S, layout, seed):
     v = wl.random_array((K, C, R, S), seed + 1, "normal", 0.01, "f32")
     b = wl.random_array((K,), seed + 2, "normal", 0.1, "f32")
     vb = wl.random_array((K,), seed + 3, "normal", 0.01, "f32")
-    return (kcrs_to_dev(w, "f32", layout), kcrs_to_dev(v, "f32", layout), torch.from_numpy(b).cuda(),
-            torch.from_numpy(vb).cuda())
+    return (kcrs_to_dev(w, "f32", layout), kcrs_to_dev(v, "f32", layout), to_gpu(b), to_gpu(vb))
 
 
 @pytest.mark.parametrize("case", SGD_CASES, ids=["x".join(map(str, c)) for c in SGD_CASES])
@@ -602,9 +601,9 @@ def test_conv_bwd_filter_sgd_matches_gradient_then_update(case):
     # reference: gradient, then the flat update
     w0, v0, b0, vb0 = _sgd_state(K, C, R, S, layout, 130)
     dw, db = singa.conv_bwd_filter(xd, dyd, wshape, pad, stride, layout=layout, with_bias=bias)
-    wr, vr, br, vbr = w0.clone(), v0.clone(), b0.clone(), vb0.clone()
-    wbr = torch.zeros(wr.shape, dtype=torch.bfloat16, device="cuda")
-    bbr = torch.zeros(br.shape, dtype=torch.bfloat16, device="cuda")
+    wr, vr, br, vbr = to_gpu(w0), to_gpu(v0), to_gpu(b0), to_gpu(vb0)
+    wbr = gpu_full(wr.shape, 0.0, torch.bfloat16)
+    bbr = gpu_full(br.shape, 0.0, torch.bfloat16)
     singa.sgd_momentum_update(wr, dw, vr, wbr, lr, mom, wd)
     if bias:
         singa.sgd_momentum_update(br, db, vbr, bbr, lr, mom, wd)
@@ -612,15 +611,15 @@ def test_conv_bwd_filter_sgd_matches_gradient_then_update(case):
     # off (element-wise epilogue); or not stored
     for mode in ("keep", "keep_unaligned", "none"):
         keep = mode != "none"
-        wf, vf, bf, vbf = w0.clone(), v0.clone(), b0.clone(), vb0.clone()
-        wbf = torch.zeros(wf.shape, dtype=torch.bfloat16, device="cuda")
-        bbf = torch.zeros(bf.shape, dtype=torch.bfloat16, device="cuda")
+        wf, vf, bf, vbf = to_gpu(w0), to_gpu(v0), to_gpu(b0), to_gpu(vb0)
+        wbf = gpu_full(wf.shape, 0.0, torch.bfloat16)
+        bbf = gpu_full(bf.shape, 0.0, torch.bfloat16)
         gw = None
         if mode == "keep":
-            gw = torch.full(dw.shape, float("nan"), device="cuda")
+            gw = gpu_full(dw.shape, float("nan"))
         elif mode == "keep_unaligned":
-            gw = torch.full((dw.numel() + 1,), float("nan"), device="cuda")[1:].view(dw.shape)
-        gb = torch.full((K,), float("nan"), device="cuda") if keep and bias else None
+            gw = gpu_full((dw.numel() + 1,), float("nan"))[1:].view(dw.shape)
+        gb = gpu_full((K,), float("nan")) if keep and bias else None
         singa.trace_enable(True)
         singa.conv_bwd_filter_sgd(xd, dyd, wshape, wf, vf, wbf, b=bf if bias else None, vb=vbf if bias else None,
                                   b_bf16=bbf if bias else None, lr=lr, momentum=mom, weight_decay=wd, pad=pad,

@@ -161,3 +161,81 @@ def test_parameter_counts():
     assert count(wl.CFG2) == 89578
     assert count(wl.CFG5) == 62378344
     assert count(wl.CFG1) == 2400
+
+
+def test_net_adagrad_branch_against_torch_optim():
+    """train_one_batch's AdaGrad branch (Sec. 4.1.4): two consecutive steps,
+    the second fed the first's parameters and sums of squared gradients,
+    against torch.optim.Adagrad (library routine) on gradients from torch
+    float64 autograd of the same net; the momentum argument must not enter."""
+    layers = _tiny_net()
+    x, params, labels = _tiny_inputs(seed=21)
+    lr, delta, wd = 0.05, 1e-3, 5e-4
+    tp = [(torch.tensor(w, requires_grad=True), torch.tensor(b, requires_grad=True)) for w, b in params]
+    opt = torch.optim.Adagrad([p for pair in tp for p in pair], lr=lr, eps=delta, weight_decay=wd,
+                              initial_accumulator_value=0.0)
+    cur, vel = params, None
+    for step in range(2):
+        res = onet.train_one_batch(layers, x, cur, labels=labels, lr=lr, momentum=0.9, wd=wd, velocity=vel,
+                                   adagrad_delta=delta)
+        opt.zero_grad()
+        h = F.conv2d(torch.tensor(x), tp[0][0], tp[0][1], padding=2)
+        h = F.relu(F.max_pool2d(h, 3, 2, ceil_mode=True))
+        h = F.relu(F.conv2d(h, tp[1][0], tp[1][1], padding=2))
+        h = F.avg_pool2d(h, 3, 2, ceil_mode=True, count_include_pad=True)
+        h = F.relu(F.conv2d(h, tp[2][0], tp[2][1], padding=1))
+        z = F.linear(h.reshape(2, -1), tp[3][0], tp[3][1])
+        F.cross_entropy(z, torch.tensor(labels, dtype=torch.long)).backward()
+        opt.step()
+        for li in range(4):
+            for j in range(2):
+                np.testing.assert_allclose(res["params"][li][j], tp[li][j].detach().numpy(), rtol=1e-11,
+                                           atol=1e-14, err_msg="step %d layer %d" % (step, li))
+                st = opt.state[tp[li][j]]["sum"].numpy()
+                np.testing.assert_allclose(res["velocity"][li][j], st, rtol=1e-11, atol=1e-18)
+        cur, vel = res["params"], res["velocity"]
+    # the step moved the weights by about lr per element (the first AdaGrad step is lr * sign(g'))
+    assert np.max(np.abs(res["params"][0][0] - params[0][0])) > lr
+
+
+def test_net_store_branch_rounds_every_stored_tensor():
+    """train_one_batch's bf16-mirror option: with store=round_bf16 every
+    layer output (and the logits' gradient) equals round_bf16 of that layer's
+    own forward on the stored input, every activation gradient equals
+    round_bf16 of that layer's own backward on the stored upstream gradient
+    and stored activations, and the parameter gradients are left unrounded:
+    layer by layer, bit for bit, through the oracle's functions alone."""
+    layers = _tiny_net()
+    x, params, labels = _tiny_inputs(seed=5)
+    res = onet.train_one_batch(layers, x, params, labels=labels, lr=0.01, momentum=0.9, store=oracle.round_bf16,
+                               need_input_grad=True)
+    acts, grads = res["acts"], res["grads"]
+    plain = onet.train_one_batch(layers, x, params, labels=labels, lr=0.01, momentum=0.9, need_input_grad=True)
+    assert not np.array_equal(acts["out"]["c2"], plain["acts"]["out"]["c2"])  # the option does something
+    pi = 0
+    for i, l in enumerate(layers):
+        kind = type(l).__name__
+        xin = acts["in"][l.name]
+        if i > 0:
+            prev = layers[i - 1]
+            assert xin is acts["out"][prev.name]  # a layer reads the stored output below it
+        lp = []
+        if kind in ("Conv", "FC"):
+            lp = [params[pi]]
+            pi += 1
+        one = onet.forward([l], xin, lp, labels=labels)
+        if kind == "SoftmaxCE":
+            np.testing.assert_array_equal(acts["dlogits"], oracle.round_bf16(one["dlogits"]))
+            assert acts["loss"] == one["loss"]
+            continue
+        np.testing.assert_array_equal(acts["out"][l.name], oracle.round_bf16(one["out"][l.name]))
+        # backward of this layer alone on the stored upstream gradient
+        up = acts["dlogits"] if isinstance(layers[i + 1], wl.SoftmaxCE) else grads["grad_in"][layers[i + 1].name]
+        one["out"][l.name] = acts["out"][l.name]
+        if kind == "Pool":
+            one["argmax"][l.name] = acts["argmax"].get(l.name)
+        g1 = onet.backward([l], lp, one, dy_top=up, need_input_grad=True)
+        np.testing.assert_array_equal(grads["grad_in"][l.name], oracle.round_bf16(g1["grad_in"][l.name]))
+        if kind in ("Conv", "FC"):
+            np.testing.assert_array_equal(grads["dw"][l.name], g1["dw"][l.name])
+            np.testing.assert_array_equal(grads["db"][l.name], g1["db"][l.name])
