@@ -63,6 +63,7 @@ extern "C" {
 #define SINGA_ERR_WORKSPACE (-4)   /* workspace smaller than singa_conv_workspace_bytes() */
 #define SINGA_ERR_ALIGN (-5)       /* a device pointer is misaligned (see below) */
 #define SINGA_ERR_HIP (-6)         /* the HIP runtime rejected a launch */
+#define SINGA_ERR_SCRATCH (-7)     /* needs more than the library's fixed scratch array holds */
 
 typedef enum { SINGA_F32 = 0, SINGA_BF16 = 1 } singa_dtype;
 /* SINGA_NHWC_S2D: the input of a strided convolution already in its
@@ -189,6 +190,29 @@ int singa_conv_bwd_filter(singa_dtype dtype, singa_layout layout,
                           const singa_filter4* w, const singa_conv_desc* d,
                           const void* dy_ptr, float* dw, float* db, int accumulate,
                           void* ws, size_t ws_bytes, singa_stream stream);
+
+/* singa_conv_bwd_filter for callers that cannot allocate device memory: code
+ * recorded under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc.  Same arguments, results and kernels, without the
+ * workspace: its scratch is a fixed array of SINGA_NOALLOC_SCRATCH_BYTES in
+ * device memory that the library holds on each GPU it runs on until the
+ * process ends (looked up on a device's first call; nothing is allocated
+ * here or later).
+ *   Returns SINGA_ERR_SCRATCH (nothing enqueued) when the call would need
+ *   more than SINGA_NOALLOC_SCRATCH_BYTES of workspace
+ *   (singa_conv_workspace_bytes(SINGA_OP_BWD_FILTER, ...) reports it; every
+ *   AlexNet-shaped layer up to batch 256 fits), and SINGA_ERR_UNSUPPORTED
+ *   when `stream` belongs to another device than the current one.
+ *   Every call on one GPU uses that GPU's one array: calls whose execution
+ *   overlaps on the same GPU (different streams, or several host threads)
+ *   race on it and give wrong results; serialize them.  Calls on one stream
+ *   are serialized by the stream.  Nothing in the array needs clearing. */
+#define SINGA_NOALLOC_SCRATCH_BYTES (128u << 20)
+int singa_conv_bwd_filter_noalloc(singa_dtype dtype, singa_layout layout,
+                                  const singa_shape4* x, const void* x_ptr,
+                                  const singa_filter4* w, const singa_conv_desc* d,
+                                  const void* dy_ptr, float* dw, float* db, int accumulate,
+                                  singa_stream stream);
 
 /* Convolution ComputeGradient for the Params followed at once by the
  * Updater's step on them (Alg. 1 calls Update on a layer's Params right after

@@ -16,7 +16,7 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB_NAME = "libsinga_mi.so"
 LIB_PATH = os.path.join(HERE, LIB_NAME)
-SOURCES = ["abi.cpp", "trace.cpp", "conv_igemm.hip", "conv_aux.hip", "eltwise.hip"]
+SOURCES = ["abi.cpp", "noalloc.cpp", "trace.cpp", "conv_igemm.hip", "conv_aux.hip", "eltwise.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 

@@ -298,6 +298,7 @@ const char* singa_strerror(int status) {
     case SINGA_ERR_WORKSPACE: return "workspace too small";
     case SINGA_ERR_ALIGN: return "device pointer not aligned";
     case SINGA_ERR_HIP: return "HIP runtime error at launch";
+    case SINGA_ERR_SCRATCH: return "needs more scratch than the library's fixed scratch array holds";
     default: return "unknown status";
   }
 }

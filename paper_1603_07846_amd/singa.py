@@ -22,7 +22,8 @@ from .build import LIB_PATH
 
 OK = 0
 ERRORS = {-1: "SINGA_ERR_NULL", -2: "SINGA_ERR_SHAPE", -3: "SINGA_ERR_UNSUPPORTED", -4: "SINGA_ERR_WORKSPACE",
-          -5: "SINGA_ERR_ALIGN", -6: "SINGA_ERR_HIP"}
+          -5: "SINGA_ERR_ALIGN", -6: "SINGA_ERR_HIP", -7: "SINGA_ERR_SCRATCH"}
+NOALLOC_SCRATCH_BYTES = 128 << 20
 F32, BF16 = 0, 1
 NCHW, NHWC, NHWC_S2D = 0, 1, 2
 POOL_MAX, POOL_AVG = 0, 1
@@ -30,7 +31,8 @@ OP_FWD, OP_BWD_DATA, OP_BWD_FILTER, OP_BWD_FILTER_SGD = 0, 1, 2, 3
 
 # every exported symbol of the C ABI (checked by the CPU tests against the header)
 EXPORTS = ["singa_strerror", "singa_conv_out_shape", "singa_pool_out_shape", "singa_conv_workspace_bytes",
-           "singa_conv_fwd", "singa_conv_bwd_data", "singa_conv_bwd_filter", "singa_conv_bwd_filter_sgd",
+           "singa_conv_fwd", "singa_conv_bwd_data", "singa_conv_bwd_filter", "singa_conv_bwd_filter_noalloc",
+           "singa_conv_bwd_filter_sgd",
            "singa_pool_fwd", "singa_pool_bwd",
            "singa_relu_fwd", "singa_relu_bwd", "singa_softmax_ce", "singa_sgd_momentum_update",
            "singa_adagrad_update", "singa_lrn_fwd", "singa_lrn_bwd", "singa_space_to_depth_bytes",
@@ -88,6 +90,7 @@ def _lib():
         lib.singa_conv_fwd.argtypes = [i32, i32, S4, vp, F4, vp, vp, CD, vp, i32, vp, sz, vp]
         lib.singa_conv_bwd_data.argtypes = [i32, i32, S4, F4, vp, CD, vp, vp, vp, vp, sz, vp]
         lib.singa_conv_bwd_filter.argtypes = [i32, i32, S4, vp, F4, CD, vp, vp, vp, i32, vp, sz, vp]
+        lib.singa_conv_bwd_filter_noalloc.argtypes = [i32, i32, S4, vp, F4, CD, vp, vp, vp, i32, vp]
         f32 = ctypes.c_float
         lib.singa_conv_bwd_filter_sgd.argtypes = [i32, i32, S4, vp, F4, CD, vp, vp, vp, vp, vp, vp, vp, vp, vp,
                                                   f32, f32, f32, vp, sz, vp]
@@ -323,6 +326,24 @@ def conv_bwd_filter(x, dy, w_shape, pad=0, stride=1, layout="NHWC", with_bias=Tr
         _dt(x), lay, ctypes.byref(_act_shape4(xs, lay)), _ptr(x), ctypes.byref(_filt4(w_shape, lay)),
         ctypes.byref(_cdesc(pad, stride)), _ptr(dy), _ptr(dw), _ptr(db if with_bias else None),
         int(bool(accumulate)), _ptr(ws), 0 if ws is None else ws.numel(), _stream()))
+    return dw, (db if with_bias else None)
+
+
+def conv_bwd_filter_noalloc(x, dy, w_shape, pad=0, stride=1, layout="NHWC", with_bias=True, dw=None, db=None,
+                            accumulate=False, x_shape=None):
+    """conv_bwd_filter with the library's fixed scratch array instead of a
+    workspace (dw / db, when not given, are still allocated here; a caller
+    that must not allocate passes them)."""
+    lay = _layout(layout)
+    xs = tuple(x.shape) if lay != NHWC_S2D else tuple(x_shape)
+    if dw is None:
+        dw = empty(tuple(w_shape), torch.float32, x.device)
+    if with_bias and db is None:
+        db = empty((w_shape[0],), torch.float32, x.device)
+    _check("singa_conv_bwd_filter_noalloc", _lib().singa_conv_bwd_filter_noalloc(
+        _dt(x), lay, ctypes.byref(_act_shape4(xs, lay)), _ptr(x), ctypes.byref(_filt4(w_shape, lay)),
+        ctypes.byref(_cdesc(pad, stride)), _ptr(dy), _ptr(dw), _ptr(db if with_bias else None),
+        int(bool(accumulate)), _stream()))
     return dw, (db if with_bias else None)
 
 
