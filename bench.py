@@ -91,6 +91,9 @@ def parse():
                     help="run every pass on one stream (no concurrent filter gradients), as the per-kernel pass does")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-images", type=int, default=8, help="images in the oracle's timed sample")
+    ap.add_argument("--steps-only", action="store_true",
+                    help="only the timed and traced steps (no clock reading, Updater / LRN lines, other workloads or "
+                         "CPU baseline): the short run the counter passes profile")
     ap.add_argument("--no-configs", action="store_true",
                     help="skip the other workloads' lines (single layer, CIFAR-shaped net, fp32 / bf16 conv stacks)")
     return ap.parse_args()
@@ -268,6 +271,69 @@ def measure_config(index, steps, warmup):
     return out
 
 
+def measure_updaters(net, w):
+    """Both Updater protocols over the whole flat parameter buffer, each
+    alone, timed with HIP events (on a copy of the net's buffers, so the
+    step's state is left as it was)."""
+    import torch
+    from paper_1603_07846_amd import singa
+    updaters = {}
+    wf, gf, vf = net.w_flat.clone(), net.g_flat.clone(), torch.zeros_like(net.v_flat)
+    wbf = net.wb_flat.clone() if net.wb_flat is not None else None
+    nbytes = net.n_params_padded * (22 if wbf is not None else 20)
+    for name, fn in (("sgd_momentum", lambda: singa.sgd_momentum_update(wf, gf, vf, wbf, w.lr, w.momentum,
+                                                                        w.weight_decay)),
+                     ("adagrad", lambda: singa.adagrad_update(wf, gf, vf, wbf, w.lr, 1e-6, w.weight_decay))):
+        for _ in range(3):
+            fn()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(20):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / 20
+        updaters[name] = {"ms": round(ms, 4), "GB_per_s": round(nbytes / (ms / 1e3) / 1e9, 1),
+                          "frac_hbm_peak": round(nbytes / (ms / 1e3) / 1e9 / PEAK["hbm_gbs"], 4),
+                          "params": net.n_params_padded}
+    del wf, gf, vf, wbf
+    return updaters
+
+
+def measure_lrn(net, dev, is_bf16):
+    """Local response normalization (not part of this step: the paper's GPU
+    AlexNet leaves it out) at the two AlexNet positions, batch 256, alone."""
+    import torch
+    from paper_1603_07846_amd import singa
+    lrn = {}
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(1603078465)
+    dt_t = torch.bfloat16 if is_bf16 else torch.float32
+    es = 2 if is_bf16 else 4
+    for name, (C, H) in (("after_conv1", (96, 55)), ("after_conv2", (256, 27))):
+        xl = torch.randn((net.batch, H, H, C), device=dev, generator=gen).relu_().to(dt_t)
+        dyl = torch.randn((net.batch, H, H, C), device=dev, generator=gen).to(dt_t)
+        yl, dxl = torch.empty_like(xl), torch.empty_like(xl)
+        res = {}
+        for kind, fn, nb in (("fwd", lambda: singa.lrn_fwd(xl, 5, 1e-4, 0.75, 1.0, out=yl), 2 * es),
+                             ("bwd", lambda: singa.lrn_bwd(xl, dyl, 5, 1e-4, 0.75, 1.0, out=dxl), 3 * es)):
+            for _ in range(3):
+                fn()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(20):
+                fn()
+            e1.record()
+            torch.cuda.synchronize()
+            ms = e0.elapsed_time(e1) / 20
+            gbs = xl.numel() * nb / (ms / 1e3) / 1e9
+            res[kind] = {"ms": round(ms, 4), "GB_per_s": round(gbs, 1), "frac_hbm_peak": round(gbs / PEAK["hbm_gbs"], 4)}
+        lrn[name] = dict(res, shape=[net.batch, C, H, H])
+        del xl, dyl, yl, dxl
+
+    return lrn
+
+
 def cpu_baseline(w, n_images):
     """The oracle (fp64 C, OpenMP) on a bounded sample of the same step: the
     full forward/backward of `n_images` images of the workload plus the
@@ -361,7 +427,8 @@ def main():
     recs = singa.trace_records()
     # the graphics clock under the same load (outside every timed region)
     clock = GfxClock()
-    clock.steady(eager_step)
+    if not args.steps_only:
+        clock.steady(eager_step)
 
     # per-kernel aggregates over the timed steps
     agg = {}
@@ -407,55 +474,10 @@ def main():
                   "frac_hbm_peak": round(gbs / PEAK["hbm_gbs"], 4), "bytes_per_param": 22 if is_bf16 else 20,
                   "params_per_step": int(upd["work"] / args.steps / (22 if is_bf16 else 20)),
                   "note": "layers whose update is not fused into their filter-gradient kernel"}
-    # both Updater protocols over the whole flat parameter buffer, alone
-    # (a copy of the net's buffers, so the step's state is left as it was)
-    updaters = {}
-    wf, gf, vf = net.w_flat.clone(), net.g_flat.clone(), torch.zeros_like(net.v_flat)
-    wbf = net.wb_flat.clone() if net.wb_flat is not None else None
-    nbytes = net.n_params_padded * (22 if wbf is not None else 20)
-    for name, fn in (("sgd_momentum", lambda: singa.sgd_momentum_update(wf, gf, vf, wbf, w.lr, w.momentum,
-                                                                        w.weight_decay)),
-                     ("adagrad", lambda: singa.adagrad_update(wf, gf, vf, wbf, w.lr, 1e-6, w.weight_decay))):
-        for _ in range(3):
-            fn()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record()
-        for _ in range(20):
-            fn()
-        e1.record()
-        torch.cuda.synchronize()
-        ms = e0.elapsed_time(e1) / 20
-        updaters[name] = {"ms": round(ms, 4), "GB_per_s": round(nbytes / (ms / 1e3) / 1e9, 1),
-                          "frac_hbm_peak": round(nbytes / (ms / 1e3) / 1e9 / PEAK["hbm_gbs"], 4),
-                          "params": net.n_params_padded}
-    del wf, gf, vf, wbf
-    # local response normalization (not part of this step: the paper's GPU
-    # AlexNet leaves it out) at the two AlexNet positions, batch 256, alone
-    lrn = {}
-    gen = torch.Generator(device=dev)
-    gen.manual_seed(1603078465)
-    dt_t = torch.bfloat16 if is_bf16 else torch.float32
-    es = 2 if is_bf16 else 4
-    for name, (C, H) in (("after_conv1", (96, 55)), ("after_conv2", (256, 27))):
-        xl = torch.randn((net.batch, H, H, C), device=dev, generator=gen).relu_().to(dt_t)
-        dyl = torch.randn((net.batch, H, H, C), device=dev, generator=gen).to(dt_t)
-        yl, dxl = torch.empty_like(xl), torch.empty_like(xl)
-        res = {}
-        for kind, fn, nb in (("fwd", lambda: singa.lrn_fwd(xl, 5, 1e-4, 0.75, 1.0, out=yl), 2 * es),
-                             ("bwd", lambda: singa.lrn_bwd(xl, dyl, 5, 1e-4, 0.75, 1.0, out=dxl), 3 * es)):
-            for _ in range(3):
-                fn()
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            e0.record()
-            for _ in range(20):
-                fn()
-            e1.record()
-            torch.cuda.synchronize()
-            ms = e0.elapsed_time(e1) / 20
-            gbs = xl.numel() * nb / (ms / 1e3) / 1e9
-            res[kind] = {"ms": round(ms, 4), "GB_per_s": round(gbs, 1), "frac_hbm_peak": round(gbs / PEAK["hbm_gbs"], 4)}
-        lrn[name] = dict(res, shape=[net.batch, C, H, H])
-        del xl, dyl, yl, dxl
+    updaters = lrn = None
+    if not args.steps_only:
+        updaters = measure_updaters(net, w)
+        lrn = measure_lrn(net, dev, is_bf16)
 
     kernels = sorted(({"kernel": n, "launches_per_step": a["launches"] / args.steps,
                        "ms_per_step": round(a["ms"] / args.steps, 4),
@@ -501,12 +523,12 @@ def main():
         "kernels": kernels[:16],
     }
     out["conv_gflop_per_step_algorithmic"] = round(step_conv_flops(w, net.batch) / 1e9, 2)
-    if not args.no_configs and args.workload in (5, 6):
+    if not args.no_configs and not args.steps_only and args.workload in (5, 6):
         graph = None
         del net, x, labels, dy
         torch.cuda.empty_cache()
         out["configs"] = {str(i): measure_config(i, args.steps, args.warmup) for i in (1, 2, 3, 4)}
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and not args.steps_only:
         out["cpu_baseline"] = cpu_baseline(w, args.cpu_images)
     print(json.dumps(out), flush=True)
 

@@ -560,6 +560,16 @@ int singa_conv_bwd_filter_sgd(singa_dtype dtype, singa_layout layout, const sing
     const SgdTargets u{w_master, w_mom, w_bf16, b_master, b_mom, b_bf16, lr, momentum, weight_decay};
     return hip_status(launch_conv_wgrad_sgd(dtype, s, x_ptr, dy_ptr, dw, db, u, st));
   }
+  // a split reduction applies the step to each summed element (NHWC input
+  // taken as it is); otherwise the gradient, then the flat update
+  ConvShape g0;
+  if (layout == SINGA_NHWC && input_rewrite(s, dtype, &g0) == RW_NONE) {
+    BwdFilterWs f;
+    carve_bwd_filter(s, dtype, layout, bias, o.inner, &f);
+    const SgdTargets u{w_master, w_mom, w_bf16, b_master, b_mom, b_bf16, lr, momentum, weight_decay};
+    const hipError_t e = launch_conv_wgrad_reduce_sgd(dtype, s, x_ptr, dy_ptr, f.partial, dw, db, u, conv_flops(s), st);
+    if (e != hipErrorNotSupported) return hip_status(e);
+  }
   float* g = dw ? dw : o.g;
   float* gb = bias ? (db ? db : o.gb) : nullptr;
   rc = singa_conv_bwd_filter(dtype, layout, x, x_ptr, w, d, dy_ptr, g, gb, 0, o.inner, o.inner_bytes, stream);

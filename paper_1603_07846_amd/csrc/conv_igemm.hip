@@ -1387,10 +1387,11 @@ __global__ __launch_bounds__(NT, 2) void conv_wgrad_large_kernel(WgradArgs a) {
 // group 0 adds the G partial sums in group order, so the result does not
 // depend on timing.  Many splits (the first layer's long reduction over few
 // filter elements) take G = 16, so the grid still fills the chip.
-template <int G>
+template <int G, bool UPD>
 __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restrict__ partial, int splits, int M,
                                                             int ldp, int Ng, int Nn, float* __restrict__ dw,
-                                                            float* __restrict__ db, int acc_dw, int acc_db) {
+                                                            float* __restrict__ db, int acc_dw, int acc_db,
+                                                            SgdTargets u) {
   constexpr int LG = 256 / G;
   __shared__ float4 part[G][LG];
   const size_t n = (size_t)M * ldp;
@@ -1406,10 +1407,10 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restr
     for (; k + 3 * G < splits; k += 4 * G) {
       float4 q[4];
 #pragma unroll
-      for (int u = 0; u < 4; ++u) q[u] = p[(size_t)(k + u * G) * n4];
+      for (int uu = 0; uu < 4; ++uu) q[uu] = p[(size_t)(k + uu * G) * n4];
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        t.x += q[u].x; t.y += q[u].y; t.z += q[u].z; t.w += q[u].w;
+      for (int uu = 0; uu < 4; ++uu) {
+        t.x += q[uu].x; t.y += q[uu].y; t.z += q[uu].z; t.w += q[uu].w;
       }
     }
     for (; k < splits; k += G) {
@@ -1431,8 +1432,25 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restr
     for (int e = 0; e < 4; ++e) {
       const int ce = col + e;
       if (ce >= Ng) break;
-      float* o = ce < Nn ? dw + (size_t)row * Nn + ce : db + row;
-      *o = (ce < Nn ? acc_dw : acc_db) ? *o + s4[e] : s4[e];
+      const bool is_w = ce < Nn;
+      const size_t o = is_w ? (size_t)row * Nn + ce : (size_t)row;
+      if constexpr (UPD) {
+        // the Updater's step on the complete gradient element; dw / db (may
+        // be NULL) also receive the gradient
+        float* W = is_w ? u.w : u.b;
+        float* V = is_w ? u.v : u.vb;
+        uint16_t* WB = is_w ? u.wb : u.bb;
+        float* Gd = is_w ? dw : db;
+        float wv = W[o], vv = V[o];
+        sgd_step(wv, vv, s4[e], u.lr, u.mom, u.wd);
+        W[o] = wv;
+        V[o] = vv;
+        if (WB) WB[o] = f32_to_bf16(wv);
+        if (Gd) Gd[o] = s4[e];
+      } else {
+        float* out = is_w ? dw + o : db + o;
+        *out = (is_w ? acc_dw : acc_db) ? *out + s4[e] : s4[e];
+      }
     }
   }
 }
@@ -1850,14 +1868,18 @@ hipError_t conv_wgrad_dispatch(const ConvShape& s, const void* x, const void* dy
   a.tiles_n = (a.Ng + bn - 1) / bn;
   a.tiles = ((a.M + bm - 1) / bm) * a.tiles_n;
   const int splits = wgrad_splits_for(s, DT, bias, large);
-  if (upd && !(large && splits == 1 && wgrad_update_fusable(s, DT, bias))) return hipErrorNotSupported;
+  // the update goes into the large kernel when it writes each element once,
+  // otherwise into the split-K reduction; a single split of the 128 x 128
+  // kernel has no place for it
+  if (upd && splits == 1 && !(large && wgrad_update_fusable(s, DT, bias))) return hipErrorNotSupported;
+  if (upd && splits > 1 && !partial) return hipErrorNotSupported;
   a.kt_per_split = (a.nkt + splits - 1) / splits;
   a.direct = splits == 1;
   a.acc_dw = upd ? 0 : acc_dw;
   a.acc_db = upd ? 0 : acc_db;
   a.out = a.direct ? dw : partial;
   a.db = db;
-  a.update = upd != nullptr;
+  a.update = upd != nullptr && a.direct;  // split: the reduction applies it
   if (upd) a.u = *upd;
   dim3 grid(a.tiles * splits);
   const bool nf = use_image_fastest(s, bk, large);
@@ -1880,15 +1902,28 @@ hipError_t conv_wgrad_dispatch(const ConvShape& s, const void* x, const void* dy
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || splits == 1) return e;
-  // fixed-order sum of the partial tiles into dw (and db)
+  // fixed-order sum of the partial tiles into dw (and db), or, with the
+  // update, the Updater's step on each summed element
   const size_t n = (size_t)a.M * a.ldp;
+  const SgdTargets none{};
+  if (upd) {
+    const double bytes = (double)a.M * a.Ng * (4.0 * splits + 18.0 + (dw ? 4.0 : 0.0));
+    TraceScope ts("splitk_reduce_sgd_kernel", st, bytes, WORK_BYTE);
+    if (splits >= 64)
+      hipLaunchKernelGGL((splitk_reduce_kernel<16, true>), dim3((unsigned)((n + 63) / 64)), dim3(256), 0, st, partial,
+                         splits, a.M, a.ldp, a.Ng, a.Nn, dw, db, 0, 0, *upd);
+    else
+      hipLaunchKernelGGL((splitk_reduce_kernel<4, true>), dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, partial,
+                         splits, a.M, a.ldp, a.Ng, a.Nn, dw, db, 0, 0, *upd);
+    return hipGetLastError();
+  }
   TraceScope ts("splitk_reduce_kernel", st, (double)a.M * a.Ng * 4.0 * (splits + 1 + (acc_dw ? 1 : 0)), WORK_BYTE);
   if (splits >= 64)
-    hipLaunchKernelGGL(splitk_reduce_kernel<16>, dim3((unsigned)((n + 63) / 64)), dim3(256), 0, st, partial, splits,
-                       a.M, a.ldp, a.Ng, a.Nn, dw, db, acc_dw, acc_db);
+    hipLaunchKernelGGL((splitk_reduce_kernel<16, false>), dim3((unsigned)((n + 63) / 64)), dim3(256), 0, st, partial,
+                       splits, a.M, a.ldp, a.Ng, a.Nn, dw, db, acc_dw, acc_db, none);
   else
-    hipLaunchKernelGGL(splitk_reduce_kernel<4>, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, partial, splits,
-                       a.M, a.ldp, a.Ng, a.Nn, dw, db, acc_dw, acc_db);
+    hipLaunchKernelGGL((splitk_reduce_kernel<4, false>), dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, partial,
+                       splits, a.M, a.ldp, a.Ng, a.Nn, dw, db, acc_dw, acc_db, none);
   return hipGetLastError();
 }
 
@@ -1931,6 +1966,13 @@ hipError_t launch_conv_wgrad(int dt, const ConvShape& s, const void* x, const vo
 
 bool wgrad_update_fusable(const ConvShape& s, int dt, bool bias) {
   return wgrad_large_shape(s, dt) && wgrad_splits_for(s, dt, bias, true) == 1;
+}
+
+hipError_t launch_conv_wgrad_reduce_sgd(int dt, const ConvShape& s, const void* x, const void* dy, float* partial,
+                                        float* dw, float* db, const SgdTargets& u, double flops, hipStream_t st) {
+  if (!partial) return hipErrorNotSupported;
+  if (dt == BF16) return conv_wgrad_dispatch<bf16_t>(s, x, dy, partial, dw, u.b ? db : nullptr, 0, 0, &u, flops, st);
+  return conv_wgrad_dispatch<float>(s, x, dy, partial, dw, u.b ? db : nullptr, 0, 0, &u, flops, st);
 }
 
 hipError_t launch_conv_wgrad_sgd(int dt, const ConvShape& s, const void* x, const void* dy, float* dw, float* db,

@@ -515,94 +515,77 @@ __global__ __launch_bounds__(256) void softmax_ce_mean_kernel(int B, float* __re
 // are written; one thread per 8 parameters, no grid-stride cap (measured
 // best of the variants tried, ~5.5 TB/s; streaming loads / stores were
 // slower).  n % 8 tail elements are handled one by one by the first threads.
-__device__ __forceinline__ void sgd4(float4& wv, float4 gv, float4& vv, float lr, float mom, float wd) {
-  sgd_step(wv.x, vv.x, gv.x, lr, mom, wd);
-  sgd_step(wv.y, vv.y, gv.y, lr, mom, wd);
-  sgd_step(wv.z, vv.z, gv.z, lr, mom, wd);
-  sgd_step(wv.w, vv.w, gv.w, lr, mom, wd);
+// The Updaters stream w, g and the state (momentum v, or AdaGrad's h) once:
+// a thread owns UPD_U float4 vectors of each array, UPD_U x 256 apart so that
+// each load instruction of a workgroup covers 4 KB of contiguous memory, and
+// issues all its loads before any arithmetic.  Loads and stores are
+// non-temporal (the buffers are read once and written once per step, larger
+// than the caches): with 16 parameters per thread this measured 6.1 TB/s on
+// the 62.4M-parameter buffer, against 5.3-5.5 with cached accesses, 8
+// parameters per thread or either kind of access alone non-temporal.
+constexpr int UPD_U = 4;
+typedef float f4v __attribute__((ext_vector_type(4)));
+typedef uint32_t u2v __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ u2v bf16x4_bits(const f4v& w) {
+  return u2v{(uint32_t)f32_to_bf16(w.x) | ((uint32_t)f32_to_bf16(w.y) << 16),
+             (uint32_t)f32_to_bf16(w.z) | ((uint32_t)f32_to_bf16(w.w) << 16)};
+}
+
+// STEP(w, state, g): one Updater step on one parameter (sgd_step or adagrad_step).
+template <typename Step>
+__device__ __forceinline__ void update_stream(size_t n, float* __restrict__ w, const float* __restrict__ g,
+                                              float* __restrict__ s, uint16_t* __restrict__ wb, Step step) {
+  const size_t n4 = n / 4;
+  const size_t base = (size_t)blockIdx.x * blockDim.x * UPD_U + threadIdx.x;
+  f4v W[UPD_U], G[UPD_U], S[UPD_U];
+#pragma unroll
+  for (int u = 0; u < UPD_U; ++u) {
+    const size_t i = base + (size_t)u * blockDim.x;
+    if (i < n4) {
+      W[u] = __builtin_nontemporal_load((const f4v*)w + i);
+      G[u] = __builtin_nontemporal_load((const f4v*)g + i);
+      S[u] = __builtin_nontemporal_load((const f4v*)s + i);
+    }
+  }
+#pragma unroll
+  for (int u = 0; u < UPD_U; ++u) {
+    const size_t i = base + (size_t)u * blockDim.x;
+    if (i < n4) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        float we = W[u][e], se = S[u][e];
+        step(we, se, G[u][e]);
+        W[u][e] = we;
+        S[u][e] = se;
+      }
+      __builtin_nontemporal_store(S[u], (f4v*)s + i);
+      __builtin_nontemporal_store(W[u], (f4v*)w + i);
+      if (wb) __builtin_nontemporal_store(bf16x4_bits(W[u]), (u2v*)wb + i);
+    }
+  }
+  // the last n % 4 parameters: one thread each in the first workgroup
+  const size_t t = n4 * 4 + threadIdx.x;
+  if (blockIdx.x == 0 && t < n) {
+    float wt = w[t], st = s[t];
+    step(wt, st, g[t]);
+    s[t] = st;
+    w[t] = wt;
+    if (wb) wb[t] = f32_to_bf16(wt);
+  }
 }
 
 __global__ __launch_bounds__(256) void sgd_kernel(size_t n, float* __restrict__ w, const float* __restrict__ g,
                                                   float* __restrict__ v, uint16_t* __restrict__ wb, float lr,
                                                   float mom, float wd) {
-  const size_t n8 = n / 8;
-  const size_t stride = (size_t)gridDim.x * blockDim.x;
-  typedef float f4 __attribute__((ext_vector_type(4)));
-  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n8; i += stride) {
-    const f4* wp = (const f4*)w + 2 * i;
-    const f4* gp = (const f4*)g + 2 * i;
-    const f4* vp = (const f4*)v + 2 * i;
-    f4 w0 = *wp, w1 = *(wp + 1);
-    const f4 g0 = *gp, g1 = *(gp + 1);
-    f4 v0 = *vp, v1 = *(vp + 1);
-    float4 a0 = make_float4(w0.x, w0.y, w0.z, w0.w), a1 = make_float4(w1.x, w1.y, w1.z, w1.w);
-    float4 m0 = make_float4(v0.x, v0.y, v0.z, v0.w), m1 = make_float4(v1.x, v1.y, v1.z, v1.w);
-    sgd4(a0, make_float4(g0.x, g0.y, g0.z, g0.w), m0, lr, mom, wd);
-    sgd4(a1, make_float4(g1.x, g1.y, g1.z, g1.w), m1, lr, mom, wd);
-    ((f4*)v)[2 * i] = f4{m0.x, m0.y, m0.z, m0.w};
-    ((f4*)v)[2 * i + 1] = f4{m1.x, m1.y, m1.z, m1.w};
-    ((f4*)w)[2 * i] = f4{a0.x, a0.y, a0.z, a0.w};
-    ((f4*)w)[2 * i + 1] = f4{a1.x, a1.y, a1.z, a1.w};
-    if (wb) {
-      typedef uint32_t u4 __attribute__((ext_vector_type(4)));
-      const u4 b = {(uint32_t)f32_to_bf16(a0.x) | ((uint32_t)f32_to_bf16(a0.y) << 16),
-                    (uint32_t)f32_to_bf16(a0.z) | ((uint32_t)f32_to_bf16(a0.w) << 16),
-                    (uint32_t)f32_to_bf16(a1.x) | ((uint32_t)f32_to_bf16(a1.y) << 16),
-                    (uint32_t)f32_to_bf16(a1.z) | ((uint32_t)f32_to_bf16(a1.w) << 16)};
-      ((u4*)wb)[i] = b;
-    }
-  }
-  const size_t t = n8 * 8 + (size_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (t < n) {
-    float wt = w[t], vt = v[t];
-    sgd_step(wt, vt, g[t], lr, mom, wd);
-    v[t] = vt;
-    w[t] = wt;
-    if (wb) wb[t] = f32_to_bf16(wt);
-  }
+  update_stream(n, w, g, v, wb, [=](float& we, float& ve, float ge) { sgd_step(we, ve, ge, lr, mom, wd); });
 }
 
-// AdaGrad over a flat parameter buffer, laid out like sgd_kernel: 8
-// consecutive parameters per thread, every load issued before the arithmetic.
+// AdaGrad over a flat parameter buffer, laid out like sgd_kernel.
 __global__ __launch_bounds__(256) void adagrad_kernel(size_t n, float* __restrict__ w, const float* __restrict__ g,
                                                       float* __restrict__ h, uint16_t* __restrict__ wb, float lr,
                                                       float delta, float wd) {
-  const size_t n8 = n / 8;
-  const size_t stride = (size_t)gridDim.x * blockDim.x;
-  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n8; i += stride) {
-    float4 w4[2], g4[2], h4[2];
-#pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      w4[u] = ((const float4*)w)[2 * i + u];
-      g4[u] = ((const float4*)g)[2 * i + u];
-      h4[u] = ((const float4*)h)[2 * i + u];
-    }
-#pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      adagrad_step(w4[u].x, h4[u].x, g4[u].x, lr, delta, wd);
-      adagrad_step(w4[u].y, h4[u].y, g4[u].y, lr, delta, wd);
-      adagrad_step(w4[u].z, h4[u].z, g4[u].z, lr, delta, wd);
-      adagrad_step(w4[u].w, h4[u].w, g4[u].w, lr, delta, wd);
-      ((float4*)h)[2 * i + u] = h4[u];
-      ((float4*)w)[2 * i + u] = w4[u];
-    }
-    if (wb) {
-      uint4 b;
-      b.x = (uint32_t)f32_to_bf16(w4[0].x) | ((uint32_t)f32_to_bf16(w4[0].y) << 16);
-      b.y = (uint32_t)f32_to_bf16(w4[0].z) | ((uint32_t)f32_to_bf16(w4[0].w) << 16);
-      b.z = (uint32_t)f32_to_bf16(w4[1].x) | ((uint32_t)f32_to_bf16(w4[1].y) << 16);
-      b.w = (uint32_t)f32_to_bf16(w4[1].z) | ((uint32_t)f32_to_bf16(w4[1].w) << 16);
-      ((uint4*)wb)[i] = b;
-    }
-  }
-  const size_t t = n8 * 8 + (size_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (t < n) {
-    float wt = w[t], ht = h[t];
-    adagrad_step(wt, ht, g[t], lr, delta, wd);
-    h[t] = ht;
-    w[t] = wt;
-    if (wb) wb[t] = f32_to_bf16(wt);
-  }
+  update_stream(n, w, g, h, wb, [=](float& we, float& he, float ge) { adagrad_step(we, he, ge, lr, delta, wd); });
 }
 
 // ------------------------------------------------- local response norm
@@ -758,7 +741,7 @@ hipError_t launch_lrn(int dt, int bwd, int N, int C, int HW, int size, float alp
 
 hipError_t launch_adagrad(size_t n, float* w, const float* g, float* h, uint16_t* wb, float lr, float delta,
                           float wd, hipStream_t st) {
-  const unsigned grid = grid_for(n / 8 + 1, 256, 1u << 20);
+  const unsigned grid = grid_for(n / 4 / UPD_U + 1, 256, 1u << 30);
   TraceScope ts("adagrad_kernel", st, (double)n * (20.0 + (wb ? 2.0 : 0.0)), WORK_BYTE);
   hipLaunchKernelGGL(adagrad_kernel, dim3(grid), dim3(256), 0, st, n, w, g, h, wb, lr, delta, wd);
   return hipGetLastError();
@@ -906,7 +889,7 @@ hipError_t launch_softmax_ce(int dt, int B, int classes, const void* z, const in
 
 hipError_t launch_sgd(size_t n, float* w, const float* g, float* v, uint16_t* wb, float lr, float mom, float wd,
                       hipStream_t st) {
-  const unsigned grid = grid_for(n / 8 + 1, 256, 1u << 20);
+  const unsigned grid = grid_for(n / 4 / UPD_U + 1, 256, 1u << 30);
   TraceScope ts("sgd_kernel", st, (double)n * (20.0 + (wb ? 2.0 : 0.0)), WORK_BYTE);
   hipLaunchKernelGGL(sgd_kernel, dim3(grid), dim3(256), 0, st, n, w, g, v, wb, lr, mom, wd);
   return hipGetLastError();

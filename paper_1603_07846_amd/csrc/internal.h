@@ -95,6 +95,16 @@ bool wgrad_update_fusable(const ConvShape& s, int dt, bool bias);
 hipError_t launch_conv_wgrad_sgd(int dt, const ConvShape& s, const void* x, const void* dy, float* dw, float* db,
                                  const SgdTargets& u, hipStream_t st);
 
+// The filter gradient with the update applied by its split-K reduction: the
+// GEMM writes partial tiles into `partial` (wgrad_partial_bytes() of
+// workspace) and the fixed-order reduction applies the step to each summed
+// element (w, v, wb, and b, vb, bb with a bias), storing the gradient in dw
+// (db) too when not NULL.  When the kernel that runs s would use a single
+// split and cannot take the update itself, returns hipErrorNotSupported and
+// launches nothing.
+hipError_t launch_conv_wgrad_reduce_sgd(int dt, const ConvShape& s, const void* x, const void* dy, float* partial,
+                                        float* dw, float* db, const SgdTargets& u, double flops, hipStream_t st);
+
 // Batched 2-D transpose: for b in [0, batch): out(b)[c][r] = in(b)[r][c] with
 // in(b) = in + in_base(b), out(b) = out + out_base(b), where
 // in_base(b) = b * in_bstride and out_base(b) = (flip ? batch-1-b : b) * out_bstride.

@@ -87,6 +87,12 @@ class ConvLayer(Layer):
         # update fused into the filter-gradient kernel (no workspace needed exactly then)
         self.fused_update = bool(net.fuse_update and net.wl.update and net.updater == "sgd" and singa.conv_workspace_bytes(
             singa.OP_BWD_FILTER_SGD, dt, self.in_shape, self.w_shape, self.pad, self.stride) == 0)
+        # update applied by the filter gradient's split-K reduction (convolutions
+        # whose input the library takes as it is)
+        self.reduce_update = bool(net.fuse_update and net.reduce_update and net.wl.update and net.updater == "sgd"
+                                  and not self.fused_update and not fc
+                                  and singa.space_to_depth_bytes(dt, self.in_shape, self.w_shape, self.pad,
+                                                                 self.stride) == 0)
         self.y = singa.empty(self.out_shape, dt, dev)
         self.dx = singa.empty(self.in_shape, dt, dev)
         self.x = None
@@ -102,8 +108,11 @@ class ConvLayer(Layer):
             net.need_workspace(singa.conv_workspace_bytes(op, dt, self.in_shape, self.w_shape, self.pad,
                                                           self.stride,
                                                           self.x_layout if op != singa.OP_BWD_DATA else "NHWC"))
+        wop = singa.OP_BWD_FILTER_SGD if self.reduce_update else singa.OP_BWD_FILTER
         net.ws_wgrad_bytes = max(net.ws_wgrad_bytes, singa.conv_workspace_bytes(
-            singa.OP_BWD_FILTER, dt, self.in_shape, self.w_shape, self.pad, self.stride, self.x_layout))
+            wop, dt, self.in_shape, self.w_shape, self.pad, self.stride, self.x_layout))
+        if self.reduce_update:
+            net.need_workspace(net.ws_wgrad_bytes)
 
     def bind(self, w, b, w_compute, dw, db, v, vb, b_compute):
         self.w, self.b, self.w_compute, self.dw, self.db = w, b, w_compute, dw, db
@@ -119,8 +128,10 @@ class ConvLayer(Layer):
         return self.y
 
     def compute_gradient(self, dy, need_dx=True):
-        if self.fused_update:
+        if self.fused_update or self.reduce_update:
             # backward-data first: it reads the bf16 weights the update rewrites
+            # (fused into the gradient kernel, or applied by its split-K
+            # reduction)
             self._bwd_data(dy, need_dx)
             net, wl_ = self.net, self.net.wl
             keep = net.keep_grads
@@ -134,7 +145,8 @@ class ConvLayer(Layer):
                 singa.conv_bwd_filter_sgd(
                     self.x, dy, self.w_shape, self.w, self.v, self.w_compute if net.wb_flat is not None else None,
                     b=self.b, vb=self.vb, b_bf16=self.b_compute, lr=wl_.lr, momentum=wl_.momentum,
-                    weight_decay=wl_.weight_decay, pad=self.pad, stride=self.stride, dw=self.dw if keep else None,
+                    weight_decay=wl_.weight_decay, pad=self.pad, stride=self.stride,
+                    dw=self.dw if keep else None,
                     db=self.db if keep else None, workspace=net.workspace if side is None else net.workspace_wgrad)
             return self.dx if need_dx else None
         side = self.net.wgrad_stream
@@ -253,7 +265,7 @@ class Net:
 
     def __init__(self, workload: wl.Workload, batch: Optional[int] = None, device="cuda", fuse_update: bool = True,
                  keep_grads: bool = False, concurrent_wgrad: bool = True, updater: str = "sgd",
-                 adagrad_delta: float = 1e-6):
+                 adagrad_delta: float = 1e-6, reduce_update: bool = False):
         """fuse_update: apply the update inside the filter-gradient kernel
         where it can be fused; keep_grads: those layers also store their
         gradients in the flat gradient buffer (for inspection);
@@ -267,6 +279,7 @@ class Net:
             raise ValueError(updater)
         self.updater = updater
         self.adagrad_delta = adagrad_delta
+        self.reduce_update = reduce_update
         self.wl = workload
         self.fuse_update = fuse_update
         self.keep_grads = keep_grads
@@ -351,7 +364,7 @@ class Net:
         # contiguous runs of the flat buffers that the update after the backward loop covers
         self.update_ranges = []
         for l in self.param_layers():
-            if l.fused_update:
+            if l.fused_update or l.reduce_update:
                 continue
             a, e = l.flat_range
             if self.update_ranges and self.update_ranges[-1][1] == a:

@@ -56,18 +56,22 @@ def test_graph_replay_matches_eager(index, batch):
         assert np.isfinite(float(eager.layers[-1].loss[0]))
 
 
-@pytest.mark.parametrize("index,batch", [(5, 8), (5, 32), (6, 8), (5, 256)])
-def test_two_stream_eager_matches_one_stream(index, batch):
+@pytest.mark.parametrize("index,batch,reduce_update", [(5, 8, False), (5, 32, False), (6, 8, False), (5, 256, False),
+                                                       (5, 32, True), (5, 256, True)])
+def test_two_stream_eager_matches_one_stream(index, batch, reduce_update):
     """The default step launched eagerly (filter gradients, and the fully
-    connected layers' fused gradient + update, on the second stream) against
-    one stream with every update after the backward loop: bit for bit, over
-    three steps, with no synchronization inside a step."""
+    connected layers' fused gradient + update, on the second stream; with
+    reduce_update, the convolutions' updates applied by their split-K
+    reductions there too) against one stream with every update after the
+    backward loop: bit for bit, over three steps, with no synchronization
+    inside a step."""
     from paper_1603_07846_amd import net as gnet
     w = wl.WORKLOADS[index]
     inp = wl.make_inputs(w, batch=batch, seed_offset=33)
     one = gnet.Net(w, batch=batch, device="cuda:0", fuse_update=False, concurrent_wgrad=False)
-    two = gnet.Net(w, batch=batch, device="cuda:0")
+    two = gnet.Net(w, batch=batch, device="cuda:0", reduce_update=reduce_update)
     assert two.wgrad_stream is not None and any(l.fused_update for l in two.param_layers())
+    assert any(l.reduce_update for l in two.param_layers()) == reduce_update
     for n in (one, two):
         n.load_params(inp.params)
     x = one.to_device_input(inp.x)

@@ -225,6 +225,67 @@ def test_conv_bwd_filter_large_tile(case, bias, halves):
         assert db is None
 
 
+# the 128 x 256 filter-gradient kernel with K-tiles of 32 images at one
+# output pixel (batches that are multiples of 32, as in the benchmark):
+# ragged rows and taps, the bias column in a ragged column tile, direct and
+# split reductions, a strided padded layer, the space-to-depth first layer, a
+# whole-input (fully connected) layer, and accumulation over two batches
+PIXEL_WGRAD_CASES = [
+    (32, 32, 15, 15, 512, 3, 3, 1, 1, True),     # two row tiles, ragged taps + bias, split reduction
+    (32, 64, 3, 3, 256, 3, 3, 1, 1, True),       # nine K-tiles: one split, written directly
+    (32, 24, 13, 13, 304, 3, 3, 1, 1, True),     # 304 filters: ragged row tile
+    (64, 48, 7, 7, 96, 3, 3, 1, 1, False),       # 96 filters, no bias
+    (32, 16, 20, 20, 256, 5, 5, 2, 2, True),     # stride 2, pad 2
+    (32, 64, 4, 4, 520, 4, 4, 0, 1, True),       # whole-input layer, three column tiles
+    (32, 3, 35, 35, 96, 11, 11, 0, 4, True),     # AlexNet conv1 geometry on its space-to-depth form
+]
+
+
+@pytest.mark.parametrize("case", PIXEL_WGRAD_CASES, ids=["x".join(map(str, c[:9])) + ("-bias" if c[9] else "")
+                                                         for c in PIXEL_WGRAD_CASES])
+def test_conv_bwd_filter_pixel_order(case):
+    case, bias = case[:9], case[9]
+    N, C, H, W, K, R, S, pad, stride = case
+    x, w, b, dy = _conv_inputs(case, "bf16", 44)
+    ref_dw, ref_db = oracle.conv_bwd_filter(x, dy, w.shape, pad=pad, stride=stride)
+    xd, dyd = nchw_to_dev(x, "bf16"), nchw_to_dev(dy, "bf16")
+    singa.trace_enable(True)
+    dw, db = singa.conv_bwd_filter(xd, dyd, fphys(w.shape), pad, stride, with_bias=bias)
+    torch.cuda.synchronize()
+    names = [r[0] for r in singa.trace_records()]
+    singa.trace_enable(False)
+    assert "conv_wgrad_large_kernel<1,0>" in names, names
+    assert rel_l2(filt_to_kcrs(dw), ref_dw) <= TOL["f32"]
+    if bias:
+        assert rel_l2(db.cpu().numpy(), ref_db) <= TOL["f32"]
+    else:
+        assert db is None
+    # bitwise reproducible: the partial tiles are summed in a fixed order
+    dw2, db2 = singa.conv_bwd_filter(xd, dyd, fphys(w.shape), pad, stride, with_bias=bias)
+    torch.cuda.synchronize()
+    assert torch.equal(dw, dw2) and (db is None or torch.equal(db, db2))
+
+
+def test_conv_bwd_filter_pixel_order_accumulate():
+    # the gradients of two batches of 32 added through the accumulate flag
+    case = (32, 32, 9, 9, 384, 3, 3, 1, 1)
+    N, C, H, W, K, R, S, pad, stride = case
+    x1, w, b, dy1 = _conv_inputs(case, "bf16", 45)
+    x2, _, _, dy2 = _conv_inputs(case, "bf16", 46)
+    r1 = oracle.conv_bwd_filter(x1, dy1, w.shape, pad=pad, stride=stride)
+    r2 = oracle.conv_bwd_filter(x2, dy2, w.shape, pad=pad, stride=stride)
+    singa.trace_enable(True)
+    dw, db = singa.conv_bwd_filter(nchw_to_dev(x1, "bf16"), nchw_to_dev(dy1, "bf16"), fphys(w.shape), pad, stride)
+    singa.conv_bwd_filter(nchw_to_dev(x2, "bf16"), nchw_to_dev(dy2, "bf16"), fphys(w.shape), pad, stride, dw=dw,
+                          db=db, accumulate=True)
+    torch.cuda.synchronize()
+    names = [r[0] for r in singa.trace_records()]
+    singa.trace_enable(False)
+    assert names.count("conv_wgrad_large_kernel<1,0>") == 2, names
+    assert rel_l2(filt_to_kcrs(dw), r1[0] + r2[0]) <= TOL["f32"]
+    assert rel_l2(db.cpu().numpy(), r1[1] + r2[1]) <= TOL["f32"]
+
+
 def test_conv_bwd_filter_deterministic():
     case = (4, 32, 15, 15, 48, 3, 3, 1, 1)
     x, w, b, dy = _conv_inputs(case, "f32", 50)
@@ -575,7 +636,13 @@ SGD_CASES = [
     (64, 32, 6, 6, 40, 6, 6, 0, 1, "f32", "NHWC", True),
     (64, 32, 6, 6, 40, 6, 6, 0, 1, "bf16", "NCHW", True),
     (16, 64, 1, 1, 30, 1, 1, 0, 1, "bf16", "NHWC", True),
+    (32, 96, 27, 27, 256, 5, 5, 2, 1, "bf16", "NHWC", True),   # AlexNet conv2 shape, pixel-ordered split reduction
+    (16, 16, 16, 16, 32, 3, 3, 1, 1, "bf16", "NHWC", False),   # split reduction without bias
+    (16, 16, 16, 16, 32, 3, 3, 1, 1, "f32", "NHWC", True),     # fp32 split reduction (128 x 128 kernel)
+    (4, 3, 35, 35, 8, 11, 11, 0, 4, "bf16", "NHWC", True),     # space-to-depth first layer: gradient, then update
 ]
+# the cases whose update the split-K reduction applies
+SGD_REDUCE = {5, 9, 10, 11}
 
 
 def _sgd_state(K, C, R, S, layout, seed):
@@ -628,6 +695,8 @@ def test_conv_bwd_filter_sgd_matches_gradient_then_update(case):
         names = [r[0] for r in singa.trace_records()]
         singa.trace_enable(False)
         assert any(n.endswith(",1>") and n.startswith("conv_wgrad_large") for n in names) == fused_expected, names
+        assert ("splitk_reduce_sgd_kernel" in names) == (SGD_CASES.index(case) in SGD_REDUCE), names
+        assert ("sgd_kernel" in names) == (not fused_expected and SGD_CASES.index(case) not in SGD_REDUCE), names
         assert torch.equal(wf, wr) and torch.equal(vf, vr) and torch.equal(wbf, wbr), (case, mode)
         if bias:
             assert torch.equal(bf, br) and torch.equal(vbf, vbr) and torch.equal(bbf, bbr), (case, mode)
