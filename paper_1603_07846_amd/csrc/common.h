@@ -20,6 +20,16 @@ __device__ __forceinline__ bf16_t f32_to_bf16(float f) {
   return (bf16_t)(u >> 16);
 }
 
+// Two fp32 values -> two bf16 (low half: a), round to nearest even, in one
+// gfx950 conversion instruction (v_cvt_pk_bf16_f32).  Same results as
+// f32_to_bf16 on every finite value the kernels produce (not relied on for
+// NaN payloads or subnormals).
+__device__ __forceinline__ uint32_t f32x2_to_bf16x2(float a, float b) {
+  typedef float f2 __attribute__((ext_vector_type(2)));
+  typedef __bf16 h2 __attribute__((ext_vector_type(2)));
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f2){a, b}, h2));
+}
+
 __device__ __forceinline__ float bf16_to_f32(bf16_t b) {
   return __uint_as_float(((uint32_t)b) << 16);
 }

@@ -16,6 +16,28 @@ template <typename T> __device__ __forceinline__ void st_f(T* p, float v);
 template <> __device__ __forceinline__ void st_f<float>(float* p, float v) { *p = v; }
 template <> __device__ __forceinline__ void st_f<bf16_t>(bf16_t* p, float v) { *p = f32_to_bf16(v); }
 
+// 16 bytes <-> VEC floats (bf16: 8, fp32: 4) without taking a local's address
+template <typename T> __device__ __forceinline__ void unpack16(const uint4& u, float* f);
+template <> __device__ __forceinline__ void unpack16<bf16_t>(const uint4& u, float* f) {
+  const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    f[2 * i] = __uint_as_float(w[i] << 16);
+    f[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+  }
+}
+template <> __device__ __forceinline__ void unpack16<float>(const uint4& u, float* f) {
+  f[0] = __uint_as_float(u.x); f[1] = __uint_as_float(u.y); f[2] = __uint_as_float(u.z); f[3] = __uint_as_float(u.w);
+}
+template <typename T> __device__ __forceinline__ uint4 pack16(const float* f);
+template <> __device__ __forceinline__ uint4 pack16<bf16_t>(const float* f) {
+  return make_uint4(f32x2_to_bf16x2(f[0], f[1]), f32x2_to_bf16x2(f[2], f[3]), f32x2_to_bf16x2(f[4], f[5]),
+                    f32x2_to_bf16x2(f[6], f[7]));
+}
+template <> __device__ __forceinline__ uint4 pack16<float>(const float* f) {
+  return make_uint4(__float_as_uint(f[0]), __float_as_uint(f[1]), __float_as_uint(f[2]), __float_as_uint(f[3]));
+}
+
 unsigned grid_for(size_t total, int block = 256, size_t cap = 1 << 20) {
   size_t g = (total + block - 1) / block;
   if (g < 1) g = 1;
@@ -528,8 +550,7 @@ typedef float f4v __attribute__((ext_vector_type(4)));
 typedef uint32_t u2v __attribute__((ext_vector_type(2)));
 
 __device__ __forceinline__ u2v bf16x4_bits(const f4v& w) {
-  return u2v{(uint32_t)f32_to_bf16(w.x) | ((uint32_t)f32_to_bf16(w.y) << 16),
-             (uint32_t)f32_to_bf16(w.z) | ((uint32_t)f32_to_bf16(w.w) << 16)};
+  return u2v{f32x2_to_bf16x2(w.x, w.y), f32x2_to_bf16x2(w.z, w.w)};
 }
 
 // STEP(w, state, g): one Updater step on one parameter (sgd_step or adagrad_step).
@@ -601,6 +622,13 @@ struct LrnGeom {
 };
 
 __device__ __forceinline__ float pow_neg(float s, float e) { return exp2f(-e * log2f(s)); }  // s^-e, s > 0
+// The same for a normal s (s >= 2^-126: the vector kernel's s >= k, which the
+// launcher checks): the hardware log2 / exp2 without the library's
+// subnormal handling, and the reciprocal, each within an ulp or two.
+__device__ __forceinline__ float pow_neg_n(float s, float e) {
+  return __builtin_amdgcn_exp2f(-e * __builtin_amdgcn_logf(s));
+}
+__device__ __forceinline__ float rcp_n(float s) { return __builtin_amdgcn_rcpf(s); }
 
 // One element per thread, any layout: channel stride cs (1 for NHWC, HW for NCHW).
 template <typename T, bool NCHW, bool BWD>
@@ -641,62 +669,135 @@ __global__ __launch_bounds__(256) void lrn_kernel(LrnGeom g, const T* __restrict
   }
 }
 
-// NHWC, VEC channels (16 bytes) per thread: the chunk and its two neighbours
-// are loaded (zeros past the ends of the channel axis, which add nothing to
-// a sum of squares), so every window the chunk needs is in registers.  The
-// window SIZE is a compile-time constant (3 or 5), so all register indices
-// are static.
+// NHWC, VEC channels (16 bytes) per thread.  A workgroup stages 256
+// consecutive chunks of x (and dy) plus one chunk on either side in LDS, so
+// every element is read from memory once; each thread takes its chunk and its
+// two neighbours from LDS (zeros past the ends of the pixel's channel axis,
+// which add nothing to a sum of squares), so every window of its channels is
+// in registers.  Backward: each thread computes s^-beta and
+// q = dy x s^(-beta-1) = dy x s^-beta / s for its own channels only (one
+// power per channel) and leaves q in LDS, where the neighbouring threads
+// take the (SIZE-1)/2 and SIZE/2 values their windows reach into; the kernel
+// is bound by its transcendental arithmetic, not its bytes.  The window
+// SIZE is a compile-time constant (3 or 5), so all register indices are
+// static.
 template <typename T, int VEC, bool BWD, int SIZE>
 __global__ __launch_bounds__(256) void lrn_vec_kernel(LrnGeom g, const T* __restrict__ x, const T* __restrict__ dy,
                                                       T* __restrict__ out, long chunks) {
   const int CV = g.C / VEC;
-  union U { uint4 u; T e[VEC]; };
-  for (long t = (long)blockIdx.x * blockDim.x + threadIdx.x; t < chunks; t += (long)gridDim.x * blockDim.x) {
+  __shared__ uint4 xs[258];
+  __shared__ float qs[BWD ? 256 * VEC : 1];
+  const uint4* __restrict__ x4 = (const uint4*)x;
+  const uint4* __restrict__ d4 = (const uint4*)dy;
+  const int tid = threadIdx.x;
+  // 16 bytes at p, or zeros when !ok, by value (a reference to a local
+  // constant would put the constant in scratch memory)
+  auto ld0 = [](bool ok, const uint4* p) {
+    uint4 v = make_uint4(0u, 0u, 0u, 0u);
+    if (ok) v = *p;
+    return v;
+  };
+  // s of channel c sums x^2 over [c - HI, c + LO]; dx of c sums q over [c - LO, c + HI]
+  constexpr int LO = (SIZE - 1) / 2, HI = SIZE / 2;
+  for (long b0 = (long)blockIdx.x * 256; b0 < chunks; b0 += (long)gridDim.x * 256) {
+    const long t = b0 + tid;
+    xs[1 + tid] = ld0(t < chunks, x4 + t);
+    float dv[VEC];
+    unpack16<T>(ld0(BWD && t < chunks, d4 + t), dv);
+    if (tid < 2) {  // the chunks just before and just after the workgroup's range
+      const long h = tid == 0 ? b0 - 1 : b0 + 256;
+      xs[tid == 0 ? 0 : 257] = ld0(h >= 0 && h < chunks, x4 + h);
+    }
+    __syncthreads();
     const int cv = (int)(t % CV);
-    const long pix = t / CV;
-    const T* xp = x + pix * g.C;
-    float xv[3 * VEC], dv[3 * VEC];
+    float xv[3 * VEC];
 #pragma unroll
     for (int h = 0; h < 3; ++h) {
-      const int q = cv - 1 + h;
-      U a, d;
-      a.u = (q >= 0 && q < CV) ? *(const uint4*)(xp + q * VEC) : make_uint4(0u, 0u, 0u, 0u);
-      if (BWD) d.u = (q >= 0 && q < CV) ? *(const uint4*)(dy + pix * g.C + q * VEC) : make_uint4(0u, 0u, 0u, 0u);
-#pragma unroll
-      for (int j = 0; j < VEC; ++j) {
-        xv[h * VEC + j] = ld_f<T>(&a.e[j]);
-        dv[h * VEC + j] = BWD ? ld_f<T>(&d.e[j]) : 0.f;
-      }
+      const bool in = (h == 0 && cv > 0) || h == 1 || (h == 2 && cv < CV - 1);  // same pixel
+      unpack16<T>(ld0(in, xs + tid + h), xv + h * VEC);
     }
     const float an = g.alpha / (float)SIZE;
-    auto scale = [&](int r) {  // r: index into xv
-      float acc = 0.f;
+    // window sums of x^2 as a running sum over the chunk (the kernel is bound
+    // by its arithmetic): squares of channels -HI .. VEC + LO - 1
+    float sq[HI + VEC + LO];
 #pragma unroll
-      for (int d = -(SIZE / 2); d <= (SIZE - 1) / 2; ++d) acc = fmaf(xv[r + d], xv[r + d], acc);
-      return fmaf(an, acc, g.k);
-    };
-    U o;
+    for (int r = 0; r < HI + VEC + LO; ++r) sq[r] = xv[VEC - HI + r] * xv[VEC - HI + r];
+    float sc[VEC], p[VEC];
+    float win = 0.f;
+#pragma unroll
+    for (int r = 0; r <= HI + LO; ++r) win += sq[r];
+#pragma unroll
+    for (int j = 0; j < VEC; ++j) {
+      if (j > 0) win += sq[j + HI + LO] - sq[j - 1];
+      sc[j] = fmaf(an, win, g.k);
+      p[j] = pow_neg_n(sc[j], g.beta);  // s^-beta
+    }
+    float o[VEC];
     if (!BWD) {
 #pragma unroll
-      for (int j = 0; j < VEC; ++j) st_f<T>(&o.e[j], xv[VEC + j] * pow_neg(scale(VEC + j), g.beta));
+      for (int j = 0; j < VEC; ++j) o[j] = xv[VEC + j] * p[j];
     } else {
-      // q[r] = dy[r] x[r] s[r]^(-beta-1) for the channels some window of the chunk needs
-      constexpr int lo = VEC - (SIZE - 1) / 2, hi = 2 * VEC - 1 + SIZE / 2;
-      float q[3 * VEC];
 #pragma unroll
-      for (int r = 0; r < 3 * VEC; ++r)
-        q[r] = (r >= lo && r <= hi) ? dv[r] * xv[r] * pow_neg(scale(r), g.beta + 1.f) : 0.f;
+      for (int j = 0; j < VEC; ++j) qs[tid * VEC + j] = dv[j] * xv[VEC + j] * p[j] * rcp_n(sc[j]);
+      __syncthreads();
+      // q of the own chunk (at LO + j) and of the LO channels before it and the
+      // HI channels after it that the windows reach into (same pixel only)
+      float q[LO + VEC + HI];
+#pragma unroll
+      for (int j = 0; j < VEC; ++j) q[LO + j] = qs[tid * VEC + j];
+#pragma unroll
+      for (int e = 0; e < LO; ++e) q[e] = (cv > 0 && tid > 0) ? qs[(tid - 1) * VEC + VEC - LO + e] : 0.f;
+#pragma unroll
+      for (int e = 0; e < HI; ++e) q[LO + VEC + e] = (cv < CV - 1 && tid < 255) ? qs[(tid + 1) * VEC + e] : 0.f;
+      // a neighbour chunk outside this workgroup's range: its q from its own
+      // values; the window sums of its channels needed here only reach into
+      // this chunk (VEC >= LO + HI)
+      static_assert(VEC >= LO + HI, "window wider than a chunk");
+      const bool left = tid == 0 && cv > 0, right = tid == 255 && cv < CV - 1 && t + 1 < chunks;
+      if (left || right) {
+        const long nb = left ? t - 1 : t + 1;
+        float dnf[VEC], xnf[VEC];
+        unpack16<T>(d4[nb], dnf);
+        unpack16<T>(x4[nb], xnf);
+        if (left) {  // channels VEC - LO .. VEC - 1 of chunk t - 1; their windows reach into this chunk
+#pragma unroll
+          for (int e = 0; e < LO; ++e) {
+            const int j = VEC - LO + e;
+            float acc = 0.f;
+#pragma unroll
+            for (int f = -HI; f <= LO; ++f) {
+              const float v = j + f < VEC ? xnf[j + f] : xv[VEC + j + f - VEC];
+              acc = fmaf(v, v, acc);
+            }
+            const float sn = fmaf(an, acc, g.k);
+            q[e] = dnf[j] * xnf[j] * pow_neg_n(sn, g.beta) * rcp_n(sn);
+          }
+        } else {  // channels 0 .. HI - 1 of chunk t + 1; their windows reach back into this chunk
+#pragma unroll
+          for (int e = 0; e < HI; ++e) {
+            float acc = 0.f;
+#pragma unroll
+            for (int f = -HI; f <= LO; ++f) {
+              const float v = e + f >= 0 ? xnf[e + f] : xv[VEC + VEC + e + f];
+              acc = fmaf(v, v, acc);
+            }
+            const float sn = fmaf(an, acc, g.k);
+            q[LO + VEC + e] = dnf[e] * xnf[e] * pow_neg_n(sn, g.beta) * rcp_n(sn);
+          }
+        }
+      }
       const float c2 = 2.f * g.alpha * g.beta / (float)SIZE;
+      float qw = 0.f;  // running sum of q over [j - LO, j + HI]
+#pragma unroll
+      for (int r = 0; r <= LO + HI; ++r) qw += q[r];
 #pragma unroll
       for (int j = 0; j < VEC; ++j) {
-        const int r = VEC + j;
-        float acc = 0.f;
-#pragma unroll
-        for (int d = -((SIZE - 1) / 2); d <= SIZE / 2; ++d) acc += q[r + d];
-        st_f<T>(&o.e[j], dv[r] * pow_neg(scale(r), g.beta) - c2 * xv[r] * acc);
+        if (j > 0) qw += q[j + LO + HI] - q[j - 1];
+        o[j] = dv[j] * p[j] - c2 * xv[VEC + j] * qw;
       }
     }
-    *(uint4*)(out + pix * g.C + cv * VEC) = o.u;
+    if (t < chunks) ((uint4*)out)[t] = pack16<T>(o);
+    __syncthreads();  // the LDS tiles are reused by the next range
   }
 }
 
@@ -707,8 +808,9 @@ hipError_t launch_lrn(int dt, int bwd, int N, int C, int HW, int size, float alp
   LrnGeom g{N, C, HW, size, alpha, beta, k};
   const long total = (long)N * C * HW;
   const int vec = dt == BF16 ? 8 : 4;
+  // (the vector kernel's arithmetic assumes a normal k, hence a normal s)
   const bool v = !nchw && C % vec == 0 && (uintptr_t)x % 16 == 0 && (uintptr_t)out % 16 == 0 &&
-                 (uintptr_t)dy % 16 == 0 && (size == 3 || size == 5);
+                 (uintptr_t)dy % 16 == 0 && (size == 3 || size == 5) && k >= 1.17549435e-38f;
   TraceScope ts(bwd ? "lrn_bwd_kernel" : "lrn_fwd_kernel", st, (double)total * dt_size(dt) * (bwd ? 3 : 2),
                 WORK_BYTE);
   if (v) {
