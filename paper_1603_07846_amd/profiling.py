@@ -15,6 +15,20 @@ Subcommands (run from the repository root):
       copy), stamped with the SHA-256 of the kernel's source file so that a
       reader can tell when the kernel has changed since the counters were
       taken.
+  counters CSV [CSV ...] --kernels NAME [NAME ...] [--copy-fetch CSV --copy-write CSV --copy-mib N]
+      Markdown table of derived figures per kernel from `rocprofv3 --pmc`
+      counter passes (each pass its own run of the same program): MFMA busy
+      fraction and MFMA rate, LDS bank conflicts, vector L1 stalls on
+      outstanding misses, mean L2 read latency, L2 hit rate, HBM bytes, and
+      the occupancy the kernel's registers and LDS allow.
+
+  libgemm [--reps N]
+      Times the vendor library's bf16 GEMM (torch.matmul, hipBLASLt) on the
+      explicit-GEMM shapes of the AlexNet-shaped layers at batch 256 (the
+      convolutions as im2col GEMMs: rows = output pixels, columns = filters,
+      reduction = taps) and a large square GEMM: a reference for what a plain
+      library GEMM of the same shape reaches on the device.  Not part of the
+      library's path (which calls no vendor GEMM).
 
 Kernel names are normalized to the library's trace names: the namespace and
 parameter list are dropped and template arguments written as in the trace
@@ -103,6 +117,44 @@ def cmd_stats(args):
             float(r["MinNs"]) / 1e3, float(r["MaxNs"]) / 1e3, 100.0 * float(r["TotalDurationNs"]) / total))
 
 
+LIBGEMM_SHAPES = [  # (name, M, N, K)
+    ("square 8192", 8192, 8192, 8192),
+    ("conv1 forward", 256 * 55 * 55, 96, 11 * 11 * 3),
+    ("conv2 forward", 256 * 27 * 27, 256, 5 * 5 * 96),
+    ("conv3 forward", 256 * 13 * 13, 384, 3 * 3 * 256),
+    ("conv4 forward", 256 * 13 * 13, 384, 3 * 3 * 384),
+    ("conv5 forward", 256 * 13 * 13, 256, 3 * 3 * 384),
+    ("conv2 filter gradient", 256, 5 * 5 * 96, 256 * 27 * 27),
+    ("conv4 filter gradient", 384, 3 * 3 * 384, 256 * 13 * 13),
+    ("fc6 forward", 256, 4096, 9216),
+    ("fc7 forward", 256, 4096, 4096),
+    ("fc8 forward", 256, 1000, 4096),
+]
+
+
+def cmd_libgemm(args):
+    import torch
+    torch.manual_seed(0)
+    print("| GEMM | M | N | K | ms | TFLOP/s | of 2516.6 |")
+    print("|---|---:|---:|---:|---:|---:|---:|")
+    for name, m, n, k in LIBGEMM_SHAPES:
+        a = torch.randn(m, k, device="cuda", dtype=torch.bfloat16)
+        b = torch.randn(k, n, device="cuda", dtype=torch.bfloat16)
+        for _ in range(3):
+            c = a @ b
+        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        ev0.record()
+        for _ in range(args.reps):
+            c = a @ b
+        ev1.record()
+        torch.cuda.synchronize()
+        ms = ev0.elapsed_time(ev1) / args.reps
+        tf = 2.0 * m * n * k / ms / 1e9
+        print("| %s | %d | %d | %d | %.4f | %.0f | %.1f%% |" % (name, m, n, k, ms, tf, 100.0 * tf / 2516.6), flush=True)
+        del a, b, c
+
+
 def _copy_factor(path, counter, nbytes):
     rows = _counter_rows(path, counter)
     vals = [v * 1024.0 for _, v in rows.values() if v > 0]
@@ -132,6 +184,122 @@ def cmd_traffic(args):
     print(json.dumps(out))
 
 
+# gfx950: 8 XCDs of 32 compute units, 4 SIMDs per CU, 512 VGPRs (arch + acc)
+# per lane per SIMD, 160 KiB of LDS per CU, at most 8 waves per SIMD.
+N_XCD, N_CU, SIMD_PER_CU, VGPR_FILE, LDS_BYTES, MAX_WAVES = 8, 256, 4, 512, 160 * 1024, 8
+
+
+def _dispatches(paths):
+    """{(path index, dispatch id): {"name", "ns", "wg", "lds", "vgpr", "agpr", counter: value}}."""
+    out = {}
+    for i, path in enumerate(paths):
+        with open(path) as f:
+            for r in csv.DictReader(f):
+                d = out.setdefault((i, r["Dispatch_Id"]), {
+                    "name": normalize(r["Kernel_Name"]), "ns": int(r["End_Timestamp"]) - int(r["Start_Timestamp"]),
+                    "grid": int(r["Grid_Size"]),
+                    "wg": int(r["Workgroup_Size"]), "lds": int(r["LDS_Block_Size"]),
+                    "vgpr": int(r["VGPR_Count"]), "agpr": int(r.get("Accum_VGPR_Count") or 0)})
+                d[r["Counter_Name"]] = d.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+    return out
+
+
+def _occupancy(wg, lds, vgpr, agpr):
+    """Waves per SIMD that the kernel's resources allow (VGPRs and AGPRs share one
+    file of 512 per lane, allocated in blocks of 8; LDS per CU)."""
+    regs = -(-(vgpr + agpr) // 8) * 8
+    by_regs = VGPR_FILE // regs if regs else MAX_WAVES
+    waves_per_wg = -(-wg // 64)
+    wg_per_cu = LDS_BYTES // lds if lds else 10 ** 9
+    by_lds = wg_per_cu * waves_per_wg / SIMD_PER_CU
+    return min(MAX_WAVES, by_regs, by_lds)
+
+
+def cmd_counters(args):
+    """MFMA busy = SQ_VALU_MFMA_BUSY_CYCLES / (cycles x SIMDs) (the counter is
+    summed over the 1024 SIMDs); MFMA TFLOP/s issued = 512 x
+    SQ_INSTS_VALU_MFMA_MOPS_* / duration (includes tile padding and the bias
+    column, unlike the algorithmic figures); LDS bank-conflict cycles per
+    cycle of LDS instruction activity; L1 miss-stall = TCP_PENDING_STALL_CYCLES
+    / (cycles x CUs); L2 read latency = TCP_TCC_READ_REQ_LATENCY /
+    TCP_TCC_READ_REQ (cycles per request, issued to returned)."""
+    disp = _dispatches(args.csv)
+    f_fetch = f_write = None
+    if args.copy_fetch and args.copy_write:
+        nbytes = args.copy_mib * (1 << 20)
+        f_fetch = _copy_factor(args.copy_fetch, "FETCH_SIZE", nbytes)
+        f_write = _copy_factor(args.copy_write, "WRITE_SIZE", nbytes)
+    cols = ["Kernel", "Launches", "us / launch", "MFMA busy", "MFMA TFLOP/s issued", "LDS bank-conflict cycles",
+            "L1 miss-stall", "L2 read latency (clk)", "L2 hit", "HBM read MB", "HBM write MB", "waves/SIMD (limit)"]
+    print("| " + " | ".join(cols) + " |")
+    print("|---|" + "---:|" * (len(cols) - 1))
+
+    def mean(rows, key):
+        vals = [r[key] for r in rows if key in r]
+        return statistics.mean(vals) if vals else None
+
+    def fmt(v, f):
+        return "-" if v is None else f % v
+
+    def pct(v):
+        return "-" if v is None else "%.1f%%" % (100.0 * v)
+
+    groups = []
+    for kernel in args.kernels:
+        rows = [d for d in disp.values() if d["name"] == kernel]
+        if not rows:
+            raise SystemExit("kernel %s not found in the counter files" % kernel)
+        groups.append((kernel, None, rows))
+        if args.by_grid:
+            # one row per launch shape (each layer of the step has its own grid)
+            for g in sorted({r["grid"] for r in rows}, reverse=True):
+                groups.append((kernel, g, [r for r in rows if r["grid"] == g]))
+    for kernel, grid, rows in groups:
+        ns = statistics.mean(r["ns"] for r in rows)
+        # GRBM_GUI_ACTIVE is summed over the XCDs: cycles of one = sum / N_XCD.
+        # It also covers the dispatch's start-up and drain, so busy fractions
+        # of launches shorter than a few tens of microseconds read low.
+        per_pass = {}
+        for r in rows:
+            if "GRBM_GUI_ACTIVE" in r:
+                for k, v in r.items():
+                    if isinstance(v, float) and k != "GRBM_GUI_ACTIVE":
+                        per_pass.setdefault(k, []).append((v, r["GRBM_GUI_ACTIVE"] / N_XCD))
+
+        def frac(key, units):
+            # counter / (cycles of the same dispatches x units)
+            pairs = per_pass.get(key)
+            if not pairs:
+                return None
+            return sum(v for v, _ in pairs) / (sum(c for _, c in pairs) * units)
+
+        mops = [(r.get("SQ_INSTS_VALU_MFMA_MOPS_BF16", 0.0) + r.get("SQ_INSTS_VALU_MFMA_MOPS_F32", 0.0), r["ns"])
+                for r in rows if "SQ_INSTS_VALU_MFMA_MOPS_BF16" in r or "SQ_INSTS_VALU_MFMA_MOPS_F32" in r]
+        # one MOP is 512 floating-point operations of a matrix instruction
+        tflops = sum(m * 512.0 for m, _ in mops) / sum(t for _, t in mops) / 1e3 if mops else None
+        lat = mean(rows, "TCP_TCC_READ_REQ_LATENCY_sum")
+        req = mean(rows, "TCP_TCC_READ_REQ_sum")
+        hit, miss = mean(rows, "TCC_HIT_sum"), mean(rows, "TCC_MISS_sum")
+        fetch, write = mean(rows, "FETCH_SIZE"), mean(rows, "WRITE_SIZE")
+        r0 = rows[0]
+        cells = [
+            ("`%s`" % kernel) if grid is None else ("&nbsp;&nbsp;grid %d threads" % grid),
+            str(sum(1 for (i, _) in disp if i == 0 and disp[(i, _)]["name"] == kernel
+                    and (grid is None or disp[(i, _)]["grid"] == grid))),
+            "%.1f" % (ns / 1e3),
+            pct(frac("SQ_VALU_MFMA_BUSY_CYCLES", N_CU * SIMD_PER_CU)), fmt(tflops, "%.0f"),
+            pct(None if not mean(rows, "SQ_ACTIVE_INST_LDS") else
+                mean(rows, "SQ_LDS_BANK_CONFLICT") / mean(rows, "SQ_ACTIVE_INST_LDS")),
+            pct(frac("TCP_PENDING_STALL_CYCLES_sum", N_CU)),
+            fmt(None if not req else lat / req, "%.0f"),
+            pct(None if hit is None or miss is None or hit + miss == 0 else hit / (hit + miss)),
+            fmt(None if fetch is None or f_fetch is None else fetch * 1024.0 / f_fetch / 1e6, "%.1f"),
+            fmt(None if write is None or f_write is None else write * 1024.0 / f_write / 1e6, "%.1f"),
+            "%g" % _occupancy(r0["wg"], r0["lds"], r0["vgpr"], r0["agpr"]),
+        ]
+        print("| " + " | ".join(cells) + " |")
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     sub = ap.add_subparsers(dest="cmd", required=True)
@@ -145,8 +313,18 @@ def main(argv=None):
     for a in ("--kernel", "--fetch", "--write", "--copy-fetch", "--copy-write", "--source", "--out"):
         t.add_argument(a, required=True)
     t.add_argument("--copy-mib", type=int, default=1024)
+    k = sub.add_parser("counters")
+    k.add_argument("csv", nargs="+")
+    k.add_argument("--kernels", nargs="+", required=True)
+    k.add_argument("--copy-fetch")
+    k.add_argument("--copy-write")
+    k.add_argument("--copy-mib", type=int, default=1024)
+    k.add_argument("--by-grid", action="store_true", help="also one row per launch shape of each kernel")
+    g = sub.add_parser("libgemm")
+    g.add_argument("--reps", type=int, default=20)
     args = ap.parse_args(argv)
-    {"copy": cmd_copy, "stats": cmd_stats, "traffic": cmd_traffic}[args.cmd](args)
+    {"copy": cmd_copy, "stats": cmd_stats, "traffic": cmd_traffic, "counters": cmd_counters,
+     "libgemm": cmd_libgemm}[args.cmd](args)
 
 
 if __name__ == "__main__":
