@@ -26,8 +26,10 @@ Subcommands (run from the repository root):
       Times the vendor library's bf16 GEMM (torch.matmul, hipBLASLt) on the
       explicit-GEMM shapes of the AlexNet-shaped layers at batch 256 (the
       convolutions as im2col GEMMs: rows = output pixels, columns = filters,
-      reduction = taps) and a large square GEMM: a reference for what a plain
-      library GEMM of the same shape reaches on the device.  Not part of the
+      reduction = taps) and a large square GEMM, beside this library's own
+      call for the same product (implicit GEMM: the im2col is never built),
+      both on normal random bf16 data: a reference for what a plain library
+      GEMM of the same shape reaches on the device.  Not part of the
       library's path (which calls no vendor GEMM).
 
 Kernel names are normalized to the library's trace names: the namespace and
@@ -117,42 +119,75 @@ def cmd_stats(args):
             float(r["MinNs"]) / 1e3, float(r["MaxNs"]) / 1e3, 100.0 * float(r["TotalDurationNs"]) / total))
 
 
-LIBGEMM_SHAPES = [  # (name, M, N, K)
-    ("square 8192", 8192, 8192, 8192),
-    ("conv1 forward", 256 * 55 * 55, 96, 11 * 11 * 3),
-    ("conv2 forward", 256 * 27 * 27, 256, 5 * 5 * 96),
-    ("conv3 forward", 256 * 13 * 13, 384, 3 * 3 * 256),
-    ("conv4 forward", 256 * 13 * 13, 384, 3 * 3 * 384),
-    ("conv5 forward", 256 * 13 * 13, 256, 3 * 3 * 384),
-    ("conv2 filter gradient", 256, 5 * 5 * 96, 256 * 27 * 27),
-    ("conv4 filter gradient", 384, 3 * 3 * 384, 256 * 13 * 13),
-    ("fc6 forward", 256, 4096, 9216),
-    ("fc7 forward", 256, 4096, 4096),
-    ("fc8 forward", 256, 1000, 4096),
+# (name, M, N, K, the same product as this library's call or None):
+# forward x (N,H,W,C), w (K,R,S,C), pad; filter gradient x, dy, w shape, pad
+LIBGEMM_SHAPES = [
+    ("square 8192", 8192, 8192, 8192, None),
+    ("conv1 forward", 256 * 55 * 55, 96, 11 * 11 * 3, None),
+    ("conv2 forward", 256 * 27 * 27, 256, 5 * 5 * 96, ("fwd", (256, 27, 27, 96), (256, 5, 5, 96), 2)),
+    ("conv3 forward", 256 * 13 * 13, 384, 3 * 3 * 256, ("fwd", (256, 13, 13, 256), (384, 3, 3, 256), 1)),
+    ("conv4 forward", 256 * 13 * 13, 384, 3 * 3 * 384, ("fwd", (256, 13, 13, 384), (384, 3, 3, 384), 1)),
+    ("conv5 forward", 256 * 13 * 13, 256, 3 * 3 * 384, ("fwd", (256, 13, 13, 384), (256, 3, 3, 384), 1)),
+    ("conv2 filter gradient", 256, 5 * 5 * 96, 256 * 27 * 27, ("wgrad", (256, 27, 27, 96), (256, 5, 5, 96), 2)),
+    ("conv4 filter gradient", 384, 3 * 3 * 384, 256 * 13 * 13, ("wgrad", (256, 13, 13, 384), (384, 3, 3, 384), 1)),
+    ("fc6 forward", 256, 4096, 9216, ("fwd", (256, 6, 6, 256), (4096, 6, 6, 256), 0)),
+    ("fc7 forward", 256, 4096, 4096, ("fwd", (256, 1, 1, 4096), (4096, 1, 1, 4096), 0)),
+    ("fc8 forward", 256, 1000, 4096, ("fwd", (256, 1, 1, 4096), (1000, 1, 1, 4096), 0)),
 ]
+
+
+def _time_ms(fn, reps):
+    import torch
+    for _ in range(3):
+        fn()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    ev0.record()
+    for _ in range(reps):
+        fn()
+    ev1.record()
+    torch.cuda.synchronize()
+    return ev0.elapsed_time(ev1) / reps
 
 
 def cmd_libgemm(args):
     import torch
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    if root not in sys.path:
+        sys.path.insert(0, root)
+    from paper_1603_07846_amd import singa
     torch.manual_seed(0)
-    print("| GEMM | M | N | K | ms | TFLOP/s | of 2516.6 |")
-    print("|---|---:|---:|---:|---:|---:|---:|")
-    for name, m, n, k in LIBGEMM_SHAPES:
-        a = torch.randn(m, k, device="cuda", dtype=torch.bfloat16)
-        b = torch.randn(k, n, device="cuda", dtype=torch.bfloat16)
-        for _ in range(3):
-            c = a @ b
-        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        torch.cuda.synchronize()
-        ev0.record()
-        for _ in range(args.reps):
-            c = a @ b
-        ev1.record()
-        torch.cuda.synchronize()
-        ms = ev0.elapsed_time(ev1) / args.reps
-        tf = 2.0 * m * n * k / ms / 1e9
-        print("| %s | %d | %d | %d | %.4f | %.0f | %.1f%% |" % (name, m, n, k, ms, tf, 100.0 * tf / 2516.6), flush=True)
-        del a, b, c
+    dev = torch.device("cuda:0")
+    print("| GEMM | M | N | K | library ms | library TFLOP/s | this library ms | this library TFLOP/s |")
+    print("|---|---:|---:|---:|---:|---:|---:|---:|")
+    for name, m, n, k, ours in LIBGEMM_SHAPES:
+        flop = 2.0 * m * n * k
+        a = torch.randn(m, k, device=dev, dtype=torch.bfloat16)
+        b = torch.randn(k, n, device=dev, dtype=torch.bfloat16)
+        ms = _time_ms(lambda: a @ b, args.reps)
+        del a, b
+        cells = ["-", "-"]
+        if ours is not None:
+            op, xs, ws, pad = ours
+            x = torch.randn(xs, device=dev, dtype=torch.bfloat16)
+            w = torch.randn(ws, device=dev, dtype=torch.bfloat16)
+            ys = singa.conv_out_shape(xs, ws, pad, 1)
+            if op == "fwd":
+                y = singa.empty(ys, torch.bfloat16, dev)
+                ws_buf = singa.empty((max(1, singa.conv_workspace_bytes(singa.OP_FWD, singa.BF16, xs, ws, pad, 1)),),
+                                     torch.uint8, dev)
+                fn = lambda: singa.conv_fwd(x, w, None, pad=pad, out=y, workspace=ws_buf)
+            else:
+                dy = torch.randn(ys, device=dev, dtype=torch.bfloat16)
+                dw = singa.empty(ws, torch.float32, dev)
+                db = singa.empty((ws[0],), torch.float32, dev)
+                ws_buf = singa.empty((max(1, singa.conv_workspace_bytes(singa.OP_BWD_FILTER, singa.BF16, xs, ws, pad,
+                                                                         1)),), torch.uint8, dev)
+                fn = lambda: singa.conv_bwd_filter(x, dy, ws, pad=pad, dw=dw, db=db, workspace=ws_buf)
+            oms = _time_ms(fn, args.reps)
+            cells = ["%.4f" % oms, "%.0f" % (flop / oms / 1e9)]
+        print("| %s | %d | %d | %d | %.4f | %.0f | %s | %s |" % (name, m, n, k, ms, flop / ms / 1e9, cells[0], cells[1]),
+              flush=True)
 
 
 def _copy_factor(path, counter, nbytes):
