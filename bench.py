@@ -90,7 +90,7 @@ def parse():
     ap.add_argument("--single-stream", action="store_true",
                     help="run every pass on one stream (no concurrent filter gradients), as the per-kernel pass does")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-images", type=int, default=8, help="images in the oracle's timed sample")
+    ap.add_argument("--cpu-images", type=int, default=40, help="images in the oracle's timed sample (about 10 s on 16 cores)")
     ap.add_argument("--steps-only", action="store_true",
                     help="only the timed and traced steps (no clock reading, Updater / LRN lines, other workloads or "
                          "CPU baseline): the short run the counter passes profile")

@@ -531,13 +531,8 @@ __global__ __launch_bounds__(256) void softmax_ce_mean_kernel(int B, float* __re
   if (threadIdx.x == 0) loss[0] = red[0] / (float)B;
 }
 
-// Fused SGD with momentum over a flat parameter buffer (the Updater).  Each
-// thread owns 8 consecutive parameters: all loads (two 16-byte vectors of w,
-// g and v) are issued before any arithmetic, then w, v and the bf16 shadow
-// are written; one thread per 8 parameters, no grid-stride cap (measured
-// best of the variants tried, ~5.5 TB/s; streaming loads / stores were
-// slower).  n % 8 tail elements are handled one by one by the first threads.
-// The Updaters stream w, g and the state (momentum v, or AdaGrad's h) once:
+// Fused SGD with momentum, and AdaGrad, over a flat parameter buffer (the
+// Updater), with the bf16 shadow written in the same pass.  The Updaters stream w, g and the state (momentum v, or AdaGrad's h) once:
 // a thread owns UPD_U float4 vectors of each array, UPD_U x 256 apart so that
 // each load instruction of a workgroup covers 4 KB of contiguous memory, and
 // issues all its loads before any arithmetic.  Loads and stores are
