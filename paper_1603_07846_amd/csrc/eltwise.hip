@@ -171,12 +171,15 @@ __global__ __launch_bounds__(256) void pool_bwd_kernel(PoolGeom g, int mode, con
 // scalar kernel, applied per channel; the VEC argmax bytes are stored together.
 // KS > 0: a KS x KS window known at compile time, whose KS^2 loads are all
 // issued before the scan (cells outside the input load a clamped, in-bounds
-// pixel and are skipped by the scan, which keeps the generic order).
-template <typename T, int VEC, int KS>
+// pixel and are skipped by the scan, which keeps the generic order); a max
+// window wholly inside the input (every window of an unpadded floor-size
+// pooling) takes cell 0 as its first maximum and compares the rest with no
+// bounds or first-cell tests.  MODE: 0 max, 1 average.  A max output is one
+// of the inputs, so bf16 results are repacked exactly from the high halves.
+template <typename T, int VEC, int KS, int MODE>
 __global__ __launch_bounds__(256) void pool_fwd_nhwc_vec_kernel(PoolGeom g, FastDiv dCV, FastDiv dQ, FastDiv dP,
-                                                                int mode, const T* __restrict__ x,
-                                                                T* __restrict__ y, uint8_t* __restrict__ argmax,
-                                                                int total) {
+                                                                const T* __restrict__ x, T* __restrict__ y,
+                                                                uint8_t* __restrict__ argmax, int total) {
   const int CV = g.C / VEC;
   for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < total; i += gridDim.x * blockDim.x) {
     const int t1 = (int)fdiv((uint32_t)i, dCV);
@@ -187,26 +190,25 @@ __global__ __launch_bounds__(256) void pool_fwd_nhwc_vec_kernel(PoolGeom g, Fast
     const int p = t2 - n * g.P;
     const int h0 = p * g.sh - g.ph, w0 = q * g.sw - g.pw;
     float best[VEC];
-    uint8_t cell[VEC];
+    int cell[VEC];
 #pragma unroll
     for (int j = 0; j < VEC; ++j) {
       best[j] = 0.f;
       cell[j] = 0;
     }
     bool found = false;
-    auto scan = [&](const uint4& u, int r, int s) {
-      union { uint4 u; T e[VEC]; } v;
-      v.u = u;
+    auto scan = [&](const uint4& u, int c) {
+      float f[VEC];
+      unpack16<T>(u, f);
 #pragma unroll
       for (int j = 0; j < VEC; ++j) {
-        const float f = ld_f<T>(&v.e[j]);
-        if (mode == 0) {
-          if (!found || f > best[j]) {
-            best[j] = f;
-            cell[j] = (uint8_t)(r * g.kw + s);
+        if constexpr (MODE == 0) {
+          if (!found || f[j] > best[j]) {
+            best[j] = f[j];
+            cell[j] = c;
           }
         } else {
-          best[j] += f;
+          best[j] += f[j];
         }
       }
       found = true;
@@ -220,11 +222,27 @@ __global__ __launch_bounds__(256) void pool_fwd_nhwc_vec_kernel(PoolGeom g, Fast
           const int h = min(max(h0 + r, 0), g.H - 1), w = min(max(w0 + s, 0), g.W - 1);
           v[r * KS + s] = *(const uint4*)(x + ((n * g.H + h) * g.W + w) * g.C + cv * VEC);
         }
+      const bool inside = h0 >= 0 && w0 >= 0 && h0 + KS <= g.H && w0 + KS <= g.W;
+      if (MODE == 0 && inside) {
+        unpack16<T>(v[0], best);
 #pragma unroll
-      for (int r = 0; r < KS; ++r)
+        for (int c = 1; c < KS * KS; ++c) {
+          float f[VEC];
+          unpack16<T>(v[c], f);
 #pragma unroll
-        for (int s = 0; s < KS; ++s)
-          if ((unsigned)(h0 + r) < (unsigned)g.H && (unsigned)(w0 + s) < (unsigned)g.W) scan(v[r * KS + s], r, s);
+          for (int j = 0; j < VEC; ++j)
+            if (f[j] > best[j]) {
+              best[j] = f[j];
+              cell[j] = c;
+            }
+        }
+      } else {
+#pragma unroll
+        for (int r = 0; r < KS; ++r)
+#pragma unroll
+          for (int s = 0; s < KS; ++s)
+            if ((unsigned)(h0 + r) < (unsigned)g.H && (unsigned)(w0 + s) < (unsigned)g.W) scan(v[r * KS + s], r * KS + s);
+      }
     } else {
       for (int r = 0; r < g.kh; ++r) {
         const int h = h0 + r;
@@ -232,23 +250,35 @@ __global__ __launch_bounds__(256) void pool_fwd_nhwc_vec_kernel(PoolGeom g, Fast
         for (int s = 0; s < g.kw; ++s) {
           const int w = w0 + s;
           if ((unsigned)w >= (unsigned)g.W) continue;
-          scan(*(const uint4*)(x + ((n * g.H + h) * g.W + w) * g.C + cv * VEC), r, s);
+          scan(*(const uint4*)(x + ((n * g.H + h) * g.W + w) * g.C + cv * VEC), r * g.kw + s);
         }
       }
     }
-    union { uint4 u; T e[VEC]; } o;
-    const float inv = mode == 0 ? 1.f : 1.f / (float)pool_divisor(g, p, q);
-#pragma unroll
-    for (int j = 0; j < VEC; ++j) st_f<T>(&o.e[j], mode == 0 ? best[j] : best[j] * inv);
-    *(uint4*)(y + (size_t)i * VEC) = o.u;
-    if (mode == 0) {
+    uint4 o;
+    if constexpr (MODE == 0) {
       if constexpr (VEC == 8) {
-        uint2 a;
-        a.x = cell[0] | (cell[1] << 8) | (cell[2] << 16) | ((uint32_t)cell[3] << 24);
-        a.y = cell[4] | (cell[5] << 8) | (cell[6] << 16) | ((uint32_t)cell[7] << 24);
-        *(uint2*)(argmax + (size_t)i * VEC) = a;
+        uint32_t d[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+          d[k] = (__float_as_uint(best[2 * k]) >> 16) | (__float_as_uint(best[2 * k + 1]) & 0xffff0000u);
+        o = make_uint4(d[0], d[1], d[2], d[3]);
       } else {
-        *(uint32_t*)(argmax + (size_t)i * VEC) = cell[0] | (cell[1] << 8) | (cell[2] << 16) | ((uint32_t)cell[3] << 24);
+        o = pack16<T>(best);
+      }
+    } else {
+      const float inv = 1.f / (float)pool_divisor(g, p, q);
+#pragma unroll
+      for (int j = 0; j < VEC; ++j) best[j] *= inv;
+      o = pack16<T>(best);
+    }
+    *(uint4*)(y + (size_t)i * VEC) = o;
+    if constexpr (MODE == 0) {
+      const uint32_t a0 = (uint32_t)cell[0] | (cell[1] << 8) | (cell[2] << 16) | ((uint32_t)cell[3] << 24);
+      if constexpr (VEC == 8) {
+        const uint32_t a1 = (uint32_t)cell[4] | (cell[5] << 8) | (cell[6] << 16) | ((uint32_t)cell[7] << 24);
+        *(uint2*)(argmax + (size_t)i * VEC) = make_uint2(a0, a1);
+      } else {
+        *(uint32_t*)(argmax + (size_t)i * VEC) = a0;
       }
     }
   }
@@ -341,10 +371,12 @@ __global__ __launch_bounds__(256) void pool_bwd_k3s2_kernel(PoolGeom g, FastDiv 
     const int n = (int)fdiv((uint32_t)t2, dHB);
     const int hb = t2 - n * HB;
     // the four windows' vectors, all loaded before any is used; a window
-    // outside the output gets arg-max cells 0xff, which match no input
-    union U { uint4 u; T e[VEC]; };
-    U v[2][2], ym[2][2];
-    uint8_t am[2][2][VEC];
+    // outside the output gets arg-max cells 0xff, which match no input.  The
+    // folded ReLU mask zeroes a window's gradient once per window (a value
+    // that goes nowhere cannot change a sum), then each input pixel sums the
+    // windows whose arg-max names it.
+    float d[2][2][VEC];
+    uint32_t am[2][2][VEC / 4];
 #pragma unroll
     for (int pi = 0; pi < 2; ++pi)
 #pragma unroll
@@ -352,19 +384,27 @@ __global__ __launch_bounds__(256) void pool_bwd_k3s2_kernel(PoolGeom g, FastDiv 
         const int p = hb - 1 + pi, q = wb - 1 + qi;
         const bool ok = p >= 0 && p < g.P && q >= 0 && q < g.Q;
         const int o = ok ? ((n * g.P + p) * g.Q + q) * g.C + cv * VEC : 0;
-        v[pi][qi].u = ok ? *(const uint4*)(dy + o) : make_uint4(0u, 0u, 0u, 0u);
-        if constexpr (MASK) ym[pi][qi].u = ok ? *(const uint4*)(ymask + o) : make_uint4(0u, 0u, 0u, 0u);
+        uint4 vu = make_uint4(0u, 0u, 0u, 0u), mu = make_uint4(0u, 0u, 0u, 0u);
+        if (ok) vu = *(const uint4*)(dy + o);
+        if constexpr (MASK) {
+          if (ok) mu = *(const uint4*)(ymask + o);
+        }
         if constexpr (VEC == 8) {
-          const uint2 a = ok ? *(const uint2*)(argmax + o) : make_uint2(~0u, ~0u);
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            am[pi][qi][j] = (uint8_t)(a.x >> (8 * j));
-            am[pi][qi][4 + j] = (uint8_t)(a.y >> (8 * j));
-          }
+          uint2 a2 = make_uint2(~0u, ~0u);
+          if (ok) a2 = *(const uint2*)(argmax + o);
+          am[pi][qi][0] = a2.x;
+          am[pi][qi][VEC / 4 - 1] = a2.y;
         } else {
-          const uint32_t a = ok ? *(const uint32_t*)(argmax + o) : ~0u;
+          uint32_t a1 = ~0u;
+          if (ok) a1 = *(const uint32_t*)(argmax + o);
+          am[pi][qi][0] = a1;
+        }
+        unpack16<T>(vu, d[pi][qi]);
+        if constexpr (MASK) {
+          float m[VEC];
+          unpack16<T>(mu, m);
 #pragma unroll
-          for (int j = 0; j < 4; ++j) am[pi][qi][j] = (uint8_t)(a >> (8 * j));
+          for (int j = 0; j < VEC; ++j) d[pi][qi][j] = m[j] > 0.f ? d[pi][qi][j] : 0.f;
         }
       }
     float acc[2][2][VEC];
@@ -386,12 +426,11 @@ __global__ __launch_bounds__(256) void pool_bwd_k3s2_kernel(PoolGeom g, FastDiv 
 #pragma unroll
           for (int dw = 0; dw < 2; ++dw) {
             if (qi == 0 && dw == 1) continue;
-            const int cell = (2 * (1 - pi) + dh) * 3 + (2 * (1 - qi) + dw);
+            const uint32_t cell = (2 * (1 - pi) + dh) * 3 + (2 * (1 - qi) + dw);
 #pragma unroll
             for (int j = 0; j < VEC; ++j) {
-              bool take = am[pi][qi][j] == cell;
-              if constexpr (MASK) take = take && ld_f<T>(&ym[pi][qi].e[j]) > 0.f;
-              if (take) acc[dh][dw][j] += ld_f<T>(&v[pi][qi].e[j]);
+              const uint32_t aj = (am[pi][qi][j / 4] >> (8 * (j % 4))) & 0xffu;
+              acc[dh][dw][j] += aj == cell ? d[pi][qi][j] : 0.f;
             }
           }
         }
@@ -405,10 +444,7 @@ __global__ __launch_bounds__(256) void pool_bwd_k3s2_kernel(PoolGeom g, FastDiv 
       for (int dw = 0; dw < 2; ++dw) {
         const int w = 2 * wb + dw;
         if (w >= g.W) continue;
-        union { uint4 u; T e[VEC]; } out;
-#pragma unroll
-        for (int j = 0; j < VEC; ++j) st_f<T>(&out.e[j], acc[dh][dw][j]);
-        *(uint4*)(dx + (size_t)((n * g.H + h) * g.W + w) * g.C + cv * VEC) = out.u;
+        *(uint4*)(dx + (size_t)((n * g.H + h) * g.W + w) * g.C + cv * VEC) = pack16<T>(acc[dh][dw]);
       }
     }
   }
@@ -859,14 +895,17 @@ hipError_t launch_pool_fwd(int dt, int mode, int N, int C, int H, int W, int P, 
     const FastDiv dCV = make_fastdiv((uint32_t)(C / vec)), dQ = make_fastdiv((uint32_t)Q),
                   dP = make_fastdiv((uint32_t)P);
     const bool k3 = kh == 3 && kw == 3;
-#define POOL_FWD_VEC(T, V, KS)                                                                                  \
-  hipLaunchKernelGGL((pool_fwd_nhwc_vec_kernel<T, V, KS>), dim3(grid), dim3(256), 0, st, g, dCV, dQ, dP, mode, \
+#define POOL_FWD_VEC(T, V, KS, M)                                                                        \
+  hipLaunchKernelGGL((pool_fwd_nhwc_vec_kernel<T, V, KS, M>), dim3(grid), dim3(256), 0, st, g, dCV, dQ, dP, \
                      (const T*)x, (T*)y, argmax, tv)
+#define POOL_FWD_VEC_M(T, V, KS) \
+  if (mode == 0) POOL_FWD_VEC(T, V, KS, 0); else POOL_FWD_VEC(T, V, KS, 1)
     if (dt == BF16) {
-      if (k3) POOL_FWD_VEC(bf16_t, 8, 3); else POOL_FWD_VEC(bf16_t, 8, 0);
+      if (k3) { POOL_FWD_VEC_M(bf16_t, 8, 3); } else { POOL_FWD_VEC_M(bf16_t, 8, 0); }
     } else {
-      if (k3) POOL_FWD_VEC(float, 4, 3); else POOL_FWD_VEC(float, 4, 0);
+      if (k3) { POOL_FWD_VEC_M(float, 4, 3); } else { POOL_FWD_VEC_M(float, 4, 0); }
     }
+#undef POOL_FWD_VEC_M
 #undef POOL_FWD_VEC
     return hipGetLastError();
   }
