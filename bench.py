@@ -211,6 +211,10 @@ CONFIG_NAMES = {1: "single_conv_layer_fwd_bwd_sgd_f32_b16", 2: "cifar_convnet_tr
                 3: "alexnet_conv_stack_fwd_bwd_f32_b128", 4: "alexnet_conv_stack_fwd_bwd_bf16_b256"}
 
 
+# images of each smaller workload in its oracle sample
+CONFIG_CPU_IMAGES = {1: 16, 2: 100, 3: 4, 4: 4}
+
+
 def measure_config(index, steps, warmup):
     """One of the other workloads, timed on its own: `steps` eager steps
     between two device synchronizations after `warmup` untimed ones (the
@@ -334,7 +338,7 @@ def measure_lrn(net, dev, is_bf16):
     return lrn
 
 
-def cpu_baseline(w, n_images):
+def cpu_baseline(w, n_images, need_input_grad=False):
     """The oracle (fp64 C, OpenMP) on a bounded sample of the same step: the
     full forward/backward of `n_images` images of the workload plus the
     update of all parameters."""
@@ -349,7 +353,7 @@ def cpu_baseline(w, n_images):
     oracle.conv_out(1, 1, 0, 1)  # load the library outside the timed region
     t0 = time.perf_counter()
     onet.train_one_batch(w.layers, inp.x, params, master=master, labels=inp.labels, dy_top=inp.dy, lr=w.lr,
-                         momentum=w.momentum, wd=w.weight_decay,
+                         momentum=w.momentum, wd=w.weight_decay, need_input_grad=need_input_grad,
                          store=oracle.round_bf16 if w.dtype == "bf16" else None)
     dt = time.perf_counter() - t0
     threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
@@ -528,6 +532,12 @@ def main():
         del net, x, labels, dy
         torch.cuda.empty_cache()
         out["configs"] = {str(i): measure_config(i, args.steps, args.warmup) for i in (1, 2, 3, 4)}
+        if not args.no_cpu_baseline:
+            # the oracle on a bounded sample of each of them (a few seconds in all)
+            for i, n_img in CONFIG_CPU_IMAGES.items():
+                c = out["configs"][str(i)]
+                c["cpu_baseline"] = cpu_baseline(wl.WORKLOADS[i], n_img, need_input_grad=i == 1)
+                c["speedup_vs_oracle"] = round(c["images_per_s"] / c["cpu_baseline"]["value"], 1)
     if not args.no_cpu_baseline and not args.steps_only:
         out["cpu_baseline"] = cpu_baseline(w, args.cpu_images)
     print(json.dumps(out), flush=True)

@@ -6,8 +6,9 @@ Subcommands (run from the repository root):
       A plain device-to-device copy of N MiB, five times: the known-size
       kernel whose FETCH_SIZE / WRITE_SIZE counters calibrate the HBM byte
       counts of the library's kernels.
-  stats KERNEL_STATS_CSV --title T --command C
-      Markdown table of a `rocprofv3 --kernel-trace --stats` summary.
+  stats KERNEL_STATS_CSV --title T --command C [--trace KERNEL_TRACE_CSV]
+      Markdown table of a `rocprofv3 --kernel-trace --stats` summary (with the
+      per-kernel median launch time when the same run's trace is given).
   traffic --kernel NAME --fetch CSV --write CSV --copy-fetch CSV --copy-write CSV
           --copy-mib N --source FILE --out JSON
       Average HBM bytes per launch of one kernel (FETCH_SIZE and WRITE_SIZE
@@ -106,17 +107,28 @@ def cmd_copy(args):
 def cmd_stats(args):
     rows = list(csv.DictReader(open(args.csv)))
     total = sum(float(r["TotalDurationNs"]) for r in rows)
+    med = {}
+    if args.trace:
+        # per-launch durations from the same run's kernel trace -> medians
+        durs = collections.defaultdict(list)
+        with open(args.trace) as f:
+            for r in csv.DictReader(f):
+                durs[normalize(r["Kernel_Name"])].append(int(r["End_Timestamp"]) - int(r["Start_Timestamp"]))
+        med = {k: statistics.median(v) for k, v in durs.items()}
     print("# %s\n" % args.title)
     print("Command (from the repository root on one MI355X, with `TMPDIR=/tmp`):\n")
     print("```\n%s\n```\n" % args.command)
     print("Kernel statistics (`*_kernel_stats.csv`) over every launch of the run; names as in the library's "
           "trace (template arguments: dtype, load modes, flags).\n")
-    print("| Kernel | Calls | Total ms | Average us | Min us | Max us | Share |")
-    print("|---|---:|---:|---:|---:|---:|---:|")
+    print("| Kernel | Calls | Total ms | Average us | Median us | Min us | Max us | Share |")
+    print("|---|---:|---:|---:|---:|---:|---:|---:|")
     for r in sorted(rows, key=lambda r: -float(r["TotalDurationNs"])):
-        print("| `%s` | %s | %.3f | %.1f | %.1f | %.1f | %.1f%% |" % (
-            normalize(r["Name"]), r["Calls"], float(r["TotalDurationNs"]) / 1e6, float(r["AverageNs"]) / 1e3,
-            float(r["MinNs"]) / 1e3, float(r["MaxNs"]) / 1e3, 100.0 * float(r["TotalDurationNs"]) / total))
+        name = normalize(r["Name"])
+        m = med.get(name)
+        print("| `%s` | %s | %.3f | %.1f | %s | %.1f | %.1f | %.1f%% |" % (
+            name, r["Calls"], float(r["TotalDurationNs"]) / 1e6, float(r["AverageNs"]) / 1e3,
+            "-" if m is None else "%.1f" % (m / 1e3), float(r["MinNs"]) / 1e3, float(r["MaxNs"]) / 1e3,
+            100.0 * float(r["TotalDurationNs"]) / total))
 
 
 # (name, M, N, K, the same product as this library's call or None):
@@ -344,6 +356,7 @@ def main(argv=None):
     s.add_argument("csv")
     s.add_argument("--title", required=True)
     s.add_argument("--command", required=True)
+    s.add_argument("--trace", help="the run's kernel_trace.csv, for per-kernel medians")
     t = sub.add_parser("traffic")
     for a in ("--kernel", "--fetch", "--write", "--copy-fetch", "--copy-write", "--source", "--out"):
         t.add_argument(a, required=True)
