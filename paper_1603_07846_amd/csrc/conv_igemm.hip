@@ -294,6 +294,9 @@ struct FwdArgs {
   // kt BK + BK) in (r, s, c) order; needs C % BK == 0.
   int tap_major, RS;
   FastDiv dRS;
+  // input patch (stride 1, tap-major): the padded input is Hp x Wp per image
+  int patch, Hp, Wp;
+  FastDiv dHp, dWp;
 };
 
 // Operand load modes.  VEC16: 16-byte vectors of VEC taps (C % VEC == 0 for
@@ -530,6 +533,10 @@ __global__ __launch_bounds__(NT) void conv_fwd_kernel(FwdArgs a) {
 // RPW rows per 256-byte bank window, so a fragment read (16 lanes, 16
 // consecutive rows, one chunk) touches 16 distinct 16-byte bank groups.
 constexpr int L_BM = 256;
+// input-patch entries (64 bytes: 32 channels of one padded input pixel) per
+// buffer: with 3 filter stages of 8 KB and 2 x 28 KB of patch the 256 x 128
+// layout keeps two workgroups per CU
+constexpr int FWD_PATCH_ENTRIES = 448;
 constexpr int L_STAGES = 3;
 template <int LBK> struct LT {
   static constexpr int RB = LBK * 2;                  // row bytes
@@ -579,7 +586,7 @@ __device__ __forceinline__ void block_barrier() { asm volatile("s_barrier" ::: "
 // tile (512 threads, one workgroup per CU): half the operand bytes per flop
 // of the 256 x 128 tile on the B side, for 256-column layers with enough
 // row tiles.
-template <bool BWD, int LBK, int WMW>
+template <bool BWD, int LBK, int WMW, bool PATCH>
 __global__ __launch_bounds__(WMW == 8 ? 2 * NT : NT, (LBK == 32 && WMW == 4) ? 3 : (LBK == 32 && WMW != 8) ? 2 : 1)
 void conv_fwd_large_kernel(FwdArgs a) {
   typedef LT<LBK> G;
@@ -588,14 +595,21 @@ void conv_fwd_large_kernel(FwdArgs a) {
   constexpr int FM = WMW == 4 ? 2 : 4, FN = WMW == 4 ? 3 : 2;
   constexpr int ABAND = L_BM / NW, BBAND = BNT / NW;  // operand rows each wave loads
   constexpr int AI = ABAND / G::RPI, BI = BBAND / G::RPI;  // its load instructions per K-tile
-  constexpr int ATILE = L_BM * G::RB, STAGE = ATILE + BNT * G::RB;
-  constexpr int LOADS = AI + BI;  // 16-byte loads per thread per K-tile
+  // with the input patch the stages hold only the filter tile
+  constexpr int ATILE = PATCH ? 0 : L_BM * G::RB, STAGE = ATILE + BNT * G::RB;
+  constexpr int LOADS = (PATCH ? 0 : AI) + BI;  // 16-byte loads per thread per K-tile
   static_assert(AI * G::RPI == ABAND && BI * G::RPI == BBAND, "load bands");
   // LDS stages: K-tiles kt+1 .. kt+NS-1 are in flight while kt is multiplied.
   // The 256 x 96 layout keeps two (48 KB, three workgroups per CU): measured
   // 5 % faster on conv2's backward-data than three stages at two per CU.
   constexpr int NS = (WMW == 4 && LBK == 32) ? 2 : L_STAGES;
-  __shared__ __attribute__((aligned(16))) char smem[NS * STAGE];
+  // input patch: two buffers of PENT 64-byte entries (32 channels of one
+  // padded input pixel), PL loads per thread per channel slice
+  static_assert(!PATCH || (LBK == 32 && WMW == 2), "the patch serves 32-tap K-tiles of the 256 x 128 layout");
+  constexpr int PENT = PATCH ? FWD_PATCH_ENTRIES : 0;
+  constexpr int PBUF = PENT * 64, PL = PENT / (NW * 16);
+  static_assert(!PATCH || PL * NW * 16 == PENT, "patch loads");
+  __shared__ __attribute__((aligned(16))) char smem[NS * STAGE + 2 * PBUF];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int L = xcd_remap(blockIdx.x, gridDim.x);
@@ -728,6 +742,116 @@ void conv_fwd_large_kernel(FwdArgs a) {
   const int kbase = split * a.kt_per_split * LBK;
   const int nkt = min(a.kt_per_split, nkt_all - split * a.kt_per_split);
   const int kend = kbase + nkt * LBK;  // K-tiles from here on are issued as all-OOB (zeros, no traffic)
+  if constexpr (PATCH) {
+    // Input patch (stride 1, tap-major K-tiles, one split).  Every tap (r, s)
+    // of a channel slice reads the same input pixels shifted by r rows and s
+    // columns, so the tile's input rows for all taps are loaded once per
+    // slice: padded rows g = n Hp + h + ph from the first output line of the
+    // tile to R - 1 past its last, each Wp padded columns wide (zeros outside
+    // the input), 32 channels per entry, swizzled like the operand rows
+    // (chunk c of entry e in slot c ^ ((e / 4) % 4)).  Output row (n, p, q)
+    // reads tap (r, s) at entry ((n Hp + p - g0) Wp + q) + r Wp + s.  The host
+    // checks that a tile's patch fits PENT entries.  The next slice's patch
+    // loads go out at its predecessor's first tap, into the other buffer.
+    char* const pbuf0 = smem + NS * STAGE;
+    const int R = a.RS / a.S;
+    const int mlast = min(m0 + L_BM, a.M) - 1;
+    auto line = [&](int m, int& n, int& p, int& q) {
+      n = (int)fdiv((uint32_t)m, a.dPQ);
+      const int pq = m - n * a.P * a.Q;
+      p = (int)fdiv((uint32_t)pq, a.dQ);
+      q = pq - p * a.Q;
+    };
+    int nf, pf, qf, nl, pl, ql;
+    line(m0, nf, pf, qf);
+    line(mlast, nl, pl, ql);
+    const int g0 = nf * a.Hp + pf;
+    const int E = (nl * a.Hp + pl + R - g0) * a.Wp;  // entries in use (<= PENT)
+    uint32_t goff[PL];
+#pragma unroll
+    for (int i = 0; i < PL; ++i) {
+      const int e = (i * NW + wave) * 16 + (lane >> 2);
+      const int c = (lane & 3) ^ ((e >> 2) & 3);
+      goff[i] = OOB;
+      if (e < E) {
+        const int gr = (int)fdiv((uint32_t)e, a.dWp);
+        const int col = e - gr * a.Wp;
+        const int g = g0 + gr;
+        const int n = (int)fdiv((uint32_t)g, a.dHp);
+        const int ih = g - n * a.Hp - a.ph, iw = col - a.pw;
+        if ((unsigned)ih < (unsigned)a.H && (unsigned)iw < (unsigned)a.W)
+          goff[i] = (uint32_t)(((n * a.H + ih) * a.W + iw) * a.C + 8 * c) * 2u;
+      }
+    }
+    const int nslices = a.C / LBK;
+    auto issue_patch = [&](int cs, char* buf) {
+#pragma unroll
+      for (int i = 0; i < PL; ++i)
+        ld_lds16(xr, (goff[i] != OOB && cs < nslices) ? goff[i] + (uint32_t)(cs * LBK * 2) : OOB,
+                 buf + (i * NW + wave) * 1024);
+    };
+    int bpos[FM];
+#pragma unroll
+    for (int b = 0; b < FM; ++b) {
+      const int mr = m0 + wm * FM * 32 + b * 32 + (lane & 31);
+      int n, p, q;
+      line(mr <= mlast ? mr : m0, n, p, q);
+      bpos[b] = (n * a.Hp + p - g0) * a.Wp + q;
+    }
+    // B slices of a K-tile: the filter rows only
+    auto issue_b_slice = [&](const Taps& t, char* St, int j) {
+#pragma unroll
+      for (int q = 0; q < BI; ++q)
+        if (q * G::KS / BI == j) issue_b(t, St, q);
+    };
+    issue_patch(0, pbuf0);
+#pragma unroll
+    for (int s = 0; s < NS - 1; ++s)
+#pragma unroll
+      for (int j = 0; j < G::KS; ++j) issue_b_slice(taps(nkt > s ? kbase + s * LBK : a.Kg), smem + s * STAGE, j);
+    int stage = 0;
+    for (int kt = 0; kt < nkt; ++kt) {
+      const int cs = (int)fdiv((uint32_t)kt, a.dRS);
+      const int rs = kt - cs * a.RS;
+      // An iteration issues the next slice's patch (at a slice's first tap)
+      // and then the B loads of tile kt + NS - 1.  B(kt) has landed for this
+      // thread once only the loads issued after it may be in flight: the B
+      // tiles kt + 1 .. kt + NS - 2 and, when iteration kt - 1 was a slice's
+      // first tap, the patch loads it issued (before B(kt + 1), after B(kt)).
+      // The patch of slice cs went out before B(kt), so it has landed too.
+      static_assert(NS == 3, "the wait below counts the loads of three stages");
+      const bool extra = kt >= 1 && (kt - 1) % a.RS == 0;
+      if (extra) wait_vmcnt<(NS - 2) * LOADS + PL>();
+      else wait_vmcnt<(NS - 2) * LOADS>();
+      block_barrier();  // ... and for everyone; everyone is done with tile kt-1 and, at rs == 0, with slice cs-1
+      const int nstage = stage == 0 ? NS - 1 : stage - 1;
+      const int knext = kbase + (kt + NS - 1) * LBK;
+      const Taps t = taps(knext < kend ? knext : a.Kg);
+      if (rs == 0) issue_patch(cs + 1, pbuf0 + ((cs + 1) & 1) * PBUF);
+      const char* S = smem + stage * STAGE;
+      const char* Pb = pbuf0 + (cs & 1) * PBUF;
+      const int r = (int)fdiv((uint32_t)rs, a.dS);
+      const int toff = r * a.Wp + (rs - r * a.S);
+#pragma unroll
+      for (int kc = 0; kc < G::KS; ++kc) {
+        bf16x8 fa[FM], fb[FN];
+#pragma unroll
+        for (int b = 0; b < FM; ++b) {
+          const int pos = bpos[b] + toff;
+          fa[b] = *(const bf16x8*)(Pb + pos * 64 + ((((2 * kc + lh) ^ ((pos >> 2) & 3))) << 4));
+        }
+#pragma unroll
+        for (int b = 0; b < FN; ++b) fb[b] = *(const bf16x8*)(S + boff + b * 32 * G::RB + ((32 * kc) ^ tsw));
+#pragma unroll
+        for (int bm = 0; bm < FM; ++bm)
+#pragma unroll
+          for (int bn = 0; bn < FN; ++bn)
+            acc[bm][bn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[bm], fb[bn], acc[bm][bn], 0, 0, 0);
+        issue_b_slice(t, smem + nstage * STAGE, kc);
+      }
+      stage = stage == NS - 1 ? 0 : stage + 1;
+    }
+  } else {
 #pragma unroll
   for (int s = 0; s < NS - 1; ++s)
 #pragma unroll
@@ -752,6 +876,7 @@ void conv_fwd_large_kernel(FwdArgs a) {
       if (kc + 1 < G::KS) f = g;
     }
     stage = stage == NS - 1 ? 0 : stage + 1;
+  }
   }
   wait_vmcnt<0>();  // the trailing all-OOB loads still write LDS
 
@@ -1517,7 +1642,7 @@ __global__ __launch_bounds__(256) void splitk_epilogue_vec_kernel(const float* _
 }
 
 // Layout and split overrides for A/B measurements (SINGA_CONV_TILE,
-// SINGA_FWD_BK, SINGA_FWD_WIDE, SINGA_WGRAD_ORDER, SINGA_WGRAD_TARGET): read
+// SINGA_FWD_BK, SINGA_FWD_WIDE, SINGA_FWD_PATCH, SINGA_WGRAD_ORDER, SINGA_WGRAD_TARGET): read
 // from the environment only in a library built with -DSINGA_TUNING.  The
 // default build ignores the environment; its dispatch rules are the tested
 // ones.
@@ -1550,8 +1675,10 @@ void launch_fwd_instance(const FwdArgs& a, dim3 grid, double flops, hipStream_t 
   hipLaunchKernelGGL((conv_fwd_kernel<T, AM, BMD, BWD>), grid, dim3(NT), 0, st, a);
 }
 
-// "conv_fwd_large_kernel<bwd,taps per K-tile,wave layout>"
-const char* fwd_large_name(bool bwd, bool deep, bool narrow, bool wide) {
+// "conv_fwd_large_kernel<bwd,taps per K-tile,wave layout>" (",1" appended:
+// the input-patch variant)
+const char* fwd_large_name(bool bwd, bool deep, bool narrow, bool wide, bool patch) {
+  if (patch) return bwd ? "conv_fwd_large_kernel<1,32,2,1>" : "conv_fwd_large_kernel<0,32,2,1>";
   static const char* names[2][2][2] = {
       {{"conv_fwd_large_kernel<0,32,2>", "conv_fwd_large_kernel<0,32,4>"},
        {"conv_fwd_large_kernel<0,64,2>", "conv_fwd_large_kernel<0,64,4>"}},
@@ -1585,6 +1712,28 @@ int fwd_large_bk(long Kg) {
   }();
   if (forced == 32 || forced == 64) return forced;
   return Kg >= 4096 ? 64 : 32;
+}
+
+// The input-patch variant of the 256 x 128 kernel: stride 1, 32-channel
+// slices (tap-major K-tiles), at least 4 taps to share a slice's loads, and
+// every tile's patch within the buffer.  (On the 256 x 256 layout, one
+// workgroup per CU, it measured 5-16 % slower and is not built.)
+// SINGA_FWD_PATCH=0 turns it off in a tuning build.
+bool use_patch_fwd(const ConvShape& s, long M, bool wide, bool narrow, bool deep) {
+  static const int forced = [] {
+    const char* e = tuning_env("SINGA_FWD_PATCH");
+    return e ? atoi(e) : -1;
+  }();
+  if (wide || narrow || deep || s.sh != 1 || s.sw != 1 || s.C % 32 != 0 || s.R * s.S < 4 || forced == 0)
+    return false;
+  const long Hp = s.H + 2L * s.ph, Wp = s.W + 2L * s.pw, PQ = (long)s.P * s.Q;
+  const long cap = FWD_PATCH_ENTRIES;
+  for (long m0 = 0; m0 < M; m0 += L_BM) {
+    const long m1 = std::min(m0 + L_BM, M) - 1;
+    const long n0 = m0 / PQ, p0 = (m0 % PQ) / s.Q, n1 = m1 / PQ, p1 = (m1 % PQ) / s.Q;
+    if ((n1 * Hp + p1 + s.R - (n0 * Hp + p0)) * Wp > cap) return false;
+  }
+  return true;
 }
 
 bool use_large_fwd(long M, long Nn, long Kg) {
@@ -1662,6 +1811,8 @@ hipError_t conv_fwd_dispatch(const ConvShape& s, const void* x, const void* w, c
   FwdArgs a;
   a.x = x; a.w = w; a.bias = bias; a.y = y; a.mask = mask;
   a.tap_major = 0;
+  a.patch = 0; a.Hp = a.Wp = 1;
+  a.dHp = a.dWp = make_fastdiv(1u);
   a.RS = s.R * s.S;
   a.dRS = make_fastdiv((uint32_t)a.RS);
   a.x_bytes = (uint32_t)((size_t)s.N * s.H * s.W * s.C * sizeof(T));
@@ -1700,10 +1851,20 @@ hipError_t conv_fwd_dispatch(const ConvShape& s, const void* x, const void* w, c
     const bool deep = !wide && fwd_large_bk(narrow ? 0 : a.Kg) == 64;
     a.kt_per_split = (a.Kg + (deep ? 64 : 32) - 1) / (deep ? 64 : 32);  // one split: every K-tile of this depth
     a.tap_major = a.RS > 1 && s.C % (deep ? 64 : 32) == 0;
-    TraceScope ts(fwd_large_name(bwd, deep, narrow, wide), st, flops, WORK_FLOP);
+    const bool patch = use_patch_fwd(s, a.M, wide, narrow, deep);
+    a.patch = patch;
+    a.Hp = s.H + 2 * s.ph;
+    a.Wp = s.W + 2 * s.pw;
+    a.dHp = make_fastdiv((uint32_t)a.Hp);
+    a.dWp = make_fastdiv((uint32_t)a.Wp);
+    TraceScope ts(fwd_large_name(bwd, deep, narrow, wide, patch), st, flops, WORK_FLOP);
 #define LAUNCH_LARGE(B, K, W) \
-  hipLaunchKernelGGL((conv_fwd_large_kernel<B, K, W>), dim3(a.tiles), dim3(W == 8 ? 2 * NT : NT), 0, st, a)
-    if (wide) {
+  hipLaunchKernelGGL((conv_fwd_large_kernel<B, K, W, false>), dim3(a.tiles), dim3(W == 8 ? 2 * NT : NT), 0, st, a)
+#define LAUNCH_PATCH(B, W) \
+  hipLaunchKernelGGL((conv_fwd_large_kernel<B, 32, W, true>), dim3(a.tiles), dim3(W == 8 ? 2 * NT : NT), 0, st, a)
+    if (patch) {
+      if (bwd) LAUNCH_PATCH(true, 2); else LAUNCH_PATCH(false, 2);
+    } else if (wide) {
       if (bwd) LAUNCH_LARGE(true, 32, 8); else LAUNCH_LARGE(false, 32, 8);
     } else if (bwd) {
       if (narrow) { if (deep) LAUNCH_LARGE(true, 64, 4); else LAUNCH_LARGE(true, 32, 4); }
@@ -1713,6 +1874,7 @@ hipError_t conv_fwd_dispatch(const ConvShape& s, const void* x, const void* w, c
       else { if (deep) LAUNCH_LARGE(false, 64, 2); else LAUNCH_LARGE(false, 32, 2); }
     }
 #undef LAUNCH_LARGE
+#undef LAUNCH_PATCH
     return hipGetLastError();
   }
   if (bwd)

@@ -590,7 +590,29 @@ LARGE_CASES = [
     ("fwd", (30, 64, 47, 47, 256, 3, 3, 1, 1)),
     ("bwd_data", (30, 256, 47, 47, 64, 3, 3, 1, 1)),
     ("fwd", (25, 64, 47, 47, 250, 3, 3, 1, 1)),  # ragged columns, element-wise epilogue
+    # stride 1 with 32-channel slices: the input-patch variant (tiles of 13 x 13
+    # images span up to three images; odd and even slice counts; pad 0 and 2;
+    # a non-square kernel; ragged rows and columns)
+    ("fwd", (400, 64, 13, 13, 128, 3, 3, 1, 1)),
+    ("bwd_data", (400, 128, 13, 13, 96, 3, 3, 1, 1)),
+    ("fwd", (401, 64, 13, 13, 120, 3, 3, 1, 1)),
+    ("fwd", (400, 32, 15, 15, 128, 3, 3, 0, 1)),
+    ("fwd", (400, 64, 13, 13, 128, 3, 2, 1, 1)),
+    ("fwd", (100, 96, 27, 27, 256, 5, 5, 2, 1)),
+    ("bwd_data", (400, 256, 13, 13, 384, 3, 3, 1, 1)),
 ]
+
+
+def _patch_fits(N, H, W, R, S, pad, cap):
+    P, Q = H + 2 * pad - R + 1, W + 2 * pad - S + 1
+    Hp, Wp, M = H + 2 * pad, W + 2 * pad, N * P * Q
+    for m0 in range(0, M, 256):
+        m1 = min(m0 + 256, M) - 1
+        n0, p0 = m0 // (P * Q), (m0 % (P * Q)) // Q
+        n1, p1 = m1 // (P * Q), (m1 % (P * Q)) // Q
+        if (n1 * Hp + p1 + R - (n0 * Hp + p0)) * Wp > cap:
+            return False
+    return True
 
 
 @pytest.mark.parametrize("op,case", LARGE_CASES, ids=[o + "-" + "x".join(map(str, c)) for o, c in LARGE_CASES])
@@ -608,13 +630,21 @@ def test_conv_large_tile_path(op, case):
     singa.trace_enable(False)
     large = [n for n in names if n.startswith("conv_fwd_large_kernel")]
     assert large, names
+    # template arguments: <bwd, taps per K-tile, wave layout[, 1 = input patch]>
+    targs = [n[n.index("<") + 1:-1].split(",") for n in large]
     cols = K if op == "fwd" else C  # GEMM columns: filters, or input channels for the data gradient
+    slice_c = C if op == "fwd" else K  # channels of the operand the taps gather
     narrow = cols <= 96
-    assert all(n.endswith(",4>") == narrow for n in large), large
+    assert all((t[2] == "4") == narrow for t in targs), large
     wide = 192 < cols <= 256  # 256-column tiles at least 3/4 used (every case here has enough row tiles)
-    assert all(n.endswith(",8>") == wide for n in large), large
-    deep = not narrow and not wide and R * S * (C if op == "fwd" else K) >= 4096  # reduction length
-    assert all((",64," in n) == deep for n in large), large
+    assert all((t[2] == "8") == wide for t in targs), large
+    deep = not narrow and not wide and R * S * slice_c >= 4096  # reduction length
+    assert all((t[1] == "64") == deep for t in targs), large
+    # the input patch: stride 1, 32-channel slices, at least 4 taps, the 256 x 128 layout with 32-tap
+    # K-tiles, and every 256-row tile's padded input rows x padded width within 448 entries
+    patch = (stride == 1 and slice_c % 32 == 0 and R * S >= 4 and not narrow and not wide and not deep
+             and _patch_fits(N, H, W, R, S, pad, 448))
+    assert all((len(t) == 4 and t[3] == "1") == patch for t in targs), large
     if op == "fwd":
         ref = oracle.relu_fwd(oracle.conv_fwd(x, w, b, pad=pad, stride=stride))
     else:
