@@ -219,7 +219,9 @@ def measure_config(index, steps, warmup):
     """One of the other workloads, timed on its own: `steps` eager steps
     between two device synchronizations after `warmup` untimed ones (the
     single-layer workload also computes its input gradient, as its three
-    passes define it), then the same steps with the kernel trace on.  The
+    passes define it), the same number replayed from a HIP graph of one step
+    (the faster of the two is the workload's step time), then the same steps
+    launched eagerly with the kernel trace on.  The
     step's algorithmic conv / FC flops over the step time and over the
     summed conv-kernel time, against the peak of the workload's dtype."""
     import torch
@@ -240,14 +242,25 @@ def measure_config(index, steps, warmup):
     def step():
         net.train_one_batch(x, labels=labels, dy_top=dy, need_input_grad=need_dx)
 
+    def timed(fn):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            fn()
+        torch.cuda.synchronize()
+        return (time.perf_counter() - t0) * 1e3 / steps
+
     for _ in range(warmup):
         step()
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(steps):
-        step()
-    torch.cuda.synchronize()
-    ms = (time.perf_counter() - t0) * 1e3 / steps
+    eager_ms = timed(step)
+    # the same steps replayed from a HIP graph of one step (these small steps
+    # are launch-bound: replay issues all their kernels at once)
+    graph = net.capture(x, labels=labels, dy_top=dy, need_input_grad=need_dx)
+    for _ in range(3):
+        graph.replay()
+    graph_ms = timed(graph.replay)
+    del graph
+    ms = min(eager_ms, graph_ms)
     side = net.wgrad_stream
     net.wgrad_stream = None
     singa.trace_enable(True)
@@ -265,6 +278,8 @@ def measure_config(index, steps, warmup):
     tf_conv = flops / (conv_ms / 1e3) / 1e12
     out = {"workload": CONFIG_NAMES[index], "description": w.name, "dtype": w.dtype, "batch": net.batch,
            "ms_per_step": round(ms, 4), "images_per_s": round(net.batch / (ms / 1e3), 1),
+           "launch": "eager" if eager_ms <= graph_ms else "hip_graph", "eager_ms_per_step": round(eager_ms, 4),
+           "graph_ms_per_step": round(graph_ms, 4),
            "conv_gflop_per_step": round(flops / 1e9, 4), "traced_conv_gflop_per_step": round(traced_flops / 1e9, 4),
            "tflops_over_step": round(tf_step, 3), "frac_peak_over_step": round(tf_step / peak, 4),
            "conv_kernel_ms_per_step": round(conv_ms, 4), "tflops_over_conv_kernels": round(tf_conv, 3),
