@@ -150,7 +150,10 @@ class ConvLayer(Layer):
                     db=self.db if keep else None, workspace=net.workspace if side is None else net.workspace_wgrad)
             return self.dx if need_dx else None
         side = self.net.wgrad_stream
-        if side is None:
+        if side is None or (not need_dx and self.net.last_wgrad_on_main):
+            # one stream; or the first layer of a training step, whose input
+            # gradient is not needed: the main stream has nothing left to do,
+            # while the second one is still busy with the layers above
             singa.conv_bwd_filter(self.x, dy, self.w_shape, self.pad, self.stride, with_bias=self.has_bias,
                                   dw=self.dw, db=self.db, workspace=self.net.workspace, layout=self.x_layout,
                                   x_shape=self.in_shape)
@@ -265,13 +268,15 @@ class Net:
 
     def __init__(self, workload: wl.Workload, batch: Optional[int] = None, device="cuda", fuse_update: bool = True,
                  keep_grads: bool = False, concurrent_wgrad: bool = True, updater: str = "sgd",
-                 adagrad_delta: float = 1e-6, reduce_update: bool = False):
+                 adagrad_delta: float = 1e-6, reduce_update: bool = False, last_wgrad_on_main: bool = True):
         """fuse_update: apply the update inside the filter-gradient kernel
         where it can be fused; keep_grads: those layers also store their
         gradients in the flat gradient buffer (for inspection);
         concurrent_wgrad: the filter gradients (with the fused update where
         there is one) run on a second stream, concurrently with the
-        backward-data passes; updater: "sgd"
+        backward-data passes, except the first layer's when its input
+        gradient is not needed (last_wgrad_on_main: that one runs on the
+        main stream, idle by then); updater: "sgd"
         (momentum, the workloads' Updater) or "adagrad" (Sec. 4.1.4's named
         protocol, with the workload's learning rate and weight decay; the
         momentum buffer holds its sums of squared gradients)."""
@@ -280,6 +285,7 @@ class Net:
         self.updater = updater
         self.adagrad_delta = adagrad_delta
         self.reduce_update = reduce_update
+        self.last_wgrad_on_main = last_wgrad_on_main
         self.wl = workload
         self.fuse_update = fuse_update
         self.keep_grads = keep_grads
