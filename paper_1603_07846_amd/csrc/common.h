@@ -12,23 +12,20 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
-// fp32 -> bf16, round to nearest even; NaN stays a (quiet) NaN.
-__device__ __forceinline__ bf16_t f32_to_bf16(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return (bf16_t)((u >> 16) | 0x40u);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return (bf16_t)(u >> 16);
-}
-
-// Two fp32 values -> two bf16 (low half: a), round to nearest even, in one
-// gfx950 conversion instruction (v_cvt_pk_bf16_f32).  Same results as
-// f32_to_bf16 on every finite value the kernels produce (not relied on for
-// NaN payloads or subnormals).
+// Two fp32 values -> two bf16 (low half: a), round to nearest even, NaN to
+// a quiet NaN, in one gfx950 conversion instruction (v_cvt_pk_bf16_f32).  On
+// all 2^32 fp32 patterns, subnormals and NaNs included, its result equals
+// the bit-level rounding (u + 0x7fff + ((u >> 16) & 1)) >> 16 (NaN: (u >> 16) |
+// 0x40) (compared exhaustively on gfx950), which takes about six VALU
+// operations per value.
 __device__ __forceinline__ uint32_t f32x2_to_bf16x2(float a, float b) {
   typedef float f2 __attribute__((ext_vector_type(2)));
   typedef __bf16 h2 __attribute__((ext_vector_type(2)));
   return __builtin_bit_cast(uint32_t, __builtin_convertvector((f2){a, b}, h2));
 }
+
+// fp32 -> bf16, round to nearest even; NaN stays a (quiet) NaN.
+__device__ __forceinline__ bf16_t f32_to_bf16(float f) { return (bf16_t)f32x2_to_bf16x2(f, 0.f); }
 
 __device__ __forceinline__ float bf16_to_f32(bf16_t b) {
   return __uint_as_float(((uint32_t)b) << 16);
