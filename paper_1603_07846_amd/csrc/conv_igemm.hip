@@ -633,13 +633,21 @@ __device__ __forceinline__ void block_barrier() { asm volatile("s_barrier" ::: "
 // tile (512 threads, one workgroup per CU): half the operand bytes per flop
 // of the 256 x 128 tile on the B side, for 256-column layers with enough
 // row tiles.
+// WMW = 6: the same 8 waves on a 192 x 256 tile, each 96 x 64: 4/3 as many
+// tiles, for layers whose 256-row tiles leave much of the chip idle in their
+// last round (AlexNet's 13 x 13 layers at batch 256: 169 tiles of 256 rows
+// on 256 CUs, 226 of 192).  Loads and LDS are those of WMW = 8; the A rows
+// 192 .. 255 of each stage are loaded as out-of-range zeros (no traffic)
+// and never read.
 template <bool BWD, int LBK, int WMW, bool PATCH>
-__global__ __launch_bounds__(WMW == 8 ? 2 * NT : NT, (LBK == 32 && WMW == 4) ? 3 : (LBK == 32 && WMW != 8) ? 2 : 1)
+__global__ __launch_bounds__(WMW >= 6 ? 2 * NT : NT, (LBK == 32 && WMW == 4) ? 3 : (LBK == 32 && WMW < 6) ? 2 : 1)
 void conv_fwd_large_kernel(FwdArgs a) {
   typedef LT<LBK> G;
-  constexpr int NW = WMW == 8 ? 8 : 4;       // waves
-  constexpr int BNT = WMW == 8 ? 256 : BN;   // tile columns
-  constexpr int FM = WMW == 4 ? 2 : 4, FN = WMW == 4 ? 3 : 2;
+  static_assert(WMW == 2 || WMW == 4 || WMW == 6 || WMW == 8, "wave layouts");
+  constexpr int NW = WMW >= 6 ? 8 : 4;       // waves
+  constexpr int BNT = WMW >= 6 ? 256 : BN;   // tile columns
+  constexpr int BMT = WMW == 6 ? 192 : L_BM;  // tile rows (the A stage keeps L_BM rows)
+  constexpr int FM = WMW == 4 ? 2 : WMW == 6 ? 3 : 4, FN = WMW == 4 ? 3 : 2;
   constexpr int ABAND = L_BM / NW, BBAND = BNT / NW;  // operand rows each wave loads
   constexpr int AI = ABAND / G::RPI, BI = BBAND / G::RPI;  // its load instructions per K-tile
   // with the input patch the stages hold only the filter tile
@@ -662,7 +670,7 @@ void conv_fwd_large_kernel(FwdArgs a) {
   const int L = xcd_remap(blockIdx.x, gridDim.x);
   const int split = L / a.tiles, tile = L - split * a.tiles;
   const int tm = tile / a.tiles_n, tn = tile - tm * a.tiles_n;
-  const int m0 = tm * L_BM, n0 = tn * BNT;
+  const int m0 = tm * BMT, n0 = tn * BNT;
   const __amdgpu_buffer_rsrc_t xr = make_rsrc(a.x, a.x_bytes);
   const __amdgpu_buffer_rsrc_t wr = make_rsrc(a.w, a.w_bytes);
 
@@ -679,7 +687,7 @@ void conv_fwd_large_kernel(FwdArgs a) {
 #pragma unroll
   for (int i = 0; i < AI; ++i) {
     const int m = m0 + ABAND * wave + G::RPI * i + lrow;
-    if (m < a.M) {
+    if (m < a.M && ABAND * wave + G::RPI * i + lrow < BMT) {
       const int n = (int)fdiv((uint32_t)m, a.dPQ);
       const int pq = m - n * a.P * a.Q;
       const int p = (int)fdiv((uint32_t)pq, a.dQ);
@@ -759,8 +767,8 @@ void conv_fwd_large_kernel(FwdArgs a) {
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
-  const int wm = WMW == 2 ? wave >> 1 : WMW == 8 ? wave >> 2 : wave;
-  const int wn = WMW == 2 ? wave & 1 : WMW == 8 ? wave & 3 : 0;
+  const int wm = WMW == 2 ? wave >> 1 : WMW >= 6 ? wave >> 2 : wave;
+  const int wn = WMW == 2 ? wave & 1 : WMW >= 6 ? wave & 3 : 0;
   const int li = lane & 31, lh = lane >> 5;
   // chunk 2 kc + lh of row r sits in slot (2 kc + lh) ^ ((r / RPW) % SL); r % 16 = li % 16
   const int tsw = (lh ^ ((li / G::RPW) % G::SL)) << 4;
@@ -945,13 +953,14 @@ void conv_fwd_large_kernel(FwdArgs a) {
   }
   __syncthreads();  // every wave is done with the operand tiles
   const bool vec = a.Nn % 8 == 0 && (((uintptr_t)a.y | (uintptr_t)a.mask) % 16) == 0;
-  if constexpr (WMW == 8) {
-    // the quadrant in two halves of 64 rows: 8 waves x 9 KB of staging
+  if constexpr (WMW >= 6) {
+    // the quadrant in passes of 64 rows (and 32 for the 96-row one): 8 waves
+    // x 9 KB of staging
     char* q = smem + wave * 64 * (FN * 32 * 2 + 16);
     store_quadrant<bf16_t, FM, FN, 0, 2>(acc, q, lane, m0 + wm * FM * 32, n0 + wn * FN * 32, a.M, a.Nn, a.bias,
                                          a.relu, a.mask, (bf16_t*)a.y, vec);
-    store_quadrant<bf16_t, FM, FN, 2, 2>(acc, q, lane, m0 + wm * FM * 32 + 64, n0 + wn * FN * 32, a.M, a.Nn,
-                                         a.bias, a.relu, a.mask, (bf16_t*)a.y, vec);
+    store_quadrant<bf16_t, FM, FN, 2, FM - 2>(acc, q, lane, m0 + wm * FM * 32 + 64, n0 + wn * FN * 32, a.M, a.Nn,
+                                              a.bias, a.relu, a.mask, (bf16_t*)a.y, vec);
   } else if constexpr (NS == 2) {
     // two LDS stages hold less than the quadrant: two passes of 32 rows
     char* q = smem + wave * 32 * (FN * 32 * 2 + 16);
@@ -1694,7 +1703,7 @@ __global__ __launch_bounds__(256) void splitk_epilogue_vec_kernel(const float* _
 }
 
 // Layout and split overrides for A/B measurements (SINGA_CONV_TILE,
-// SINGA_FWD_BK, SINGA_FWD_WIDE, SINGA_FWD_PATCH, SINGA_WGRAD_ORDER, SINGA_WGRAD_TARGET): read
+// SINGA_FWD_BK, SINGA_FWD_WIDE, SINGA_FWD_SHORT, SINGA_FWD_PATCH, SINGA_WGRAD_ORDER, SINGA_WGRAD_TARGET): read
 // from the environment only in a library built with -DSINGA_TUNING.  The
 // default build ignores the environment; its dispatch rules are the tested
 // ones.
@@ -1738,6 +1747,20 @@ const char* fwd_large_name(bool bwd, bool deep, bool narrow, bool wide, bool pat
        {"conv_fwd_large_kernel<1,64,2>", "conv_fwd_large_kernel<1,64,4>"}}};
   if (wide) return bwd ? "conv_fwd_large_kernel<1,32,8>" : "conv_fwd_large_kernel<0,32,8>";
   return names[bwd][deep][narrow];
+}
+
+// The 192 x 256 layout instead of 256 x 256 when it takes at most 90 % of
+// the 256-row layout's time, counted as rounds of 256 workgroups (one per
+// CU) times the rows of a tile.
+bool use_short_wide_fwd(long M, long Nn) {
+  static const int forced = [] {
+    const char* e = tuning_env("SINGA_FWD_SHORT");
+    return e ? atoi(e) : -1;
+  }();
+  if (forced == 0 || forced == 1) return forced == 1;
+  const long cols = (Nn + 255) / 256;
+  const long t256 = (M + 255) / 256 * cols, t192 = (M + 191) / 192 * cols;
+  return 10 * ((t192 + 255) / 256) * 192 <= 9 * ((t256 + 255) / 256) * 256;
 }
 
 // Workgroups of the 256 x 128 kernel per full round of the chip (one per CU)
@@ -1893,8 +1916,10 @@ hipError_t conv_fwd_dispatch(const ConvShape& s, const void* x, const void* w, c
   if (!wt && sizeof(T) == 2 && am == VEC16 && bm == VEC16 && splits == 1 && use_large_fwd(a.M, a.Nn, a.Kg)) {
     const bool narrow = a.Nn <= 96;  // one 96-column tile
     const bool wide = use_wide_fwd(a.M, a.Nn);
+    const bool short_wide = wide && use_short_wide_fwd(a.M, a.Nn);
+    const int tile_rows = short_wide ? 192 : L_BM;
     a.tiles_n = (a.Nn + (wide ? 255 : BN - 1)) / (wide ? 256 : BN);
-    a.tiles = ((a.M + L_BM - 1) / L_BM) * a.tiles_n;
+    a.tiles = ((a.M + tile_rows - 1) / tile_rows) * a.tiles_n;
     a.partial = nullptr;
     // 64-tap K-tiles only for the 256 x 128 layout (the 256 x 96 one measured
     // faster at 32 taps, two workgroups per CU, on a 6400-tap reduction; the
@@ -1909,13 +1934,17 @@ hipError_t conv_fwd_dispatch(const ConvShape& s, const void* x, const void* w, c
     a.Wp = s.W + 2 * s.pw;
     a.dHp = make_fastdiv((uint32_t)a.Hp);
     a.dWp = make_fastdiv((uint32_t)a.Wp);
-    TraceScope ts(fwd_large_name(bwd, deep, narrow, wide, patch), st, flops, WORK_FLOP);
+    TraceScope ts(short_wide ? (bwd ? "conv_fwd_large_kernel<1,32,6>" : "conv_fwd_large_kernel<0,32,6>")
+                             : fwd_large_name(bwd, deep, narrow, wide, patch),
+                  st, flops, WORK_FLOP);
 #define LAUNCH_LARGE(B, K, W) \
-  hipLaunchKernelGGL((conv_fwd_large_kernel<B, K, W, false>), dim3(a.tiles), dim3(W == 8 ? 2 * NT : NT), 0, st, a)
+  hipLaunchKernelGGL((conv_fwd_large_kernel<B, K, W, false>), dim3(a.tiles), dim3(W >= 6 ? 2 * NT : NT), 0, st, a)
 #define LAUNCH_PATCH(B, W) \
   hipLaunchKernelGGL((conv_fwd_large_kernel<B, 32, W, true>), dim3(a.tiles), dim3(W == 8 ? 2 * NT : NT), 0, st, a)
     if (patch) {
       if (bwd) LAUNCH_PATCH(true, 2); else LAUNCH_PATCH(false, 2);
+    } else if (short_wide) {
+      if (bwd) LAUNCH_LARGE(true, 32, 6); else LAUNCH_LARGE(false, 32, 6);
     } else if (wide) {
       if (bwd) LAUNCH_LARGE(true, 32, 8); else LAUNCH_LARGE(false, 32, 8);
     } else if (bwd) {
