@@ -1281,9 +1281,9 @@ __global__ __launch_bounds__(NT) void conv_wgrad_kernel(WgradArgs a) {
 // ----------------------------------------------- filter gradient, large tiles
 //
 // The same product for bf16 operands with whole 16-byte filter and tap chunks
-// (K % 8 == 0, C % 8 == 0), on a 128 (filters) x 256 (taps) tile: each of the
-// 4 waves owns 64 x 128 (2 x 4 blocks of 32 x 32), so one transpose read feeds
-// more MFMAs than in the 128 x 128 kernel.  Operands go from buffer loads
+// (K % 8 == 0, C % 8 == 0), on a 128 (filters) x 256 (taps) tile: each of 8
+// waves owns 64 x 64 (2 x 2 blocks of 32 x 32), or, with the update fused,
+// each of 4 waves 64 x 128 (2 x 4 blocks).  Operands go from buffer loads
 // straight into LDS as t-major rows (256 bytes of filters, 512 bytes of taps
 // per reduction index); one load instruction fills 1 KB, i.e. 4 (A) or 2 (B)
 // rows.  Rows are unpadded and XOR-swizzled: the 16-byte chunk c of row r sits
@@ -1302,12 +1302,16 @@ constexpr int WL_AT = WL_BK * WL_ARB, WL_BT = WL_BK * WL_BRB;
 constexpr int WL_STAGE = WL_AT + WL_BT;
 constexpr int WL_SMEM = 3 * WL_STAGE;  // 72 KB: two workgroups per CU
 
-template <bool NFAST, bool UPD>
-__global__ __launch_bounds__(NT, 2) void conv_wgrad_large_kernel(WgradArgs a) {
+template <bool NFAST, bool UPD, bool W8>
+__device__ __forceinline__ void wgrad_large_body(const WgradArgs& a) {
   constexpr uint32_t ES = 2;
-  constexpr int RPW = WL_BK / 4;    // K-tile rows loaded by each wave (of A and of B)
-  constexpr int AI = WL_BK / 16;    // A load instructions per wave (4 rows each)
-  constexpr int BI = WL_BK / 8;     // B load instructions per wave (2 rows each)
+  // waves: 4 of 64 x 128 (2 x 4 blocks of 32 x 32), or with W8 8 of 64 x 64
+  constexpr int NWV = W8 ? 8 : 4;
+  constexpr int FM = 2, FN = W8 ? 2 : 4;
+  constexpr int RPW = WL_BK / NWV;  // K-tile rows loaded by each wave (of A and of B)
+  constexpr int AI = RPW / 4;       // A load instructions per wave (4 rows each)
+  constexpr int BI = RPW / 2;       // B load instructions per wave (2 rows each)
+  static_assert(AI >= 1 && BI >= 2 && BI % 2 == 0, "load split");
   __shared__ __attribute__((aligned(16))) char smem[WL_SMEM];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int L = xcd_remap(blockIdx.x, gridDim.x);
@@ -1389,38 +1393,38 @@ __global__ __launch_bounds__(NT, 2) void conv_wgrad_large_kernel(WgradArgs a) {
     }
   };
 
-  f32x16 acc[2][4];
+  f32x16 acc[FM][FN];
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < FM; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+    for (int j = 0; j < FN; ++j)
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
   // transpose-read addresses: lane -> column (lane & 31) of a 32-column block,
   // reduction rows 8 (lane / 32) + 0..7 of a 16-row step
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wrow = W8 ? (wave >> 2) * 64 : (wave >> 1) * 64, wcol = W8 ? (wave & 3) * 64 : (wave & 1) * 128;
   const int trow = 8 * (lane >> 5) + ((lane & 15) >> 2);
   const int low = 2 * ((lane >> 4) & 1) + ((lane & 3) >> 1);  // chunk bits 0-1 within a 32-column block
   const int rr = (lane & 15) >> 2;                                // row & 3 (same for every step)
   const int off = 8 * (lane & 1);
-  int aaddr[2], baddr[4];
+  int aaddr[FM], baddr[FN];
 #pragma unroll
-  for (int b = 0; b < 2; ++b) {
-    const int x32 = (wm * 64 + b * 32) / 32;  // chunk = 4 x32 + low, stored in slot chunk ^ (4 rr)
+  for (int b = 0; b < FM; ++b) {
+    const int x32 = (wrow + b * 32) / 32;  // chunk = 4 x32 + low, stored in slot chunk ^ (4 rr)
     aaddr[b] = trow * WL_ARB + ((4 * (x32 ^ rr) + low) << 4) + off;
   }
 #pragma unroll
-  for (int b = 0; b < 4; ++b) {
-    const int x32 = (wn * 128 + b * 32) / 32;
+  for (int b = 0; b < FN; ++b) {
+    const int x32 = (wcol + b * 32) / 32;
     baddr[b] = WL_AT + trow * WL_BRB + ((4 * (x32 ^ rr) + low) << 4) + off;
   }
   // the bias column as ones in the B fragments of the wave that holds it
-  uint32_t onesm[4];
+  uint32_t onesm[FN];
   bool bias_wave = false;
 #pragma unroll
-  for (int b = 0; b < 4; ++b) {
-    const int cb = n0 + wn * 128 + b * 32;
+  for (int b = 0; b < FN; ++b) {
+    const int cb = n0 + wcol + b * 32;
     onesm[b] = (a.Ng > a.Nn && cb + (lane & 31) == a.Nn) ? 0x3f803f80u : 0u;
     bias_wave |= a.Ng > a.Nn && cb <= a.Nn && a.Nn < cb + 32;
   }
@@ -1428,22 +1432,22 @@ __global__ __launch_bounds__(NT, 2) void conv_wgrad_large_kernel(WgradArgs a) {
   auto compute = [&](const char* S) {
 #pragma unroll
     for (int kc = 0; kc < WL_BK / 16; ++kc) {
-      bf16x8 af[2], bfr[4];
+      bf16x8 af[FM], bfr[FN];
 #pragma unroll
-      for (int b = 0; b < 2; ++b) {
+      for (int b = 0; b < FM; ++b) {
         const v4i16 lo = lds_tr16(S + aaddr[b] + kc * 16 * WL_ARB);
         const v4i16 hi = lds_tr16(S + aaddr[b] + (kc * 16 + 4) * WL_ARB);
         af[b] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
       }
 #pragma unroll
-      for (int b = 0; b < 4; ++b) {
+      for (int b = 0; b < FN; ++b) {
         const v4i16 lo = lds_tr16(S + baddr[b] + kc * 16 * WL_BRB);
         const v4i16 hi = lds_tr16(S + baddr[b] + (kc * 16 + 4) * WL_BRB);
         bfr[b] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
       }
       if (bias_wave) {
 #pragma unroll
-        for (int b = 0; b < 4; ++b) {
+        for (int b = 0; b < FN; ++b) {
           uint4 u = __builtin_bit_cast(uint4, bfr[b]);
           u.x |= onesm[b];
           u.y |= onesm[b];
@@ -1453,9 +1457,9 @@ __global__ __launch_bounds__(NT, 2) void conv_wgrad_large_kernel(WgradArgs a) {
         }
       }
 #pragma unroll
-      for (int bm = 0; bm < 2; ++bm)
+      for (int bm = 0; bm < FM; ++bm)
 #pragma unroll
-        for (int bn = 0; bn < 4; ++bn)
+        for (int bn = 0; bn < FN; ++bn)
           acc[bm][bn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[bm], bfr[bn], acc[bm][bn], 0, 0, 0);
     }
   };
@@ -1490,14 +1494,14 @@ __global__ __launch_bounds__(NT, 2) void conv_wgrad_large_kernel(WgradArgs a) {
   if (!a.direct) {
     float* __restrict__ out = a.out + (size_t)split * a.M * a.ldp;
 #pragma unroll
-    for (int bn = 0; bn < 4; ++bn) {
-      const int col = n0 + wn * 128 + bn * 32 + li;
+    for (int bn = 0; bn < FN; ++bn) {
+      const int col = n0 + wcol + bn * 32 + li;
       if (col >= a.Ng) continue;
 #pragma unroll
-      for (int bm = 0; bm < 2; ++bm)
+      for (int bm = 0; bm < FM; ++bm)
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
-          const int row = m0 + wm * 64 + bm * 32 + (v >> 2) * 8 + lh * 4 + (v & 3);
+          const int row = m0 + wrow + bm * 32 + (v >> 2) * 8 + lh * 4 + (v & 3);
           if (row < a.M) out[(size_t)row * a.ldp + col] = acc[bm][bn][v];
         }
     }
@@ -1507,8 +1511,8 @@ __global__ __launch_bounds__(NT, 2) void conv_wgrad_large_kernel(WgradArgs a) {
     // Update fused: each lane owns one column (filter tap, or the bias) of
     // 32 rows per block; the rows' w and v are loaded before any is used.
 #pragma unroll
-    for (int bn = 0; bn < 4; ++bn) {
-      const int col = n0 + wn * 128 + bn * 32 + li;
+    for (int bn = 0; bn < FN; ++bn) {
+      const int col = n0 + wcol + bn * 32 + li;
       if (col >= a.Ng) continue;
       const bool is_db = col == a.Nn;
       float* __restrict__ W = is_db ? a.u.b : a.u.w + col;
@@ -1518,19 +1522,19 @@ __global__ __launch_bounds__(NT, 2) void conv_wgrad_large_kernel(WgradArgs a) {
       const size_t stride = is_db ? 1 : (size_t)a.Nn;
       float wv[2][16], vv[2][16];
 #pragma unroll
-      for (int bm = 0; bm < 2; ++bm)
+      for (int bm = 0; bm < FM; ++bm)
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
-          const int row = m0 + wm * 64 + bm * 32 + (v >> 2) * 8 + lh * 4 + (v & 3);
+          const int row = m0 + wrow + bm * 32 + (v >> 2) * 8 + lh * 4 + (v & 3);
           const size_t o = (size_t)(row < a.M ? row : 0) * stride;
           wv[bm][v] = W[o];
           vv[bm][v] = V[o];
         }
 #pragma unroll
-      for (int bm = 0; bm < 2; ++bm)
+      for (int bm = 0; bm < FM; ++bm)
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
-          const int row = m0 + wm * 64 + bm * 32 + (v >> 2) * 8 + lh * 4 + (v & 3);
+          const int row = m0 + wrow + bm * 32 + (v >> 2) * 8 + lh * 4 + (v & 3);
           if (row >= a.M) continue;
           const size_t o = (size_t)row * stride;
           const float g = acc[bm][bn][v];
@@ -1544,24 +1548,34 @@ __global__ __launch_bounds__(NT, 2) void conv_wgrad_large_kernel(WgradArgs a) {
     return;
   }
 #pragma unroll
-  for (int bn = 0; bn < 4; ++bn) {
-    const int col = n0 + wn * 128 + bn * 32 + li;
+  for (int bn = 0; bn < FN; ++bn) {
+    const int col = n0 + wcol + bn * 32 + li;
     if (col >= a.Ng) continue;
     const bool is_db = col == a.Nn;
     float* __restrict__ base = is_db ? a.db : a.out + col;
     const size_t stride = is_db ? 1 : (size_t)a.Nn;
     const int accum = is_db ? a.acc_db : a.acc_dw;
 #pragma unroll
-    for (int bm = 0; bm < 2; ++bm)
+    for (int bm = 0; bm < FM; ++bm)
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
-        const int row = m0 + wm * 64 + bm * 32 + (v >> 2) * 8 + lh * 4 + (v & 3);
+        const int row = m0 + wrow + bm * 32 + (v >> 2) * 8 + lh * 4 + (v & 3);
         if (row < a.M) {
           float* o = base + (size_t)row * stride;
           *o = accum ? *o + acc[bm][bn][v] : acc[bm][bn][v];
         }
       }
   }
+}
+
+// Eight waves of 64 x 64 for the gradient alone: four waves per SIMD (109
+// VGPRs) cover more of the operand stream's latency than two of 64 x 128,
+// for a third more fragment reads per MFMA (conv2 0.2512 -> 0.2293 ms,
+// conv4 0.1305 -> 0.1201, the others 1-3 %; bitwise the same results).  The
+// fused update keeps four waves.
+template <bool NFAST, bool UPD>
+__global__ __launch_bounds__(UPD ? NT : 2 * NT, 2) void conv_wgrad_large_kernel(WgradArgs a) {
+  wgrad_large_body<NFAST, UPD, !UPD>(a);
 }
 
 // Filter-gradient split-K reduction over partial[split][M][Ng] (rows of ldp
@@ -2135,8 +2149,8 @@ hipError_t conv_wgrad_dispatch(const ConvShape& s, const void* x, const void* dy
       if (nf) hipLaunchKernelGGL((conv_wgrad_large_kernel<true, true>), grid, dim3(NT), 0, st, a);
       else hipLaunchKernelGGL((conv_wgrad_large_kernel<false, true>), grid, dim3(NT), 0, st, a);
     } else {
-      if (nf) hipLaunchKernelGGL((conv_wgrad_large_kernel<true, false>), grid, dim3(NT), 0, st, a);
-      else hipLaunchKernelGGL((conv_wgrad_large_kernel<false, false>), grid, dim3(NT), 0, st, a);
+      if (nf) hipLaunchKernelGGL((conv_wgrad_large_kernel<true, false>), grid, dim3(2 * NT), 0, st, a);
+      else hipLaunchKernelGGL((conv_wgrad_large_kernel<false, false>), grid, dim3(2 * NT), 0, st, a);
     }
   } else if (nf) {
     launch_wgrad_variant<T, true>(va, vb, a, grid, flops, st);
