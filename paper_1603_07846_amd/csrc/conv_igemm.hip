@@ -186,17 +186,6 @@ __device__ __forceinline__ int xcd_remap(int b, int G) {
   return x * q + min(x, r) + l;
 }
 
-// ------------------------------------------------------------ epilogue
-//
-// y[row][col] = act(acc + bias[col]), optionally zeroed where mask <= 0, for
-// row blocks B0 .. B0 + NB - 1 of one wave's (32 FM) x (32 FN) quadrant of
-// the output tile (row0: the first row of block B0).  The accumulators hold
-// one column per lane (rows 8 (v / 4) + 4 (lane / 32) + v % 4 of each 32 x 32
-// block); they go through the wave's own LDS region as T so that the global
-// stores (and the mask loads) are 16-byte vectors of consecutive columns.
-// Needs (32 NB) * (32 FN * sizeof(T) + 16) bytes of LDS at `lds`; the caller
-// has finished with the operand tiles there (barrier).  `vec`: y, mask and Nn
-// allow 16-byte vectors; otherwise the staged values are stored one by one.
 // All-ones in the bits of each element of a 32-bit word that is > 0 (not
 // NaN), zero elsewhere, from the bit patterns alone: with x = bits - 1 taken
 // as a signed integer, an element is > 0 exactly when 0 <= x < bits(+inf).
@@ -216,6 +205,17 @@ template <> __device__ __forceinline__ uint32_t positive_bits<float>(uint32_t w)
   return (uint32_t)(((int32_t)(x - 0x7f800000u) >> 31) & ~((int32_t)x >> 31));
 }
 
+// ------------------------------------------------------------ epilogue
+//
+// y[row][col] = act(acc + bias[col]), optionally zeroed where mask <= 0, for
+// row blocks B0 .. B0 + NB - 1 of one wave's (32 FM) x (32 FN) quadrant of
+// the output tile (row0: the first row of block B0).  The accumulators hold
+// one column per lane (rows 8 (v / 4) + 4 (lane / 32) + v % 4 of each 32 x 32
+// block); they go through the wave's own LDS region as T so that the global
+// stores (and the mask loads) are 16-byte vectors of consecutive columns.
+// Needs (32 NB) * (32 FN * sizeof(T) + 16) bytes of LDS at `lds`; the caller
+// has finished with the operand tiles there (barrier).  `vec`: y, mask and Nn
+// allow 16-byte vectors; otherwise the staged values are stored one by one.
 template <typename T, int FM, int FN, int B0 = 0, int NB = FM>
 __device__ __forceinline__ void store_quadrant(const f32x16 (&acc)[FM][FN], char* lds, int lane, int row0, int col0,
                                                int M, int Nn, const float* bias, int relu, const void* mask,
