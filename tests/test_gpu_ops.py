@@ -793,3 +793,49 @@ def test_lrn_errors():
         with pytest.raises(singa.SingaError) as e:
             singa.lrn_fwd(x, *bad)
         assert e.value.status == -3
+
+
+# The folded ReLU backward keeps an element exactly where the mask value is
+# > 0: not at +0 or -0, not at negative values or NaNs (any payload), yes at
+# +inf and at positive subnormals.  The epilogue decides that from the bit
+# patterns; the masks here hold every such class, and the masked output must
+# equal the unmasked one zeroed where !(mask > 0), bit for bit.  Cases: the
+# 256 x 96, 192 x 256 and input-patch layouts, the 128 x 128 kernel in both
+# dtypes, and the dense layer through its split-K epilogue.
+MASK_CASES = [("bf16", (30, 96, 47, 47, 40, 3, 3, 1, 1)), ("bf16", (30, 256, 47, 47, 64, 3, 3, 1, 1)),
+              ("bf16", (400, 128, 13, 13, 96, 3, 3, 1, 1)), ("bf16", (4, 16, 8, 8, 24, 3, 3, 1, 1)),
+              ("f32", (4, 16, 8, 8, 24, 3, 3, 1, 1)), ("bf16", (256, 1024, 1, 1, 4096, 1, 1, 0, 1))]
+
+
+def _special_mask(shape, dt, seed):
+    """Mask values of every class, as the raw bits of dt."""
+    rng = np.random.default_rng(seed)
+    if dt == "bf16":
+        specials = np.array([0x0000, 0x8000, 0x3f80, 0xbf80, 0x7f80, 0xff80, 0x7fc0, 0x7f81, 0xffc1, 0x0001,
+                             0x007f, 0x8001, 0x4120, 0x0080], np.uint16)
+        bits = rng.choice(specials, size=shape).astype(np.uint16)
+        vals = (bits.astype(np.uint32) << 16).view(np.float32)
+        return bits, vals
+    specials = np.array([0x00000000, 0x80000000, 0x3f800000, 0xbf800000, 0x7f800000, 0xff800000, 0x7fc00000,
+                         0x7f800001, 0xffc00001, 0x00000001, 0x007fffff, 0x80000001, 0x41200000, 0x00800000],
+                        np.uint32)
+    bits = rng.choice(specials, size=shape).astype(np.uint32)
+    return bits, bits.view(np.float32)
+
+
+@pytest.mark.parametrize("dt,case", MASK_CASES, ids=[d + "-" + "x".join(map(str, c)) for d, c in MASK_CASES])
+def test_folded_relu_backward_special_mask_values(dt, case):
+    N, C, H, W, K, R, S, pad, stride = case
+    _, w, _, dy = _conv_inputs(case, dt, 140)
+    bits, vals = _special_mask((N, H, W, C), dt, 141)  # NHWC, the layout of the input gradient
+    tdt = torch.bfloat16 if dt == "bf16" else torch.float32
+    ibits = bits.view(np.int16) if dt == "bf16" else bits.view(np.int32)
+    mask = to_gpu(torch.from_numpy(np.ascontiguousarray(ibits))).view(tdt)
+    dyd, wd = nchw_to_dev(dy, dt), kcrs_to_dev(w, dt)
+    plain = singa.conv_bwd_data(dyd, wd, phys((N, C, H, W)), pad, stride)
+    masked = singa.conv_bwd_data(dyd, wd, phys((N, C, H, W)), pad, stride, relu_y=mask)
+    torch.cuda.synchronize()
+    keep = torch.from_numpy(vals > 0).to(plain.device)
+    want = torch.where(keep, plain, torch.zeros_like(plain))
+    assert torch.equal(masked.view(torch.int16 if dt == "bf16" else torch.int32),
+                       want.view(torch.int16 if dt == "bf16" else torch.int32)), case
