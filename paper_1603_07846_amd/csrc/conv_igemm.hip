@@ -192,6 +192,7 @@ __device__ __forceinline__ int xcd_remap(int b, int G) {
 // Integer arithmetic only, so a mask of many elements needs no condition
 // registers.
 typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2_t __attribute__((ext_vector_type(2)));
 
 template <typename T> __device__ __forceinline__ uint32_t positive_bits(uint32_t w);
 template <> __device__ __forceinline__ uint32_t positive_bits<bf16_t>(uint32_t w) {
@@ -1508,7 +1509,97 @@ __device__ __forceinline__ void wgrad_large_body(const WgradArgs& a) {
     return;
   }
   if constexpr (UPD) {
-    // Update fused: each lane owns one column (filter tap, or the bias) of
+    static_assert(!W8 && FM == 2 && FN == 4, "the update epilogue assumes waves of 64 x 128");
+    // Update fused, vector form (taps a multiple of 4, w / v / g 16-byte and
+    // the bf16 copy 8-byte aligned): a wave's 64 x 128 block goes through
+    // its own LDS region in four passes of 16 rows, so that a lane updates 4
+    // consecutive taps of a row with 16-byte non-temporal loads and stores
+    // (a wave instruction covers 512 contiguous bytes of each of two rows,
+    // against 128 bytes of each with one column per lane); a pass's 16 loads
+    // are issued before its staging.  The bias column (tap index Nn, the
+    // first of its 4-tap group) is updated on its own.
+    const bool v4 = a.Nn % 4 == 0 && (((uintptr_t)a.u.w | (uintptr_t)a.u.v | (uintptr_t)a.out) % 16) == 0 &&
+                    ((uintptr_t)a.u.wb % 8) == 0;
+    if (v4) {
+      constexpr int UP = 128 * 4 + 32;  // row pitch: rows r and r + 4 of a lane pair 32 banks apart
+      constexpr int PR = 16;            // rows per pass
+      static_assert(4 * PR * UP <= WL_SMEM, "staging fits the operand stages");
+      __syncthreads();  // every wave is done with the operand tiles
+      char* const q = smem + wave * PR * UP;
+      const int g4 = lane & 31, rh = lane >> 5;  // taps 4 g4 .. 4 g4 + 3 of the wave's 128, rows rh, rh + 2, ...
+      const int col = n0 + wcol + 4 * g4;
+      const bool in_w = col < a.Nn, is_db = col == a.Nn && a.Ng > a.Nn;
+#pragma unroll
+      for (int pass = 0; pass < 4; ++pass) {
+        // block bm = pass / 2, accumulator elements v = 8 (pass % 2) .. + 7
+        const int bm = pass >> 1, vb0 = 8 * (pass & 1);
+        const int row0 = m0 + wrow + 16 * pass;
+        f32x4 wv[PR / 2], vv[PR / 2];
+#pragma unroll
+        for (int i = 0; i < PR / 2; ++i) {
+          // every lane loads (element 0 stands in for rows and taps past the
+          // end), so no load sits in a branch that the next must wait for
+          const int row = row0 + 2 * i + rh;
+          const size_t o = (in_w && row < a.M) ? (size_t)row * a.Nn + col : 0;
+          wv[i] = __builtin_nontemporal_load((const f32x4*)(a.u.w + o));
+          vv[i] = __builtin_nontemporal_load((const f32x4*)(a.u.v + o));
+        }
+        // element v of column bn 32 + li is row 8 (v / 4) + 4 lh + v % 4 of the block
+#pragma unroll
+        for (int bn = 0; bn < FN; ++bn)
+#pragma unroll
+          for (int v = vb0; v < vb0 + 8; ++v)
+            *(float*)(q + (((v >> 2) & 1) * 8 + lh * 4 + (v & 3)) * UP + (bn * 32 + li) * 4) = acc[bm][bn][v];
+        __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's LDS writes are done
+        __builtin_amdgcn_wave_barrier();
+#pragma unroll
+        for (int i = 0; i < PR / 2; ++i) {
+          const int r = 2 * i + rh, row = row0 + r;
+          if (row >= a.M) continue;
+          const f32x4 gr = *(const f32x4*)(q + r * UP + g4 * 16);
+          if (in_w) {
+            const size_t o = (size_t)row * a.Nn + col;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              float we = wv[i][e], ve = vv[i][e];
+              sgd_step(we, ve, gr[e], a.u.lr, a.u.mom, a.u.wd);
+              wv[i][e] = we;
+              vv[i][e] = ve;
+            }
+            __builtin_nontemporal_store(vv[i], (f32x4*)(a.u.v + o));
+            __builtin_nontemporal_store(wv[i], (f32x4*)(a.u.w + o));
+            if (a.u.wb) {
+              const u32x2_t pb = {f32x2_to_bf16x2(wv[i][0], wv[i][1]), f32x2_to_bf16x2(wv[i][2], wv[i][3])};
+              __builtin_nontemporal_store(pb, (u32x2_t*)(a.u.wb + o));
+            }
+            if (a.out) __builtin_nontemporal_store(gr, (f32x4*)(a.out + o));
+          }
+        }
+        if (is_db) {
+          // the two lanes that hold the bias column (rows rh, rh + 2, ...)
+          float bw[PR / 2], bv[PR / 2];
+#pragma unroll
+          for (int i = 0; i < PR / 2; ++i) {
+            const int row = row0 + 2 * i + rh;
+            bw[i] = a.u.b[row < a.M ? row : 0];
+            bv[i] = a.u.vb[row < a.M ? row : 0];
+          }
+#pragma unroll
+          for (int i = 0; i < PR / 2; ++i) {
+            const int r = 2 * i + rh, row = row0 + r;
+            if (row >= a.M) continue;
+            const float gb = *(const float*)(q + r * UP + g4 * 16);
+            sgd_step(bw[i], bv[i], gb, a.u.lr, a.u.mom, a.u.wd);
+            a.u.b[row] = bw[i];
+            a.u.vb[row] = bv[i];
+            if (a.u.bb) a.u.bb[row] = f32_to_bf16(bw[i]);
+            if (a.db) a.db[row] = gb;
+          }
+        }
+      }
+      return;
+    }
+    // Element form: each lane owns one column (filter tap, or the bias) of
     // 32 rows per block; the rows' w and v are loaded before any is used.
 #pragma unroll
     for (int bn = 0; bn < FN; ++bn) {
