@@ -581,6 +581,9 @@ LARGE_CASES = [
     ("fwd", (15, 512, 47, 47, 136, 3, 3, 1, 1)),       # 4608 taps: 64-tap K-tiles
     ("bwd_data", (15, 136, 47, 47, 512, 3, 3, 1, 1)),
     # at most 96 output columns: the 256 x 96 wave layout
+    ("fwd", (40, 48, 57, 57, 96, 3, 3, 0, 1)),   # the space-to-depth first layer's shape: 472.7 row tiles
+    ("fwd", (100, 128, 27, 27, 96, 3, 3, 1, 1)),
+    ("bwd_data", (30, 96, 47, 47, 128, 3, 3, 1, 1)),
     ("fwd", (30, 64, 47, 47, 96, 3, 3, 1, 1)),
     ("fwd", (30, 32, 47, 47, 90, 3, 3, 1, 1)),   # ragged columns, element-wise epilogue
     ("fwd", (30, 32, 47, 47, 40, 3, 3, 1, 1)),
