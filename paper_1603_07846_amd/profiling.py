@@ -23,6 +23,14 @@ Subcommands (run from the repository root):
       outstanding misses, mean L2 read latency, L2 hit rate, HBM bytes, and
       the occupancy the kernel's registers and LDS allow.
 
+  timeline KERNEL_TRACE_CSV [--marker NAME] [--back N]
+      One step of a run as a markdown table, from a `rocprofv3 --kernel-trace`
+      CSV: every launch between two consecutive launches of the marker kernel
+      (the step's first kernel; by default the N-th step from the end, N = 2),
+      with its stream (main: the marker's queue; second: any other), start and
+      end in microseconds from the step's start, and duration; then each
+      stream's busy time over the step.
+
   libgemm [--reps N]
       Times the vendor library's bf16 GEMM (torch.matmul, hipBLASLt) on the
       explicit-GEMM shapes of the AlexNet-shaped layers at batch 256 (the
@@ -347,6 +355,29 @@ def cmd_counters(args):
         print("| " + " | ".join(cells) + " |")
 
 
+def cmd_timeline(args):
+    with open(args.csv) as f:
+        rows = list(csv.DictReader(f))
+    qkey = "Queue_Id" if rows and "Queue_Id" in rows[0] else "Stream_Id"
+    ks = sorted((int(r["Start_Timestamp"]), int(r["End_Timestamp"]), normalize(r["Kernel_Name"]), r[qkey])
+                for r in rows)
+    marks = [i for i, k in enumerate(ks) if k[2] == args.marker]
+    if len(marks) < args.back + 1:
+        raise SystemExit("fewer than %d launches of %s in the trace" % (args.back + 1, args.marker))
+    a, b = marks[-args.back - 1], marks[-args.back]
+    t0, main_q = ks[a][0], ks[a][3]
+    busy = collections.defaultdict(float)
+    print("| Stream | Start us | End us | us | Kernel |")
+    print("|---|---:|---:|---:|---|")
+    for s0, e0, name, q in ks[a:b]:
+        st = "main" if q == main_q else "second"
+        busy[st] += (e0 - s0) / 1e3
+        print("| %s | %.1f | %.1f | %.1f | `%s` |" % (st, (s0 - t0) / 1e3, (e0 - t0) / 1e3, (e0 - s0) / 1e3, name))
+    print("\nStep: %.1f us from one `%s` to the next; kernels busy %s." % (
+        (ks[b][0] - t0) / 1e3, args.marker,
+        ", ".join("%s stream %.1f us" % (k, v) for k, v in sorted(busy.items()))))
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     sub = ap.add_subparsers(dest="cmd", required=True)
@@ -368,11 +399,15 @@ def main(argv=None):
     k.add_argument("--copy-write")
     k.add_argument("--copy-mib", type=int, default=1024)
     k.add_argument("--by-grid", action="store_true", help="also one row per launch shape of each kernel")
+    tl = sub.add_parser("timeline")
+    tl.add_argument("csv")
+    tl.add_argument("--marker", default="space_to_depth_kernel<bf16>")
+    tl.add_argument("--back", type=int, default=2)
     g = sub.add_parser("libgemm")
     g.add_argument("--reps", type=int, default=20)
     args = ap.parse_args(argv)
     {"copy": cmd_copy, "stats": cmd_stats, "traffic": cmd_traffic, "counters": cmd_counters,
-     "libgemm": cmd_libgemm}[args.cmd](args)
+     "libgemm": cmd_libgemm, "timeline": cmd_timeline}[args.cmd](args)
 
 
 if __name__ == "__main__":

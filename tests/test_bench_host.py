@@ -132,3 +132,29 @@ def test_occupancy_limits():
     assert occ(256, 49152, 159, 0) == 3       # 160 registers -> 3 waves; LDS for 3 workgroups
     assert occ(256, 0, 24, 0) == 8            # bandwidth kernels: the 8-wave limit
     assert occ(256, 147456, 272, 128) == 1    # 400 registers, one workgroup
+
+
+def test_timeline_of_one_step(tmp_path, capsys):
+    """profiling.py timeline: the launches between two consecutive marker
+    launches, main = the marker's queue, times from the step's start."""
+    p = tmp_path / "trace.csv"
+    rows = [("void singa::(anonymous namespace)::space_to_depth_kernel<unsigned short>(int)", 1, 0, 10),
+            ("void singa::(anonymous namespace)::conv_fwd_large_kernel<true, 32, 4, false>(A)", 1, 10, 40),
+            ("void singa::(anonymous namespace)::conv_wgrad_large_kernel<true, false>(W)", 2, 15, 55),
+            ("void singa::(anonymous namespace)::space_to_depth_kernel<unsigned short>(int)", 1, 60, 70),
+            ("void singa::(anonymous namespace)::sgd_kernel(unsigned long)", 1, 70, 75),
+            ("void singa::(anonymous namespace)::space_to_depth_kernel<unsigned short>(int)", 1, 100, 110)]
+    with open(p, "w") as f:
+        f.write("Kernel_Name,Queue_Id,Start_Timestamp,End_Timestamp\n")
+        for name, q, s, e in rows:
+            f.write('"%s",%d,%d,%d\n' % (name, q, s * 1000, e * 1000))
+    profiling.main(["timeline", str(p)])  # the second-to-last step: 0 .. 60 us
+    out = capsys.readouterr().out
+    lines = [l for l in out.splitlines() if l.startswith("| main") or l.startswith("| second")]
+    assert lines == ["| main | 0.0 | 10.0 | 10.0 | `space_to_depth_kernel<bf16>` |",
+                     "| main | 10.0 | 40.0 | 30.0 | `conv_fwd_large_kernel<1,32,4,0>` |",
+                     "| second | 15.0 | 55.0 | 40.0 | `conv_wgrad_large_kernel<1,0>` |"]
+    assert "Step: 60.0 us" in out and "main stream 40.0 us" in out and "second stream 40.0 us" in out
+    profiling.main(["timeline", str(p), "--back", "1"])  # the last complete step: 60 .. 100 us
+    out = capsys.readouterr().out
+    assert "| main | 10.0 | 15.0 | 5.0 | `sgd_kernel` |" in out and "Step: 40.0 us" in out
